@@ -1,0 +1,21 @@
+"""Float64 CPU oracle for the JARQ refinement sweep.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path (the C-ABI library and
+its Python binding) imports, links or calls this package; only the tests, the
+smoke check and the CPU-baseline leg of the benchmark do.  It shares no code,
+constants or helpers with the HIP path.
+
+Modules
+-------
+jarq      The method in the Hessian form F_j = (w_j - what_j)^T H (w_j - what_j),
+          float64, vectorised over rows (rows are independent, Sec. 3.3).
+qrform    The paper's own least-squares form with A = [X; nu I], thin QR of
+          each group block and v = U_i^T y / s (eqs. (3), (7)-(10)); used on
+          small layers where X is available to pin the Hessian form.
+replay    Teacher-forced re-evaluation of one code sweep conditioned on the
+          decisions of another implementation (parity protocol).
+hosts     GPTQ-style sequential-compensation host used for the wide-MLP
+          layer; written from the GPTQ recursion.
+"""
+
+from . import jarq, qrform, replay, hosts  # noqa: F401

@@ -1,0 +1,169 @@
+/*
+ * jarq.h - C ABI of the JARQ refinement sweep for one quantized linear layer
+ * on an AMD Instinct MI355X (gfx950).
+ *
+ * Problem (paper Sec. 3.1-3.2).  A layer with weights W (rows = output
+ * channels, cols = input channels) is held in group-wise uniform form,
+ * eq. (1): row j, group i is s_ij * (q_ij - z_ij), with g consecutive weights
+ * per group, one signed fp32 scale and one integer zero point per group, and
+ * b-bit codes q in {0, ..., 2^b - 1}.  Refinement changes the scales S and
+ * the codes Q and never the bit width, the groups or the zero points Z
+ * (Sec. 3.1).  It minimises the layer objective of eq. (4) written with the
+ * calibration Hessian H = X^T X + nu^2 I:
+ *     F_j = (w_j - what_j)^T H (w_j - what_j),   F = sum_j F_j.
+ *
+ * One sweep (Sec. 3.3, App. E.2) is, for every row independently:
+ *   (b) joint scale update: solve the G x G normal equations eq. (6),
+ *       B_j^T B_j s = B_j^T y_j, with entries c_i^T H_ih c_h and c_i^T (H w)_i
+ *       (c_i = q_i - z_i), adding 1e-4 I when the Gram matrix is near singular;
+ *   (a) residual product P = (W - What) H at the new scales and the previous
+ *       codes, and L_j = sum_c E_jc P_jc (the objective right after the scale
+ *       update, used for early stopping);
+ *   (c) Gauss-Seidel code update over the groups i = 1..G (eq. (7)): one
+ *       bounded Babai nearest-plane proposal per group on the upper Cholesky
+ *       factor R_i of H_ii (eqs. (9)-(10)), kept only if it strictly lowers
+ *       F_j (eq. (8)).  Groups with |s_ij| <= 2^-23 keep their codes.
+ *
+ * Conventions for every entry point:
+ *   - Pointers are device pointers unless marked [host].  Arrays are dense
+ *     row-major.  The caller owns every buffer; the library allocates no
+ *     device memory and keeps no global state.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All device work is enqueued on it in order.
+ *   - W, H and scales must be 16-byte aligned, codes 4-byte aligned,
+ *     the workspace 256-byte aligned.
+ *   - Argument errors return JARQ_EINVAL before anything is enqueued; the
+ *     outputs are then untouched.
+ *   - The workspace of a jarq_prepare call is reused by the later calls on
+ *     the same layer; calls that share a workspace must not overlap.
+ */
+#ifndef JARQ_H_
+#define JARQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define JARQ_ABI_VERSION 1
+#define JARQ_MAX_RECORDED_SWEEPS 64
+
+typedef enum jarq_status {
+  JARQ_OK = 0,
+  JARQ_EINVAL = 1,        /* bad argument (shape, pointer, alignment, code range) */
+  JARQ_ENOT_SPD = 2,      /* some diagonal block H_ii is not positive definite (eq. (9)) */
+  JARQ_ESCALE_SOLVE = 3,  /* a row's Gram matrix failed Cholesky after the ridge (App. E.2) */
+  JARQ_EHIP = 4,          /* a HIP runtime call or kernel launch failed */
+  JARQ_EWORKSPACE = 5     /* workspace missing, too small or misaligned */
+} jarq_status;
+
+/* Problem description.  Sizes are those of eq. (1). */
+typedef struct jarq_params {
+  int32_t rows;          /* d_out >= 1: output channels = rows of W */
+  int32_t cols;          /* d_in: columns of W and order of H; a multiple of group_size */
+  int32_t group_size;    /* g in {32, 64, 128} */
+  int32_t bits;          /* b in [1, 8] */
+  int32_t sweeps;        /* iteration budget K in [0, 4096]; K = 0 leaves the host state */
+  float tau;             /* early-stopping threshold of App. E.2 (1e-5 there); < 0 disables */
+  float ridge_lambda;    /* lambda added on a near-singular Gram matrix (1e-4, App. E.2) */
+  float ridge_rcond;     /* r_cond of the near-singularity test (1e-10, App. E.2) */
+} jarq_params;
+
+/* Filled by jarq_sweeps / jarq_refine when a stats pointer is given [host].
+ * Per-sweep arrays hold the first JARQ_MAX_RECORDED_SWEEPS sweeps. */
+typedef struct jarq_stats {
+  int32_t sweeps_run;                /* sweeps started (a sweep in which every row had stopped is not run) */
+  int32_t rows_active_end;           /* rows still active after the last sweep */
+  double objective_after_scales[JARQ_MAX_RECORDED_SWEEPS];  /* sum_j L_j, fp64 */
+  int64_t accepted_groups[JARQ_MAX_RECORDED_SWEEPS];
+  int64_t codes_changed[JARQ_MAX_RECORDED_SWEEPS];
+  int64_t skipped_groups[JARQ_MAX_RECORDED_SWEEPS];          /* |s| <= 2^-23 */
+  int32_t ridge_rows[JARQ_MAX_RECORDED_SWEEPS];              /* stabilised scale solves */
+  int32_t rows_active[JARQ_MAX_RECORDED_SWEEPS];             /* rows that ran the code update */
+  int64_t correction_blocks[JARQ_MAX_RECORDED_SWEEPS];      /* 16-row x g x g correction products run */
+  float stage_ms[JARQ_MAX_RECORDED_SWEEPS][4];               /* Gram, scale solve, residual product, code update */
+  float prep_ms;                                             /* jarq_refine only */
+} jarq_stats;
+
+/* Bytes of device workspace needed for `p`; 0 if `p` is invalid. */
+size_t jarq_workspace_bytes(const jarq_params* p);
+
+/*
+ * Per-layer set-up (eq. (9) and the right-hand-side shortcut of App. G.8):
+ * factor every diagonal block H_ii = R_i^T R_i (fp64 Cholesky), store R_i,
+ * R_i^{-1} and 1/diag(R_i) in fp32, and compute WH = W H in fp32.  Synchronises
+ * `stream` and returns JARQ_ENOT_SPD if a block is not positive definite.
+ * W [rows][cols] fp32; H [cols][cols] fp32, symmetric, full storage.
+ */
+jarq_status jarq_prepare(const jarq_params* p, const float* W, const float* H,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Scale update (b) for every row from the given codes (eqs. (5)-(6), App. E.2),
+ * on a prepared workspace.  scales [rows][G] fp32 are overwritten; codes
+ * [rows][cols] uint8 and zeros [rows][G] int32 are read.  Asynchronous; a row
+ * whose solve fails after the ridge keeps its previous scales and is counted
+ * in the workspace (reported by jarq_sweeps / jarq_refine).
+ */
+jarq_status jarq_scale_step(const jarq_params* p, const float* H, const uint8_t* codes,
+                            float* scales, const int32_t* zeros,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Residual product (a) and Gauss-Seidel code update (c) at the given scales,
+ * on a prepared workspace.  codes [rows][cols] are updated in place.
+ * Optional trace outputs (NULL to skip), written for every row and group:
+ *   cand     [rows][cols] uint8: the Babai proposal of eq. (10) for the group
+ *            (the unchanged codes where the group was skipped);
+ *   decision [rows][G] uint8: 0 rejected, 1 accepted, 2 skipped (|s| <= 2^-23).
+ * Asynchronous.
+ */
+jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
+                           uint8_t* codes, const float* scales, const int32_t* zeros,
+                           void* workspace, size_t workspace_bytes, void* stream,
+                           uint8_t* cand, uint8_t* decision);
+
+/*
+ * K = p->sweeps sweeps (b) -> (a) -> [early stop] -> (c) on a prepared
+ * workspace, starting with every row active.  codes and scales are updated
+ * in place; zeros are read only.  Checks first that every code is in
+ * [0, 2^b - 1] and every |zero point| <= 2^20 (JARQ_EINVAL otherwise, nothing
+ * changed).  Synchronises `stream` before returning.  `stats` [host] may be
+ * NULL.  Returns JARQ_ESCALE_SOLVE if any row's solve failed after the ridge
+ * (that row keeps its previous scales).
+ */
+jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H,
+                        uint8_t* codes, float* scales, const int32_t* zeros,
+                        void* workspace, size_t workspace_bytes, void* stream,
+                        jarq_stats* stats);
+
+/* jarq_prepare followed by jarq_sweeps. */
+jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H,
+                        uint8_t* codes, float* scales, const int32_t* zeros,
+                        void* workspace, size_t workspace_bytes, void* stream,
+                        jarq_stats* stats);
+
+/*
+ * Layer objective eq. (4) in the Hessian form for the given state:
+ * row_objective [rows] fp64 receives F_j = (w_j - what_j)^T H (w_j - what_j),
+ * with H (w_j - what_j) accumulated in fp32 and the dot product in fp64.
+ * Needs a workspace sized for `p` (it need not be prepared).  Asynchronous.
+ */
+jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,
+                           const uint8_t* codes, const float* scales, const int32_t* zeros,
+                           void* workspace, size_t workspace_bytes, void* stream,
+                           double* row_objective);
+
+/* Static, NUL-terminated description of a status code. */
+const char* jarq_status_string(jarq_status s);
+
+/* JARQ_ABI_VERSION of the built library. */
+int32_t jarq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JARQ_H_ */

@@ -1,0 +1,221 @@
+"""ctypes binding of libjarq (include/jarq.h).
+
+Argument marshalling only: every step of the refinement runs in the HIP
+library.  torch provides device memory and the current stream.  Loading
+fails loudly when the library has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libjarq.so")
+
+MAX_RECORDED_SWEEPS = 64
+JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
+DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
+
+
+class JarqError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int32), ("cols", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("sweeps", ctypes.c_int32), ("tau", ctypes.c_float),
+                ("ridge_lambda", ctypes.c_float), ("ridge_rcond", ctypes.c_float)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("sweeps_run", ctypes.c_int32), ("rows_active_end", ctypes.c_int32),
+                ("objective_after_scales", ctypes.c_double * MAX_RECORDED_SWEEPS),
+                ("accepted_groups", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
+                ("codes_changed", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
+                ("skipped_groups", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
+                ("ridge_rows", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
+                ("rows_active", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
+                ("correction_blocks", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
+                ("stage_ms", (ctypes.c_float * 4) * MAX_RECORDED_SWEEPS),
+                ("prep_ms", ctypes.c_float)]
+
+    def to_dict(self):
+        n = min(self.sweeps_run, MAX_RECORDED_SWEEPS)
+        return {
+            "sweeps_run": self.sweeps_run,
+            "rows_active_end": self.rows_active_end,
+            "objective_after_scales": [self.objective_after_scales[k] for k in range(n)],
+            "accepted_groups": [self.accepted_groups[k] for k in range(n)],
+            "codes_changed": [self.codes_changed[k] for k in range(n)],
+            "skipped_groups": [self.skipped_groups[k] for k in range(n)],
+            "ridge_rows": [self.ridge_rows[k] for k in range(n)],
+            "rows_active": [self.rows_active[k] for k in range(n)],
+            "correction_blocks": [self.correction_blocks[k] for k in range(n)],
+            "stage_ms": [list(self.stage_ms[k]) for k in range(n)],
+            "prep_ms": self.prep_ms,
+        }
+
+
+_vp = ctypes.c_void_p
+_SIGNATURES = {
+    "jarq_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
+    "jarq_prepare": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "jarq_scale_step": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp,
+                                       ctypes.c_size_t, _vp]),
+    "jarq_code_step": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                      ctypes.c_size_t, _vp, _vp, _vp]),
+    "jarq_sweeps": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                   ctypes.c_size_t, _vp, ctypes.POINTER(Stats)]),
+    "jarq_refine": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                   ctypes.c_size_t, _vp, ctypes.POINTER(Stats)]),
+    "jarq_objective": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                      ctypes.c_size_t, _vp, _vp]),
+    "jarq_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "jarq_abi_version": (ctypes.c_int32, []),
+}
+EXPORTED = tuple(_SIGNATURES)
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libjarq.so; raises ImportError if it is missing (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"libjarq.so not built at {path}; run paper_2609_38599_amd/build.py")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().jarq_status_string(int(status)).decode()
+
+
+def make_params(rows, cols, group_size, bits, sweeps=1, tau=-1.0, ridge_lambda=1e-4,
+                ridge_rcond=1e-10) -> Params:
+    return Params(int(rows), int(cols), int(group_size), int(bits), int(sweeps), float(tau),
+                  float(ridge_lambda), float(ridge_rcond))
+
+
+def workspace_bytes(p: Params) -> int:
+    return int(load_library().jarq_workspace_bytes(ctypes.byref(p)))
+
+
+def alloc_workspace(p: Params, device=None) -> torch.Tensor:
+    n = workspace_bytes(p)
+    if n == 0:
+        raise JarqError(JARQ_EINVAL, "workspace_bytes")
+    ws = torch.empty(n + 256, dtype=torch.uint8, device=device or "cuda")
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + n]
+
+
+def _ptr(t, dtype, name):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(status, what):
+    if status != JARQ_OK:
+        raise JarqError(status, what)
+
+
+def prepare(p: Params, W, H, ws, stream=None):
+    lib = load_library()
+    _check(lib.jarq_prepare(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                            _ptr(H, torch.float32, "H"), _ptr(ws, torch.uint8, "workspace"),
+                            ws.numel(), _stream(stream)), "jarq_prepare")
+
+
+def scale_step(p: Params, H, codes, scales, zeros, ws, stream=None):
+    lib = load_library()
+    _check(lib.jarq_scale_step(ctypes.byref(p), _ptr(H, torch.float32, "H"),
+                               _ptr(codes, torch.uint8, "codes"),
+                               _ptr(scales, torch.float32, "scales"),
+                               _ptr(zeros, torch.int32, "zeros"),
+                               _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream)),
+           "jarq_scale_step")
+
+
+def code_step(p: Params, W, H, codes, scales, zeros, ws, cand=None, decision=None, stream=None):
+    lib = load_library()
+    _check(lib.jarq_code_step(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                              _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
+                              _ptr(scales, torch.float32, "scales"),
+                              _ptr(zeros, torch.int32, "zeros"),
+                              _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream),
+                              _ptr(cand, torch.uint8, "cand"),
+                              _ptr(decision, torch.uint8, "decision")), "jarq_code_step")
+
+
+def sweeps(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=True, check=True):
+    lib = load_library()
+    st = Stats() if want_stats else None
+    status = lib.jarq_sweeps(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                             _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
+                             _ptr(scales, torch.float32, "scales"),
+                             _ptr(zeros, torch.int32, "zeros"),
+                             _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream),
+                             ctypes.byref(st) if st is not None else None)
+    if check:
+        _check(status, "jarq_sweeps")
+    return (st.to_dict() if st is not None else None) if check else (status, st)
+
+
+def refine(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=True, check=True):
+    lib = load_library()
+    st = Stats() if want_stats else None
+    status = lib.jarq_refine(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                             _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
+                             _ptr(scales, torch.float32, "scales"),
+                             _ptr(zeros, torch.int32, "zeros"),
+                             _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream),
+                             ctypes.byref(st) if st is not None else None)
+    if check:
+        _check(status, "jarq_refine")
+    return (st.to_dict() if st is not None else None) if check else (status, st)
+
+
+def objective(p: Params, W, H, codes, scales, zeros, ws, out=None, stream=None):
+    lib = load_library()
+    if out is None:
+        out = torch.empty(p.rows, dtype=torch.float64, device=W.device)
+    _check(lib.jarq_objective(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                              _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
+                              _ptr(scales, torch.float32, "scales"),
+                              _ptr(zeros, torch.int32, "zeros"),
+                              _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream),
+                              _ptr(out, torch.float64, "row_objective")), "jarq_objective")
+    return out
+
+
+def abi_version() -> int:
+    return int(load_library().jarq_abi_version())

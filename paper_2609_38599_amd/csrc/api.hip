@@ -1,0 +1,373 @@
+// C ABI of libjarq (declared in include/jarq.h): argument checks, workspace
+// layout, and the stream-ordered sequence of kernels of one refinement run.
+#include <math.h>
+#include <string.h>
+
+#include <vector>
+
+#include "jarq.h"
+#include "jarq_internal.h"
+
+namespace jarq {
+
+static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Layout make_layout(int rows, int cols, int g) {
+  Layout L{};
+  const size_t R = (size_t)rows, C = (size_t)cols, G = (size_t)(cols / g), gg = (size_t)g * g;
+  const size_t nt = (C + kObjTile - 1) / kObjTile;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align256(off + bytes);
+    return at;
+  };
+  L.lfac = take(G * gg * sizeof(double));
+  L.rinv = take(G * gg * sizeof(float));
+  L.rcol = take(G * gg * sizeof(float));
+  L.rdinv = take(G * g * sizeof(float));
+  L.rdsq = take(G * g * sizeof(float));
+  L.wh = take(R * C * sizeof(float));
+  L.gram = take(R * G * G * sizeof(float));
+  L.p = take(R * C * sizeof(float));
+  L.dlt = take(R * C * sizeof(float));
+  L.objpart = take(R * nt * sizeof(double));
+  L.lcur = take(R * sizeof(double));
+  L.lprev = take(R * sizeof(double));
+  L.active = take(R);
+  L.counters = take(sizeof(Counters));
+  L.hist = take(JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord));
+  L.flags = take(sizeof(Flags));
+  L.total = off;
+  return L;
+}
+
+}  // namespace jarq
+
+using namespace jarq;
+
+namespace {
+
+bool valid_params(const jarq_params* p) {
+  if (p == nullptr) return false;
+  if (p->rows < 1 || p->cols < 1) return false;
+  if (p->group_size != 32 && p->group_size != 64 && p->group_size != 128) return false;
+  if (p->cols % p->group_size != 0) return false;
+  if (p->cols / p->group_size > 128) return false;   // G x G fp64 solve must fit in LDS
+  if (p->bits < 1 || p->bits > 8) return false;
+  if (p->sweeps < 0 || p->sweeps > 4096) return false;
+  if (!(p->ridge_lambda >= 0.f) || !isfinite(p->ridge_lambda)) return false;
+  if (!(p->ridge_rcond >= 0.f) || !isfinite(p->ridge_rcond)) return false;
+  if (isnan(p->tau)) return false;
+  if ((size_t)p->rows * (size_t)p->cols > ((size_t)1 << 40)) return false;
+  return true;
+}
+
+bool aligned(const void* ptr, size_t a) { return ptr != nullptr && ((uintptr_t)ptr % a) == 0; }
+
+jarq_status check_ws(const jarq_params* p, const void* ws, size_t bytes) {
+  if (ws == nullptr || ((uintptr_t)ws % 256) != 0) return JARQ_EWORKSPACE;
+  if (bytes < make_layout(p->rows, p->cols, p->group_size).total) return JARQ_EWORKSPACE;
+  return JARQ_OK;
+}
+
+#define JQ_HIP(expr)                          \
+  do {                                        \
+    if ((expr) != hipSuccess) return JARQ_EHIP; \
+  } while (0)
+
+struct Ctx {
+  int rows, cols, g, G, bits;
+  char* ws;
+  Layout lay;
+  hipStream_t st;
+  Counters* cnt() const { return (Counters*)(ws + lay.counters); }
+  Flags* flags() const { return (Flags*)(ws + lay.flags); }
+  SweepRecord* hist() const { return (SweepRecord*)(ws + lay.hist); }
+  uint8_t* active() const { return (uint8_t*)(ws + lay.active); }
+  float* wh() const { return (float*)(ws + lay.wh); }
+  float* gram() const { return (float*)(ws + lay.gram); }
+  float* pbuf() const { return (float*)(ws + lay.p); }
+  float* dlt() const { return (float*)(ws + lay.dlt); }
+  double* objpart() const { return (double*)(ws + lay.objpart); }
+  int nt() const { return (cols + kObjTile - 1) / kObjTile; }
+};
+
+Ctx make_ctx(const jarq_params* p, void* ws, void* stream) {
+  Ctx c;
+  c.rows = p->rows;
+  c.cols = p->cols;
+  c.g = p->group_size;
+  c.G = p->cols / p->group_size;
+  c.bits = p->bits;
+  c.ws = (char*)ws;
+  c.lay = make_layout(c.rows, c.cols, c.g);
+  c.st = (hipStream_t)stream;
+  return c;
+}
+
+hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes, float* scales,
+                              const int32_t* zeros, const uint8_t* active, float lam,
+                              float rcond) {
+  hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, H, codes, zeros, c.gram());
+  if (e != hipSuccess) return e;
+  return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, active,
+                      c.cnt(), c.flags(), lam, rcond);
+}
+
+hipError_t enqueue_babai(const Ctx& c, const float* H, uint8_t* codes, const float* scales,
+                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
+                         uint8_t* decision) {
+  return launch_babai(c.st, c.rows, c.cols, c.g, c.bits, c.pbuf(), H, c.ws, c.lay, codes, scales,
+                      zeros, active, c.dlt(), cand, decision, c.cnt());
+}
+
+jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, void* ws,
+                         void* stream) {
+  Ctx c = make_ctx(p, ws, stream);
+  JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
+  JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
+  JQ_HIP(launch_chol_groups(c.st, c.cols, c.g, H, c.ws, c.lay));
+  JQ_HIP(launch_gemm_ah(c.st, c.rows, c.cols, c.g, false, W, nullptr, nullptr, nullptr, H, c.wh(),
+                        nullptr));
+  Flags f{};
+  JQ_HIP(hipMemcpyAsync(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost, c.st));
+  JQ_HIP(hipStreamSynchronize(c.st));
+  if (f.not_spd) return JARQ_ENOT_SPD;
+  return JARQ_OK;
+}
+
+jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
+                        float* scales, const int32_t* zeros, void* ws, void* stream,
+                        jarq_stats* stats) {
+  Ctx c = make_ctx(p, ws, stream);
+  // Device-side input checks (codes in range, zero points bounded).
+  JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
+  JQ_HIP(launch_validate(c.st, c.rows, c.cols, c.g, c.bits, codes, zeros, c.flags()));
+  Flags f{};
+  JQ_HIP(hipMemcpyAsync(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost, c.st));
+  JQ_HIP(hipStreamSynchronize(c.st));
+  if (f.bad_codes || f.bad_zeros) return JARQ_EINVAL;
+
+  JQ_HIP(launch_fill_u8(c.st, c.active(), (size_t)c.rows, 1));
+  JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
+  JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lcur, (size_t)c.rows * sizeof(double)));
+  JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lprev, (size_t)c.rows * sizeof(double)));
+  JQ_HIP(launch_zero_bytes(c.st, c.hist(), JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord)));
+
+  const int K = p->sweeps;
+  const int nrec = K < JARQ_MAX_RECORDED_SWEEPS ? K : JARQ_MAX_RECORDED_SWEEPS;
+  std::vector<hipEvent_t> ev;
+  if (stats != nullptr) {
+    memset(stats, 0, sizeof(*stats));
+    ev.resize((size_t)nrec * 5);
+    for (auto& e : ev) JQ_HIP(hipEventCreate(&e));
+  }
+  auto mark = [&](int k, int j) -> hipError_t {
+    if (stats == nullptr || k >= nrec) return hipSuccess;
+    return hipEventRecord(ev[(size_t)k * 5 + j], c.st);
+  };
+  jarq_status status = JARQ_OK;
+  int run = 0;
+  for (int k = 0; k < K; ++k) {
+    hipError_t e = hipSuccess;
+    if (e == hipSuccess) e = mark(k, 0);
+    if (e == hipSuccess) e = launch_gram(c.st, c.rows, c.cols, c.g, H, codes, zeros, c.gram());
+    if (e == hipSuccess) e = mark(k, 1);
+    if (e == hipSuccess)
+      e = launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales,
+                       c.active(), c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond);
+    if (e == hipSuccess) e = mark(k, 2);
+    if (e == hipSuccess)
+      e = launch_gemm_ah(c.st, c.rows, c.cols, c.g, true, W, codes, scales, zeros, H, c.pbuf(),
+                         c.objpart());
+    if (e == hipSuccess)
+      e = launch_stop_check(c.st, c.rows, c.nt(), c.objpart(), (double*)(c.ws + c.lay.lcur),
+                            (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau);
+    if (e == hipSuccess) e = mark(k, 3);
+    if (e == hipSuccess) e = enqueue_babai(c, H, codes, scales, zeros, c.active(), nullptr, nullptr);
+    if (e == hipSuccess) e = mark(k, 4);
+    if (e == hipSuccess)
+      e = launch_record_sweep(c.st, c.rows, (const double*)(c.ws + c.lay.lcur), c.active(),
+                              c.cnt(),
+                              c.hist() + (k < JARQ_MAX_RECORDED_SWEEPS ? k
+                                                                        : JARQ_MAX_RECORDED_SWEEPS - 1));
+    if (e != hipSuccess) {
+      status = JARQ_EHIP;
+      break;
+    }
+    ++run;
+    if (p->tau >= 0.f) {
+      // With early stopping on, stop launching once every row has stopped.
+      SweepRecord rec{};
+      const int slot = k < JARQ_MAX_RECORDED_SWEEPS ? k : JARQ_MAX_RECORDED_SWEEPS - 1;
+      if (hipMemcpyAsync(&rec, c.hist() + slot, sizeof(rec), hipMemcpyDeviceToHost, c.st) !=
+              hipSuccess ||
+          hipStreamSynchronize(c.st) != hipSuccess) {
+        status = JARQ_EHIP;
+        break;
+      }
+      if (rec.active_rows == 0) break;
+    }
+  }
+  if (hipStreamSynchronize(c.st) != hipSuccess) status = JARQ_EHIP;
+  if (status == JARQ_OK) {
+    if (hipMemcpy(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost) != hipSuccess)
+      status = JARQ_EHIP;
+    else if (f.solve_failed)
+      status = JARQ_ESCALE_SOLVE;
+  }
+  if (stats != nullptr) {
+    stats->sweeps_run = run;
+    std::vector<SweepRecord> hist(JARQ_MAX_RECORDED_SWEEPS);
+    if (hipMemcpy(hist.data(), c.hist(), hist.size() * sizeof(SweepRecord),
+                  hipMemcpyDeviceToHost) == hipSuccess) {
+      const int n = run < nrec ? run : nrec;
+      for (int k = 0; k < n; ++k) {
+        stats->objective_after_scales[k] = hist[k].objective_after_scales;
+        stats->accepted_groups[k] = (int64_t)hist[k].accepted;
+        stats->codes_changed[k] = (int64_t)hist[k].changed;
+        stats->skipped_groups[k] = (int64_t)hist[k].skipped;
+        stats->ridge_rows[k] = (int32_t)hist[k].ridge_rows;
+        stats->rows_active[k] = (int32_t)hist[k].active_rows;
+        stats->correction_blocks[k] = (int64_t)hist[k].corr_blocks;
+        for (int j = 0; j < 4; ++j) {
+          float ms = 0.f;
+          hipEventElapsedTime(&ms, ev[(size_t)k * 5 + j], ev[(size_t)k * 5 + j + 1]);
+          stats->stage_ms[k][j] = ms;
+        }
+      }
+      if (run > 0) {
+        const int last = run - 1 < JARQ_MAX_RECORDED_SWEEPS ? run - 1 : JARQ_MAX_RECORDED_SWEEPS - 1;
+        stats->rows_active_end = (int32_t)hist[last].active_rows;
+      } else {
+        stats->rows_active_end = c.rows;
+      }
+    }
+    for (auto& e : ev) hipEventDestroy(e);
+  }
+  return status;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t jarq_workspace_bytes(const jarq_params* p) {
+  if (!valid_params(p)) return 0;
+  return make_layout(p->rows, p->cols, p->group_size).total;
+}
+
+jarq_status jarq_prepare(const jarq_params* p, const float* W, const float* H, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16)) return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  return prepare_impl(p, W, H, workspace, stream);
+}
+
+jarq_status jarq_scale_step(const jarq_params* p, const float* H, const uint8_t* codes,
+                            float* scales, const int32_t* zeros, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  if (!valid_params(p) || !aligned(H, 16) || !aligned(codes, 4) || !aligned(scales, 16) ||
+      !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  Ctx c = make_ctx(p, workspace, stream);
+  if (enqueue_scale_step(c, H, codes, scales, zeros, nullptr, p->ridge_lambda, p->ridge_rcond) !=
+      hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
+                           const float* scales, const int32_t* zeros, void* workspace,
+                           size_t workspace_bytes, void* stream, uint8_t* cand,
+                           uint8_t* decision) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+      !aligned(scales, 16) || !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  Ctx c = make_ctx(p, workspace, stream);
+  if (launch_gemm_ah(c.st, c.rows, c.cols, c.g, true, W, codes, scales, zeros, H, c.pbuf(),
+                     nullptr) != hipSuccess)
+    return JARQ_EHIP;
+  if (enqueue_babai(c, H, codes, scales, zeros, nullptr, cand, decision) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
+                        float* scales, const int32_t* zeros, void* workspace,
+                        size_t workspace_bytes, void* stream, jarq_stats* stats) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+      !aligned(scales, 16) || !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  return sweeps_impl(p, W, H, codes, scales, zeros, workspace, stream, stats);
+}
+
+jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
+                        float* scales, const int32_t* zeros, void* workspace,
+                        size_t workspace_bytes, void* stream, jarq_stats* stats) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+      !aligned(scales, 16) || !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (stats != nullptr) {
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return JARQ_EHIP;
+    hipEventRecord(e0, (hipStream_t)stream);
+  }
+  s = prepare_impl(p, W, H, workspace, stream);
+  float prep_ms = 0.f;
+  if (stats != nullptr) {
+    hipEventRecord(e1, (hipStream_t)stream);
+    hipEventSynchronize(e1);
+    hipEventElapsedTime(&prep_ms, e0, e1);
+    hipEventDestroy(e0);
+    hipEventDestroy(e1);
+  }
+  if (s != JARQ_OK) return s;
+  s = sweeps_impl(p, W, H, codes, scales, zeros, workspace, stream, stats);
+  if (stats != nullptr) stats->prep_ms = prep_ms;
+  return s;
+}
+
+jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,
+                           const uint8_t* codes, const float* scales, const int32_t* zeros,
+                           void* workspace, size_t workspace_bytes, void* stream,
+                           double* row_objective) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+      !aligned(scales, 16) || !aligned(zeros, 4) || !aligned(row_objective, 8))
+    return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  Ctx c = make_ctx(p, workspace, stream);
+  if (launch_gemm_ah(c.st, c.rows, c.cols, c.g, true, W, codes, scales, zeros, H, nullptr,
+                     c.objpart()) != hipSuccess)
+    return JARQ_EHIP;
+  if (launch_row_objective(c.st, c.rows, c.nt(), c.objpart(), row_objective) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+const char* jarq_status_string(jarq_status s) {
+  switch (s) {
+    case JARQ_OK: return "ok";
+    case JARQ_EINVAL: return "invalid argument";
+    case JARQ_ENOT_SPD: return "a diagonal Hessian block is not positive definite";
+    case JARQ_ESCALE_SOLVE: return "a scale solve failed after the ridge";
+    case JARQ_EHIP: return "HIP runtime error";
+    case JARQ_EWORKSPACE: return "workspace missing, too small or misaligned";
+    default: return "unknown status";
+  }
+}
+
+int32_t jarq_abi_version(void) { return JARQ_ABI_VERSION; }
+
+}  // extern "C"

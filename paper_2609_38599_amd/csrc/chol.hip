@@ -1,0 +1,125 @@
+// Per-layer factors of the diagonal Hessian blocks (paper eq. (9)).
+//
+// The paper factors each group block of the design, A_i = U_i R_i (thin QR,
+// no column permutation).  Only R_i enters the code update, and
+// R_i^T R_i = A_i^T A_i = H_ii, so R_i is the upper Cholesky factor of H_ii
+// (the Babai proposal does not depend on the row signs of R_i).  One work-group
+// factors one g x g block in LDS in fp64, inverts the lower factor L_i = R_i^T
+// column by column, and writes the fp32 forms the sweep kernels read:
+//   rinv  row n = row n of L_i^{-1}       (u = R_i^{-T} he = L_i^{-1} he)
+//   rcol  [l][j][t] = R_i(j + 16 t, l)   (column l of R_i, interleaved as the
+//                                         16 lanes of a row own it)
+//   rdinv 1 / R_i(l, l),  rdsq R_i(l, l)^2.
+#include "jarq_internal.h"
+
+namespace jarq {
+
+template <int G_SIZE>
+__global__ __launch_bounds__(256) void chol_groups_kernel(const float* __restrict__ H, int cols,
+                                                          double* __restrict__ lfac,
+                                                          float* __restrict__ rinv,
+                                                          float* __restrict__ rcol,
+                                                          float* __restrict__ rdinv,
+                                                          float* __restrict__ rdsq,
+                                                          Flags* __restrict__ flags) {
+  constexpr int g = G_SIZE;
+  constexpr int LD = g + 1;
+  constexpr int NT = g / 16;
+  extern __shared__ double A[];  // g x LD
+  __shared__ int fail;
+  const int blk = blockIdx.x;
+  const int tid = threadIdx.x;
+  const float* Hb = H + (size_t)blk * g * cols + (size_t)blk * g;
+  for (int e = tid; e < g * g; e += blockDim.x) {
+    const int r = e / g, c = e % g;
+    A[r * LD + c] = (double)Hb[(size_t)r * cols + c];
+  }
+  if (tid == 0) fail = 0;
+  __syncthreads();
+  // Right-looking Cholesky H_ii = L L^T on the lower triangle.
+  for (int k = 0; k < g; ++k) {
+    if (tid == 0) {
+      double piv = A[k * LD + k];
+      if (!(piv > 0.0) || !isfinite(piv)) {
+        fail = 1;
+        piv = 1.0;
+      }
+      A[k * LD + k] = sqrt(piv);
+    }
+    __syncthreads();
+    const double d = A[k * LD + k];
+    for (int i = k + 1 + tid; i < g; i += blockDim.x) A[i * LD + k] /= d;
+    __syncthreads();
+    const int n = g - k - 1;
+    for (int e = tid; e < n * n; e += blockDim.x) {
+      const int i = k + 1 + e / n, j = k + 1 + e % n;
+      if (j <= i) A[i * LD + j] -= A[i * LD + k] * A[j * LD + k];
+    }
+    __syncthreads();
+  }
+  double* Lb = lfac + (size_t)blk * g * g;
+  for (int e = tid; e < g * g; e += blockDim.x) {
+    const int r = e / g, c = e % g;
+    Lb[e] = (c <= r) ? A[r * LD + c] : 0.0;
+  }
+  __syncthreads();
+  // Column j of L^{-1}: Linv(i, j) = (delta_ij - sum_{j<=k<i} L(i,k) Linv(k,j)) / L(i,i).
+  // Thread j owns column j of A, which now receives L^{-1}; L is read back from lfac.
+  if (tid < g) {
+    const int j = tid;
+    for (int i = 0; i < g; ++i) {
+      double v = 0.0;
+      if (i >= j) {
+        double acc = (i == j) ? 1.0 : 0.0;
+        for (int k = j; k < i; ++k) acc -= Lb[i * g + k] * A[k * LD + j];
+        v = acc / Lb[i * g + i];
+      }
+      A[i * LD + j] = v;
+    }
+  }
+  __syncthreads();
+  float* rinv_b = rinv + (size_t)blk * g * g;
+  float* rcol_b = rcol + (size_t)blk * g * g;
+  for (int e = tid; e < g * g; e += blockDim.x) {
+    const int r = e / g, c = e % g;
+    rinv_b[e] = (float)A[r * LD + c];
+    // rcol[l][j][t] with e = (l * 16 + j) * NT + t  ->  R(j + 16 t, l) = L(l, j + 16 t)
+    const int l = e / (16 * NT);
+    const int j = (e / NT) % 16;
+    const int t = e % NT;
+    const int m = j + 16 * t;
+    rcol_b[e] = (float)(m <= l ? Lb[l * g + m] : 0.0);
+  }
+  for (int l = tid; l < g; l += blockDim.x) {
+    const double d = Lb[l * g + l];
+    rdinv[(size_t)blk * g + l] = (float)(1.0 / d);
+    rdsq[(size_t)blk * g + l] = (float)(d * d);
+  }
+  if (tid == 0 && fail) atomicAdd(&flags->not_spd, 1);
+}
+
+template <int G_SIZE>
+static hipError_t launch_chol_t(hipStream_t st, int cols, const float* H, char* ws,
+                                const Layout& lay) {
+  const int G = cols / G_SIZE;
+  const size_t lds = (size_t)G_SIZE * (G_SIZE + 1) * sizeof(double);
+  hipError_t e = hipFuncSetAttribute((const void*)chol_groups_kernel<G_SIZE>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(chol_groups_kernel<G_SIZE>, dim3(G), dim3(256), lds, st, H, cols,
+                     (double*)(ws + lay.lfac), (float*)(ws + lay.rinv), (float*)(ws + lay.rcol),
+                     (float*)(ws + lay.rdinv), (float*)(ws + lay.rdsq), (Flags*)(ws + lay.flags));
+  return hipGetLastError();
+}
+
+hipError_t launch_chol_groups(hipStream_t st, int cols, int g, const float* H, char* ws,
+                              const Layout& lay) {
+  switch (g) {
+    case 32: return launch_chol_t<32>(st, cols, H, ws, lay);
+    case 64: return launch_chol_t<64>(st, cols, H, ws, lay);
+    case 128: return launch_chol_t<128>(st, cols, H, ws, lay);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace jarq

@@ -1,0 +1,119 @@
+// Internal declarations shared by the HIP translation units of libjarq.
+// Nothing here is part of the public ABI (include/jarq.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace jarq {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr float kFp32Eps = 1.1920928955078125e-07f;  // 2^-23, App. E.2 "FP32 machine epsilon"
+constexpr int kObjTile = 64;                           // columns per objective partial
+
+// Per-group outcome of the code update.
+enum : uint8_t { kDecReject = 0, kDecAccept = 1, kDecSkip = 2, kDecStopped = 3 };
+
+// Device-side counters of one sweep.  Integer atomics only, so totals do not
+// depend on scheduling.
+struct Counters {
+  unsigned long long accepted;
+  unsigned long long changed;
+  unsigned long long skipped;
+  unsigned long long corr_blocks;  // 16-row x g x g correction products executed
+  unsigned int ridge_rows;
+  unsigned int solve_failed;
+  unsigned int active_rows;
+  unsigned int pad;
+};
+
+// One recorded sweep.
+struct SweepRecord {
+  double objective_after_scales;
+  unsigned long long accepted;
+  unsigned long long changed;
+  unsigned long long skipped;
+  unsigned long long corr_blocks;
+  unsigned int ridge_rows;
+  unsigned int solve_failed;
+  unsigned int active_rows;
+  unsigned int pad;
+};
+
+// Status words written by device checks and read by the host.
+struct Flags {
+  int not_spd;         // blocks H_ii that failed Cholesky
+  int bad_codes;       // codes > 2^b - 1
+  int bad_zeros;       // |z| > 2^20
+  int solve_failed;    // rows whose scale solve failed after the ridge (all sweeps)
+  int pad[4];
+};
+
+// Offsets (bytes) of the workspace regions for one problem size.
+struct Layout {
+  size_t lfac;      // [G][g][g] f64: Cholesky factor L_i (prep scratch)
+  size_t rinv;      // [G][g][g] f32: row n = row n of L_i^{-1} = column n of R_i^{-1}
+  size_t rcol;      // [G][g][16][g/16] f32: R_i columns interleaved for the back substitution
+  size_t rdinv;     // [G][g] f32: 1 / R_i(l,l)
+  size_t rdsq;      // [G][g] f32: R_i(l,l)^2
+  size_t wh;        // [rows][cols] f32: W H
+  size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
+  size_t p;         // [rows][cols] f32: (W - What) H
+  size_t dlt;       // [rows][cols] f32: s_i (q_new - q_old) of accepted groups, 0 elsewhere
+  size_t objpart;   // [rows][ceil(cols/64)] f64: partial row objectives
+  size_t lcur;      // [rows] f64
+  size_t lprev;     // [rows] f64
+  size_t active;    // [rows] u8
+  size_t counters;  // Counters
+  size_t hist;      // [64] SweepRecord
+  size_t flags;     // Flags
+  size_t total;
+};
+
+Layout make_layout(int rows, int cols, int g);
+
+// ---- launchers (each returns hipGetLastError() of its launches) ----
+
+hipError_t launch_chol_groups(hipStream_t st, int cols, int g, const float* H, char* ws,
+                              const Layout& lay);
+
+// C = A H with A = W (quant == false) or A = W - What (quant == true).  When
+// objpart is non-null, objpart[row][col/64] receives sum over the 64-column
+// slice of A(row, c) * C(row, c) in fp64.  C may be null (objective only).
+hipError_t launch_gemm_ah(hipStream_t st, int rows, int cols, int g, bool quant,
+                          const float* W, const uint8_t* codes, const float* scales,
+                          const int32_t* zeros, const float* H, float* C, double* objpart);
+
+hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const float* H,
+                       const uint8_t* codes, const int32_t* zeros, float* gram);
+
+hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
+                        const float* wh, const uint8_t* codes, const int32_t* zeros,
+                        float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
+                        float lam, float rcond);
+
+hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, const float* P,
+                        const float* H, const char* ws, const Layout& lay, uint8_t* codes,
+                        const float* scales, const int32_t* zeros, const uint8_t* active,
+                        float* dlt, uint8_t* cand, uint8_t* decision, Counters* cnt);
+
+hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
+                                double* out);
+
+hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
+                             double* lcur, double* lprev, uint8_t* active, int sweep,
+                             float tau);
+
+hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);
+hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n);
+
+hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
+                               const uint8_t* active, Counters* cnt, SweepRecord* rec);
+
+hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
+                           const uint8_t* codes, const int32_t* zeros, Flags* flags);
+
+}  // namespace jarq

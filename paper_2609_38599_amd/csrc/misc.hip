@@ -1,0 +1,146 @@
+// Small per-sweep kernels: row objectives, the early-stopping rule of App. E.2,
+// fills (kernels rather than hipMemsetAsync so a captured graph replays them
+// reliably), the per-sweep record, and the device-side input checks.
+#include "jarq_internal.h"
+
+namespace jarq {
+
+__global__ void row_objective_kernel(int rows, int nt, const double* __restrict__ part,
+                                     double* __restrict__ out) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows) return;
+  double s = 0.0;
+  for (int t = 0; t < nt; ++t) s += part[(size_t)r * nt + t];
+  out[r] = s;
+}
+
+hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
+                                double* out) {
+  hipLaunchKernelGGL(row_objective_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, rows, nt,
+                     objpart, out);
+  return hipGetLastError();
+}
+
+// L_j^(k) = sum of the partials; at k >= 2 an active row stops (before its
+// code update) when (L^(k-1) - L^(k)) / max(|L^(k-1)|, eps) <= tau or
+// |L^(k-1) - L^(k)| <= tau (App. E.2, eq. (strict_stopping)).  The new scales
+// are kept.
+__global__ void stop_check_kernel(int rows, int nt, const double* __restrict__ part,
+                                  double* __restrict__ lcur, double* __restrict__ lprev,
+                                  uint8_t* __restrict__ active, int sweep, float tau) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows) return;
+  if (!active[r]) return;
+  double s = 0.0;
+  for (int t = 0; t < nt; ++t) s += part[(size_t)r * nt + t];
+  lcur[r] = s;
+  if (tau >= 0.f && sweep >= 2) {
+    const double prev = lprev[r];
+    const double dec = prev - s;
+    const double rel = dec / fmax(fabs(prev), (double)kFp32Eps);
+    if (rel <= (double)tau || fabs(dec) <= (double)tau) active[r] = 0;
+  }
+  lprev[r] = s;
+}
+
+hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
+                             double* lcur, double* lprev, uint8_t* active, int sweep,
+                             float tau) {
+  hipLaunchKernelGGL(stop_check_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, rows, nt,
+                     objpart, lcur, lprev, active, sweep, tau);
+  return hipGetLastError();
+}
+
+__global__ void fill_u8_kernel(uint8_t* __restrict__ p, size_t n, uint8_t v) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v) {
+  if (n == 0) return hipSuccess;
+  const size_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(fill_u8_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0,
+                     st, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n) {
+  return launch_fill_u8(st, (uint8_t*)p, n, 0);
+}
+
+// Sum of L over all rows (a stopped row keeps its last L, which is still its
+// objective) in a fixed order, plus the counters; the counters are then reset.
+__global__ __launch_bounds__(256) void record_sweep_kernel(int rows, const double* __restrict__ lcur,
+                                                           const uint8_t* __restrict__ active,
+                                                           Counters* __restrict__ cnt,
+                                                           SweepRecord* __restrict__ rec) {
+  __shared__ double red[256];
+  __shared__ unsigned int act[256];
+  double s = 0.0;
+  unsigned int a = 0;
+  for (int r = threadIdx.x; r < rows; r += 256) {
+    s += lcur[r];
+    a += active[r] ? 1u : 0u;
+  }
+  red[threadIdx.x] = s;
+  act[threadIdx.x] = a;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      red[threadIdx.x] += red[threadIdx.x + w];
+      act[threadIdx.x] += act[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    rec->objective_after_scales = red[0];
+    rec->accepted = cnt->accepted;
+    rec->changed = cnt->changed;
+    rec->skipped = cnt->skipped;
+    rec->corr_blocks = cnt->corr_blocks;
+    rec->ridge_rows = cnt->ridge_rows;
+    rec->solve_failed = cnt->solve_failed;
+    rec->active_rows = act[0];
+    cnt->accepted = 0;
+    cnt->changed = 0;
+    cnt->skipped = 0;
+    cnt->corr_blocks = 0;
+    cnt->ridge_rows = 0;
+    cnt->solve_failed = 0;
+    cnt->active_rows = 0;
+  }
+}
+
+hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
+                               const uint8_t* active, Counters* cnt, SweepRecord* rec) {
+  hipLaunchKernelGGL(record_sweep_kernel, dim3(1), dim3(256), 0, st, rows, lcur, active, cnt, rec);
+  return hipGetLastError();
+}
+
+__global__ void validate_kernel(int rows, int cols, int g, int qmax,
+                                const uint8_t* __restrict__ codes,
+                                const int32_t* __restrict__ zeros, Flags* __restrict__ flags) {
+  const size_t n = (size_t)rows * cols;
+  const int G = cols / g;
+  int bad_q = 0, bad_z = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    bad_q += codes[i] > qmax;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < (size_t)rows * G;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const int z = zeros[i];
+    bad_z += (z > (1 << 20) || z < -(1 << 20));
+  }
+  if (bad_q) atomicAdd(&flags->bad_codes, bad_q);
+  if (bad_z) atomicAdd(&flags->bad_zeros, bad_z);
+}
+
+hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
+                           const uint8_t* codes, const int32_t* zeros, Flags* flags) {
+  hipLaunchKernelGGL(validate_kernel, dim3(1024), dim3(256), 0, st, rows, cols, g,
+                     (1 << bits) - 1, codes, zeros, flags);
+  return hipGetLastError();
+}
+
+}  // namespace jarq

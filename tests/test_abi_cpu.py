@@ -1,0 +1,81 @@
+"""The C-ABI library loads and exports what include/jarq.h declares (CPU only).
+
+Only calls that return before touching the GPU are made here: workspace
+sizing, status strings, the ABI version and argument checks.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_38599_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "jarq.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(jarq_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared_functions()
+    assert "jarq_refine" in names and "jarq_code_step" in names
+    for name in names:
+        assert hasattr(lib, name), name
+        assert name in binding.EXPORTED, name
+
+
+def test_abi_version_and_status_strings(lib):
+    assert binding.abi_version() == 1
+    for s in range(6):
+        assert binding.status_string(s)
+    assert binding.status_string(99) == "unknown status"
+
+
+def test_workspace_bytes_valid_and_invalid():
+    p = binding.make_params(4096, 4096, 128, 3, 10)
+    n = binding.workspace_bytes(p)
+    # W H, P and the accepted-change buffer dominate: 3 x 64 MiB plus the Gram matrices
+    assert 3 * 64 * 2**20 < n < 260 * 2**20
+    for bad in [dict(rows=0), dict(cols=100), dict(group_size=48), dict(bits=0), dict(bits=9),
+                dict(sweeps=-1), dict(cols=128 * 129), dict(ridge_lambda=-1.0)]:
+        kw = dict(rows=64, cols=256, group_size=64, bits=3, sweeps=5)
+        kw.update(bad)
+        assert binding.workspace_bytes(binding.make_params(**kw)) == 0, bad
+
+
+def _vp(x):
+    return ctypes.c_void_p(x)
+
+
+def test_argument_errors_return_before_any_launch(lib):
+    p = binding.make_params(64, 256, 64, 3, 5)
+    fake = _vp(1 << 20)          # aligned, never dereferenced: every call below fails its checks
+    bad = binding.make_params(64, 250, 64, 3, 5)
+    P = ctypes.POINTER(binding.Params)
+    assert lib.jarq_prepare(ctypes.byref(bad), fake, fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
+    assert lib.jarq_prepare(ctypes.byref(p), None, fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
+    assert lib.jarq_prepare(ctypes.byref(p), _vp((1 << 20) + 4), fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
+    assert lib.jarq_prepare(ctypes.byref(p), fake, fake, None, 1 << 30, None) == binding.JARQ_EWORKSPACE
+    assert lib.jarq_prepare(ctypes.byref(p), fake, fake, _vp((1 << 20) + 128), 1 << 30, None) == binding.JARQ_EWORKSPACE
+    assert lib.jarq_prepare(ctypes.byref(p), fake, fake, fake, 1024, None) == binding.JARQ_EWORKSPACE
+    assert lib.jarq_sweeps(ctypes.byref(p), fake, fake, _vp((1 << 20) + 2), fake, fake, fake, 1 << 30,
+                           None, None) == binding.JARQ_EINVAL
+    assert lib.jarq_code_step(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, 1 << 30, None,
+                              None, None) == binding.JARQ_EINVAL
+    assert lib.jarq_scale_step(ctypes.byref(p), fake, fake, _vp((1 << 20) + 8), fake, fake, 1 << 30,
+                               None) == binding.JARQ_EINVAL
+    assert lib.jarq_objective(ctypes.byref(p), fake, fake, fake, fake, fake, fake, 1 << 30, None,
+                              None) == binding.JARQ_EINVAL
+    assert lib.jarq_refine(None, fake, fake, fake, fake, fake, fake, 1 << 30, None, None) == binding.JARQ_EINVAL
+    del P

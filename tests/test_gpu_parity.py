@@ -1,0 +1,287 @@
+"""HIP path vs the float64 oracle (needs an MI355X and the built libjarq.so).
+
+Per stage: the objective, the scale step (scales within 1e-4 relative) and the
+code step checked decision by decision against the oracle conditioned on the
+GPU's earlier decisions (codes identical except within 1e-4 of a rounding
+boundary, at most 0.1% of codes).  End to end: K free-running sweeps, final
+objective within 1e-5 relative.  Shapes cover several tiles with ragged
+tails, every group size and bit width, the degenerate cases of the method,
+and the full-size layers (checked on sampled rows, rows being independent).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from tests._gpu_common import (CONFIGS, OBJ_RTOL, GpuLayer, check_code_step, check_scales, jarq,
+                               jq, layer, random_layer, rel, say)
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def _oracle_final_objective(W, H, q, s, z, g):
+    return jarq.objective_rows(W, H, q, s, z, g)
+
+
+# --------------------------------------------------------------------------
+# tiny layer (64 x 256, g = 64, 3 bits, 5 sweeps)
+# --------------------------------------------------------------------------
+
+def test_objective_tiny():
+    cfg, W, H, q, s, z = layer(0)
+    gl = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits)
+    F = gl.objective()
+    F_ref = jarq.objective_rows(W, H, q, s, z, cfg.group_size)
+    say(f"[objective] worst rel {np.max(np.abs(F - F_ref) / F_ref):.3e}")
+    assert np.all(np.abs(F - F_ref) <= OBJ_RTOL * F_ref)
+
+
+def test_scale_step_tiny():
+    cfg, W, H, q, s, z = layer(0)
+    gl = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits)
+    gl.scale_step()
+    _, s_gpu = gl.state()
+    s_ref, ridge = jarq.scale_step(W, H, q, z, cfg.group_size)
+    assert not ridge.any()
+    check_scales(s_gpu, s_ref)
+
+
+def test_code_step_tiny_teacher_forced():
+    cfg, W, H, q, s, z = layer(0)
+    g, bits = cfg.group_size, cfg.bits
+    gl = GpuLayer(W, H, q, s, z, g, bits)
+    R = jarq.group_factors(H, g)
+    for sweep in range(3):
+        gl.scale_step()
+        q0, s1 = gl.state()
+        cand, dec = gl.code_step()
+        q1, _ = gl.state()
+        check_code_step(W, H, R, q0, s1, z, g, bits, cand, dec, f" sweep {sweep + 1}")
+        expect = q0.copy()
+        for i in range(cfg.groups):
+            acc = dec[:, i] == jq.DEC_ACCEPT
+            expect[acc, i * g:(i + 1) * g] = cand[acc, i * g:(i + 1) * g]
+        assert np.array_equal(q1, expect)
+        if sweep == 0:
+            assert (dec == jq.DEC_ACCEPT).sum() > 0
+
+
+def test_refine_tiny_end_to_end():
+    cfg, W, H, q, s, z = layer(0)
+    g, bits, K = cfg.group_size, cfg.bits, cfg.sweeps
+    gl = GpuLayer(W, H, q, s, z, g, bits, sweeps=K)
+    st = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws)
+    qg, sg = gl.state()
+    qo, so, hist = jarq.refine(W, H, q, s, z, g, bits, K)
+    F_gpu = _oracle_final_objective(W, H, qg, sg, z, g).sum()
+    F_or = _oracle_final_objective(W, H, qo, so, z, g).sum()
+    F_host = jarq.objective_rows(W, H, q, s, z, g).sum()
+    agree = np.mean(qg == qo)
+    say(f"[e2e tiny] F_host {F_host:.6e} F_gpu {F_gpu:.9e} F_oracle {F_or:.9e} "
+        f"rel {rel(F_gpu, F_or):.2e} code agreement {agree:.6f} stats {st['accepted_groups']}")
+    assert st["sweeps_run"] == K
+    assert rel(F_gpu, F_or) <= OBJ_RTOL
+    assert F_gpu < F_host
+    L = st["objective_after_scales"]
+    for k in range(K):
+        assert rel(L[k], np.nansum(hist[k].L)) <= OBJ_RTOL
+    # the GPU objective of its own final state
+    F_dev = gl.objective()
+    F_dev_ref = jarq.objective_rows(W, H, qg, sg, z, g)
+    assert np.all(np.abs(F_dev - F_dev_ref) <= OBJ_RTOL * F_dev_ref)
+
+
+def test_zero_sweeps_is_identity():
+    cfg, W, H, q, s, z = layer(0)
+    gl = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits, sweeps=0)
+    st = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws)
+    qg, sg = gl.state()
+    assert st["sweeps_run"] == 0
+    assert np.array_equal(qg, q) and np.array_equal(sg, s)
+
+
+def test_deterministic():
+    cfg, W, H, q, s, z = layer(0)
+    outs = []
+    for _ in range(2):
+        gl = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits, sweeps=cfg.sweeps)
+        jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws)
+        outs.append(gl.state())
+    assert np.array_equal(outs[0][0], outs[1][0])
+    assert np.array_equal(outs[0][1].view(np.uint32), outs[1][1].view(np.uint32))
+
+
+def test_refine_entry_equals_prepare_plus_sweeps():
+    cfg, W, H, q, s, z = layer(0)
+    a = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits, sweeps=3)
+    jq.sweeps(a.p, a.W, a.H, a.codes, a.scales, a.zeros, a.ws)
+    b = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits, sweeps=3, prepare=False)
+    st = jq.refine(b.p, b.W, b.H, b.codes, b.scales, b.zeros, b.ws)
+    assert st["prep_ms"] > 0
+    qa, sa = a.state()
+    qb, sb = b.state()
+    assert np.array_equal(qa, qb) and np.array_equal(sa, sb)
+
+
+def test_early_stopping_tiny():
+    cfg, W, H, q, s, z = layer(0)
+    g, bits = cfg.group_size, cfg.bits
+    tau = 1e-5
+    gl = GpuLayer(W, H, q, s, z, g, bits, sweeps=12, tau=tau)
+    st = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws)
+    qg, sg = gl.state()
+    qo, so, hist = jarq.refine(W, H, q, s, z, g, bits, 12, tau=tau)
+    act_o = [int(h.active.sum()) for h in hist]
+    say(f"[early stop] gpu active {st['rows_active']} oracle {act_o}")
+    n = min(len(act_o), st["sweeps_run"])
+    for k in range(n):
+        assert abs(st["rows_active"][k] - act_o[k]) <= 2
+    F_gpu = jarq.objective_rows(W, H, qg, sg, z, g).sum()
+    F_or = jarq.objective_rows(W, H, qo, so, z, g).sum()
+    assert rel(F_gpu, F_or) <= 1e-4
+
+
+# --------------------------------------------------------------------------
+# shapes: ragged row tiles, every group size, several bit widths
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,cols,g,bits", [
+    (37, 96, 32, 2), (50, 192, 64, 4), (129, 384, 128, 3), (16, 128, 128, 8),
+    (1, 64, 32, 1), (200, 256, 64, 3), (65, 640, 128, 4)])
+def test_shapes(rows, cols, g, bits):
+    W, H, q, s, z = random_layer(rows, cols, g, bits, seed=rows * 7 + cols + bits)
+    say(f"[shape] rows {rows} cols {cols} g {g} bits {bits}")
+    gl = GpuLayer(W, H, q, s, z, g, bits)
+    F = gl.objective()
+    F_ref = jarq.objective_rows(W, H, q, s, z, g)
+    assert np.all(np.abs(F - F_ref) <= OBJ_RTOL * F_ref)
+    R = jarq.group_factors(H, g)
+    for sweep in range(2):
+        q_before, _ = gl.state()
+        gl.scale_step()
+        q0, s1 = gl.state()
+        assert np.array_equal(q0, q_before)
+        s_ref, _ = jarq.scale_step(W, H, q0, z, g)
+        check_scales(s1, s_ref, f" {rows}x{cols} sweep {sweep + 1}")
+        cand, dec = gl.code_step()
+        check_code_step(W, H, R, q0, s1, z, g, bits, cand, dec, f" {rows}x{cols} sweep {sweep + 1}")
+    K = 4
+    gk = GpuLayer(W, H, q, s, z, g, bits, sweeps=K)
+    jq.sweeps(gk.p, gk.W, gk.H, gk.codes, gk.scales, gk.zeros, gk.ws)
+    qg, sg = gk.state()
+    qo, so, _ = jarq.refine(W, H, q, s, z, g, bits, K)
+    F_gpu = jarq.objective_rows(W, H, qg, sg, z, g).sum()
+    F_or = jarq.objective_rows(W, H, qo, so, z, g).sum()
+    say(f"[shape e2e] rel {rel(F_gpu, F_or):.2e} agreement {np.mean(qg == qo):.6f}")
+    assert rel(F_gpu, F_or) <= OBJ_RTOL
+
+
+# --------------------------------------------------------------------------
+# degenerate cases of the method
+# --------------------------------------------------------------------------
+
+def test_ridge_branch_matches_oracle():
+    W, H, q, s, z = random_layer(40, 256, 64, 3, seed=5)
+    q = q.copy()
+    q[3, 64:128] = z[3, 1]           # group 1 of row 3 all at its zero point: B_j rank deficient
+    q[17, 0:64] = z[17, 0]
+    gl = GpuLayer(W, H, q, s, z, 64, 3, sweeps=1)
+    gl.scale_step()
+    _, s_gpu = gl.state()
+    s_ref, ridge = jarq.scale_step(W, H, q, z, 64)
+    assert ridge[3] and ridge[17] and ridge.sum() == 2
+    check_scales(s_gpu, s_ref, " ridge")
+    assert s_gpu[3, 1] == 0.0 and s_gpu[17, 0] == 0.0
+    g2 = GpuLayer(W, H, q, s, z, 64, 3, sweeps=1)
+    st = jq.sweeps(g2.p, g2.W, g2.H, g2.codes, g2.scales, g2.zeros, g2.ws)
+    assert st["ridge_rows"][0] == 2
+
+
+def test_small_scale_groups_are_skipped():
+    W, H, q, s, z = random_layer(20, 256, 64, 3, seed=6)
+    gl = GpuLayer(W, H, q, s, z, 64, 3)
+    gl.scale_step()
+    s_t = gl.scales
+    s_t[2, 1] = 1e-9
+    s_t[5, 3] = 0.0
+    q0, s1 = gl.state()
+    cand, dec = gl.code_step()
+    q1, _ = gl.state()
+    assert dec[2, 1] == jq.DEC_SKIP and dec[5, 3] == jq.DEC_SKIP
+    assert np.array_equal(q1[2, 64:128], q0[2, 64:128])
+    assert np.array_equal(q1[5, 192:256], q0[5, 192:256])
+    check_code_step(W, H, jarq.group_factors(H, 64), q0, s1, z, 64, 3, cand, dec, " skip")
+
+
+def test_failed_scale_solve_reports_and_keeps_scales():
+    W, H, q, s, z = random_layer(24, 128, 64, 3, seed=7)
+    H = H.copy()
+    H[0, 64] = H[64, 0] = np.nan     # nonfinite coupling block: Gram nonfinite, ridge fails too
+    gl = GpuLayer(W, H, q, s, z, 64, 3, sweeps=2)
+    status, _ = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws, check=False)
+    assert status == jq.JARQ_ESCALE_SOLVE
+    qg, sg = gl.state()
+    assert np.array_equal(sg, s)
+
+
+def test_not_spd_block_is_reported():
+    W, H, q, s, z = random_layer(8, 128, 64, 3, seed=8)
+    H = H.copy()
+    H[70, 70] = -1.0
+    gl = GpuLayer(W, H, q, s, z, 64, 3, prepare=False)
+    with pytest.raises(jq.JarqError) as ei:
+        jq.prepare(gl.p, gl.W, gl.H, gl.ws)
+    assert ei.value.status == jq.JARQ_ENOT_SPD
+
+
+def test_out_of_range_codes_are_rejected_untouched():
+    W, H, q, s, z = random_layer(8, 128, 64, 3, seed=9)
+    q = q.copy()
+    q[4, 10] = 9
+    gl = GpuLayer(W, H, q, s, z, 64, 3, sweeps=2)
+    status, _ = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws, check=False)
+    assert status == jq.JARQ_EINVAL
+    qg, sg = gl.state()
+    assert np.array_equal(qg, q) and np.array_equal(sg, s)
+
+
+# --------------------------------------------------------------------------
+# full-size layers, checked on sampled rows
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4])
+def test_full_size_layer(cfg_id):
+    cfg, W, H, q, s, z = layer(cfg_id)
+    g, bits, K = cfg.group_size, cfg.bits, cfg.sweeps
+    rng = np.random.default_rng(cfg_id)
+    sample = np.unique(np.concatenate([[0, cfg.rows - 1], rng.choice(cfg.rows, 14, replace=False)]))
+    R = jarq.group_factors(H, g)
+    gl = GpuLayer(W, H, q, s, z, g, bits, sweeps=K)
+    # traced first sweep, checked on the sample
+    gl.scale_step()
+    q0, s1 = gl.state()
+    s_ref, _ = jarq.scale_step(W[sample], H, q0[sample], z[sample], g)
+    check_scales(s1[sample], s_ref, f" cfg{cfg_id}")
+    cand, dec = gl.code_step()
+    check_code_step(W[sample], H, R, q0[sample], s1[sample], z[sample], g, bits, cand[sample],
+                    dec[sample], f" cfg{cfg_id}")
+    say(f"[cfg{cfg_id}] sweep-1 accept rate {(dec == jq.DEC_ACCEPT).mean():.4f}")
+    del gl
+    torch.cuda.empty_cache()
+    # K free-running sweeps from the host state, as timed by the benchmark
+    gk = GpuLayer(W, H, q, s, z, g, bits, sweeps=K)
+    st = jq.sweeps(gk.p, gk.W, gk.H, gk.codes, gk.scales, gk.zeros, gk.ws)
+    qg, sg = gk.state()
+    F_dev = gk.objective()
+    say(f"[cfg{cfg_id}] L per sweep {['%.6e' % v for v in st['objective_after_scales']]}")
+    say(f"[cfg{cfg_id}] accepted {st['accepted_groups']} stage ms {st['stage_ms'][-1]}")
+    qo, so, _ = jarq.refine(W[sample], H, q[sample], s[sample], z[sample], g, bits, K, R=R)
+    F_gpu = jarq.objective_rows(W[sample], H, qg[sample], sg[sample], z[sample], g)
+    F_or = jarq.objective_rows(W[sample], H, qo, so, z[sample], g)
+    say(f"[cfg{cfg_id}] sample F rel {rel(F_gpu.sum(), F_or.sum()):.2e} "
+        f"code agreement {np.mean(qg[sample] == qo):.6f}")
+    assert rel(F_gpu.sum(), F_or.sum()) <= OBJ_RTOL
+    assert np.all(np.abs(F_dev[sample] - F_gpu) <= OBJ_RTOL * F_gpu)
+    L = st["objective_after_scales"]
+    assert all(L[k + 1] <= L[k] * (1 + 1e-6) for k in range(len(L) - 1))

@@ -190,31 +190,32 @@ __global__ __launch_bounds__(256, 1) void babai_kernel(
       for (int t = 0; t <= tl; ++t) acc[t] += rl[t] * db;
     }
     float unorm = 0.f;
+    int changed = 0;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) unorm += u[t] * u[t];
+    for (int t = 0; t < NT; ++t) {
+      unorm += u[t] * u[t];
+      changed += qc[t] != qold[t];
+    }
 #pragma unroll
     for (int off = 8; off >= 1; off >>= 1) {
       unorm += __shfl_xor(unorm, off);
       rsum += __shfl_xor(rsum, off);
+      changed += __shfl_xor(changed, off);
     }
-    const bool accept = do_row && isfinite(rsum) && (rsum < unorm);
+    // A proposal equal to the current codes changes F by exactly 0, which the
+    // strict test rejects whatever the rounding of the two norms.
+    const bool accept = do_row && changed > 0 && isfinite(rsum) && (rsum < unorm);
     // 4. outputs
-    int changed = 0;
     if (row_in) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         const int l = cj + 16 * t;
         const int dq = qc[t] - qold[t];
-        if (accept) {
-          codes[cbase + l] = (uint8_t)qc[t];
-          changed += dq != 0;
-        }
+        if (accept) codes[cbase + l] = (uint8_t)qc[t];
         dlt[cbase + l] = accept ? s * (float)dq : 0.f;
         if (cand_out != nullptr) cand_out[cbase + l] = (uint8_t)(do_row ? qc[t] : qold[t]);
       }
     }
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) changed += __shfl_xor(changed, off);
     if (row_in && cj == 0) {
       if (dec_out != nullptr) {
         uint8_t d = !row_act ? kDecStopped : (skip ? kDecSkip : (accept ? kDecAccept : kDecReject));

@@ -27,6 +27,12 @@ Layout make_layout(int rows, int cols, int g) {
   L.rcol = take(G * gg * sizeof(float));
   L.rdinv = take(G * g * sizeof(float));
   L.rdsq = take(G * g * sizeof(float));
+  L.hhi = take(C * C * 2);
+  L.hlo = take(C * C * 2);
+  L.hscale = take(2 * sizeof(float));
+  L.ehi = take(R * C * 2);
+  L.elo = take(R * C * 2);
+  L.erow = take(R * sizeof(float));
   L.wh = take(R * C * sizeof(float));
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
@@ -128,6 +134,7 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
   JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
   JQ_HIP(launch_chol_groups(c.st, c.cols, c.g, H, c.ws, c.lay));
+  JQ_HIP(launch_split_h(c.st, c.cols, H, c.ws, c.lay));
   JQ_HIP(launch_gemm_ah(c.st, c.rows, c.cols, c.g, false, W, nullptr, nullptr, nullptr, H, c.wh(),
                         nullptr));
   Flags f{};
@@ -179,8 +186,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
                        c.active(), c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond);
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
-      e = launch_gemm_ah(c.st, c.rows, c.cols, c.g, true, W, codes, scales, zeros, H, c.pbuf(),
-                         c.objpart());
+      e = launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay);
+    if (e == hipSuccess) e = launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf(), c.objpart());
     if (e == hipSuccess)
       e = launch_stop_check(c.st, c.rows, c.nt(), c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau);
@@ -291,8 +298,9 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
   jarq_status s = check_ws(p, workspace, workspace_bytes);
   if (s != JARQ_OK) return s;
   Ctx c = make_ctx(p, workspace, stream);
-  if (launch_gemm_ah(c.st, c.rows, c.cols, c.g, true, W, codes, scales, zeros, H, c.pbuf(),
-                     nullptr) != hipSuccess)
+  if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay) !=
+          hipSuccess ||
+      launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf(), nullptr) != hipSuccess)
     return JARQ_EHIP;
   if (enqueue_babai(c, H, codes, scales, zeros, nullptr, cand, decision) != hipSuccess)
     return JARQ_EHIP;

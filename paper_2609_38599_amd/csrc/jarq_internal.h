@@ -59,6 +59,12 @@ struct Layout {
   size_t rcol;      // [G][g][16][g/16] f32: R_i columns interleaved for the back substitution
   size_t rdinv;     // [G][g] f32: 1 / R_i(l,l)
   size_t rdsq;      // [G][g] f32: R_i(l,l)^2
+  size_t hhi;       // [cols][cols] f16: H 2^t, high term
+  size_t hlo;       // [cols][cols] f16: H 2^t, low term
+  size_t hscale;    // f32[2]: 2^-t, max |H|
+  size_t ehi;       // [rows][cols] f16: E 2^t_row, high term
+  size_t elo;       // [rows][cols] f16: E 2^t_row, low term
+  size_t erow;      // [rows] f32: 2^-t_row
   size_t wh;        // [rows][cols] f32: W H
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
   size_t p;         // [rows][cols] f32: (W - What) H
@@ -86,6 +92,17 @@ hipError_t launch_chol_groups(hipStream_t st, int cols, int g, const float* H, c
 hipError_t launch_gemm_ah(hipStream_t st, int rows, int cols, int g, bool quant,
                           const float* W, const uint8_t* codes, const float* scales,
                           const int32_t* zeros, const float* H, float* C, double* objpart);
+
+hipError_t launch_split_h(hipStream_t st, int cols, const float* H, char* ws, const Layout& lay);
+
+hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
+                          const uint8_t* codes, const float* scales, const int32_t* zeros,
+                          char* ws, const Layout& lay);
+
+// P = E H from the fp16 planes of E and H in the workspace (three products);
+// objpart as for launch_gemm_ah (may be null).
+hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
+                             const Layout& lay, float* C, double* objpart);
 
 hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const float* H,
                        const uint8_t* codes, const int32_t* zeros, float* gram);

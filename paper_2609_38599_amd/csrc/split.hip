@@ -1,0 +1,128 @@
+// Two-term fp16 representations for the matrix-core contractions.
+//
+// gfx950 has no xf32 matrix instruction; its fp16 matrix rate is 16x the fp32
+// one.  A fp32 value x scaled by a power of two 2^t is written as
+// hi = fp16(x 2^t), lo = fp16(x 2^t - hi), which carries 22 significant bits.
+// Products of such planes accumulate in fp32 on the matrix cores.
+//   H:  one scale for the whole matrix, chosen so max |H| 2^t lies in [2^13, 2^14).
+//   E = W - What (eq. (1)), per sweep: one scale per row, same rule.
+// Small-integer operands (codes minus zero points, code changes) are exact in fp16.
+#include "jarq_internal.h"
+
+namespace jarq {
+
+__device__ __forceinline__ void atomic_max_abs(float* dst, float v) {
+  // |v| >= 0: IEEE ordering of non-negative floats equals their bit ordering.
+  atomicMax((unsigned int*)dst, __float_as_uint(fabsf(v)));
+}
+
+__global__ void absmax_kernel(const float* __restrict__ x, size_t n, float* __restrict__ out) {
+  float m = 0.f;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    m = fmaxf(m, fabsf(x[i]));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((threadIdx.x & 63) == 0) atomic_max_abs(out, m);
+}
+
+__device__ __forceinline__ int pow2_exponent(float amax) {
+  // t with amax * 2^t in [2^13, 2^14); 0 for an all-zero or nonfinite input.
+  if (!(amax > 0.f) || !isfinite(amax)) return 0;
+  return 13 - ilogbf(amax);
+}
+
+__global__ void split_h_kernel(const float* __restrict__ H, size_t n,
+                               const float* __restrict__ amax, _Float16* __restrict__ hi,
+                               _Float16* __restrict__ lo, float* __restrict__ inv_scale) {
+  const int t = pow2_exponent(*amax);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *inv_scale = ldexpf(1.f, -t);
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const float x = ldexpf(H[i], t);
+    const _Float16 h = (_Float16)x;
+    hi[i] = h;
+    lo[i] = (_Float16)(x - (float)h);
+  }
+}
+
+hipError_t launch_split_h(hipStream_t st, int cols, const float* H, char* ws, const Layout& lay) {
+  const size_t n = (size_t)cols * cols;
+  float* amax = (float*)(ws + lay.hscale) + 1;
+  hipError_t e = launch_zero_bytes(st, amax, sizeof(float));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(absmax_kernel, dim3(1024), dim3(256), 0, st, H, n, amax);
+  hipLaunchKernelGGL(split_h_kernel, dim3(2048), dim3(256), 0, st, H, n, amax,
+                     (_Float16*)(ws + lay.hhi), (_Float16*)(ws + lay.hlo),
+                     (float*)(ws + lay.hscale));
+  return hipGetLastError();
+}
+
+// One work-group per row: E = W - s (q - z) in fp32 (as in eq. (1)), its
+// row maximum, then the two fp16 planes and the row's inverse scale 2^-t.
+__global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
+                                                      const float* __restrict__ W,
+                                                      const uint8_t* __restrict__ codes,
+                                                      const float* __restrict__ scales,
+                                                      const int32_t* __restrict__ zeros,
+                                                      _Float16* __restrict__ ehi,
+                                                      _Float16* __restrict__ elo,
+                                                      float* __restrict__ erow_inv) {
+  const int row = blockIdx.x;
+  if (row >= rows) return;
+  const int G = cols / g;
+  __shared__ float red[4];
+  const float* wr = W + (size_t)row * cols;
+  const uint8_t* qr = codes + (size_t)row * cols;
+  float m = 0.f;
+  for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
+    const f32x4 w = *(const f32x4*)(wr + c);
+    const uint32_t q4 = *(const uint32_t*)(qr + c);
+    const int grp = c / g;
+    const float s = scales[(size_t)row * G + grp];
+    const int z = zeros[(size_t)row * G + grp];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float e = w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z);
+      m = fmaxf(m, fabsf(e));
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const int t = pow2_exponent(m);
+  if (threadIdx.x == 0) erow_inv[row] = ldexpf(1.f, -t);
+  _Float16* hr = ehi + (size_t)row * cols;
+  _Float16* lr = elo + (size_t)row * cols;
+  for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
+    const f32x4 w = *(const f32x4*)(wr + c);
+    const uint32_t q4 = *(const uint32_t*)(qr + c);
+    const int grp = c / g;
+    const float s = scales[(size_t)row * G + grp];
+    const int z = zeros[(size_t)row * G + grp];
+    typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+    h4 hv, lv;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float e = ldexpf(w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z), t);
+      const _Float16 h = (_Float16)e;
+      hv[i] = h;
+      lv[i] = (_Float16)(e - (float)h);
+    }
+    *(h4*)(hr + c) = hv;
+    *(h4*)(lr + c) = lv;
+  }
+}
+
+hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
+                          const uint8_t* codes, const float* scales, const int32_t* zeros,
+                          char* ws, const Layout& lay) {
+  hipLaunchKernelGGL(split_e_kernel, dim3(rows), dim3(256), 0, st, rows, cols, g, W, codes, scales,
+                     zeros, (_Float16*)(ws + lay.ehi), (_Float16*)(ws + lay.elo),
+                     (float*)(ws + lay.erow));
+  return hipGetLastError();
+}
+
+}  // namespace jarq

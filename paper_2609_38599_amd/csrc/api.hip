@@ -36,7 +36,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.wh = take(R * C * sizeof(float));
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
-  L.dlt = take(R * C * sizeof(float));
+  L.dq = take(R * C * 2);
   L.objpart = take(R * nt * sizeof(double));
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
@@ -94,7 +94,6 @@ struct Ctx {
   float* wh() const { return (float*)(ws + lay.wh); }
   float* gram() const { return (float*)(ws + lay.gram); }
   float* pbuf() const { return (float*)(ws + lay.p); }
-  float* dlt() const { return (float*)(ws + lay.dlt); }
   double* objpart() const { return (double*)(ws + lay.objpart); }
   int nt() const { return (cols + kObjTile - 1) / kObjTile; }
 };
@@ -124,8 +123,8 @@ hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes
 hipError_t enqueue_babai(const Ctx& c, const float* H, uint8_t* codes, const float* scales,
                          const int32_t* zeros, const uint8_t* active, uint8_t* cand,
                          uint8_t* decision) {
-  return launch_babai(c.st, c.rows, c.cols, c.g, c.bits, c.pbuf(), H, c.ws, c.lay, codes, scales,
-                      zeros, active, c.dlt(), cand, decision, c.cnt());
+  return launch_babai(c.st, c.rows, c.cols, c.g, c.bits, c.pbuf(), c.ws, c.lay, codes, scales,
+                      zeros, active, cand, decision, c.cnt());
 }
 
 jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, void* ws,

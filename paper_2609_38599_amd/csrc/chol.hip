@@ -7,8 +7,9 @@
 // factors one g x g block in LDS in fp64, inverts the lower factor L_i = R_i^T
 // column by column, and writes the fp32 forms the sweep kernels read:
 //   rinv  row n = row n of L_i^{-1}       (u = R_i^{-T} he = L_i^{-1} he)
-//   rcol  [l][j][t] = R_i(j + 16 t, l)   (column l of R_i, interleaved as the
-//                                         16 lanes of a row own it)
+//   rcol  [l][j][t] = R_i(m, l) / R_i(m, m) with m = j + 16 t (column l of R_i
+//         with each row scaled by its inverse diagonal, interleaved as the 16
+//         lanes of a row own its positions)
 //   rdinv 1 / R_i(l, l),  rdsq R_i(l, l)^2.
 #include "jarq_internal.h"
 
@@ -83,12 +84,12 @@ __global__ __launch_bounds__(256) void chol_groups_kernel(const float* __restric
   for (int e = tid; e < g * g; e += blockDim.x) {
     const int r = e / g, c = e % g;
     rinv_b[e] = (float)A[r * LD + c];
-    // rcol[l][j][t] with e = (l * 16 + j) * NT + t  ->  R(j + 16 t, l) = L(l, j + 16 t)
+    // rcol[l][j][t] with e = (l * 16 + j) * NT + t: R(m, l) / R(m, m), m = j + 16 t, R = L^T
     const int l = e / (16 * NT);
     const int j = (e / NT) % 16;
     const int t = e % NT;
     const int m = j + 16 * t;
-    rcol_b[e] = (float)(m <= l ? Lb[l * g + m] : 0.0);
+    rcol_b[e] = (float)(m <= l ? Lb[l * g + m] / Lb[m * g + m] : 0.0);
   }
   for (int l = tid; l < g; l += blockDim.x) {
     const double d = Lb[l * g + l];

@@ -68,7 +68,7 @@ struct Layout {
   size_t wh;        // [rows][cols] f32: W H
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
   size_t p;         // [rows][cols] f32: (W - What) H
-  size_t dlt;       // [rows][cols] f32: s_i (q_new - q_old) of accepted groups, 0 elsewhere
+  size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
   size_t objpart;   // [rows][ceil(cols/64)] f64: partial row objectives
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64
@@ -113,9 +113,9 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                         float lam, float rcond);
 
 hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, const float* P,
-                        const float* H, const char* ws, const Layout& lay, uint8_t* codes,
-                        const float* scales, const int32_t* zeros, const uint8_t* active,
-                        float* dlt, uint8_t* cand, uint8_t* decision, Counters* cnt);
+                        const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
+                        const int32_t* zeros, const uint8_t* active, uint8_t* cand,
+                        uint8_t* decision, Counters* cnt);
 
 hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
                                 double* out);

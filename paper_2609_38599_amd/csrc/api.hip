@@ -120,11 +120,24 @@ hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes
                       c.cnt(), c.flags(), lam, rcond);
 }
 
+// The Gauss-Seidel code update, panel by panel: each panel's groups are
+// decoded in order by the Babai kernel, then their accepted changes are folded
+// into the residual product of every later column.
 hipError_t enqueue_babai(const Ctx& c, const float* H, uint8_t* codes, const float* scales,
                          const int32_t* zeros, const uint8_t* active, uint8_t* cand,
                          uint8_t* decision) {
-  return launch_babai(c.st, c.rows, c.cols, c.g, c.bits, c.pbuf(), c.ws, c.lay, codes, scales,
-                      zeros, active, cand, decision, c.cnt());
+  (void)H;
+  const int nb = panel_groups(c.g);
+  for (int i0 = 0; i0 < c.G; i0 += nb) {
+    const int i1 = i0 + nb < c.G ? i0 + nb : c.G;
+    hipError_t e = launch_babai(c.st, c.rows, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay,
+                                codes, scales, zeros, active, cand, decision, c.cnt());
+    if (e != hipSuccess) return e;
+    e = launch_panel_update(c.st, c.rows, c.cols, c.g, i0 * c.g, i1 * c.g, c.ws, c.lay, scales,
+                            c.pbuf());
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, void* ws,

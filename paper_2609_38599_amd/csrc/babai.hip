@@ -15,11 +15,11 @@
 // a_l = (R_i d)_l / R_i(l,l), whose terms vanish exactly where no change
 // reaches, so its rounding scales with the change rather than with ||u||^2.
 //
-// One 256-thread work-group owns 16 rows and visits the groups in order.
-// Per group:
-//   1. correction: he = P_i - sum_{h<i} s_h (dq_h H_hi), P = E H from the start
-//      of the sweep, dq_h the accepted code changes of earlier groups (exact in
-//      fp16, zero elsewhere).  H is read as its two fp16 planes, so each block
+// One 256-thread work-group owns 16 rows and visits the groups of one panel
+// [i0, i1) in order; P already holds the changes of earlier panels (folded in
+// by pupdate.hip).  Per group:
+//   1. correction: he = P_i - sum_{i0<=h<i} s_h (dq_h H_hi), dq_h the accepted
+//      code changes of earlier groups of the panel (exact in fp16, zero elsewhere).  H is read as its two fp16 planes, so each block
 //      is two v_mfma_f32_16x16x32_f16 products per k-slice, scaled by s_h per
 //      row.  Blocks in which no row of the tile accepted are skipped.
 //   2. u = he L_i^{-T} / s_i (L_i^{-1} = R_i^{-T}) on fp32 matrix cores.
@@ -50,40 +50,59 @@ __device__ __forceinline__ float row_bcast(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + JL, 0xf, 0xf, false));
 }
 
+// R~ column l as seen by lane j: the NT values R~(j + 16 t, l), t < NT.  Only
+// t <= l / 16 can be nonzero.
+template <int NT>
+struct RCol {
+  f32x4 v[(NT + 3) / 4];
+};
+
+template <int L, int NT>
+__device__ __forceinline__ RCol<NT> load_rcol(const float* __restrict__ rc, int cj) {
+  RCol<NT> r;
+  if (L >= 0) {
+    const float* p = rc + (L * 16 + cj) * NT;
+#pragma unroll
+    for (int c = 0; c * 4 <= (L >> 4); ++c) r.v[c] = *(const f32x4*)(p + 4 * c);
+  }
+  return r;
+}
+
+// One step of the back substitution; the R~ columns of the next two steps are
+// already in flight (loaded two steps ahead so LDS latency stays off the chain).
 template <int L, int NT>
 struct ChainStep {
   static __device__ __forceinline__ void run(ChainState<NT>& s, const float* __restrict__ rc,
-                                             int cj, float qmax) {
+                                             int cj, float qmax, const RCol<NT>& cur,
+                                             const RCol<NT>& nxt) {
     constexpr int TL = L >> 4;
     constexpr int JL = L & 15;
+    const RCol<NT> nn = load_rcol<L - 2, NT>(rc, cj);
     const float xv = s.base[TL] - s.acc[TL];
     const float qv = fminf(fmaxf(rintf(xv), 0.f), qmax);
     s.qc[TL] = cj == JL ? qv : s.qc[TL];
     const float db = row_bcast<JL>(qv - s.qold[TL]);
-    const float* rl = rc + (L * 16 + cj) * NT;
 #pragma unroll
-    for (int c = 0; c * 4 <= TL; ++c) {
-      const f32x4 r4 = *(const f32x4*)(rl + 4 * c);
+    for (int c = 0; c * 4 <= TL; ++c)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (4 * c + q <= TL) s.acc[4 * c + q] = fmaf(r4[q], db, s.acc[4 * c + q]);
-    }
-    // Keep the scheduler from hoisting LDS reads of far-away steps (register
-    // pressure); 16 steps of look-ahead are enough to hide their latency.
+        if (4 * c + q <= TL) s.acc[4 * c + q] = fmaf(cur.v[c][q], db, s.acc[4 * c + q]);
+    // Keep the scheduler from hoisting far-away work (register pressure).
     if (JL == 0) __builtin_amdgcn_sched_barrier(0);
-    ChainStep<L - 1, NT>::run(s, rc, cj, qmax);
+    ChainStep<L - 1, NT>::run(s, rc, cj, qmax, nxt, nn);
   }
 };
 
 template <int NT>
 struct ChainStep<-1, NT> {
   static __device__ __forceinline__ void run(ChainState<NT>&, const float* __restrict__, int,
-                                             float) {}
+                                             float, const RCol<NT>&, const RCol<NT>&) {}
 };
 
 template <int G_SIZE>
 __global__ __launch_bounds__(256, 1) void babai_kernel(
-    int rows, int cols, int bits, const float* __restrict__ P, const _Float16* __restrict__ Hh,
+    int rows, int cols, int bits, int i0, int i1, const float* __restrict__ P,
+    const _Float16* __restrict__ Hh,
     const _Float16* __restrict__ Hl, const float* __restrict__ h_inv,
     const float* __restrict__ rinv, const float* __restrict__ rcol,
     const float* __restrict__ rdinv, const float* __restrict__ rdsq, uint8_t* __restrict__ codes,
@@ -130,7 +149,7 @@ __global__ __launch_bounds__(256, 1) void babai_kernel(
   for (int h = tid; h < G; h += 256) tacc_s[h] = 0;
   if (tid < 4) cnt_s[tid] = 0;
 
-  for (int i = 0; i < G; ++i) {
+  for (int i = i0; i < i1; ++i) {
     __syncthreads();  // previous group's dq stores and LDS reuse
     {
       const float* src = rcol + (size_t)i * g * g;
@@ -161,7 +180,7 @@ __global__ __launch_bounds__(256, 1) void babai_kernel(
       f32x4 acc[BPW];
 #pragma unroll
       for (int b = 0; b < BPW; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int h = 0; h < i; ++h) {
+      for (int h = i0; h < i; ++h) {
         if (tacc_s[h] == 0) continue;
         if (tid == 0) cnt_s[3] += 1;
         f16x8 a[KS], bh[BPW][KS], bl[BPW][KS];
@@ -247,7 +266,8 @@ __global__ __launch_bounds__(256, 1) void babai_kernel(
       cs.base[t] = q + ut[t];
       cs.acc[t] = 0.f;
     }
-    ChainStep<g - 1, NT>::run(cs, rc_s, cj, qmax);
+    ChainStep<g - 1, NT>::run(cs, rc_s, cj, qmax, load_rcol<g - 1, NT>(rc_s, cj),
+                              load_rcol<g - 2, NT>(rc_s, cj));
     float dF = 0.f;  // change of F divided by s_i^2
     int changed = 0;
 #pragma unroll
@@ -297,7 +317,8 @@ __global__ __launch_bounds__(256, 1) void babai_kernel(
 }
 
 template <int G_SIZE>
-static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, const float* P,
+static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, int i0, int i1,
+                                 const float* P,
                                  const char* ws, const Layout& lay, uint8_t* codes,
                                  const float* scales, const int32_t* zeros,
                                  const uint8_t* active, uint8_t* cand, uint8_t* decision,
@@ -310,7 +331,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, c
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(babai_kernel<g>, dim3((rows + 15) / 16), dim3(256), lds, st, rows, cols, bits,
-                     P, (const _Float16*)(ws + lay.hhi), (const _Float16*)(ws + lay.hlo),
+                     i0, i1, P, (const _Float16*)(ws + lay.hhi), (const _Float16*)(ws + lay.hlo),
                      (const float*)(ws + lay.hscale), (const float*)(ws + lay.rinv),
                      (const float*)(ws + lay.rcol), (const float*)(ws + lay.rdinv),
                      (const float*)(ws + lay.rdsq), codes, scales, zeros, active,
@@ -318,19 +339,20 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, c
   return hipGetLastError();
 }
 
-hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, const float* P,
+hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,
+                        const float* P,
                         const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
                         uint8_t* decision, Counters* cnt) {
   switch (g) {
     case 32:
-      return launch_babai_t<32>(st, rows, cols, bits, P, ws, lay, codes, scales, zeros, active,
+      return launch_babai_t<32>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, zeros, active,
                                 cand, decision, cnt);
     case 64:
-      return launch_babai_t<64>(st, rows, cols, bits, P, ws, lay, codes, scales, zeros, active,
+      return launch_babai_t<64>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, zeros, active,
                                 cand, decision, cnt);
     case 128:
-      return launch_babai_t<128>(st, rows, cols, bits, P, ws, lay, codes, scales, zeros, active,
+      return launch_babai_t<128>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, zeros, active,
                                  cand, decision, cnt);
     default:
       return hipErrorInvalidValue;

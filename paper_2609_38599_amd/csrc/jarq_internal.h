@@ -112,10 +112,18 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
                         float lam, float rcond);
 
-hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, const float* P,
-                        const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
-                        const int32_t* zeros, const uint8_t* active, uint8_t* cand,
-                        uint8_t* decision, Counters* cnt);
+// Code update of the groups [i0, i1) (one panel).
+hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,
+                        const float* P, const char* ws, const Layout& lay, uint8_t* codes,
+                        const float* scales, const int32_t* zeros, const uint8_t* active,
+                        uint8_t* cand, uint8_t* decision, Counters* cnt);
+
+// Groups per panel of the code update.
+int panel_groups(int g);
+
+// P(:, c1:) -= the accepted changes of the groups in columns [c0, c1).
+hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0, int c1,
+                               const char* ws, const Layout& lay, const float* scales, float* P);
 
 hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
                                 double* out);

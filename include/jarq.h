@@ -36,6 +36,9 @@
  *     outputs are then untouched.
  *   - The workspace of a jarq_prepare call is reused by the later calls on
  *     the same layer; calls that share a workspace must not overlap.
+ *   - Zero points must satisfy |z| <= 1024 (codes minus zero points are held
+ *     exactly in fp16 on the matrix cores); jarq_sweeps and jarq_refine check
+ *     this, the stage entry points assume it.
  */
 #ifndef JARQ_H_
 #define JARQ_H_
@@ -129,7 +132,7 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
  * K = p->sweeps sweeps (b) -> (a) -> [early stop] -> (c) on a prepared
  * workspace, starting with every row active.  codes and scales are updated
  * in place; zeros are read only.  Checks first that every code is in
- * [0, 2^b - 1] and every |zero point| <= 2^20 (JARQ_EINVAL otherwise, nothing
+ * [0, 2^b - 1] and every |zero point| <= 1024 (JARQ_EINVAL otherwise, nothing
  * changed).  Synchronises `stream` before returning.  `stats` [host] may be
  * NULL.  Returns JARQ_ESCALE_SOLVE if any row's solve failed after the ridge
  * (that row keeps its previous scales).

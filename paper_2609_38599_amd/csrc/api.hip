@@ -114,7 +114,8 @@ Ctx make_ctx(const jarq_params* p, void* ws, void* stream) {
 hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes, float* scales,
                               const int32_t* zeros, const uint8_t* active, float lam,
                               float rcond) {
-  hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, H, codes, zeros, c.gram());
+  (void)H;
+  hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram());
   if (e != hipSuccess) return e;
   return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, active,
                       c.cnt(), c.flags(), lam, rcond);
@@ -160,7 +161,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
                         float* scales, const int32_t* zeros, void* ws, void* stream,
                         jarq_stats* stats) {
   Ctx c = make_ctx(p, ws, stream);
-  // Device-side input checks (codes in range, zero points bounded).
+  // Device-side input checks (codes in range, |zero point| <= 1024).
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
   JQ_HIP(launch_validate(c.st, c.rows, c.cols, c.g, c.bits, codes, zeros, c.flags()));
   Flags f{};
@@ -191,7 +192,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   for (int k = 0; k < K; ++k) {
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = mark(k, 0);
-    if (e == hipSuccess) e = launch_gram(c.st, c.rows, c.cols, c.g, H, codes, zeros, c.gram());
+    if (e == hipSuccess) e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram());
     if (e == hipSuccess) e = mark(k, 1);
     if (e == hipSuccess)
       e = launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales,

@@ -3,132 +3,197 @@
 // For row j with c_i = q_i - z_i 1 (exact small integers), entry (a, h) of
 // B_j^T B_j is c_a^T H_ah c_h (B_j has columns A_i c_i and H = A^T A).  The
 // matrix is symmetric, so only h >= a is formed.  A work-group takes a tile of
-// 64 rows and a pair of row-groups {p, G-1-p} (so every work-group walks G+1
+// 256 rows and a pair of row-groups {p, G-1-p} (so every work-group walks G+1
 // blocks); for each block h it forms T = H(a-group, h-group) C(rows, h-group)^T
-// with v_mfma_f32_32x32x2f32 (M = the g weights of group a, N = 32 rows,
-// K = the g weights of group h) and reduces T against c_a per row in fp64.
+// on fp16 matrix cores (v_mfma_f32_32x32x16_f16, M = the g weights of group a,
+// N = 32 rows, K = the g weights of group h) with H as its two fp16 planes and
+// the codes exact in fp16, then reduces T against c_a for every row.
+//
+// Waves split the a-group into 32-weight blocks and the tile's rows; each H
+// fragment is used for all of a wave's rows.  The codes of block h are staged
+// in LDS as fp16 once per work-group (bit trick: the fp16 with bits
+// 0x6400 | q is 1024 + q) and the next block's codes and H fragments are
+// fetched while the current block runs on the matrix cores.
 #include "jarq_internal.h"
 
 namespace jarq {
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+namespace {
+constexpr int RT = 256;  // rows per work-group
+
+// Four codes (one byte each) -> four fp16 values q - z, exactly.
+__device__ __forceinline__ void codes_to_f16(uint32_t q4, f16x2 zz, f16x2* out) {
+  // 0x64qq as fp16 is 1024 + q
+  const uint32_t lo = __builtin_amdgcn_perm(0x64646464u, q4, 0x07010700u);  // [q1, 0x64, q0, 0x64]
+  const uint32_t hi = __builtin_amdgcn_perm(0x64646464u, q4, 0x07030702u);  // [q3, 0x64, q2, 0x64]
+  out[0] = __builtin_bit_cast(f16x2, lo) - zz;
+  out[1] = __builtin_bit_cast(f16x2, hi) - zz;
+}
+}  // namespace
+
 template <int G_SIZE>
-__global__ __launch_bounds__(256) void gram_kernel(int rows, int cols,
-                                                   const float* __restrict__ H,
-                                                   const uint8_t* __restrict__ codes,
-                                                   const int32_t* __restrict__ zeros,
-                                                   float* __restrict__ gram) {
+__global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
+                                                      const _Float16* __restrict__ Hh,
+                                                      const _Float16* __restrict__ Hl,
+                                                      const float* __restrict__ h_inv,
+                                                      const uint8_t* __restrict__ codes,
+                                                      const int32_t* __restrict__ zeros,
+                                                      float* __restrict__ gram) {
   constexpr int g = G_SIZE;
-  constexpr int NAB = g / 32;              // 32-weight blocks of the a-group
-  constexpr int PAIRS = NAB * 2;           // (a-block, 32-row block) pairs per tile
-  constexpr int PPW = PAIRS >= 4 ? PAIRS / 4 : 1;  // pairs per wave
+  constexpr int NAB = g / 32;            // 32-weight blocks of an a-group
+  constexpr int WPA = 4 / NAB;           // waves sharing an a-block
+  constexpr int RW = RT / WPA;           // rows per wave
+  constexpr int JB = RW / 32;            // 32-row blocks per wave
+  constexpr int KS = g / 16;             // k-steps of one block
+  constexpr int LDC = g + 8;             // fp16 row stride of staged code tiles
   const int G = cols / g;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
   const int lm = lane & 31, kh = lane >> 5;
-  const int r0 = blockIdx.x * 64;
+  const int ab = wave % NAB;
+  const int rbase = (wave / NAB) * RW;
+  const int r0 = blockIdx.x * RT;
   const int p = blockIdx.y;
-  __shared__ double red[NAB][64];
+  const float hinv = *h_inv;
 
-  int ab[PPW], jb[PPW];
-  bool live[PPW];
+  extern __shared__ _Float16 sm[];
+  _Float16* ch_s = sm;                  // RT x LDC: c of block h
+  _Float16* ca_s = ch_s + RT * LDC;     // RT x LDC: c of the a-group
+  double* red = (double*)(ca_s + RT * LDC);  // NAB x RT
+
+  // Stage the codes of column block `blk` of the tile as fp16 (c = q - z):
+  // thread t owns row t of the tile (g bytes, one zero point).
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 stq[g / 16];
+  int stz = 0;
+  const int srow = r0 + tid;
+  auto fetch_codes = [&](int blk) {
+    if (srow < rows) {
+      const u32x4* src = (const u32x4*)(codes + (size_t)srow * cols + (size_t)blk * g);
 #pragma unroll
-  for (int q = 0; q < PPW; ++q) {
-    const int pair = (PAIRS >= 4) ? wave * PPW + q : wave;
-    live[q] = pair < PAIRS;
-    ab[q] = live[q] ? pair / 2 : 0;
-    jb[q] = live[q] ? pair % 2 : 0;
-  }
+      for (int i = 0; i < g / 16; ++i) stq[i] = src[i];
+      stz = zeros[(size_t)srow * G + blk];
+    } else {
+#pragma unroll
+      for (int i = 0; i < g / 16; ++i) stq[i] = u32x4{0u, 0u, 0u, 0u};
+      stz = 0;
+    }
+  };
+  auto store_codes = [&](_Float16* dst) {
+    const _Float16 zb = (_Float16)(1024 + stz);
+    const f16x2 zz = srow < rows ? f16x2{zb, zb} : f16x2{(_Float16)1024, (_Float16)1024};
+#pragma unroll
+    for (int i = 0; i < g / 16; ++i) {
+      f16x2 v[8];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) codes_to_f16(stq[i][w], zz, v + 2 * w);
+      *(f16x8*)(dst + tid * LDC + i * 16) = f16x8{v[0][0], v[0][1], v[1][0], v[1][1], v[2][0], v[2][1], v[3][0], v[3][1]};
+      *(f16x8*)(dst + tid * LDC + i * 16 + 8) = f16x8{v[4][0], v[4][1], v[5][0], v[5][1], v[6][0], v[6][1], v[7][0], v[7][1]};
+    }
+  };
+  // H fragments of block (a-group ga, column block h) for this wave's a-block.
+  f16x8 hf[2][KS];
+  auto fetch_h = [&](int ga, int h) {
+    const size_t rowoff = (size_t)(ga * g + ab * 32 + lm) * cols + (size_t)h * g + 8 * kh;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      hf[0][ks] = *(const f16x8*)(Hh + rowoff + ks * 16);
+      hf[1][ks] = *(const f16x8*)(Hl + rowoff + ks * 16);
+    }
+  };
 
   for (int side = 0; side < 2; ++side) {
     const int ga = side == 0 ? p : G - 1 - p;
     if (side == 1 && ga == p) break;
-    // c_a values this lane needs in the reduction: rows jb*32+lm, weights
-    // ab*32 + 8*jj + 4*kh + i (the accumulator rows it holds).
-    float ca[PPW][16];
-#pragma unroll
-    for (int q = 0; q < PPW; ++q) {
-      const int row = r0 + jb[q] * 32 + lm;
-      const bool ok = live[q] && row < rows;
-      const int z = ok ? zeros[(size_t)row * G + ga] : 0;
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        uint32_t q4 = 0;
-        if (ok) q4 = *(const uint32_t*)(codes + (size_t)row * cols + ga * g + ab[q] * 32 + 8 * jj + 4 * kh);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          ca[q][4 * jj + i] = ok ? (float)((int)((q4 >> (8 * i)) & 0xffu) - z) : 0.f;
-      }
-    }
+    __syncthreads();
+    fetch_codes(ga);
+    store_codes(ca_s);
+    fetch_codes(ga);     // block h = ga comes first
+    fetch_h(ga, ga);
     for (int h = ga; h < G; ++h) {
-      f32x16 acc[PPW];
+      __syncthreads();   // previous block's reads of ch_s are done
+      store_codes(ch_s);
+      f16x8 cur[2][KS];
 #pragma unroll
-      for (int q = 0; q < PPW; ++q) acc[q] = f32x16{};
-      int zh[PPW];
-      bool okr[PPW];
-#pragma unroll
-      for (int q = 0; q < PPW; ++q) {
-        const int row = r0 + jb[q] * 32 + lm;
-        okr[q] = live[q] && row < rows;
-        zh[q] = okr[q] ? zeros[(size_t)row * G + h] : 0;
+      for (int ks = 0; ks < KS; ++ks) {
+        cur[0][ks] = hf[0][ks];
+        cur[1][ks] = hf[1][ks];
       }
-      for (int k0 = 0; k0 < g; k0 += 8) {
-        const int kk = k0 + 4 * kh;
+      if (h + 1 < G) {
+        fetch_codes(h + 1);
+        fetch_h(ga, h + 1);
+      }
+      __syncthreads();
+      f32x16 acc[JB];
 #pragma unroll
-        for (int q = 0; q < PPW; ++q) {
-          const int arow = ga * g + ab[q] * 32 + lm;
-          const f32x4 a4 = *(const f32x4*)(H + (size_t)arow * cols + h * g + kk);
-          const int row = r0 + jb[q] * 32 + lm;
-          uint32_t q4 = 0;
-          if (okr[q]) q4 = *(const uint32_t*)(codes + (size_t)row * cols + h * g + kk);
-          f32x4 b4;
+      for (int b = 0; b < JB; ++b) acc[b] = f32x16{};
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            b4[i] = okr[q] ? (float)((int)((q4 >> (8 * i)) & 0xffu) - zh[q]) : 0.f;
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-          for (int t = 0; t < 4; ++t)
-            acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[t], b4[t], acc[q], 0, 0, 0);
+        for (int b = 0; b < JB; ++b) {
+          const f16x8 cf = *(const f16x8*)(ch_s + (rbase + b * 32 + lm) * LDC + ks * 16 + 8 * kh);
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[0][ks], cf, acc[b], 0, 0, 0);
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[1][ks], cf, acc[b], 0, 0, 0);
         }
-      }
-      // acc element v of lane l: T(a = ab*32 + 8*(v/4) + 4*kh + v%4, row = jb*32 + l%32).
+      // acc element v of lane l: T(a = ab*32 + 8*(v/4) + 4*kh + v%4, row = rbase + b*32 + l%32).
 #pragma unroll
-      for (int q = 0; q < PPW; ++q) {
-        double s = 0.0;
+      for (int b = 0; b < JB; ++b) {
+        const int rr = rbase + b * 32 + lm;
+        float s = 0.f;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s += (double)ca[q][v] * (double)acc[q][v];
-        s += __shfl_xor(s, 32);
-        if (live[q] && kh == 0) red[ab[q]][jb[q] * 32 + lm] = s;
-      }
-      __syncthreads();
-      if (threadIdx.x < 64) {
-        double s = 0.0;
+        for (int jj = 0; jj < 4; ++jj) {
+          typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+          const f16x4 c4 = *(const f16x4*)(ca_s + rr * LDC + ab * 32 + 8 * jj + 4 * kh);
 #pragma unroll
-        for (int a = 0; a < NAB; ++a) s += red[a][threadIdx.x];
-        const int row = r0 + threadIdx.x;
-        if (row < rows) gram[((size_t)row * G + ga) * G + h] = (float)s;
+          for (int i = 0; i < 4; ++i) s = fmaf((float)c4[i], acc[b][4 * jj + i], s);
+        }
+        double d = (double)s;
+        d += __shfl_xor(d, 32);
+        if (kh == 0) red[ab * RT + rr] = d;
       }
       __syncthreads();
+      {
+        const int rr = tid;  // RT == 256 == blockDim.x
+        double s = 0.0;
+#pragma unroll
+        for (int a = 0; a < NAB; ++a) s += red[a * RT + rr];
+        const int row = r0 + rr;
+        if (row < rows) gram[((size_t)row * G + ga) * G + h] = (float)(s * (double)hinv);
+      }
     }
   }
 }
 
-hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const float* H,
-                       const uint8_t* codes, const int32_t* zeros, float* gram) {
+template <int G_SIZE>
+static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* ws,
+                                const Layout& lay, const uint8_t* codes, const int32_t* zeros,
+                                float* gram) {
+  constexpr int g = G_SIZE;
   const int G = cols / g;
-  dim3 grid((rows + 63) / 64, (G + 1) / 2);
-  switch (g) {
-    case 32:
-      hipLaunchKernelGGL(gram_kernel<32>, grid, dim3(256), 0, st, rows, cols, H, codes, zeros, gram);
-      break;
-    case 64:
-      hipLaunchKernelGGL(gram_kernel<64>, grid, dim3(256), 0, st, rows, cols, H, codes, zeros, gram);
-      break;
-    case 128:
-      hipLaunchKernelGGL(gram_kernel<128>, grid, dim3(256), 0, st, rows, cols, H, codes, zeros, gram);
-      break;
-    default:
-      return hipErrorInvalidValue;
-  }
+  const size_t lds = (size_t)2 * RT * (g + 8) * sizeof(_Float16) + (size_t)(g / 32) * RT * sizeof(double);
+  hipError_t e = hipFuncSetAttribute((const void*)gram_kernel<g>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  dim3 grid((rows + RT - 1) / RT, (G + 1) / 2);
+  hipLaunchKernelGGL(gram_kernel<g>, grid, dim3(256), lds, st, rows, cols,
+                     (const _Float16*)(ws + lay.hhi), (const _Float16*)(ws + lay.hlo),
+                     (const float*)(ws + lay.hscale), codes, zeros, gram);
   return hipGetLastError();
+}
+
+hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,
+                       const Layout& lay, const uint8_t* codes, const int32_t* zeros,
+                       float* gram) {
+  switch (g) {
+    case 32: return launch_gram_t<32>(st, rows, cols, ws, lay, codes, zeros, gram);
+    case 64: return launch_gram_t<64>(st, rows, cols, ws, lay, codes, zeros, gram);
+    case 128: return launch_gram_t<128>(st, rows, cols, ws, lay, codes, zeros, gram);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace jarq

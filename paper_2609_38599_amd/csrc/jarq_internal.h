@@ -47,7 +47,7 @@ struct SweepRecord {
 struct Flags {
   int not_spd;         // blocks H_ii that failed Cholesky
   int bad_codes;       // codes > 2^b - 1
-  int bad_zeros;       // |z| > 2^20
+  int bad_zeros;       // |z| > 1024
   int solve_failed;    // rows whose scale solve failed after the ridge (all sweeps)
   int pad[4];
 };
@@ -104,8 +104,10 @@ hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float
 hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
                              const Layout& lay, float* C, double* objpart);
 
-hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const float* H,
-                       const uint8_t* codes, const int32_t* zeros, float* gram);
+// Upper triangles of the grouped Gram matrices from the fp16 planes of H.
+hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,
+                       const Layout& lay, const uint8_t* codes, const int32_t* zeros,
+                       float* gram);
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,

@@ -136,6 +136,9 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   }
   // Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
+  // All loads of P are issued before any store: the compiler cannot prove the
+  // addresses distinct and would otherwise serialise 64 round trips to memory.
+  float pold[2][2][16];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -144,7 +147,18 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-        if (row < rows && col < cols) P[(size_t)row * cols + col] -= acc[a][b][v];
+        pold[a][b][v] = (row < rows && col < cols) ? P[(size_t)row * cols + col] : 0.f;
+      }
+    }
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int col = n0 + wn * 64 + b * 32 + lm;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
+        if (row < rows && col < cols) P[(size_t)row * cols + col] = pold[a][b][v] - acc[a][b][v];
       }
     }
 }

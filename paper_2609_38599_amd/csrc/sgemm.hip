@@ -1,19 +1,27 @@
-// Residual product P = E H of the sweep on fp16 matrix cores (paper Sec. 3.3.2:
-// the conditional residual of eq. (7) needs (H e)_i for every row and group).
+// Split-precision products on fp16 matrix cores: the residual product P = E H
+// of the sweep (paper Sec. 3.3.2: the conditional residual of eq. (7) needs
+// (H e)_i for every row and group).
 //
-// E and H arrive as two-term fp16 planes (split.hip) with power-of-two scales:
-// E = (Eh + El) re_m, H = (Hh + Hl) rh.  The product keeps the three terms
-// above 2^-22 relative, P = (Eh Hh + Eh Hl + El Hh) re_m rh, accumulated in fp32
-// by v_mfma_f32_32x32x16_f16 — fp32-class accuracy at 3/16 of the fp32 matrix
-// work.  With kObj the epilogue writes, per row and 64-column slice,
-// sum_c E(row, c) P(row, c) in fp64; summed over slices that is L_j, the
-// objective right after the scale update (App. E.2).
+// Operands arrive as two-term fp16 planes with power-of-two scales (split.hip):
+// A = (Ah + Al) ra_m per row, B = (Bh + Bl) rb.  The product keeps the three
+// terms above 2^-22 relative, A B = (Ah Bh + Ah Bl + Al Bh) ra_m rb, accumulated
+// in fp32 by v_mfma_f32_32x32x16_f16 — fp32-class accuracy at 3/16 of the fp32
+// matrix work.  B is read as rows (B(k, n) = Bt(n, k)); for the residual
+// product Bt = H, which is symmetric.
 //
-// Tiling: 256 x 128 output tile per 256-thread work-group, 2 x 2 waves of
-// 128 x 64 (4 x 2 accumulators of 32 x 32), K in steps of 32 staged through
-// LDS with double buffering (both planes of both operands, 120 KB).  H is
-// symmetric, so B(k, n) = H(n, k): both operands are read along k with 16-byte
-// loads, and each lane's MFMA fragment is 8 consecutive k of one row.
+// Epilogues: store C = A B, or subtract, C -= A B.  After the residual
+// product a second kernel forms, per row and 64-column slice, sum_c E P in
+// fp64; summed over the slices that is L_j, the objective right after the
+// scale update (App. E.2).
+//
+// Tiling: 256 x BN output tile per 256-thread work-group, 2 x 2 waves of
+// 128 x BN/2, K in steps of 32.  Both planes of both operands go straight from
+// global memory to LDS (global_load_lds_dwordx4, no register staging) into
+// one of two stages (128 KB for BN = 256).  One work-group per CU; a 256 x 256
+// tile gives every k-step 96 matrix instructions per wave, enough to cover
+// the latency of the next step's loads.  Tiles are ordered so that
+// each XCD (work-groups are dealt to the 8 XCDs round-robin) works on a
+// compact block of tiles that share A row-tiles and B column-tiles in its L2.
 #include "jarq_internal.h"
 
 namespace jarq {
@@ -21,174 +29,259 @@ namespace jarq {
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 namespace {
-constexpr int BM = 256, BN = 128, BK = 32, PADK = BK + 8;  // row stride 80 B: no bank conflicts
-constexpr int A_PLANE = BM * PADK, B_PLANE = BN * PADK;
-constexpr int STAGE = 2 * A_PLANE + 2 * B_PLANE;  // halves per stage
+constexpr int BM = 256, BK = 32;
+
+__device__ __forceinline__ void tile_of(int wid, int nbm, int nbn, int& tm, int& tn) {
+  const int total = nbm * nbn;
+  const int q = total / 8, r = total % 8;
+  const int x = wid % 8, loc = wid / 8;
+  const int id = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + loc;
+  constexpr int GM = 4;  // tile-rows per band
+  const int band = id / (GM * nbn);
+  const int first = band * GM;
+  const int gsz = min(nbm - first, GM);
+  const int within = id - band * GM * nbn;
+  tm = first + within % gsz;
+  tn = within / gsz;
+}
+
+// LDS holds each plane tile as rows of 32 halves (four 16-byte chunks); chunk
+// c of row r sits at position c ^ swz(r).  Fragment reads (lane = row, two
+// chunks across the wave halves) then touch distinct banks within every group
+// of 8 or 16 consecutive lanes.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) + (r >> 3)) & 3; }
+
+// One 16-byte direct global -> LDS load per lane (lane L writes lds + 16 L bytes).
+// A plain device function: the builtin and the LDS address space exist on the
+// device side only.
+__device__ __forceinline__ void dma16(const _Float16* src, _Float16* lds) {
+  __builtin_amdgcn_global_load_lds((const void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
 }  // namespace
 
-template <bool kObj>
-__global__ __launch_bounds__(256, 1) void split_gemm_kernel(
-    int M, int N, int K, const _Float16* __restrict__ Ah, const _Float16* __restrict__ Al,
-    const float* __restrict__ arow_inv, const _Float16* __restrict__ Bh,
-    const _Float16* __restrict__ Bl, const float* __restrict__ b_inv, float* __restrict__ C,
-    double* __restrict__ objpart) {
-  extern __shared__ _Float16 lds[];
+template <int BN, int kMode>
+__global__ __launch_bounds__(256, 1) void split3_kernel(
+    int M, int N, int K, int lda, int ldb, int ldc, const _Float16* __restrict__ Ah,
+    const _Float16* __restrict__ Al, const float* __restrict__ arow_inv,
+    const _Float16* __restrict__ Bh, const _Float16* __restrict__ Bl,
+    const float* __restrict__ b_inv, float* __restrict__ C) {
+  constexpr int WN = BN / 2;   // wave tile columns
+  constexpr int NB = WN / 32;  // 32-column blocks per wave
+  constexpr int A_PLANE = BM * BK, B_PLANE = BN * BK;  // halves
+  constexpr int STAGE = 2 * A_PLANE + 2 * B_PLANE;
+  // Two stages in two distinct arrays, so that the compiler can tell which
+  // one an outstanding direct-to-LDS load writes.
+  __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
+  __shared__ __attribute__((aligned(1024))) _Float16 buf1[STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int lm = lane & 31, kh = lane >> 5;
-  const int m0 = blockIdx.y * BM;
-  const int n0 = blockIdx.x * BN;
+  const int nbm = (M + BM - 1) / BM, nbn = (N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, nbm, nbn, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
 
-  // global -> LDS chunk assignment (16-byte chunks, 4 per 32-wide k row)
-  const int crow = tid >> 2;   // 0..63
-  const int ckc = tid & 3;     // k chunk
-  f16x8 ra[8], rb[4];
-  auto gload = [&](int k0) {
+  // Direct global -> LDS loads, 16 bytes per lane: one instruction fills 1 KB
+  // of LDS (16 rows of a plane tile).  Wave w fills the 1 KB pieces w, w + 4,
+  // ...; lane L of a piece holds row 16 j + L / 4 at chunk position L % 4, i.e.
+  // chunk (L % 4) ^ swz(row).  Rows past the edge read row 0 instead: their
+  // products only reach output rows and columns that are never stored.
+  // Element offsets are 32-bit (operands stay below 2^31 elements).
+  constexpr int APW = A_PLANE / 512 / 4;  // 1 KB pieces per wave per A plane
+  constexpr int BPW = B_PLANE / 512 / 4;
+  unsigned aoff[APW], boff[BPW];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = crow + 64 * (i & 3);
-      const _Float16* src = (i < 4 ? Ah : Al);
-      const int gm = m0 + row;
-      ra[i] = gm < M ? *(const f16x8*)(src + (size_t)gm * K + k0 + ckc * 8) : f16x8{};
+  for (int i = 0; i < APW; ++i) {
+    const int r = 16 * (wave + 4 * i) + (lane >> 2);
+    const int gm = m0 + r;
+    aoff[i] = (unsigned)(gm < M ? gm : 0) * (unsigned)lda + (unsigned)(((lane & 3) ^ swz(r)) * 8);
+  }
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int r = 16 * (wave + 4 * i) + (lane >> 2);
+    const int gn = n0 + r;
+    boff[i] = (unsigned)(gn < N ? gn : 0) * (unsigned)ldb + (unsigned)(((lane & 3) ^ swz(r)) * 8);
+  }
+  auto issue = [&](int k0, _Float16* stage) {
+#pragma unroll
+    for (int i = 0; i < APW; ++i) {
+      _Float16* dst = stage + (wave + 4 * i) * 512;
+      dma16(Ah + k0 + aoff[i], dst);
+      dma16(Al + k0 + aoff[i], dst + A_PLANE);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = crow + 64 * (i & 1);
-      const _Float16* src = (i < 2 ? Bh : Bl);
-      const int gn = n0 + row;
-      rb[i] = gn < N ? *(const f16x8*)(src + (size_t)gn * K + k0 + ckc * 8) : f16x8{};
+    for (int i = 0; i < BPW; ++i) {
+      _Float16* dst = stage + 2 * A_PLANE + (wave + 4 * i) * 512;
+      dma16(Bh + k0 + boff[i], dst);
+      dma16(Bl + k0 + boff[i], dst + B_PLANE);
     }
   };
-  auto lstore = [&](int st) {
-    _Float16* base = lds + st * STAGE;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = crow + 64 * (i & 3);
-      *(f16x8*)(base + (i >> 2) * A_PLANE + row * PADK + ckc * 8) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = crow + 64 * (i & 1);
-      *(f16x8*)(base + 2 * A_PLANE + (i >> 1) * B_PLANE + row * PADK + ckc * 8) = rb[i];
-    }
-  };
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][NB];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < NB; ++b) acc[a][b] = f32x16{};
 
-  const int nk = K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const _Float16* base = lds + st * STAGE;
+  auto frag = [&](const _Float16* plane, int r, int ks) {
+    const int c = (ks >> 3) + kh;
+    return *(const f16x8*)(plane + r * BK + ((c ^ swz(r)) << 3));
+  };
+  auto compute = [&](const _Float16* base) {
 #pragma unroll
     for (int ks = 0; ks < BK; ks += 16) {
-      const int kk = ks + 8 * kh;
-      f16x8 ah[4], al[4], bh[2], bl[2];
+      f16x8 bh[NB], bl[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int r = wn * WN + b * 32 + lm;
+        bh[b] = frag(base + 2 * A_PLANE, r, ks);
+        bl[b] = frag(base + 2 * A_PLANE + B_PLANE, r, ks);
+      }
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const int r = wm * 128 + a * 32 + lm;
-        ah[a] = *(const f16x8*)(base + r * PADK + kk);
-        al[a] = *(const f16x8*)(base + A_PLANE + r * PADK + kk);
-      }
+        const f16x8 ah = frag(base, r, ks);
+        const f16x8 al = frag(base + A_PLANE, r, ks);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int r = wn * 64 + b * 32 + lm;
-        bh[b] = *(const f16x8*)(base + 2 * A_PLANE + r * PADK + kk);
-        bl[b] = *(const f16x8*)(base + 2 * A_PLANE + B_PLANE + r * PADK + kk);
-      }
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[a], bh[b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[a], bl[b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[a], bh[b], acc[a][b], 0, 0, 0);
+        for (int b = 0; b < NB; ++b) {
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bh[b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bl[b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, bh[b], acc[a][b], 0, 0, 0);
         }
+      }
+      // Keep the fragment loads of the next k-slice from being hoisted here
+      // (register pressure).
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) lstore(st ^ 1);
+  };
+
+  // Double buffering: the loads of step k + 1 fly while step k computes; the
+  // barrier at the end of a step (which waits for this thread's outstanding
+  // loads) makes the next stage visible and frees the one just read.
+  const int nk = K / BK;
+  issue(0, buf0);
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 2 <= nk; kt += 2) {
+    issue((kt + 1) * BK, buf1);
+    compute(buf0);
+    __syncthreads();
+    if (kt + 2 < nk) issue((kt + 2) * BK, buf0);
+    compute(buf1);
     __syncthreads();
   }
+  if (kt < nk) compute(buf0);  // odd step count: the last step sits in buf0
 
   // Epilogue.  Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
   const float bs = *b_inv;
-  const int nt = (N + kObjTile - 1) / kObjTile;
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
-    double part[16];
+    const int rb0 = m0 + wm * 128 + a * 32 + 4 * kh;  // row of element v: rb0 + 8 (v / 4) + v % 4
     float rsc[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int row = m0 + wm * 128 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-      rsc[v] = row < M ? arow_inv[row] : 0.f;
-      part[v] = 0.0;
+      const int row = rb0 + 8 * (v / 4) + (v % 4);
+      rsc[v] = row < M ? arow_inv[row] * bs : 0.f;
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int col = n0 + wn * 64 + b * 32 + lm;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 128 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-        if (row < M && col < N) {
-          const float p = acc[a][b][v] * (rsc[v] * bs);
-          C[(size_t)row * N + col] = p;
-          if (kObj) {
-            const size_t ix = (size_t)row * K + col;
-            const float e = ((float)Ah[ix] + (float)Al[ix]) * rsc[v];
-            part[v] += (double)e * (double)p;
-          }
-        }
-      }
-    }
-    if (kObj) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        double x = part[v];
-#pragma unroll
-        for (int off = 16; off >= 1; off >>= 1) x += __shfl_xor(x, off);
-        part[v] = x;
-      }
-      if (lm == 0) {
-        const int slice = (n0 + wn * 64) / kObjTile;
+    for (int b = 0; b < NB; ++b) {
+      const int col = n0 + wn * WN + b * 32 + lm;
+      if (kMode == 1) {
+        // All loads of the block before its stores: the compiler cannot prove
+        // the addresses distinct and would otherwise serialise the round trips.
+        float old[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 128 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-          if (row < M && slice < nt) objpart[(size_t)row * nt + slice] = part[v];
+          const int row = rb0 + 8 * (v / 4) + (v % 4);
+          old[v] = (row < M && col < N) ? C[(size_t)row * ldc + col] : 0.f;
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = rb0 + 8 * (v / 4) + (v % 4);
+          if (row < M && col < N) C[(size_t)row * ldc + col] = old[v] - acc[a][b][v] * rsc[v];
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = rb0 + 8 * (v / 4) + (v % 4);
+          if (row < M && col < N) C[(size_t)row * ldc + col] = acc[a][b][v] * rsc[v];
         }
       }
     }
   }
 }
 
+// Per row and 64-column slice, sum_c E(row, c) P(row, c) in fp64 with E read
+// from its planes; summed over the slices of a row (in a fixed order) that is
+// L_j = e^T H e at the current scales and codes.  One wave per row: lane l
+// reads columns 8 l + 512 i .. + 7 (contiguous across the wave), and the eight
+// lanes that share a slice combine their sums.
+__global__ __launch_bounds__(256) void row_dot_kernel(int rows, int cols, int nt,
+                                                      const _Float16* __restrict__ Eh,
+                                                      const _Float16* __restrict__ El,
+                                                      const float* __restrict__ erow_inv,
+                                                      const float* __restrict__ P,
+                                                      double* __restrict__ objpart) {
+  static_assert(kObjTile == 64, "eight lanes of eight columns per slice");
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const size_t base = (size_t)row * cols;
+  const double rs = (double)erow_inv[row];
+  for (int c0 = 0; c0 < cols; c0 += 512) {
+    const int c = c0 + 8 * lane;
+    double s = 0.0;
+    if (c < cols) {  // cols is a multiple of 32, so a lane's 8 columns are all in range
+      const f16x8 h = *(const f16x8*)(Eh + base + c);
+      const f16x8 l = *(const f16x8*)(El + base + c);
+      const f32x4 p0 = *(const f32x4*)(P + base + c);
+      const f32x4 p1 = *(const f32x4*)(P + base + c + 4);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float e = (float)h[t] + (float)l[t];
+        s = fma((double)e, (double)(t < 4 ? p0[t] : p1[t - 4]), s);
+      }
+    }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    const int sl = c / kObjTile;
+    if ((lane & 7) == 0 && sl < nt) objpart[(size_t)row * nt + sl] = s * rs;
+  }
+}
+
+template <int BN, int kMode>
+static hipError_t launch_split3_t(hipStream_t st, int M, int N, int K, int lda, int ldb,
+                                  int ldc, const _Float16* ah, const _Float16* al,
+                                  const float* arow, const _Float16* bh, const _Float16* bl,
+                                  const float* bi, float* C) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % BK != 0) return hipErrorInvalidValue;
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  hipLaunchKernelGGL((split3_kernel<BN, kMode>), dim3(tiles), dim3(256), 0, st, M, N, K, lda, ldb,
+                     ldc, ah, al, arow, bh, bl, bi, C);
+  return hipGetLastError();
+}
+
 hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
                              const Layout& lay, float* C, double* objpart) {
-  const size_t lds = (size_t)2 * STAGE * sizeof(_Float16);
-  const void* fn = objpart != nullptr ? (const void*)split_gemm_kernel<true>
-                                      : (const void*)split_gemm_kernel<false>;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  dim3 grid((cols + BN - 1) / BN, (rows + BM - 1) / BM);
+  if (rows <= 0 || cols <= 0) return hipSuccess;
   const _Float16* ah = (const _Float16*)(ws + lay.ehi);
   const _Float16* al = (const _Float16*)(ws + lay.elo);
   const _Float16* bh = (const _Float16*)(ws + lay.hhi);
   const _Float16* bl = (const _Float16*)(ws + lay.hlo);
   const float* ar = (const float*)(ws + lay.erow);
   const float* bi = (const float*)(ws + lay.hscale);
-  if (objpart != nullptr)
-    hipLaunchKernelGGL(split_gemm_kernel<true>, grid, dim3(256), lds, st, rows, cols, cols, ah, al,
-                       ar, bh, bl, bi, C, objpart);
-  else
-    hipLaunchKernelGGL(split_gemm_kernel<false>, grid, dim3(256), lds, st, rows, cols, cols, ah, al,
-                       ar, bh, bl, bi, C, objpart);
+  const int nt = (cols + kObjTile - 1) / kObjTile;
+  hipError_t e = launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, ah, al, ar, bh,
+                                         bl, bi, C);
+  if (e != hipSuccess || objpart == nullptr) return e;
+  hipLaunchKernelGGL(row_dot_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, rows, cols, nt, ah,
+                     al, ar, C, objpart);
   return hipGetLastError();
 }
 

@@ -30,6 +30,11 @@ Layout make_layout(int rows, int cols, int g) {
   L.hhi = take(C * C * 2);
   L.hlo = take(C * C * 2);
   L.hscale = take(2 * sizeof(float));
+  L.rmat = take(G * gg * sizeof(float));
+  L.mhi = take(C * C * 2);
+  L.mlo = take(C * C * 2);
+  L.mrow = take(C * sizeof(float));
+  L.mmax = take(C * sizeof(float));
   L.ehi = take(R * C * 2);
   L.elo = take(R * C * 2);
   L.erow = take(R * sizeof(float));
@@ -37,7 +42,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
-  L.objpart = take(R * nt * sizeof(double));
+  L.objpart = take(R * (nt > G ? nt : G) * sizeof(double));  // per-group sweep partials or 64-column slices
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
   L.active = take(R);
@@ -147,6 +152,7 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
   JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
   JQ_HIP(launch_chol_groups(c.st, c.cols, c.g, H, c.ws, c.lay));
+  JQ_HIP(launch_split_m(c.st, c.cols, c.g, H, c.ws, c.lay));
   JQ_HIP(launch_split_h(c.st, c.cols, H, c.ws, c.lay));
   JQ_HIP(launch_gemm_ah(c.st, c.rows, c.cols, c.g, false, W, nullptr, nullptr, nullptr, H, c.wh(),
                         nullptr));
@@ -200,9 +206,9 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
       e = launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay);
-    if (e == hipSuccess) e = launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf(), c.objpart());
+    if (e == hipSuccess) e = launch_split_gemm(c.st, c.rows, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
     if (e == hipSuccess)
-      e = launch_stop_check(c.st, c.rows, c.nt(), c.objpart(), (double*)(c.ws + c.lay.lcur),
+      e = launch_stop_check(c.st, c.rows, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau);
     if (e == hipSuccess) e = mark(k, 3);
     if (e == hipSuccess) e = enqueue_babai(c, H, codes, scales, zeros, c.active(), nullptr, nullptr);
@@ -313,7 +319,7 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
   Ctx c = make_ctx(p, workspace, stream);
   if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay) !=
           hipSuccess ||
-      launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf(), nullptr) != hipSuccess)
+      launch_split_gemm(c.st, c.rows, c.cols, c.g, c.ws, c.lay, c.pbuf(), nullptr) != hipSuccess)
     return JARQ_EHIP;
   if (enqueue_babai(c, H, codes, scales, zeros, nullptr, cand, decision) != hipSuccess)
     return JARQ_EHIP;

@@ -5,12 +5,13 @@
 // R_i^T R_i = A_i^T A_i = H_ii, so R_i is the upper Cholesky factor of H_ii
 // (the Babai proposal does not depend on the row signs of R_i).  One work-group
 // factors one g x g block in LDS in fp64, inverts the lower factor L_i = R_i^T
-// column by column, and writes the fp32 forms the sweep kernels read:
+// column by column, and writes the fp32 forms the sweep kernels read (and
+// keeps L_i^{-1} in fp64 in place of L_i):
 //   rinv  row n = row n of L_i^{-1}       (u = R_i^{-T} he = L_i^{-1} he)
 //   rcol  [l][j][t] = R_i(m, l) / R_i(m, m) with m = j + 16 t (column l of R_i
 //         with each row scaled by its inverse diagonal, interleaved as the 16
 //         lanes of a row own its positions)
-//   rdinv 1 / R_i(l, l),  rdsq R_i(l, l)^2.
+//   rdinv 1 / R_i(l, l),  rdsq R_i(l, l)^2,  rmat R_i (row-major).
 #include "jarq_internal.h"
 
 namespace jarq {
@@ -22,6 +23,7 @@ __global__ __launch_bounds__(256) void chol_groups_kernel(const float* __restric
                                                           float* __restrict__ rcol,
                                                           float* __restrict__ rdinv,
                                                           float* __restrict__ rdsq,
+                                                          float* __restrict__ rmat,
                                                           Flags* __restrict__ flags) {
   constexpr int g = G_SIZE;
   constexpr int LD = g + 1;
@@ -91,11 +93,20 @@ __global__ __launch_bounds__(256) void chol_groups_kernel(const float* __restric
     const int m = j + 16 * t;
     rcol_b[e] = (float)(m <= l ? Lb[l * g + m] / Lb[m * g + m] : 0.0);
   }
+  // R_i = L_i^T in fp32, row m: rmat[m][n] = L_i(n, m) (zero below the diagonal).
+  float* rmat_b = rmat + (size_t)blk * g * g;
+  for (int e = tid; e < g * g; e += blockDim.x) {
+    const int m = e / g, n = e % g;
+    rmat_b[e] = (float)(n >= m ? Lb[n * g + m] : 0.0);
+  }
   for (int l = tid; l < g; l += blockDim.x) {
     const double d = Lb[l * g + l];
     rdinv[(size_t)blk * g + l] = (float)(1.0 / d);
     rdsq[(size_t)blk * g + l] = (float)(d * d);
   }
+  __syncthreads();  // every read of L is done
+  // Keep L_i^{-1} in fp64 (it replaces L_i in lfac) for M = blockdiag(L^{-1}) H.
+  for (int e = tid; e < g * g; e += blockDim.x) Lb[e] = A[(e / g) * LD + e % g];
   if (tid == 0 && fail) atomicAdd(&flags->not_spd, 1);
 }
 
@@ -109,7 +120,8 @@ static hipError_t launch_chol_t(hipStream_t st, int cols, const float* H, char* 
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(chol_groups_kernel<G_SIZE>, dim3(G), dim3(256), lds, st, H, cols,
                      (double*)(ws + lay.lfac), (float*)(ws + lay.rinv), (float*)(ws + lay.rcol),
-                     (float*)(ws + lay.rdinv), (float*)(ws + lay.rdsq), (Flags*)(ws + lay.flags));
+                     (float*)(ws + lay.rdinv), (float*)(ws + lay.rdsq), (float*)(ws + lay.rmat),
+                     (Flags*)(ws + lay.flags));
   return hipGetLastError();
 }
 

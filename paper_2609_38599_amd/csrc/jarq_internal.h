@@ -54,7 +54,7 @@ struct Flags {
 
 // Offsets (bytes) of the workspace regions for one problem size.
 struct Layout {
-  size_t lfac;      // [G][g][g] f64: Cholesky factor L_i (prep scratch)
+  size_t lfac;      // [G][g][g] f64: L_i^{-1} (holds L_i while it is factored)
   size_t rinv;      // [G][g][g] f32: row n = row n of L_i^{-1} = column n of R_i^{-1}
   size_t rcol;      // [G][g][16][g/16] f32: R_i columns interleaved for the back substitution
   size_t rdinv;     // [G][g] f32: 1 / R_i(l,l)
@@ -62,6 +62,11 @@ struct Layout {
   size_t hhi;       // [cols][cols] f16: H 2^t, high term
   size_t hlo;       // [cols][cols] f16: H 2^t, low term
   size_t hscale;    // f32[2]: 2^-t, max |H|
+  size_t rmat;      // [G][g][g] f32: R_i = L_i^T, row-major
+  size_t mhi;       // [cols][cols] f16: M = blockdiag(L_i^{-1}) H, row n scaled by 2^t_n, high term
+  size_t mlo;       // [cols][cols] f16: low term
+  size_t mrow;      // [cols] f32: 2^-t_n
+  size_t mmax;      // [cols] f32: row maxima of M (prep scratch)
   size_t ehi;       // [rows][cols] f16: E 2^t_row, high term
   size_t elo;       // [rows][cols] f16: E 2^t_row, low term
   size_t erow;      // [rows] f32: 2^-t_row
@@ -94,6 +99,10 @@ hipError_t launch_gemm_ah(hipStream_t st, int rows, int cols, int g, bool quant,
                           const int32_t* zeros, const float* H, float* C, double* objpart);
 
 hipError_t launch_split_h(hipStream_t st, int cols, const float* H, char* ws, const Layout& lay);
+// M = blockdiag(L_i^{-1}) H as two fp16 planes with per-row scales (after
+// launch_chol_groups; uses the H planes as scratch, so call launch_split_h after).
+hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char* ws,
+                          const Layout& lay);
 
 hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
                           const uint8_t* codes, const float* scales, const int32_t* zeros,
@@ -101,7 +110,7 @@ hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float
 
 // P = E H from the fp16 planes of E and H in the workspace (three products);
 // objpart as for launch_gemm_ah (may be null).
-hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
+hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, int g, const char* ws,
                              const Layout& lay, float* C, double* objpart);
 
 // Upper triangles of the grouped Gram matrices from the fp16 planes of H.
@@ -121,6 +130,9 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
                         uint8_t* cand, uint8_t* decision, Counters* cnt);
 
 // Groups per panel of the code update.
+// Groups per panel of the code update (512 columns, at most 16 groups).
+constexpr int kMaxPanelGroups = 16;
+constexpr int panel_groups_of(int g) { return 512 / g < kMaxPanelGroups ? 512 / g : kMaxPanelGroups; }
 int panel_groups(int g);
 
 // P(:, c1:) -= the accepted changes of the groups in columns [c0, c1).

@@ -1,19 +1,21 @@
-// Gauss-Seidel residual update between panels of groups (paper eq. (7)).
+// Gauss-Seidel update between panels of groups (paper eq. (7), in the
+// coordinates of eq. (10)).
 //
 // The code update visits the groups of a row in order; group i must see the
 // accepted changes of every earlier group.  Groups are processed in panels of
 // consecutive groups: inside a panel the Babai kernel corrects its own later
 // groups, and once a panel is done this kernel folds its accepted changes into
-// the residual product of every later column, for all rows at once:
-//   P(:, c) -= sum_{h in panel} s_h (dq_h H(h-block, c))       for c >= panel end,
-// with dq_h the exact integer code changes (fp16) and H read as its two fp16
+// U = E M^T (M = blockdiag(L_i^{-1}) H) for every later column, all rows at once:
+//   U(:, c) -= sum_{h in panel} s_h (dq_h M(c, h-block)^T)       for c >= panel end,
+// with dq_h the exact integer code changes (fp16) and M read as its two fp16
 // planes (v_mfma_f32_32x32x16_f16, two products); the per-row, per-group scale
-// s_h is applied to each group's partial sum in fp32.  H is symmetric, so
-// B(k, n) = H(n, k) is read along k.
+// s_h is applied to each group's partial sum in fp32 and the per-column scale
+// of M at the end.  B(k, c) = M(c, k) is read along k.
 //
 // Tiling: 128 x 128 output tile per 256-thread work-group, 2 x 2 waves of
-// 64 x 64, K (the panel's columns) in steps of 32 staged through LDS with
-// double buffering.
+// 64 x 64, K (the panel's columns) in steps of 32 moved straight from global
+// memory into a three-stage LDS ring (global_load_lds_dwordx4); two
+// work-groups per CU.
 #include "jarq_internal.h"
 
 namespace jarq {
@@ -21,18 +23,43 @@ namespace jarq {
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 namespace {
-constexpr int BM = 128, BN = 128, BK = 32, PADK = BK + 8;
-constexpr int A_TILE = BM * PADK, B_TILE = BN * PADK;
-constexpr int STAGE = A_TILE + 2 * B_TILE;  // halves per stage
-constexpr int MAX_PANEL_GROUPS = 16;
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int A_TILE = BM * BK, B_TILE = BN * BK;  // halves
+constexpr int STAGE = A_TILE + 2 * B_TILE;
+constexpr int DMA_PER_WAVE = STAGE / 512 / 4;     // 1 KB pieces per wave per stage
+
+// Chunk c (16 bytes) of row r of a staged tile sits at position c ^ swz(r):
+// fragment reads then touch distinct banks (see sgemm.hip).
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) + (r >> 3)) & 3; }
+
+__device__ __forceinline__ void dma16(const _Float16* src, _Float16* lds) {
+  __builtin_amdgcn_global_load_lds((const void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// Wait until at most n of this wave's vector-memory operations are in flight
+// (other counters untouched), then meet the other waves.  The empty asm
+// statements keep the compiler from moving LDS accesses across the barrier.
+template <int N>
+__device__ __forceinline__ void wait_vm_and_barrier() {
+  static_assert(N < 16, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 }  // namespace
 
 __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     int rows, int cols, int g, int c0, int c1, const _Float16* __restrict__ dq,
-    const _Float16* __restrict__ Hh, const _Float16* __restrict__ Hl,
-    const float* __restrict__ h_inv, const float* __restrict__ scales, float* __restrict__ P) {
-  extern __shared__ _Float16 lds[];
-  __shared__ float sc_s[BM][MAX_PANEL_GROUPS];
+    const _Float16* __restrict__ Mh, const _Float16* __restrict__ Ml,
+    const float* __restrict__ bcol_inv, const float* __restrict__ scales, float* __restrict__ P) {
+  // Three stages in three distinct arrays: the loads of steps k + 1 and k + 2
+  // fly while step k computes.
+  __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
+  __shared__ __attribute__((aligned(1024))) _Float16 buf1[STAGE];
+  __shared__ __attribute__((aligned(1024))) _Float16 buf2[STAGE];
+  __shared__ float sc_s[BM][kMaxPanelGroups];
   const int G = cols / g;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -43,39 +70,45 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   const int n0 = c1 + blockIdx.x * BN;
   const int h0 = c0 / g;
   const int ng = (c1 - c0) / g;
-  const float hinv = *h_inv;
 
   for (int e = tid; e < BM * ng; e += 256) {
     const int r = e / ng, h = e % ng;
     const int gr = m0 + r;
-    sc_s[r][h] = gr < rows ? scales[(size_t)gr * G + h0 + h] * hinv : 0.f;
+    sc_s[r][h] = gr < rows ? scales[(size_t)gr * G + h0 + h] : 0.f;
   }
 
-  // global -> LDS chunks of 16 bytes: A 128 rows x 4 chunks, B 2 planes x 128 rows x 4 chunks
-  const int crow = tid >> 2;   // 0..63
-  const int ckc = tid & 3;
-  f16x8 ra[2], rb[4];
-  auto gload = [&](int k0) {
+
+  // Piece j (1 KB = 16 rows of one plane tile) of a stage goes to wave j % 4;
+  // lane L holds row 16 (j % 8) + L / 4, chunk (L % 4) ^ swz(row).  Pieces
+  // 0-7: dq rows, 8-15: M high plane rows, 16-23: M low plane rows.  Rows past
+  // the edge read row 0: their products reach no stored output.
+  unsigned off[DMA_PER_WAVE];
+  const _Float16* base[DMA_PER_WAVE];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int gm = m0 + crow + 64 * i;
-      ra[i] = gm < rows ? *(const f16x8*)(dq + (size_t)gm * cols + k0 + ckc * 8) : f16x8{};
+  for (int q = 0; q < DMA_PER_WAVE; ++q) {
+    const int j = wave + 4 * q;
+    const int r = 16 * (j % 8) + (lane >> 2);
+    const int chunk = (lane & 3) ^ swz(r);
+    if (j < 8) {
+      const int gm = m0 + r;
+      off[q] = (unsigned)(gm < rows ? gm : 0) * (unsigned)cols + (unsigned)(chunk * 8);
+      base[q] = dq;
+    } else {
+      const int gn = n0 + r;
+      off[q] = (unsigned)(gn < cols ? gn : 0) * (unsigned)cols + (unsigned)(chunk * 8);
+      base[q] = j < 16 ? Mh : Ml;
     }
+  }
+  auto issue = [&](int k0, _Float16* stage) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int gn = n0 + crow + 64 * (i & 1);
-      const _Float16* src = (i < 2 ? Hh : Hl);
-      rb[i] = gn < cols ? *(const f16x8*)(src + (size_t)gn * cols + k0 + ckc * 8) : f16x8{};
+    for (int q = 0; q < DMA_PER_WAVE; ++q) {
+      const int j = wave + 4 * q;
+      dma16(base[q] + k0 + off[q], stage + j * 512);
     }
   };
-  auto lstore = [&](int st) {
-    _Float16* base = lds + st * STAGE;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      *(f16x8*)(base + (crow + 64 * i) * PADK + ckc * 8) = ra[i];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *(f16x8*)(base + A_TILE + (i >> 1) * B_TILE + (crow + 64 * (i & 1)) * PADK + ckc * 8) = rb[i];
+  auto frag = [&](const _Float16* tile, int r, int ks) {
+    const int c = (ks >> 3) + kh;
+    return *(const f16x8*)(tile + r * BK + ((c ^ swz(r)) << 3));
   };
 
   f32x16 acc[2][2], seg[2][2];
@@ -86,27 +119,18 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
       acc[a][b] = f32x16{};
       seg[a][b] = f32x16{};
     }
-
-  const int nk = (c1 - c0) / BK;
   const int steps_per_group = g / BK;
-  gload(c0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
-    if (kt + 1 < nk) gload(c0 + (kt + 1) * BK);
-    const _Float16* base = lds + st * STAGE;
+  auto compute = [&](const _Float16* st, int kt) {
 #pragma unroll
     for (int ks = 0; ks < BK; ks += 16) {
-      const int kk = ks + 8 * kh;
       f16x8 af[2], bh[2], bl[2];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) af[a] = *(const f16x8*)(base + (wm * 64 + a * 32 + lm) * PADK + kk);
+      for (int a = 0; a < 2; ++a) af[a] = frag(st, wm * 64 + a * 32 + lm, ks);
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const int r = wn * 64 + b * 32 + lm;
-        bh[b] = *(const f16x8*)(base + A_TILE + r * PADK + kk);
-        bl[b] = *(const f16x8*)(base + A_TILE + B_TILE + r * PADK + kk);
+        bh[b] = frag(st + A_TILE, r, ks);
+        bl[b] = frag(st + A_TILE + B_TILE, r, ks);
       }
 #pragma unroll
       for (int a = 0; a < 2; ++a)
@@ -131,9 +155,31 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
           }
         }
     }
-    if (kt + 1 < nk) lstore(st ^ 1);
-    __syncthreads();
+  };
+
+  // Step k reads stage k % 3.  Before it: this wave's loads of step k are done
+  // (only the loads of step k + 1, issued later, may still fly: at most one
+  // stage's worth outstanding, since vector-memory loads complete in order),
+  // then all waves meet, which also frees the stage read at step k - 1 for the
+  // loads of step k + 2.
+  const int nk = (c1 - c0) / BK;  // >= 1
+  issue(c0, buf0);
+  if (nk > 1) issue(c0 + BK, buf1);
+  __syncthreads();  // sc_s
+  for (int kt = 0; kt < nk; kt += 3) {
+    if (kt + 1 < nk) wait_vm_and_barrier<DMA_PER_WAVE>(); else wait_vm_and_barrier<0>();
+    if (kt + 2 < nk) issue(c0 + (kt + 2) * BK, buf2);
+    compute(buf0, kt);
+    if (kt + 1 >= nk) break;
+    if (kt + 2 < nk) wait_vm_and_barrier<DMA_PER_WAVE>(); else wait_vm_and_barrier<0>();
+    if (kt + 3 < nk) issue(c0 + (kt + 3) * BK, buf0);
+    compute(buf1, kt + 1);
+    if (kt + 2 >= nk) break;
+    if (kt + 3 < nk) wait_vm_and_barrier<DMA_PER_WAVE>(); else wait_vm_and_barrier<0>();
+    if (kt + 4 < nk) issue(c0 + (kt + 4) * BK, buf1);
+    compute(buf2, kt + 2);
   }
+
   // Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
   // All loads of P are issued before any store: the compiler cannot prove the
@@ -155,27 +201,25 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int col = n0 + wn * 64 + b * 32 + lm;
+      const float cs = col < cols ? bcol_inv[col] : 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-        if (row < rows && col < cols) P[(size_t)row * cols + col] = pold[a][b][v] - acc[a][b][v];
+        if (row < rows && col < cols) P[(size_t)row * cols + col] = pold[a][b][v] - acc[a][b][v] * cs;
       }
     }
 }
 
-int panel_groups(int g) { return 512 / g < MAX_PANEL_GROUPS ? 512 / g : MAX_PANEL_GROUPS; }
+int panel_groups(int g) { return panel_groups_of(g); }
 
 hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0, int c1,
                                const char* ws, const Layout& lay, const float* scales, float* P) {
   if (c1 >= cols) return hipSuccess;
-  const size_t lds = (size_t)2 * STAGE * sizeof(_Float16);
-  hipError_t e = hipFuncSetAttribute((const void*)panel_update_kernel,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
+  if ((c1 - c0) % BK != 0 || (c1 - c0) / g > kMaxPanelGroups) return hipErrorInvalidValue;
   dim3 grid((cols - c1 + BN - 1) / BN, (rows + BM - 1) / BM);
-  hipLaunchKernelGGL(panel_update_kernel, grid, dim3(256), lds, st, rows, cols, g, c0, c1,
-                     (const _Float16*)(ws + lay.dq), (const _Float16*)(ws + lay.hhi),
-                     (const _Float16*)(ws + lay.hlo), (const float*)(ws + lay.hscale), scales, P);
+  hipLaunchKernelGGL(panel_update_kernel, grid, dim3(256), 0, st, rows, cols, g, c0, c1,
+                     (const _Float16*)(ws + lay.dq), (const _Float16*)(ws + lay.mhi),
+                     (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow), scales, P);
   return hipGetLastError();
 }
 

@@ -1,18 +1,20 @@
-// Split-precision products on fp16 matrix cores: the residual product P = E H
-// of the sweep (paper Sec. 3.3.2: the conditional residual of eq. (7) needs
-// (H e)_i for every row and group).
+// Split-precision products on fp16 matrix cores: the residual product of the
+// sweep (paper Sec. 3.3.2: the conditional residual of eq. (7) needs (H e)_i
+// for every row and group, used in the coordinates of eq. (10)).
 //
 // Operands arrive as two-term fp16 planes with power-of-two scales (split.hip):
-// A = (Ah + Al) ra_m per row, B = (Bh + Bl) rb.  The product keeps the three
-// terms above 2^-22 relative, A B = (Ah Bh + Ah Bl + Al Bh) ra_m rb, accumulated
-// in fp32 by v_mfma_f32_32x32x16_f16 — fp32-class accuracy at 3/16 of the fp32
-// matrix work.  B is read as rows (B(k, n) = Bt(n, k)); for the residual
-// product Bt = H, which is symmetric.
+// A = (Ah + Al) ra_m per row m, B(k, n) = Bt(n, k) with Bt = (Bh + Bl) rb_n per
+// row n.  The product keeps the three terms above 2^-22 relative,
+// A B = (Ah Bh + Ah Bl + Al Bh) ra_m rb_n, accumulated in fp32 by
+// v_mfma_f32_32x32x16_f16 — fp32-class accuracy at 3/16 of the fp32 matrix
+// work.  For the sweep Bt = M = blockdiag(L_i^{-1}) H, so the product is
+// U = E M^T: group i's columns of row j hold L_i^{-1} (H e_j)_i, the u of
+// eq. (10) before division by the scale.
 //
 // Epilogues: store C = A B, or subtract, C -= A B.  After the residual
-// product a second kernel forms, per row and 64-column slice, sum_c E P in
-// fp64; summed over the slices that is L_j, the objective right after the
-// scale update (App. E.2).
+// product a second kernel forms, per row and group, (R_i e_i) . U_i =
+// e_i^T (H e)_i in fp64; summed over the groups that is L_j, the objective
+// right after the scale update (App. E.2).
 //
 // Tiling: 256 x BN output tile per 256-thread work-group, 2 x 2 waves of
 // 128 x BN/2, K in steps of 32.  Both planes of both operands go straight from
@@ -65,7 +67,7 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
     int M, int N, int K, int lda, int ldb, int ldc, const _Float16* __restrict__ Ah,
     const _Float16* __restrict__ Al, const float* __restrict__ arow_inv,
     const _Float16* __restrict__ Bh, const _Float16* __restrict__ Bl,
-    const float* __restrict__ b_inv, float* __restrict__ C) {
+    const float* __restrict__ bcol_inv, float* __restrict__ C) {
   constexpr int WN = BN / 2;   // wave tile columns
   constexpr int NB = WN / 32;  // 32-column blocks per wave
   constexpr int A_PLANE = BM * BK, B_PLANE = BN * BK;  // halves
@@ -177,7 +179,6 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
 
   // Epilogue.  Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
-  const float bs = *b_inv;
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     const int rb0 = m0 + wm * 128 + a * 32 + 4 * kh;  // row of element v: rb0 + 8 (v / 4) + v % 4
@@ -185,11 +186,12 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int row = rb0 + 8 * (v / 4) + (v % 4);
-      rsc[v] = row < M ? arow_inv[row] * bs : 0.f;
+      rsc[v] = row < M ? arow_inv[row] : 0.f;
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int col = n0 + wn * WN + b * 32 + lm;
+      const float cs = col < N ? bcol_inv[col] : 0.f;
       if (kMode == 1) {
         // All loads of the block before its stores: the compiler cannot prove
         // the addresses distinct and would otherwise serialise the round trips.
@@ -202,55 +204,95 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int row = rb0 + 8 * (v / 4) + (v % 4);
-          if (row < M && col < N) C[(size_t)row * ldc + col] = old[v] - acc[a][b][v] * rsc[v];
+          if (row < M && col < N)
+            C[(size_t)row * ldc + col] = old[v] - acc[a][b][v] * (rsc[v] * cs);
         }
       } else {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int row = rb0 + 8 * (v / 4) + (v % 4);
-          if (row < M && col < N) C[(size_t)row * ldc + col] = acc[a][b][v] * rsc[v];
+          if (row < M && col < N) C[(size_t)row * ldc + col] = acc[a][b][v] * (rsc[v] * cs);
         }
       }
     }
   }
 }
 
-// Per row and 64-column slice, sum_c E(row, c) P(row, c) in fp64 with E read
-// from its planes; summed over the slices of a row (in a fixed order) that is
-// L_j = e^T H e at the current scales and codes.  One wave per row: lane l
-// reads columns 8 l + 512 i .. + 7 (contiguous across the wave), and the eight
-// lanes that share a slice combine their sums.
-__global__ __launch_bounds__(256) void row_dot_kernel(int rows, int cols, int nt,
-                                                      const _Float16* __restrict__ Eh,
-                                                      const _Float16* __restrict__ El,
-                                                      const float* __restrict__ erow_inv,
-                                                      const float* __restrict__ P,
-                                                      double* __restrict__ objpart) {
-  static_assert(kObjTile == 64, "eight lanes of eight columns per slice");
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+// Per row j and group i: (R_i e_i) . U_i = e_i^T L_i L_i^{-1} (H e)_i in fp64,
+// with E read from its planes and R_i = L_i^T in fp32.  V = E_i L_i on fp32
+// matrix cores (v_mfma_f32_16x16x4f32; L_i is lower triangular, so output
+// block mb only takes k-blocks kc >= mb).  Work-group: 256 rows x one group,
+// R_i staged once in LDS; wave w takes rows 64 w .. 64 w + 63 in blocks of 16.
+template <int G_SIZE>
+__global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
+                                                        const _Float16* __restrict__ Eh,
+                                                        const _Float16* __restrict__ El,
+                                                        const float* __restrict__ erow_inv,
+                                                        const float* __restrict__ rmat,
+                                                        const float* __restrict__ U,
+                                                        double* __restrict__ objpart) {
+  constexpr int g = G_SIZE;
+  constexpr int NBK = g / 16;
+  constexpr int LDR = g + 4;  // padded row stride of R_i in LDS
+  typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) float rs[g * LDR];
+  const int G = cols / g;
+  const int i = blockIdx.y;
   const int lane = threadIdx.x & 63;
-  if (row >= rows) return;
-  const size_t base = (size_t)row * cols;
-  const double rs = (double)erow_inv[row];
-  for (int c0 = 0; c0 < cols; c0 += 512) {
-    const int c = c0 + 8 * lane;
-    double s = 0.0;
-    if (c < cols) {  // cols is a multiple of 32, so a lane's 8 columns are all in range
-      const f16x8 h = *(const f16x8*)(Eh + base + c);
-      const f16x8 l = *(const f16x8*)(El + base + c);
-      const f32x4 p0 = *(const f32x4*)(P + base + c);
-      const f32x4 p1 = *(const f32x4*)(P + base + c + 4);
+  const int wave = threadIdx.x >> 6;
+  const int mr = lane & 15, kq = lane >> 4;
+  const float* Ri = rmat + (size_t)i * g * g;
+  for (int e = threadIdx.x; e < g * g / 4; e += 256) {
+    const int r = e / (g / 4), c4 = e % (g / 4);
+    *(f32x4*)(rs + r * LDR + 4 * c4) = *(const f32x4*)(Ri + (size_t)r * g + 4 * c4);
+  }
+  __syncthreads();
+  for (int rb = 0; rb < 4; ++rb) {
+    const int r0 = blockIdx.x * 256 + wave * 64 + rb * 16;
+    if (r0 >= rows) break;
+    const int arow = r0 + mr;
+    const size_t ab = (size_t)(arow < rows ? arow : 0) * cols + (size_t)i * g;
+    // A fragments: E(row mr, k = 16 kc + 4 kq + t)
+    f32x4 ea[NBK];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const float e = (float)h[t] + (float)l[t];
-        s = fma((double)e, (double)(t < 4 ? p0[t] : p1[t - 4]), s);
-      }
+    for (int kc = 0; kc < NBK; ++kc) {
+      const f16x4 h = *(const f16x4*)(Eh + ab + kc * 16 + 4 * kq);
+      const f16x4 l = *(const f16x4*)(El + ab + kc * 16 + 4 * kq);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) ea[kc][t] = arow < rows ? (float)h[t] + (float)l[t] : 0.f;
     }
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
-    s += __shfl_xor(s, 4);
-    const int sl = c / kObjTile;
-    if ((lane & 7) == 0 && sl < nt) objpart[(size_t)row * nt + sl] = s * rs;
+    double part[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int mb = 0; mb < NBK; ++mb) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      const int m = mb * 16 + mr;
+      float u[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = r0 + 4 * kq + v;
+        u[v] = U[(size_t)(row < rows ? row : 0) * cols + (size_t)i * g + m];
+      }
+#pragma unroll
+      for (int kc = 0; kc < NBK; ++kc) {
+        if (kc < mb) continue;  // zero block of the triangle (constant trip count keeps ea in registers)
+        // B(k, m) = L_i(k, m) = R_i(m, k)
+        const f32x4 bv = *(const f32x4*)(rs + m * LDR + kc * 16 + 4 * kq);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ea[kc][t], bv[t], acc, 0, 0, 0);
+      }
+      // element v of lane l: (row 4 (l / 16) + v, column l % 16) of the block
+#pragma unroll
+      for (int v = 0; v < 4; ++v) part[v] = fma((double)acc[v], (double)u[v], part[v]);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      double x = part[v];
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+      const int row = r0 + 4 * kq + v;
+      if (mr == 0 && row < rows) objpart[(size_t)row * G + i] = x * (double)erow_inv[row];
+    }
   }
 }
 
@@ -258,31 +300,43 @@ template <int BN, int kMode>
 static hipError_t launch_split3_t(hipStream_t st, int M, int N, int K, int lda, int ldb,
                                   int ldc, const _Float16* ah, const _Float16* al,
                                   const float* arow, const _Float16* bh, const _Float16* bl,
-                                  const float* bi, float* C) {
+                                  const float* bcol, float* C) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % BK != 0) return hipErrorInvalidValue;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   hipLaunchKernelGGL((split3_kernel<BN, kMode>), dim3(tiles), dim3(256), 0, st, M, N, K, lda, ldb,
-                     ldc, ah, al, arow, bh, bl, bi, C);
+                     ldc, ah, al, arow, bh, bl, bcol, C);
   return hipGetLastError();
 }
 
-hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
+template <int G_SIZE>
+static hipError_t launch_group_dot_t(hipStream_t st, int rows, int cols, const char* ws,
+                                     const Layout& lay, const float* U, double* objpart) {
+  dim3 grid((rows + 255) / 256, cols / G_SIZE);
+  hipLaunchKernelGGL(group_dot_kernel<G_SIZE>, grid, dim3(256), 0, st, rows, cols,
+                     (const _Float16*)(ws + lay.ehi), (const _Float16*)(ws + lay.elo),
+                     (const float*)(ws + lay.erow), (const float*)(ws + lay.rmat), U, objpart);
+  return hipGetLastError();
+}
+
+hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, int g, const char* ws,
                              const Layout& lay, float* C, double* objpart) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
   const _Float16* ah = (const _Float16*)(ws + lay.ehi);
   const _Float16* al = (const _Float16*)(ws + lay.elo);
-  const _Float16* bh = (const _Float16*)(ws + lay.hhi);
-  const _Float16* bl = (const _Float16*)(ws + lay.hlo);
+  const _Float16* bh = (const _Float16*)(ws + lay.mhi);
+  const _Float16* bl = (const _Float16*)(ws + lay.mlo);
   const float* ar = (const float*)(ws + lay.erow);
-  const float* bi = (const float*)(ws + lay.hscale);
-  const int nt = (cols + kObjTile - 1) / kObjTile;
+  const float* bc = (const float*)(ws + lay.mrow);
   hipError_t e = launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, ah, al, ar, bh,
-                                         bl, bi, C);
+                                         bl, bc, C);
   if (e != hipSuccess || objpart == nullptr) return e;
-  hipLaunchKernelGGL(row_dot_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, rows, cols, nt, ah,
-                     al, ar, C, objpart);
-  return hipGetLastError();
+  switch (g) {
+    case 32: return launch_group_dot_t<32>(st, rows, cols, ws, lay, C, objpart);
+    case 64: return launch_group_dot_t<64>(st, rows, cols, ws, lay, C, objpart);
+    case 128: return launch_group_dot_t<128>(st, rows, cols, ws, lay, C, objpart);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace jarq

@@ -5,6 +5,8 @@
 // hi = fp16(x 2^t), lo = fp16(x 2^t - hi), which carries 22 significant bits.
 // Products of such planes accumulate in fp32 on the matrix cores.
 //   H:  one scale for the whole matrix, chosen so max |H| 2^t lies in [2^13, 2^14).
+//   M = blockdiag(L_i^{-1}) H (the code update's coordinates, eq. (10)): one
+//       scale per row of M, same rule.
 //   E = W - What (eq. (1)), per sweep: one scale per row, same rule.
 // Small-integer operands (codes minus zero points, code changes) are exact in fp16.
 #include "jarq_internal.h"
@@ -56,6 +58,87 @@ hipError_t launch_split_h(hipStream_t st, int cols, const float* H, char* ws, co
                      (_Float16*)(ws + lay.hhi), (_Float16*)(ws + lay.hlo),
                      (float*)(ws + lay.hscale));
   return hipGetLastError();
+}
+
+// M = blockdiag(L_i^{-1}) H.  Row n of M (group i = n / g, local index nl) is
+// sum_{m <= nl} L_i^{-1}(nl, m) H(i g + m, :): the residual product with M in
+// place of H gives u = L_i^{-1} (H e)_i for every group at once, and its
+// blocks M(i-block, h-block) = L_i^{-1} H_ih carry a code change of group h
+// into u_i.  Formed in fp64 from the fp64 inverse, rounded to fp32 into a
+// temporary, with each row's maximum; then split with one scale per row.
+// Work-group: the g rows of group i for 256 columns, thread = column.
+template <int G_SIZE>
+__global__ __launch_bounds__(256) void form_m_kernel(const float* __restrict__ H, int cols,
+                                                     const double* __restrict__ linv,
+                                                     float* __restrict__ mtmp,
+                                                     float* __restrict__ rowmax) {
+  constexpr int g = G_SIZE;
+  const int i = blockIdx.y;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  __shared__ double li[g * g];
+  const double* Li = linv + (size_t)i * g * g;
+  for (int e = threadIdx.x; e < g * g; e += 256) li[e] = Li[e];
+  __syncthreads();
+  const bool cin = c < cols;
+  float hc[g];
+#pragma unroll
+  for (int m = 0; m < g; ++m) hc[m] = cin ? H[(size_t)(i * g + m) * cols + c] : 0.f;
+  for (int nl = 0; nl < g; ++nl) {
+    double acc = 0.0;
+#pragma unroll
+    for (int m = 0; m < g; ++m)
+      if (m <= nl) acc = fma(li[nl * g + m], (double)hc[m], acc);
+    const float v = (float)acc;
+    float mx = fabsf(v);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (cin) mtmp[(size_t)(i * g + nl) * cols + c] = v;
+    if ((threadIdx.x & 63) == 0) atomic_max_abs(rowmax + i * g + nl, mx);
+  }
+}
+
+__global__ void split_rows_kernel(const float* __restrict__ x, int cols, int nrows,
+                                  const float* __restrict__ rowmax, _Float16* __restrict__ hi,
+                                  _Float16* __restrict__ lo, float* __restrict__ row_inv) {
+  const size_t n = (size_t)nrows * cols;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (size_t)gridDim.x * blockDim.x) {
+    const int r = (int)(e / cols);
+    const int t = pow2_exponent(rowmax[r]);
+    if (e % cols == 0) row_inv[r] = ldexpf(1.f, -t);
+    const float v = ldexpf(x[e], t);
+    const _Float16 h = (_Float16)v;
+    hi[e] = h;
+    lo[e] = (_Float16)(v - (float)h);
+  }
+}
+
+template <int G_SIZE>
+static hipError_t launch_split_m_t(hipStream_t st, int cols, const float* H, char* ws,
+                                   const Layout& lay) {
+  // The H planes (written afterwards by launch_split_h) serve as the fp32
+  // temporary: together they span cols * cols * 4 bytes.
+  float* mtmp = (float*)(ws + lay.hhi);
+  float* rowmax = (float*)(ws + lay.mmax);
+  hipError_t e = launch_zero_bytes(st, rowmax, (size_t)cols * sizeof(float));
+  if (e != hipSuccess) return e;
+  dim3 grid((cols + 255) / 256, cols / G_SIZE);
+  hipLaunchKernelGGL(form_m_kernel<G_SIZE>, grid, dim3(256), 0, st, H, cols,
+                     (const double*)(ws + lay.lfac), mtmp, rowmax);
+  hipLaunchKernelGGL(split_rows_kernel, dim3(2048), dim3(256), 0, st, mtmp, cols, cols, rowmax,
+                     (_Float16*)(ws + lay.mhi), (_Float16*)(ws + lay.mlo),
+                     (float*)(ws + lay.mrow));
+  return hipGetLastError();
+}
+
+hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char* ws,
+                          const Layout& lay) {
+  switch (g) {
+    case 32: return launch_split_m_t<32>(st, cols, H, ws, lay);
+    case 64: return launch_split_m_t<64>(st, cols, H, ws, lay);
+    case 128: return launch_split_m_t<128>(st, cols, H, ws, lay);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 // One work-group per row: E = W - s (q - z) in fp32 (as in eq. (1)), its

@@ -183,7 +183,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int gr = r0 + 4 * kq + v;
-        uacc[b][v] = gr < rows ? P[(size_t)gr * cols + (size_t)i * g + n] : 0.f;
+        // rows past the edge read row 0 (unconditional load); never used
+        uacc[b][v] = P[(size_t)(gr < rows ? gr : 0) * cols + (size_t)i * g + n];
       }
     }
   };

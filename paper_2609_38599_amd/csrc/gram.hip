@@ -71,21 +71,19 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
   u32x4 stq[g / 16];
   int stz = 0;
   const int srow = r0 + tid;
+  // Rows past the edge load row 0 (unconditional loads, so that none is
+  // waited for here): each row's Gram entries depend on that row only, and
+  // those of rows past the edge are never stored.
+  const int lrow = srow < rows ? srow : 0;
   auto fetch_codes = [&](int blk) {
-    if (srow < rows) {
-      const u32x4* src = (const u32x4*)(codes + (size_t)srow * cols + (size_t)blk * g);
+    const u32x4* src = (const u32x4*)(codes + (size_t)lrow * cols + (size_t)blk * g);
 #pragma unroll
-      for (int i = 0; i < g / 16; ++i) stq[i] = src[i];
-      stz = zeros[(size_t)srow * G + blk];
-    } else {
-#pragma unroll
-      for (int i = 0; i < g / 16; ++i) stq[i] = u32x4{0u, 0u, 0u, 0u};
-      stz = 0;
-    }
+    for (int i = 0; i < g / 16; ++i) stq[i] = src[i];
+    stz = zeros[(size_t)lrow * G + blk];
   };
   auto store_codes = [&](_Float16* dst) {
     const _Float16 zb = (_Float16)(1024 + stz);
-    const f16x2 zz = srow < rows ? f16x2{zb, zb} : f16x2{(_Float16)1024, (_Float16)1024};
+    const f16x2 zz = f16x2{zb, zb};
 #pragma unroll
     for (int i = 0; i < g / 16; ++i) {
       f16x2 v[8];

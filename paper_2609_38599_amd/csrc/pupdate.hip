@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   for (int e = tid; e < BM * ng; e += 256) {
     const int r = e / ng, h = e % ng;
     const int gr = m0 + r;
-    sc_s[r][h] = gr < rows ? scales[(size_t)gr * G + h0 + h] : 0.f;
+    sc_s[r][h] = scales[(size_t)(gr < rows ? gr : 0) * G + h0 + h];  // rows past the edge: never stored
   }
 
 
@@ -182,18 +182,20 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 
   // Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
-  // All loads of P are issued before any store: the compiler cannot prove the
-  // addresses distinct and would otherwise serialise 64 round trips to memory.
+  // All loads of P are issued before any store (the compiler cannot prove the
+  // addresses distinct and would otherwise serialise the round trips), and
+  // they are unconditional, from a clamped address (a load under a branch is
+  // waited for inside the branch).
   float pold[2][2][16];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-      const int col = n0 + wn * 64 + b * 32 + lm;
+      const int col = min(n0 + wn * 64 + b * 32 + lm, cols - 1);
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-        pold[a][b][v] = (row < rows && col < cols) ? P[(size_t)row * cols + col] : 0.f;
+        const int row = min(m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4), rows - 1);
+        pold[a][b][v] = P[(size_t)row * cols + col];
       }
     }
 #pragma unroll
@@ -201,7 +203,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int col = n0 + wn * 64 + b * 32 + lm;
-      const float cs = col < cols ? bcol_inv[col] : 0.f;
+      const float cs = bcol_inv[min(col, cols - 1)];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);

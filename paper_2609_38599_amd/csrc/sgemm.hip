@@ -182,16 +182,15 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     const int rb0 = m0 + wm * 128 + a * 32 + 4 * kh;  // row of element v: rb0 + 8 (v / 4) + v % 4
+    // Unconditional loads from clamped addresses (a load under a branch is
+    // waited for inside the branch); out-of-range elements are never stored.
     float rsc[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = rb0 + 8 * (v / 4) + (v % 4);
-      rsc[v] = row < M ? arow_inv[row] : 0.f;
-    }
+    for (int v = 0; v < 16; ++v) rsc[v] = arow_inv[min(rb0 + 8 * (v / 4) + (v % 4), M - 1)];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int col = n0 + wn * WN + b * 32 + lm;
-      const float cs = col < N ? bcol_inv[col] : 0.f;
+      const float cs = bcol_inv[min(col, N - 1)];
       if (kMode == 1) {
         // All loads of the block before its stores: the compiler cannot prove
         // the addresses distinct and would otherwise serialise the round trips.
@@ -199,7 +198,7 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int row = rb0 + 8 * (v / 4) + (v % 4);
-          old[v] = (row < M && col < N) ? C[(size_t)row * ldc + col] : 0.f;
+          old[v] = C[(size_t)min(row, M - 1) * ldc + min(col, N - 1)];
         }
 #pragma unroll
         for (int v = 0; v < 16; ++v) {

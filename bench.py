@@ -1,17 +1,18 @@
 """Benchmark of the JARQ refinement sweep on one MI355X.
 
-A step is one sweep of the hot path over the whole layer: Gram build and
-joint scale solve, residual product E H with the row objectives, and the
+A step is one sweep of the hot path over the whole layer: Gram matrices and
+joint scale solve, residual product with the row objectives, and the
 Gauss-Seidel Babai code update.  The workload is the 4096 x 4096 attention
 projection layer (Student-t weights, AR(1)-correlated calibration inputs with
 outlier channels, RTN 3-bit host, g = 128), with every input resident in HBM
 before the timed region.  W untimed warm-up sweeps run on a copy of the host
 state; then K sweeps from the host state are timed as one call bracketed by
-device synchronisation.  Per-kernel durations come from HIP events that the
-library records on its stream around each stage.
+device synchronisation.  Per-stage durations come from HIP events that the
+library records on its own stream around each stage of each sweep.
 
-Prints one JSON line (see the keys below).  --gpus above 1 is refused: this
-build runs on one GPU.
+Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
+--copy-probe runs only a plain device copy of known size (used to calibrate
+the HBM byte counters of rocprofv3) and prints nothing else.
 """
 
 from __future__ import annotations
@@ -29,66 +30,88 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "ms per JARQ sweep, 4096x4096 G128 3-bit layer; MFMA% and HBM GB/s of peak"
+PEAK_FP16_MFMA_TFLOPS = 2500.0   # dense
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_FP64_TFLOPS = 78.6
 PEAK_HBM_GBS = 8000.0
+COPY_PROBE_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_residual_product_4096x4096.txt")
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def stage_work(cfg, rows, stats_k):
-    """Algorithmic FLOP per launch of each stage for one sweep."""
+def stage_work(cfg, rows, corr_blocks):
+    """Algorithmic FLOP of each stage for one sweep."""
     d, g = cfg.cols, cfg.group_size
     G = d // g
     return {
-        "gram": rows * (d * d + d * g),             # sum over h >= a of c_a^T H_ah c_h
+        "gram": 2.0 * 2.0 * rows * (d * d + d * g) / 2.0,   # two fp16 planes x (d^2+dg)/2 MACs
         "solve": rows * (G ** 3 / 3.0 + 4 * G * G + 2 * d),
-        "residual": 2.0 * rows * d * d,             # E H
-        "code": 2.0 * rows * d * g + 2.0 * 16 * g * g * stats_k,  # core + executed corrections
+        "esplit": 0.0,
+        "residual": 3 * 2.0 * rows * d * d,                 # three fp16 products of U = E M^T
+        "objective": 2.0 * rows * d * g / 2.0,              # (R_i e_i) per group, triangular
+        "code": 2.0 * rows * d * g + 2.0 * 16 * g * g * 2 * corr_blocks,
     }
 
 
-def traffic_from_profile(kernel_key):
-    """Per-launch HBM bytes measured with rocprofv3 counters, if still valid."""
-    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-    if not os.path.exists(path):
+def traffic_from_profile():
+    """Per-launch HBM bytes of the residual product kernel from rocprofv3 counters.
+
+    Read from the committed summary; None once the kernel source has changed
+    since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
-        data = json.load(open(path))
-        ent = data[kernel_key]
-        src = os.path.join(ROOT, ent["source"])
+        kv = {}
+        for line in open(TRAFFIC_FILE):
+            if "=" in line and not line.lstrip().startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+        src = os.path.join(ROOT, kv["source"])
         digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        if digest != ent["source_sha256"]:
+        if digest != kv["source_sha256"]:
             return None
-        return float(ent["bytes_per_launch"])
+        return float(kv["hbm_bytes_per_launch"])
     except Exception:
         return None
 
 
-def cpu_baseline(cfg, W, H, q, s, z, budget_rows):
-    """The float64 oracle on the host cores: one sweep over a row sample, per full layer."""
+def cpu_baseline(cfg, W, H, q, s, z, rows, sweeps):
+    """The float64 oracle on the host cores, over a bounded sample of the workload."""
     from oracle import jarq
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    rows = min(budget_rows, W.shape[0])
-    Ws, qs, ss, zs = W[:rows], q[:rows], s[:rows], z[:rows]
+    rows = min(rows, W.shape[0])
+    Ws, qs, ss, zs = W[:rows], q[:rows].copy(), s[:rows].copy(), z[:rows]
     g, bits = cfg.group_size, cfg.bits
     R = jarq.group_factors(H, g)                   # per-layer set-up, not timed
     t0 = time.perf_counter()
-    s1, _ = jarq.scale_step(Ws, H, qs, zs, g)
-    jarq.objective_rows(Ws, H, qs, s1, zs, g)
-    jarq.code_step(Ws, H, R, qs, s1, zs, g, bits)
+    for _ in range(sweeps):
+        ss, _ = jarq.scale_step(Ws, H, qs, zs, g)
+        jarq.objective_rows(Ws, H, qs, ss, zs, g)
+        qs = jarq.code_step(Ws, H, R, qs, ss, zs, g, bits)
     dt = time.perf_counter() - t0
-    ms_full = dt * 1e3 * (W.shape[0] / rows)
-    return {"value": ms_full, "unit": "ms/sweep", "cores": int(threads), "kind": "oracle",
-            "sample": f"one sweep (scale update, objective, code update) from the RTN host over "
-                      f"rows 0..{rows - 1} of {W.shape[0]}, float64 NumPy, {dt:.1f} s wall, "
-                      f"scaled by rows (rows are independent)"}
+    ms = dt * 1e3 / sweeps * (W.shape[0] / rows)
+    return {"value": ms, "unit": "ms/sweep", "cores": int(threads), "kind": "oracle",
+            "sample": f"{sweeps} sweeps (scale update, objective, code update) from the RTN host "
+                      f"over rows 0..{rows - 1} of {W.shape[0]}, float64 NumPy, {dt:.1f} s wall"
+                      + ("" if rows == W.shape[0] else ", scaled by rows (rows are independent)")}
+
+
+def copy_probe():
+    import torch
+    n = COPY_PROBE_BYTES // 4
+    a = torch.rand(n, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"[bench] copy probe: 5 copies of {COPY_PROBE_BYTES} bytes")
 
 
 def main():
@@ -97,17 +120,25 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=1)
-    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-rows", type=int, default=4096)
+    ap.add_argument("--cpu-sweeps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--inputs", default=None,
+                    help="cache file (.npz) of the synthetic layer: loaded if present, else written")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the refinement path of this build is single-GPU "
               "(rows would shard across GPUs with no per-sweep exchange; not built here).",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
 
     import torch
     import paper_2609_38599_amd as jq
+    from paper_2609_38599_amd.binding import STAGE_NAMES
     if not os.path.exists(jq.LIB_PATH):
         from paper_2609_38599_amd.build import build
         build()
@@ -115,10 +146,17 @@ def main():
 
     cfg = CONFIGS[args.config]
     g, bits = cfg.group_size, cfg.bits
-    log(f"[bench] building inputs for {cfg.name}")
-    W = make_weights(cfg)
-    H = make_hessian(cfg, device="cuda")
-    q, s, z = rtn_quantize(W, g, bits)
+    if args.inputs and os.path.exists(args.inputs):
+        log(f"[bench] loading inputs for {cfg.name} from {args.inputs}")
+        with np.load(args.inputs, allow_pickle=False) as f:
+            W, H, q, s, z = (f[k] for k in ("W", "H", "q", "s", "z"))
+    else:
+        log(f"[bench] building inputs for {cfg.name}")
+        W = make_weights(cfg)
+        H = make_hessian(cfg, device="cuda")
+        q, s, z = rtn_quantize(W, g, bits)
+        if args.inputs:
+            np.savez(args.inputs, W=W, H=H, q=q, s=s, z=z)
     dev = torch.device("cuda:0")
     Wd, Hd = torch.from_numpy(W).to(dev), torch.from_numpy(H).to(dev)
     qh, sh, zd = torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev), torch.from_numpy(z).to(dev)
@@ -147,18 +185,26 @@ def main():
     ms_per_step = wall_ms / args.steps
     log(f"[bench] {args.steps} sweeps in {wall_ms:.2f} ms")
 
-    stage_names = ["gram", "solve", "residual", "code"]
     n = min(args.steps, len(st["stage_ms"]))
     stage_ms = {name: float(np.mean([st["stage_ms"][k][j] for k in range(n)]))
-                for j, name in enumerate(stage_names)}
+                for j, name in enumerate(STAGE_NAMES)}
     blocks = float(np.mean(st["correction_blocks"][:n]))
     work = stage_work(cfg, rows, blocks)
-    dom = max(stage_names, key=lambda k: stage_ms[k])
-    bound = "alu" if dom == "solve" else "mfma"
-    peak = PEAK_FP64_TFLOPS if dom == "solve" else PEAK_FP32_MFMA_TFLOPS
-    achieved = work[dom] / (stage_ms[dom] * 1e-3) / 1e12
-    kernel_key = {"gram": "gram_kernel", "solve": "solve_kernel", "residual": "gemm_ah_kernel",
-                  "code": "babai_kernel"}[dom]
+
+    # Roofline of the residual product kernel (split3_kernel, one launch per
+    # sweep, timed alone by the library's events): the single kernel with the
+    # largest time per sweep.  Its work is three fp16 matrix products (the
+    # two-term split of E and M), against the dense fp16 matrix-core peak; the
+    # fp32-equivalent rate of the 2 rows d^2 product it stands for is given too.
+    t_res = stage_ms["residual"] * 1e-3
+    achieved = work["residual"] / t_res / 1e12
+    fp32_equiv = 2.0 * rows * cols * cols / t_res / 1e12
+    roofline = {"bound": "mfma", "kernel": "split3_kernel", "achieved": achieved,
+                "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_FP16_MFMA_TFLOPS, "traffic": traffic_from_profile(),
+                "launch_ms": stage_ms["residual"],
+                "fp32_equivalent_tflops": fp32_equiv,
+                "fp32_equivalent_frac_of_fp32_mfma_peak": fp32_equiv / PEAK_FP32_MFMA_TFLOPS}
     out = {
         "metric": METRIC,
         "value": ms_per_step,
@@ -174,25 +220,20 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: W {rows}x{cols} Student-t(5) std 0.02, H from "
                                f"{cfg.n_tokens} AR(1) tokens with {cfg.n_outliers} outlier channels, "
-                               f"RTN {bits}-bit host, g {g}, sweeps from the host state",
+                               f"RTN {bits}-bit host, g {g}, {args.steps} sweeps from the host state",
                    "rows": rows, "cols": cols, "group_size": g, "bits": bits},
         "rows_per_s": rows / (ms_per_step * 1e-3),
         "prep_ms": prep_ms,
         "stage_ms": stage_ms,
         "accepted_groups": st["accepted_groups"][:n],
         "objective_after_scales": st["objective_after_scales"][:n],
-        "roofline": {"bound": bound, "kernel": kernel_key, "achieved": achieved, "peak": peak,
-                     "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_from_profile(kernel_key)},
+        "roofline": roofline,
+        "stage_rates_tflops": {name: (work[name] / (stage_ms[name] * 1e-3) / 1e12
+                                      if stage_ms[name] > 0 else None) for name in STAGE_NAMES},
     }
-    other = {}
-    for name in stage_names:
-        tf = work[name] / (stage_ms[name] * 1e-3) / 1e12
-        other[name] = {"ms": stage_ms[name], "tflops": tf}
-    out["stage_rates"] = other
     if not args.no_cpu_baseline:
         log("[bench] timing the float64 oracle on the host")
-        out["cpu_baseline"] = cpu_baseline(cfg, W, H, q, s, z, args.cpu_rows)
+        out["cpu_baseline"] = cpu_baseline(cfg, W, H, q, s, z, args.cpu_rows, args.cpu_sweeps)
     print(json.dumps(out), flush=True)
 
 

@@ -50,7 +50,12 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 1
+#define JARQ_ABI_VERSION 2
+/* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
+ * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
+ * 3 residual product U = E M^T, 4 row objectives and stopping test,
+ * 5 code update (Babai kernels and panel updates). */
+#define JARQ_NUM_STAGES 6
 #define JARQ_MAX_RECORDED_SWEEPS 64
 
 typedef enum jarq_status {
@@ -86,7 +91,7 @@ typedef struct jarq_stats {
   int32_t ridge_rows[JARQ_MAX_RECORDED_SWEEPS];              /* stabilised scale solves */
   int32_t rows_active[JARQ_MAX_RECORDED_SWEEPS];             /* rows that ran the code update */
   int64_t correction_blocks[JARQ_MAX_RECORDED_SWEEPS];      /* 16-row x g x g correction products run */
-  float stage_ms[JARQ_MAX_RECORDED_SWEEPS][4];               /* Gram, scale solve, residual product, code update */
+  float stage_ms[JARQ_MAX_RECORDED_SWEEPS][JARQ_NUM_STAGES]; /* HIP-event ms per stage, see JARQ_NUM_STAGES */
   float prep_ms;                                             /* jarq_refine only */
 } jarq_stats;
 

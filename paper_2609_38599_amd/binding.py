@@ -16,6 +16,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libjarq.so")
 
 MAX_RECORDED_SWEEPS = 64
+NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
+STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
+ABI_VERSION = 2
 JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
@@ -42,7 +45,7 @@ class Stats(ctypes.Structure):
                 ("ridge_rows", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
                 ("rows_active", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
                 ("correction_blocks", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
-                ("stage_ms", (ctypes.c_float * 4) * MAX_RECORDED_SWEEPS),
+                ("stage_ms", (ctypes.c_float * NUM_STAGES) * MAX_RECORDED_SWEEPS),
                 ("prep_ms", ctypes.c_float)]
 
     def to_dict(self):
@@ -96,6 +99,9 @@ def load_library(path: str = LIB_PATH):
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
+    if lib.jarq_abi_version() != ABI_VERSION:
+        raise ImportError(f"{path} has ABI version {lib.jarq_abi_version()}, this binding expects "
+                          f"{ABI_VERSION}; rebuild with paper_2609_38599_amd/build.py")
     _lib = lib
     return lib
 

@@ -186,12 +186,12 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   std::vector<hipEvent_t> ev;
   if (stats != nullptr) {
     memset(stats, 0, sizeof(*stats));
-    ev.resize((size_t)nrec * 5);
+    ev.resize((size_t)nrec * (JARQ_NUM_STAGES + 1));
     for (auto& e : ev) JQ_HIP(hipEventCreate(&e));
   }
   auto mark = [&](int k, int j) -> hipError_t {
     if (stats == nullptr || k >= nrec) return hipSuccess;
-    return hipEventRecord(ev[(size_t)k * 5 + j], c.st);
+    return hipEventRecord(ev[(size_t)k * (JARQ_NUM_STAGES + 1) + j], c.st);
   };
   jarq_status status = JARQ_OK;
   int run = 0;
@@ -206,13 +206,17 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
       e = launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay);
-    if (e == hipSuccess) e = launch_split_gemm(c.st, c.rows, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
+    if (e == hipSuccess) e = mark(k, 3);
+    if (e == hipSuccess) e = launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf());
+    if (e == hipSuccess) e = mark(k, 4);
+    if (e == hipSuccess)
+      e = launch_group_objective(c.st, c.rows, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
     if (e == hipSuccess)
       e = launch_stop_check(c.st, c.rows, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau);
-    if (e == hipSuccess) e = mark(k, 3);
+    if (e == hipSuccess) e = mark(k, 5);
     if (e == hipSuccess) e = enqueue_babai(c, H, codes, scales, zeros, c.active(), nullptr, nullptr);
-    if (e == hipSuccess) e = mark(k, 4);
+    if (e == hipSuccess) e = mark(k, 6);
     if (e == hipSuccess)
       e = launch_record_sweep(c.st, c.rows, (const double*)(c.ws + c.lay.lcur), c.active(),
                               c.cnt(),
@@ -257,9 +261,10 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
         stats->ridge_rows[k] = (int32_t)hist[k].ridge_rows;
         stats->rows_active[k] = (int32_t)hist[k].active_rows;
         stats->correction_blocks[k] = (int64_t)hist[k].corr_blocks;
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < JARQ_NUM_STAGES; ++j) {
           float ms = 0.f;
-          hipEventElapsedTime(&ms, ev[(size_t)k * 5 + j], ev[(size_t)k * 5 + j + 1]);
+          const size_t b = (size_t)k * (JARQ_NUM_STAGES + 1) + j;
+          hipEventElapsedTime(&ms, ev[b], ev[b + 1]);
           stats->stage_ms[k][j] = ms;
         }
       }
@@ -319,7 +324,7 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
   Ctx c = make_ctx(p, workspace, stream);
   if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay) !=
           hipSuccess ||
-      launch_split_gemm(c.st, c.rows, c.cols, c.g, c.ws, c.lay, c.pbuf(), nullptr) != hipSuccess)
+      launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf()) != hipSuccess)
     return JARQ_EHIP;
   if (enqueue_babai(c, H, codes, scales, zeros, nullptr, cand, decision) != hipSuccess)
     return JARQ_EHIP;

@@ -110,8 +110,11 @@ hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float
 
 // P = E H from the fp16 planes of E and H in the workspace (three products);
 // objpart as for launch_gemm_ah (may be null).
-hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, int g, const char* ws,
-                             const Layout& lay, float* C, double* objpart);
+hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
+                             const Layout& lay, float* C);
+// Per row and group, (R_i e_i) . U_i = e_i^T (H e)_i (fp64) into objpart[row][group].
+hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, const char* ws,
+                                  const Layout& lay, const float* C, double* objpart);
 
 // Upper triangles of the grouped Gram matrices from the fp16 planes of H.
 hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,

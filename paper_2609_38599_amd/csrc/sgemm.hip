@@ -318,8 +318,8 @@ static hipError_t launch_group_dot_t(hipStream_t st, int rows, int cols, const c
   return hipGetLastError();
 }
 
-hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, int g, const char* ws,
-                             const Layout& lay, float* C, double* objpart) {
+hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
+                             const Layout& lay, float* C) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
   const _Float16* ah = (const _Float16*)(ws + lay.ehi);
   const _Float16* al = (const _Float16*)(ws + lay.elo);
@@ -327,9 +327,13 @@ hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, int g, const ch
   const _Float16* bl = (const _Float16*)(ws + lay.mlo);
   const float* ar = (const float*)(ws + lay.erow);
   const float* bc = (const float*)(ws + lay.mrow);
-  hipError_t e = launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, ah, al, ar, bh,
-                                         bl, bc, C);
-  if (e != hipSuccess || objpart == nullptr) return e;
+  return launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, ah, al, ar, bh, bl, bc,
+                                 C);
+}
+
+hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, const char* ws,
+                                  const Layout& lay, const float* C, double* objpart) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
   switch (g) {
     case 32: return launch_group_dot_t<32>(st, rows, cols, ws, lay, C, objpart);
     case 64: return launch_group_dot_t<64>(st, rows, cols, ws, lay, C, objpart);

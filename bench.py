@@ -10,7 +10,7 @@ state; then K sweeps from the host state are timed as one call bracketed by
 device synchronisation.  Per-stage durations come from HIP events that the
 library records on its own stream around each stage of each sweep.
 
-Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
+Prints one JSON line.  --gpus above 1 is refused: the path runs on one GPU.
 --copy-probe runs only a plain device copy of known size (used to calibrate
 the HBM byte counters of rocprofv3) and prints nothing else.
 """
@@ -43,7 +43,8 @@ def log(msg):
 
 
 def stage_work(cfg, rows, corr_blocks):
-    """Algorithmic FLOP of each stage for one sweep."""
+    """Algorithmic FLOP of each stage for one sweep (per row: residual product 2 d^2 as three
+    fp16 products, Gram (d^2 + d g)/2 MACs on two planes, Babai core 2 d g plus corrections)."""
     d, g = cfg.cols, cfg.group_size
     G = d // g
     return {
@@ -128,8 +129,8 @@ def main():
                     help="cache file (.npz) of the synthetic layer: loaded if present, else written")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: the refinement path of this build is single-GPU "
-              "(rows would shard across GPUs with no per-sweep exchange; not built here).",
+        print("bench.py runs on one GPU only: the refinement path is single-GPU "
+              "(rows would shard across GPUs with no per-sweep exchange; not implemented).",
               file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:

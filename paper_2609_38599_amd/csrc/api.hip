@@ -42,6 +42,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
+  L.rowflag = take(R);
   L.objpart = take(R * (nt > G ? nt : G) * sizeof(double));  // per-group sweep partials or 64-column slices
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));

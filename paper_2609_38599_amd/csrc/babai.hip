@@ -114,8 +114,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     const float* __restrict__ rdinv,
     const float* __restrict__ rdsq, uint8_t* __restrict__ codes,
     const float* __restrict__ scales, const uint8_t* __restrict__ active,
-    _Float16* __restrict__ dq, uint8_t* __restrict__ cand_out, uint8_t* __restrict__ dec_out,
-    Counters* __restrict__ cnt) {
+    _Float16* __restrict__ dq, uint8_t* __restrict__ rowflag, uint8_t* __restrict__ cand_out,
+    uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt) {
   constexpr int g = G_SIZE;
   constexpr int RT = 16;                 // rows per work-group
   constexpr int NT = g / 16;             // positions per lane in the back substitution
@@ -263,6 +263,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     ns = scales[(size_t)srow * G + i];
   };
   if (chain_wave) chain_prefetch(i0);
+  bool any_acc = false;  // chain role: this row accepted a change in the panel
 
   if (!chain_wave) {
     stage_rcol(i0, (i0 & 1) ? rc1_s : rc0_s);
@@ -328,6 +329,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
           if (cand_out != nullptr) cand_out[cbase + l] = (uint8_t)(do_row ? cs.qc[t] : cs.qold[t]);
         }
       }
+      any_acc |= accept;
       if (row_in && cj == 0) {
         if (dec_out != nullptr) {
           uint8_t dd = !row_act ? kDecStopped : (skip ? kDecSkip : (accept ? kDecAccept : kDecReject));
@@ -362,6 +364,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     }
     __syncthreads();  // u and R~ of group i + 1 ready
   }
+  if (chain_wave && row_in && cj == 0) rowflag[grow] = any_acc ? 1 : 0;
   if (tid == 0) {
     if (cnt_s[0]) atomicAdd(&cnt->accepted, (unsigned long long)cnt_s[0]);
     if (cnt_s[1]) atomicAdd(&cnt->changed, (unsigned long long)cnt_s[1]);
@@ -383,7 +386,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.mrow), (const float*)(ws + lay.rcol),
                      (const float*)(ws + lay.rdinv),
                      (const float*)(ws + lay.rdsq), codes, scales, active,
-                     (_Float16*)(ws + lay.dq), cand, decision, cnt);
+                     (_Float16*)(ws + lay.dq), (uint8_t*)(ws + lay.rowflag), cand, decision, cnt);
   return hipGetLastError();
 }
 

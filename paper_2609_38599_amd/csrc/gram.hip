@@ -104,16 +104,19 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
     }
   };
 
+  float outv[32];
+#pragma unroll
+  for (int q = 0; q < 32; ++q) outv[q] = 0.f;
   for (int side = 0; side < 2; ++side) {
     const int ga = side == 0 ? p : G - 1 - p;
     if (side == 1 && ga == p) break;
-    __syncthreads();
+    lds_barrier();
     fetch_codes(ga);
     store_codes(ca_s);
     fetch_codes(ga);     // block h = ga comes first
     fetch_h(ga, ga);
     for (int h = ga; h < G; ++h) {
-      __syncthreads();   // previous block's reads of ch_s are done
+      lds_barrier();   // previous block's reads of ch_s are done
       store_codes(ch_s);
       f16x8 cur[2][KS];
 #pragma unroll
@@ -125,18 +128,30 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
         fetch_codes(h + 1);
         fetch_h(ga, h + 1);
       }
-      __syncthreads();
+      lds_barrier();
       f32x16 acc[JB];
 #pragma unroll
       for (int b = 0; b < JB; ++b) acc[b] = f32x16{};
+      // Code fragments of k-slice ks + 1 are read while slice ks is on the
+      // matrix cores (LDS latency off the critical path).
+      f16x8 cf[2][JB];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
+      for (int b = 0; b < JB; ++b)
+        cf[0][b] = *(const f16x8*)(ch_s + (rbase + b * 32 + lm) * LDC + 8 * kh);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) {
+#pragma unroll
+          for (int b = 0; b < JB; ++b)
+            cf[(ks + 1) & 1][b] =
+                *(const f16x8*)(ch_s + (rbase + b * 32 + lm) * LDC + (ks + 1) * 16 + 8 * kh);
+        }
 #pragma unroll
         for (int b = 0; b < JB; ++b) {
-          const f16x8 cf = *(const f16x8*)(ch_s + (rbase + b * 32 + lm) * LDC + ks * 16 + 8 * kh);
-          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[0][ks], cf, acc[b], 0, 0, 0);
-          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[1][ks], cf, acc[b], 0, 0, 0);
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[0][ks], cf[ks & 1][b], acc[b], 0, 0, 0);
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[1][ks], cf[ks & 1][b], acc[b], 0, 0, 0);
         }
+      }
       // acc element v of lane l: T(a = ab*32 + 8*(v/4) + 4*kh + v%4, row = rbase + b*32 + l%32).
 #pragma unroll
       for (int b = 0; b < JB; ++b) {
@@ -153,14 +168,25 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
         d += __shfl_xor(d, 32);
         if (kh == 0) red[ab * RT + rr] = d;
       }
-      __syncthreads();
+      lds_barrier();
       {
+        // Thread tid owns row r0 + tid: keep its entries (ga, h) for up to 32
+        // consecutive h in registers and store them as one contiguous run.
         const int rr = tid;  // RT == 256 == blockDim.x
         double s = 0.0;
 #pragma unroll
         for (int a = 0; a < NAB; ++a) s += red[a * RT + rr];
+        const float val = (float)(s * (double)hinv);
+        const int j = (h - ga) & 31;
+#pragma unroll
+        for (int q = 0; q < 32; ++q) outv[q] = q == j ? val : outv[q];
         const int row = r0 + rr;
-        if (row < rows) gram[((size_t)row * G + ga) * G + h] = (float)(s * (double)hinv);
+        if ((j == 31 || h == G - 1) && row < rows) {
+          float* dst = gram + ((size_t)row * G + ga) * G + (h - j);
+#pragma unroll
+          for (int q = 0; q < 32; ++q)
+            if (q <= j) dst[q] = outv[q];
+        }
       }
     }
   }

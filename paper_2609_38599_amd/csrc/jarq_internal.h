@@ -74,6 +74,7 @@ struct Layout {
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
   size_t p;         // [rows][cols] f32: (W - What) H
   size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
+  size_t rowflag;   // [rows] u8: the row accepted a change in the last panel of the code update
   size_t objpart;   // [rows][ceil(cols/64)] f64: partial row objectives
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64
@@ -132,7 +133,17 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
                         const float* scales, const int32_t* zeros, const uint8_t* active,
                         uint8_t* cand, uint8_t* decision, Counters* cnt);
 
-// Groups per panel of the code update.
+// Work-group barrier for LDS only: waits for this wave's LDS operations,
+// not for its outstanding global loads (a __syncthreads would, which drains
+// any prefetch in flight).  The empty asm statements keep the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maximum
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Groups per panel of the code update (512 columns, at most 16 groups).
 constexpr int kMaxPanelGroups = 16;
 constexpr int panel_groups_of(int g) { return 512 / g < kMaxPanelGroups ? 512 / g : kMaxPanelGroups; }

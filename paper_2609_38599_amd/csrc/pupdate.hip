@@ -53,7 +53,8 @@ __device__ __forceinline__ void wait_vm_and_barrier() {
 __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     int rows, int cols, int g, int c0, int c1, const _Float16* __restrict__ dq,
     const _Float16* __restrict__ Mh, const _Float16* __restrict__ Ml,
-    const float* __restrict__ bcol_inv, const float* __restrict__ scales, float* __restrict__ P) {
+    const float* __restrict__ bcol_inv, const float* __restrict__ scales,
+    const uint8_t* __restrict__ rowflag, float* __restrict__ P) {
   // Three stages in three distinct arrays: the loads of steps k + 1 and k + 2
   // fly while step k computes.
   __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
@@ -71,11 +72,69 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   const int h0 = c0 / g;
   const int ng = (c1 - c0) / g;
 
+  // Only rows that accepted a change in the panel (rowflag) need an update.
+  // Every work-group forms the same compacted list (ascending rows) by a
+  // prefix sum over the flags and takes positions m0 .. m0 + BM - 1 of it;
+  // work-groups past its end have nothing to do.
+  // Scratch for the list lives in the third stage, first loaded after set-up.
+  int* pre_s = (int*)buf2;  // 256
+  int* rl_s = pre_s + 256;  // BM
+  // Flags are 0 or 1; thread t reads words t * wpt .. of the flag array (four
+  // rows a word; the workspace region is padded to 256 bytes, and rows past
+  // the end are masked).
+  const int nw = (rows + 3) / 4;
+  const int wpt = (nw + 255) / 256;  // words per thread
+  const uint32_t* fw = (const uint32_t*)rowflag;
+  auto word = [&](int w) {
+    if (w >= nw) return 0u;
+    const uint32_t x = fw[w] & 0x01010101u;
+    const int valid = rows - 4 * w;  // rows of this word inside the layer
+    return valid >= 4 ? x : (x & ((1u << (8 * valid)) - 1u));
+  };
+  int cntl = 0;
+#pragma unroll 4
+  for (int q = 0; q < wpt; ++q) cntl += __builtin_popcount(word(tid * wpt + q));
+  pre_s[tid] = cntl;
+  __syncthreads();
+  for (int w = 1; w < 256; w <<= 1) {  // inclusive scan (Hillis-Steele)
+    const int v = tid >= w ? pre_s[tid - w] : 0;
+    __syncthreads();
+    pre_s[tid] += v;
+    __syncthreads();
+  }
+  const int total = pre_s[255];
+  if (m0 >= total) return;  // uniform across the work-group
+  {
+    int pos = pre_s[tid] - cntl;  // exclusive prefix
+    for (int q = 0; q < wpt; ++q) {
+      const int w = tid * wpt + q;
+      const uint32_t x = word(w);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        if ((x >> (8 * b)) & 1u) {
+          if (pos >= m0 && pos < m0 + BM) rl_s[pos - m0] = 4 * w + b;
+          ++pos;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int nvalid = min(BM, total - m0);
+  // Tile row t is row rl_s[t] for t < nvalid; later tile rows repeat a valid row
+  // and are never stored.
+  auto row_of = [&](int t) { return rl_s[t < nvalid ? t : 0]; };
+
   for (int e = tid; e < BM * ng; e += 256) {
     const int r = e / ng, h = e % ng;
-    const int gr = m0 + r;
-    sc_s[r][h] = scales[(size_t)(gr < rows ? gr : 0) * G + h0 + h];  // rows past the edge: never stored
+    sc_s[r][h] = scales[(size_t)row_of(r) * G + h0 + h];
   }
+  // Rows of this lane's accumulator elements (element v of a 32x32 block is
+  // row 8 (v / 4) + 4 (lane / 32) + v % 4), kept for the epilogue.
+  int erow[2][16];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) erow[a][v] = row_of(wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4));
 
 
   // Piece j (1 KB = 16 rows of one plane tile) of a stage goes to wave j % 4;
@@ -90,8 +149,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     const int r = 16 * (j % 8) + (lane >> 2);
     const int chunk = (lane & 3) ^ swz(r);
     if (j < 8) {
-      const int gm = m0 + r;
-      off[q] = (unsigned)(gm < rows ? gm : 0) * (unsigned)cols + (unsigned)(chunk * 8);
+      off[q] = (unsigned)row_of(r) * (unsigned)cols + (unsigned)(chunk * 8);
       base[q] = dq;
     } else {
       const int gn = n0 + r;
@@ -193,10 +251,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     for (int b = 0; b < 2; ++b) {
       const int col = min(n0 + wn * 64 + b * 32 + lm, cols - 1);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = min(m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4), rows - 1);
-        pold[a][b][v] = P[(size_t)row * cols + col];
-      }
+      for (int v = 0; v < 16; ++v) pold[a][b][v] = P[(size_t)erow[a][v] * cols + col];
     }
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -206,8 +261,9 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
       const float cs = bcol_inv[min(col, cols - 1)];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
-        if (row < rows && col < cols) P[(size_t)row * cols + col] = pold[a][b][v] - acc[a][b][v] * cs;
+        const int t = wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
+        if (t < nvalid && col < cols)
+          P[(size_t)erow[a][v] * cols + col] = pold[a][b][v] - acc[a][b][v] * cs;
       }
     }
 }
@@ -221,7 +277,8 @@ hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0
   dim3 grid((cols - c1 + BN - 1) / BN, (rows + BM - 1) / BM);
   hipLaunchKernelGGL(panel_update_kernel, grid, dim3(256), 0, st, rows, cols, g, c0, c1,
                      (const _Float16*)(ws + lay.dq), (const _Float16*)(ws + lay.mhi),
-                     (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow), scales, P);
+                     (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow), scales,
+                     (const uint8_t*)(ws + lay.rowflag), P);
   return hipGetLastError();
 }
 

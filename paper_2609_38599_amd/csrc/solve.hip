@@ -33,8 +33,11 @@ __device__ __forceinline__ double wave_max(double x) {
   return x;
 }
 
-// In-place Cholesky of the lower triangle of A (G x G, leading dimension LD).
-// Returns the smallest pivot before the square root (<= 0 or NaN on failure).
+// In-place Cholesky of the lower triangle of A (G x G, leading dimension LD),
+// one wavefront.  Step k scales column k, then the trailing triangle's
+// elements are spread over the lanes (independent updates, no dependent chain
+// per lane).  Returns the smallest pivot before the square root (<= 0 or NaN
+// on failure).
 __device__ double chol_lower(double* A, int G, int LD, int lane) {
   double minpiv = INFINITY;
   for (int k = 0; k < G; ++k) {
@@ -44,11 +47,18 @@ __device__ double chol_lower(double* A, int G, int LD, int lane) {
     const double d = sqrt(piv);
     __syncthreads();
     if (lane == 0) A[k * LD + k] = d;
-    for (int i = k + 1 + lane; i < G; i += 64) A[i * LD + k] /= d;
+    const double inv = 1.0 / d;
+    for (int i = k + 1 + lane; i < G; i += 64) A[i * LD + k] *= inv;
     __syncthreads();
-    for (int i = k + 1 + lane; i < G; i += 64) {
-      const double lik = A[i * LD + k];
-      for (int j = k + 1; j <= i; ++j) A[i * LD + j] -= lik * A[j * LD + k];
+    const int n = G - k - 1;            // trailing block rows k+1 .. G-1
+    const int ne = n * (n + 1) / 2;     // its lower triangle, row by row
+    for (int e = lane; e < ne; e += 64) {
+      int ii = (int)((sqrtf(8.f * (float)e + 1.f) - 1.f) * 0.5f);
+      if ((ii + 1) * (ii + 2) / 2 <= e) ++ii;  // guard the float estimate
+      if (ii * (ii + 1) / 2 > e) --ii;
+      const int jj = e - ii * (ii + 1) / 2;
+      const int i = k + 1 + ii, j = k + 1 + jj;
+      A[i * LD + j] -= A[i * LD + k] * A[j * LD + k];
     }
     __syncthreads();
   }
@@ -78,31 +88,66 @@ __global__ __launch_bounds__(64) void solve_kernel(int rows, int cols, int g,
   const float* gr = gram + (size_t)row * G * G;
   bool finite = true;
   double dmax = 0.0;
-  for (int e = lane; e < G * G; e += 64) {
-    const int i = e / G, h = e % G;
-    const float v = (h >= i) ? gr[i * G + h] : gr[h * G + i];
-    finite &= isfinite(v);
-    A[i * LD + h] = (double)v;
-    if (i == h) {
-      diag[i] = (double)v;
-      dmax = fmax(dmax, (double)v);
-    }
-  }
-  // r_a = sum over the group of c * (W H)
-  for (int a = lane; a < G; a += 64) {
-    const int z = zeros[(size_t)row * G + a];
-    const float* whp = wh + (size_t)row * cols + (size_t)a * g;
-    const uint8_t* qp = codes + (size_t)row * cols + (size_t)a * g;
-    double s = 0.0;
-    for (int c = 0; c < g; c += 4) {
-      const f32x4 w4 = *(const f32x4*)(whp + c);
-      const uint32_t q4 = *(const uint32_t*)(qp + c);
+  // Only the upper triangle of the Gram matrix is stored: entry (i, h) is read
+  // at (min, max).  Loads go in batches of 16 per lane into registers first
+  // (unconditional, from clamped indices), then to LDS.
+  const int GG = G * G;
+  for (int base = 0; base < GG; base += 64 * 16) {
+    float vv[16];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) s += (double)((int)((q4 >> (8 * i)) & 0xffu) - z) * (double)w4[i];
+    for (int q = 0; q < 16; ++q) {
+      const int e = min(base + lane + 64 * q, GG - 1);
+      const int i = e / G, h = e % G;
+      vv[q] = gr[(i < h ? i : h) * G + (i < h ? h : i)];
     }
-    r[a] = s;
-    finite &= isfinite(s);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int e = base + lane + 64 * q;
+      if (e < GG) {
+        const int i = e / G, h = e % G;
+        finite &= isfinite(vv[q]);
+        A[i * LD + h] = (double)vv[q];
+        if (i == h) {
+          diag[i] = (double)vv[q];
+          dmax = fmax(dmax, (double)vv[q]);
+        }
+      }
+    }
   }
+  // r_a = sum over group a of c * (W H): lane l takes 4 consecutive columns of
+  // every 256 (coalesced), the g / 4 lanes that share a group combine their
+  // sums, and one of them adds the result into r.  Loads of 8 chunks are
+  // issued together (unconditional, clamped), then reduced.
+  for (int a = lane; a < G; a += 64) r[a] = 0.0;
+  __syncthreads();
+  const int lpg = g / 4;  // lanes per group in one 256-column chunk
+  const float* whr = wh + (size_t)row * cols;
+  const uint8_t* qr = codes + (size_t)row * cols;
+  for (int c00 = 0; c00 < cols; c00 += 256 * 8) {
+    f32x4 w4[8];
+    uint32_t q4[8];
+    int zz[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int c = min(c00 + 256 * t + 4 * lane, cols - 4);  // cols is a multiple of 32
+      w4[t] = *(const f32x4*)(whr + c);
+      q4[t] = *(const uint32_t*)(qr + c);
+      zz[t] = zeros[(size_t)row * G + c / g];
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int c = c00 + 256 * t + 4 * lane;
+      double sum = 0.0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        sum = fma((double)((int)((q4[t] >> (8 * i)) & 0xffu) - zz[t]), (double)w4[t][i], sum);
+      if (c >= cols) sum = 0.0;
+      for (int off = lpg / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+      if (c < cols && (lane % lpg) == 0) r[c / g] += sum;  // one writer per group
+    }
+  }
+  __syncthreads();
+  for (int a = lane; a < G; a += 64) finite &= isfinite(r[a]);
   const bool all_finite = __all(finite);
   dmax = wave_max(dmax);
   __syncthreads();

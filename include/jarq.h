@@ -30,7 +30,7 @@
  *     device memory and keeps no global state.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     All device work is enqueued on it in order.
- *   - W, H and scales must be 16-byte aligned, codes 4-byte aligned,
+ *   - W, H, scales and codes must be 16-byte aligned,
  *     the workspace 256-byte aligned.
  *   - Argument errors return JARQ_EINVAL before anything is enqueued; the
  *     outputs are then untouched.
@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 2
+#define JARQ_ABI_VERSION 3
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
  * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
  * 3 residual product U = E M^T, 4 row objectives and stopping test,

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libjarq.so")
 MAX_RECORDED_SWEEPS = 64
 NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
 STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
-ABI_VERSION = 2
+ABI_VERSION = 3
 JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 

@@ -301,7 +301,7 @@ jarq_status jarq_prepare(const jarq_params* p, const float* W, const float* H, v
 jarq_status jarq_scale_step(const jarq_params* p, const float* H, const uint8_t* codes,
                             float* scales, const int32_t* zeros, void* workspace,
                             size_t workspace_bytes, void* stream) {
-  if (!valid_params(p) || !aligned(H, 16) || !aligned(codes, 4) || !aligned(scales, 16) ||
+  if (!valid_params(p) || !aligned(H, 16) || !aligned(codes, 16) || !aligned(scales, 16) ||
       !aligned(zeros, 4))
     return JARQ_EINVAL;
   jarq_status s = check_ws(p, workspace, workspace_bytes);
@@ -317,7 +317,7 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
                            const float* scales, const int32_t* zeros, void* workspace,
                            size_t workspace_bytes, void* stream, uint8_t* cand,
                            uint8_t* decision) {
-  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 16) ||
       !aligned(scales, 16) || !aligned(zeros, 4))
     return JARQ_EINVAL;
   jarq_status s = check_ws(p, workspace, workspace_bytes);
@@ -335,7 +335,7 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
 jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
                         float* scales, const int32_t* zeros, void* workspace,
                         size_t workspace_bytes, void* stream, jarq_stats* stats) {
-  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 16) ||
       !aligned(scales, 16) || !aligned(zeros, 4))
     return JARQ_EINVAL;
   jarq_status s = check_ws(p, workspace, workspace_bytes);
@@ -346,7 +346,7 @@ jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H, ui
 jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
                         float* scales, const int32_t* zeros, void* workspace,
                         size_t workspace_bytes, void* stream, jarq_stats* stats) {
-  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 16) ||
       !aligned(scales, 16) || !aligned(zeros, 4))
     return JARQ_EINVAL;
   jarq_status s = check_ws(p, workspace, workspace_bytes);
@@ -375,7 +375,7 @@ jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,
                            const uint8_t* codes, const float* scales, const int32_t* zeros,
                            void* workspace, size_t workspace_bytes, void* stream,
                            double* row_objective) {
-  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 4) ||
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 16) ||
       !aligned(scales, 16) || !aligned(zeros, 4) || !aligned(row_objective, 8))
     return JARQ_EINVAL;
   jarq_status s = check_ws(p, workspace, workspace_bytes);

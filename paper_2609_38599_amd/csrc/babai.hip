@@ -15,27 +15,44 @@
 // a_l = (R_i d)_l / R_i(l,l), whose terms vanish exactly where no change
 // reaches, so its rounding scales with the change rather than with ||u||^2.
 //
-// One 256-thread work-group owns 16 rows and visits the groups of one panel
-// [i0, i1) in order; P already holds the changes of earlier panels (folded in
-// by pupdate.hip).  Per group:
-//   1. correction: he = P_i - sum_{i0<=h<i} s_h (dq_h H_hi), dq_h the accepted
-//      code changes of earlier groups of the panel (exact in fp16, zero elsewhere).  H is read as its two fp16 planes, so each block
-//      is two v_mfma_f32_16x16x32_f16 products per k-slice, scaled by s_h per
-//      row.  Blocks in which no row of the tile accepted are skipped.
-//   2. u = he L_i^{-T} / s_i (L_i^{-1} = R_i^{-T}) on fp32 matrix cores.
-//   3. back substitution: 16 lanes per row, lane j owns positions j + 16 t and
-//      keeps base_l = q_l + u_l / R(l,l) and acc_l = sum_{m>l} R(l,m) d_m / R(l,l)
-//      (after the last step acc_l = a_l above);
-//      at step l every lane evaluates its candidate, the owner's change d_l is
-//      broadcast within the row (DPP row broadcast) and each lane folds
-//      R(m, l) / R(m, m) d_l into its own acc_m.  No branches, no LDS round trip
-//      on the dependency chain.
-//   4. accept test per row, in-place code update, dq_i, trace and counters.
+// One 512-thread work-group owns 16 rows and visits the groups of one panel
+// [i0, i1) in order; P holds U = E M^T (M = blockdiag(L_i^{-1}) H) with the
+// changes of earlier panels already folded in (pupdate.hip), so its group-i
+// columns are L_i^{-1} (H e)_i for codes as they were when the panel began.
+// Waves 0-3 run the back substitution of group i while waves 4-7 prepare
+// group i + 1:
+//   correction: u_{i+1} s_{i+1} = P_{i+1} - sum_{i0<=h<=i} s_h dq_h M(i+1, h)^T,
+//     dq_h the accepted code changes of the panel's earlier groups (exact in
+//     fp16, zero elsewhere) and the block M(i+1, h) = L_{i+1}^{-1} H_{i+1,h}
+//     read as two fp16 terms: two v_mfma_f32_16x16x32_f16 per k-slice.  Blocks
+//     in which no row of the tile accepted are skipped; the block of group i
+//     itself waits for its decision, the others are applied meanwhile.
+//   R~ = R_{i+1} with unit diagonal, staged into LDS by direct loads.
+// Back substitution: 16 lanes per row, lane j owns positions j + 16 t and keeps
+// y_l = u_l / R(l,l) - sum of R~(l, m) d_m over the positions m decided so far;
+// at step l the owner's change d_l = clip(rint(y_l)) is broadcast within the
+// row (DPP row broadcast) and every lane subtracts R~(m, l) d_l from its y_m.
+// After the last step u_l / R(l,l) - y_l = a_l above.  No branches and no LDS
+// round trip on the dependency chain.  The accept test then reduces over the
+// row's lanes with DPP.  Decisions stay in LDS: codes and dq of the panel are
+// written once, with 16-byte stores, after its last group.
 #include "jarq_internal.h"
 
 namespace jarq {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Load / store at base + byte offset.  With a wave-uniform base and a 32-bit
+// offset the access takes the scalar-base form (SGPR pair + one offset VGPR):
+// no 64-bit per-lane addresses to keep live.
+template <typename T>
+__device__ __forceinline__ T ld_at(const T* base, uint32_t byte_off) {
+  return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+template <typename T>
+__device__ __forceinline__ void st_at(T* base, uint32_t byte_off, T v) {
+  *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + byte_off) = v;
+}
 
 // One 16-byte direct global -> LDS load per lane (lane L writes lds + 16 L
 // bytes; lds is the same for the whole wave).
@@ -44,66 +61,110 @@ __device__ __forceinline__ void dma16(const float* src, float* lds) {
                                    (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
+// Per lane and position l = j + 16 t of the row: y = u~_l - sum_m R~(l, m) d_m
+// over the positions m already decided (R~ = R_i with unit diagonal, so the
+// position's own change is in the sum once it is decided), the code change d
+// taken at l, and the bounds -q_l, 2^b - 1 - q_l of that change.
 template <int NT>
 struct ChainState {
-  float base[NT];
-  float acc[NT];
-  float qold[NT];
-  float qc[NT];
+  float y[NT];
+  float d[NT];
+  float lo[NT];
+  float hi[NT];
 };
 
-template <int JL>
-__device__ __forceinline__ float row_bcast(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + JL, 0xf, 0xf, false));
+// Sum over each row of 16 lanes, in every lane of the row (xor 1 and 2 within
+// quads, then the half-row and row mirrors); every lane adds the same two
+// operands in each round, so all lanes hold the same bits.
+__device__ __forceinline__ float row_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false));
+  return v;
+}
+__device__ __forceinline__ int row_sum(int v) {
+  v += __builtin_amdgcn_mov_dpp(v, 0xB1, 0xf, 0xf, false);
+  v += __builtin_amdgcn_mov_dpp(v, 0x4E, 0xf, 0xf, false);
+  v += __builtin_amdgcn_mov_dpp(v, 0x141, 0xf, 0xf, false);
+  v += __builtin_amdgcn_mov_dpp(v, 0x140, 0xf, 0xf, false);
+  return v;
 }
 
-// R~ column l as seen by lane j: the NT values R~(j + 16 t, l), t < NT.  Only
-// t <= l / 16 can be nonzero.
+// Compile-time loop: Unroll<K, N>::run(f) calls f(IntC<k>) for k = K .. N - 1.
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+template <int K, int N>
+struct Unroll {
+  template <typename F>
+  static __device__ __forceinline__ void run(F&& f) {
+    if constexpr (K < N) {
+      f(IntC<K>{});
+      Unroll<K + 1, N>::run(f);
+    }
+  }
+};
+
+// Value of lane JL of each row of 16 lanes, in every lane of that row.
+template <int JL>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + JL, 0xf, 0xf, false));
+}
+
+// R~ column l as seen by lane j: the NT values R~(j + 16 t, l), t < NT, in
+// chunks of W = min(4, NT) (the layout of the staged columns:
+// [l][chunk][lane][W], so the 16 lanes of a row read consecutive bytes).
+// Only t <= l / 16 can be nonzero and only those are read, one float at a
+// time (adjacent ones merge into one wide access; a wide access with unused
+// parts would let the compiler reuse their registers while it is in flight).
 template <int NT>
 struct RCol {
-  f32x4 v[(NT + 3) / 4];
+  static constexpr int W = NT < 4 ? NT : 4;
+  float v[NT];
 };
 
 template <int L, int NT>
 __device__ __forceinline__ RCol<NT> load_rcol(const float* __restrict__ rc, int cj) {
+  constexpr int W = RCol<NT>::W;
   RCol<NT> r;
-  if (L >= 0) {
-    const float* p = rc + (L * 16 + cj) * NT;
+  if constexpr (L >= 0) {
 #pragma unroll
-    for (int c = 0; c * 4 <= (L >> 4); ++c) r.v[c] = *(const f32x4*)(p + 4 * c);
+    for (int t = 0; t <= (L >> 4); ++t)
+      r.v[t] = rc[((L * (NT / W) + t / W) * 16 + cj) * W + t % W];
   }
   return r;
 }
 
-// One step of the back substitution; the R~ columns of the next two steps are
-// already in flight (loaded two steps ahead so LDS latency stays off the chain).
+// One step of the back substitution; the R~ columns of the next four steps are
+// in flight (loaded ahead so that LDS latency stays off the chain).  The change
+// at position L is the rounded y clipped to the code range (clip(round(q + y))
+// - q, up to the rounding of exact ties).
 template <int L, int NT>
 struct ChainStep {
   static __device__ __forceinline__ void run(ChainState<NT>& s, const float* __restrict__ rc,
-                                             int cj, float qmax, const RCol<NT>& cur,
-                                             const RCol<NT>& nxt) {
+                                             int cj, const RCol<NT>& c0, const RCol<NT>& c1,
+                                             const RCol<NT>& c2, const RCol<NT>& c3) {
     constexpr int TL = L >> 4;
     constexpr int JL = L & 15;
-    const RCol<NT> nn = load_rcol<L - 2, NT>(rc, cj);
-    const float xv = s.base[TL] - s.acc[TL];
-    const float qv = fminf(fmaxf(rintf(xv), 0.f), qmax);
-    s.qc[TL] = cj == JL ? qv : s.qc[TL];
-    const float db = row_bcast<JL>(qv - s.qold[TL]);
+    const RCol<NT> c4 = load_rcol<L - 4, NT>(rc, cj);
+    const float dv = __builtin_amdgcn_fmed3f(rintf(s.y[TL]), s.lo[TL], s.hi[TL]);
+    s.d[TL] = cj == JL ? dv : s.d[TL];
+    const float db = row_bcast<JL>(dv);
 #pragma unroll
-    for (int c = 0; c * 4 <= TL; ++c)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (4 * c + q <= TL) s.acc[4 * c + q] = fmaf(cur.v[c][q], db, s.acc[4 * c + q]);
+    for (int t = 0; t <= TL; ++t) s.y[t] = fmaf(-c0.v[t], db, s.y[t]);
     // Keep the scheduler from hoisting far-away work (register pressure).
     if (JL == 0) __builtin_amdgcn_sched_barrier(0);
-    ChainStep<L - 1, NT>::run(s, rc, cj, qmax, nxt, nn);
+    ChainStep<L - 1, NT>::run(s, rc, cj, c1, c2, c3, c4);
   }
 };
 
 template <int NT>
 struct ChainStep<-1, NT> {
   static __device__ __forceinline__ void run(ChainState<NT>&, const float* __restrict__, int,
-                                             float, const RCol<NT>&, const RCol<NT>&) {}
+                                             const RCol<NT>&, const RCol<NT>&, const RCol<NT>&,
+                                             const RCol<NT>&) {}
 };
 
 template <int G_SIZE>
@@ -161,6 +222,17 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   if (tid < PG) tacc_s[tid] = 0;
   if (tid < 4) cnt_s[tid] = 0;
 
+  // Bases of this work-group's 16 rows (wave-uniform); offsets from them fit
+  // in 32 bits (16 rows of at most 2^26 columns).
+  const float* __restrict__ P_t = P + (size_t)r0 * cols;
+  uint8_t* __restrict__ codes_t = codes + (size_t)r0 * cols;
+  _Float16* __restrict__ dq_t = dq + (size_t)r0 * cols;
+  const float* __restrict__ scales_t = scales + (size_t)r0 * G;
+  // Local row of a lane, or row 0 past the edge (loads stay unconditional;
+  // such values are never used).
+  auto lrow = [&](int lr) { return (uint32_t)(r0 + lr < rows ? lr : 0); };
+  const uint32_t ucols = (uint32_t)cols;
+
   // ---- preparation: u s = L^{-1} (H e) of the next group, this wave's columns ----
   f32x4 uacc[BPW];
   // R~ of group i into dst: 1 KB pieces, piece j by prep wave j % 4 (lane L
@@ -171,7 +243,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 #pragma unroll
     for (int q = 0; q < RC_PER_THREAD; ++q) {
       const int j = pw + 4 * q;
-      dma16(src + j * 256 + lane * 4, dst + j * 256);
+      dma16((const float*)((const char*)src + (uint32_t)((j * 256 + lane * 4) * 4)), dst + j * 256);
     }
   };
   // u of group i as the residual product left it (U = E M^T, changes of
@@ -181,11 +253,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     for (int b = 0; b < BPW; ++b) {
       const int n = (pw * BPW + b) * 16 + mr;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int gr = r0 + 4 * kq + v;
-        // rows past the edge read row 0 (unconditional load); never used
-        uacc[b][v] = P[(size_t)(gr < rows ? gr : 0) * cols + (size_t)i * g + n];
-      }
+      for (int v = 0; v < 4; ++v)
+        uacc[b][v] = ld_at(P_t, (lrow(4 * kq + v) * ucols + (uint32_t)(i * g + n)) * 4u);
     }
   };
   // Fragments of M(i-block, h-block) = L_i^{-1} H_ih for this wave's columns,
@@ -196,27 +265,33 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     float cs[BPW];
   };
   auto load_t = [&](int i, int h, TFrag& f) {
+    // rows i g .. i g + g - 1 of M (uniform bases), this lane's row n within
+    const _Float16* mh_i = Mh + (size_t)i * g * cols;
+    const _Float16* ml_i = Ml + (size_t)i * g * cols;
 #pragma unroll
     for (int b = 0; b < BPW; ++b) {
-      const int n = i * g + (pw * BPW + b) * 16 + mr;
-      const size_t trow = (size_t)n * cols + (size_t)h * g + 8 * kq;
+      const int n = (pw * BPW + b) * 16 + mr;
+      const uint32_t trow = ((uint32_t)n * ucols + (uint32_t)(h * g + 8 * kq)) * 2u;
 #pragma unroll
       for (int kc = 0; kc < KS; ++kc) {
-        f.bh[b][kc] = *(const f16x8*)(Mh + trow + kc * 32);
-        f.bl[b][kc] = *(const f16x8*)(Ml + trow + kc * 32);
+        f.bh[b][kc] = ld_at((const f16x8*)mh_i, trow + kc * 64);
+        f.bl[b][kc] = ld_at((const f16x8*)ml_i, trow + kc * 64);
       }
-      f.cs[b] = mrow_inv[n];
+      f.cs[b] = ld_at(mrow_inv + i * g, (uint32_t)(n * 4));
     }
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int gr = r0 + 4 * kq + v;
-      f.sh[v] = scales[(size_t)(gr < rows ? gr : 0) * G + h];
-    }
+    for (int v = 0; v < 4; ++v)
+      f.sh[v] = ld_at(scales_t, (lrow(4 * kq + v) * (uint32_t)G + (uint32_t)h) * 4u);
   };
-  // uacc -= s_h dq_h M(i-block, h-block)^T (dq_h exact in fp16, M as two fp16 terms).
-  auto apply_t = [&](int h, const TFrag& f) {
-    if (tacc_s[h - i0] == 0) return;
-    if (ptid == 0) cnt_s[3] += 1;
+  // uacc -= s_h dq_h M(i-block, h-block)^T (dq_h exact in fp16, M as two fp16
+  // terms).  dq_h is zero in every row of the tile unless one of them accepted
+  // group h: then the product can be skipped (may_skip) or computed anyway,
+  // which keeps the fragment loads ahead of their use (a use under a branch
+  // drags the loads into it).
+  auto apply_t = [&](int h, const TFrag& f, bool may_skip) {
+    const bool any = tacc_s[h - i0] != 0;
+    if (may_skip && !any) return;
+    if (ptid == 0 && any) cnt_s[3] += 1;
     f16x8 a[KS];
 #pragma unroll
     for (int kc = 0; kc < KS; ++kc)
@@ -250,84 +325,78 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   // them waits for its data here; row_in is applied where they are used.
   uint32_t nq[NT];
   float nrdinv[NT], nrdsq[NT], ns = 0.f;
-  const int srow = row_in ? grow : 0;
+  const uint32_t srow = lrow(crow);
   auto chain_prefetch = [&](int i) {
-    const size_t cb = (size_t)srow * cols + (size_t)i * g;
+    const uint32_t cb = srow * ucols + (uint32_t)(i * g + cj);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const int l = cj + 16 * t;
-      nq[t] = codes[cb + l];
-      nrdinv[t] = rdinv[(size_t)i * g + l];
-      nrdsq[t] = rdsq[(size_t)i * g + l];
+      nq[t] = ld_at(codes_t, cb + 16 * t);
+      nrdinv[t] = ld_at(rdinv + i * g, (uint32_t)((cj + 16 * t) * 4));
+      nrdsq[t] = ld_at(rdsq + i * g, (uint32_t)((cj + 16 * t) * 4));
     }
-    ns = scales[(size_t)srow * G + i];
+    ns = ld_at(scales_t, (srow * (uint32_t)G + (uint32_t)i) * 4u);
   };
-  if (chain_wave) chain_prefetch(i0);
-  bool any_acc = false;  // chain role: this row accepted a change in the panel
-
-  if (!chain_wave) {
-    stage_rcol(i0, (i0 & 1) ? rc1_s : rc0_s);
-    if (prep_live) {
-      u_from_p(i0);
-      write_u();
-    }
-  }
-  __syncthreads();
-
-  for (int i = i0; i < i1; ++i) {
-    const bool has_next = i + 1 < i1;
-    TFrag tnext;
-    if (chain_wave) {
+  // The two roles run separate loops with the same barriers (two per group),
+  // so neither role's loop-carried registers are live in the other's code.
+  // Barriers inside the loops are on LDS only: global loads stay in flight
+  // across them.
+  if (chain_wave) {
+    chain_prefetch(i0);
+    bool any_acc = false;  // this row accepted a change in the panel
+    __syncthreads();       // u and R~ of group i0 staged
+    for (int i = i0; i < i1; ++i) {
       // ---- back substitution of group i, 16 lanes per row ----
+      const bool has_next = i + 1 < i1;
       const float* rc_i = (i & 1) ? rc1_s : rc0_s;
       const float s = row_in ? ns : 0.f;
-      float rdsq_i[NT];
+      float rdsq_i[NT], qold[NT];
       ChainState<NT> cs;
       float ut[NT];
       const bool skip = !(fabsf(s) > kFp32Eps);
       const bool do_row = row_act && !skip;
       const float inv_s = do_row ? 1.f / s : 0.f;
-      const size_t cbase = (size_t)grow * cols + (size_t)i * g;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         const int l = cj + 16 * t;
         ut[t] = u_s[crow * LDH + l] * inv_s * nrdinv[t];
         rdsq_i[t] = nrdsq[t];
         const float q = row_in ? (float)nq[t] : 0.f;
-        cs.qold[t] = q;
-        cs.qc[t] = q;
-        cs.base[t] = q + ut[t];
-        cs.acc[t] = 0.f;
+        qold[t] = q;
+        cs.y[t] = ut[t];
+        cs.d[t] = 0.f;
+        cs.lo[t] = -q;
+        cs.hi[t] = qmax - q;
       }
       if (has_next) chain_prefetch(i + 1);
-      ChainStep<g - 1, NT>::run(cs, rc_i, cj, qmax, load_rcol<g - 1, NT>(rc_i, cj),
-                                load_rcol<g - 2, NT>(rc_i, cj));
-      float dF = 0.f;  // change of F divided by s_i^2
+      ChainStep<g - 1, NT>::run(cs, rc_i, cj, load_rcol<g - 1, NT>(rc_i, cj),
+                                load_rcol<g - 2, NT>(rc_i, cj), load_rcol<g - 3, NT>(rc_i, cj),
+                                load_rcol<g - 4, NT>(rc_i, cj));
+      // a_l = sum_{m >= l} R~(l, m) d_m = u~_l - y_l; the change of F divided
+      // by s_i^2 is sum_l R(l, l)^2 a_l (a_l - 2 u~_l).
+      float dF = 0.f;
       int changed = 0;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const float a = cs.acc[t];
+        const float a = ut[t] - cs.y[t];
         dF = fmaf(rdsq_i[t] * a, a - 2.f * ut[t], dF);
-        changed += cs.qc[t] != cs.qold[t];
+        changed += cs.d[t] != 0.f;
       }
-#pragma unroll
-      for (int off = 8; off >= 1; off >>= 1) {
-        dF += __shfl_xor(dF, off);
-        changed += __shfl_xor(changed, off);
-      }
+      dF = row_sum(dF);
+      changed = row_sum(changed);
       // A proposal equal to the current codes changes F by exactly 0, which the
-      // strict test rejects.
+      // strict test rejects; NaN changes (non-finite u) give a NaN dF.
       const bool accept = do_row && changed > 0 && isfinite(dF) && (dF < 0.f);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         const int l = cj + 16 * t;
-        const _Float16 d = accept ? (_Float16)(cs.qc[t] - cs.qold[t]) : (_Float16)0.f;
-        dqp_s[crow * PW + (i - i0) * g + l] = d;
-        if (row_in) {
-          if (accept) codes[cbase + l] = (uint8_t)cs.qc[t];
-          dq[cbase + l] = d;
-          if (cand_out != nullptr) cand_out[cbase + l] = (uint8_t)(do_row ? cs.qc[t] : cs.qold[t]);
-        }
+        dqp_s[crow * PW + (i - i0) * g + l] = accept ? (_Float16)cs.d[t] : (_Float16)0.f;
+      }
+      if (cand_out != nullptr && row_in) {
+        const size_t cbase = (size_t)grow * cols + (size_t)i * g;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          cand_out[cbase + cj + 16 * t] =
+              (uint8_t)(do_row ? fminf(fmaxf(qold[t] + cs.d[t], 0.f), qmax) : qold[t]);
       }
       any_acc |= accept;
       if (row_in && cj == 0) {
@@ -342,29 +411,102 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         }
         if (row_act && skip) atomicAdd(&cnt_s[2], 1);
       }
-    } else if (has_next) {
-      // ---- meanwhile: everything of group i + 1 that does not wait for group i ----
-      stage_rcol(i + 1, ((i + 1) & 1) ? rc1_s : rc0_s);
-      if (prep_live) {
-        u_from_p(i + 1);
-        // Fragments of the next block load while the current one is applied;
-        // the last load, T(i + 1, i), stays in flight across the barrier.
-        load_t(i + 1, i0, tnext);
-        for (int h = i0; h < i; ++h) {
-          const TFrag f = tnext;
-          load_t(i + 1, h + 1, tnext);
-          apply_t(h, f);
-        }
-      }
+      lds_barrier();  // group i decided: its changes are in dqp_s, tacc_s
+      lds_barrier();  // u and R~ of group i + 1 ready
     }
-    __syncthreads();  // group i decided: its changes are in dqp_s, tacc_s
-    if (has_next && prep_live) {
-      apply_t(i, tnext);
+    if (row_in && cj == 0) rowflag[grow] = any_acc ? 1 : 0;
+  } else {
+    // Group i0 + p stages group i0 + p + 1 and applies the changes of groups
+    // i0 .. i0 + p to it.  Each position p has its own body, so the
+    // fragment buffers alternate without copies (a copy would wait for the
+    // loads in flight) and the R~ buffer is known at compile time (i0 is
+    // even: group i0 + p + 1 goes to rc1_s for even p).
+    static_assert(PG % 2 == 0, "panels hold an even number of groups");
+    stage_rcol(i0, rc0_s);
+    if (prep_live) {
+      u_from_p(i0);
       write_u();
     }
-    __syncthreads();  // u and R~ of group i + 1 ready
+    __syncthreads();  // u and R~ of group i0 staged
+    auto prep_at = [&](auto pc) {
+      constexpr int p = decltype(pc)::value;
+      const int i = i0 + p;
+      TFrag fa, fb;
+      if (prep_live) {
+        u_from_p(i + 1);
+        // block h = i0 + k sits in fa for even k, fb for odd k; the next
+        // block loads while the current one is applied, and the last one,
+        // M(i + 1, i), stays in flight across the barrier
+        load_t(i + 1, i0, fa);
+        Unroll<0, p>::run([&](auto kc) {
+          constexpr int k = decltype(kc)::value;
+          if constexpr (k % 2 == 0) {
+            load_t(i + 1, i0 + k + 1, fb);
+            apply_t(i0 + k, fa, false);
+          } else {
+            load_t(i + 1, i0 + k + 1, fa);
+            apply_t(i0 + k, fb, false);
+          }
+        });
+      }
+      // R~ (i + 1) last: LDS reads issued after a direct load to LDS wait for
+      // it (the compiler cannot tell the buffers apart), and it has the rest
+      // of the back substitution of group i to land.
+      if constexpr (p % 2 == 0)
+        stage_rcol(i + 1, rc1_s);
+      else
+        stage_rcol(i + 1, rc0_s);
+      lds_barrier();  // group i decided: its changes are in dqp_s, tacc_s
+      if (prep_live) {
+        if constexpr (p % 2 == 0)
+          apply_t(i, fa, true);
+        else
+          apply_t(i, fb, true);
+        write_u();
+      }
+      // The direct loads of R~ (i + 1) are complete once this wave's vector
+      // memory counter is zero.
+      __builtin_amdgcn_s_waitcnt(kVmcnt0);
+      lds_barrier();  // u and R~ of group i + 1 ready
+    };
+    // straight-line over the positions (no loop to hoist addresses out of)
+    Unroll<0, PG - 1>::run([&](auto pc) {
+      if (i0 + decltype(pc)::value + 1 < i1) prep_at(pc);
+    });
+    // last group of the panel: nothing to prepare
+    if (i1 > i0) {
+      lds_barrier();
+      lds_barrier();
+    }
   }
-  if (chain_wave && row_in && cj == 0) rowflag[grow] = any_acc ? 1 : 0;
+
+  // ---- codes += accepted changes and dq = accepted changes, over the panel's
+  // columns: 16 columns per thread and step (16-byte code and 2 x 16-byte dq
+  // accesses).  dqp_s is complete since the last barrier.
+  {
+    const int per_row = (i1 - i0) * g / 16;
+    for (int c = tid; c < RT * per_row; c += 512) {
+      const int r = c / per_row;
+      const int k = (c - r * per_row) * 16;
+      if (r0 + r < rows) {
+        const uint32_t o = (uint32_t)r * ucols + (uint32_t)(i0 * g + k);
+        const f16x8 d0 = *(const f16x8*)(dqp_s + r * PW + k);
+        const f16x8 d1 = *(const f16x8*)(dqp_s + r * PW + k + 8);
+        const uint4 qw = ld_at((const uint4*)codes_t, o);
+        uint32_t w[4] = {qw.x, qw.y, qw.z, qw.w};
+        // Byte b of word b / 4 gains d_b; new codes stay in [0, 2^bits - 1],
+        // so the word-wide add never carries into a neighbouring byte.
+#pragma unroll
+        for (int b = 0; b < 16; ++b) {
+          const int dv = (int)(b < 8 ? d0[b] : d1[b - 8]);
+          w[b >> 2] += (uint32_t)dv << (8 * (b & 3));
+        }
+        st_at((uint4*)codes_t, o, make_uint4(w[0], w[1], w[2], w[3]));
+        st_at((f16x8*)dq_t, 2 * o, d0);
+        st_at((f16x8*)dq_t, 2 * o + 16, d1);
+      }
+    }
+  }
   if (tid == 0) {
     if (cnt_s[0]) atomicAdd(&cnt->accepted, (unsigned long long)cnt_s[0]);
     if (cnt_s[1]) atomicAdd(&cnt->changed, (unsigned long long)cnt_s[1]);
@@ -381,6 +523,10 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
   constexpr int g = G_SIZE;
   constexpr int PG = panel_groups_of(g);
   if (i1 - i0 > PG || i0 % PG != 0) return hipErrorInvalidValue;
+  if (i1 <= i0) return hipSuccess;
+  // 32-bit offsets: 16 rows of fp32 and g rows of fp16 M from a uniform base
+  if ((size_t)cols * 64 >= (size_t(1) << 32) || (size_t)cols * g * 2 >= (size_t(1) << 32))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(babai_kernel<g>, dim3((rows + 15) / 16), dim3(512), 0, st, rows, cols, bits,
                      i0, i1, P, (const _Float16*)(ws + lay.mhi), (const _Float16*)(ws + lay.mlo),
                      (const float*)(ws + lay.mrow), (const float*)(ws + lay.rcol),

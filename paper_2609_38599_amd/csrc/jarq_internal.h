@@ -56,7 +56,7 @@ struct Flags {
 struct Layout {
   size_t lfac;      // [G][g][g] f64: L_i^{-1} (holds L_i while it is factored)
   size_t rinv;      // [G][g][g] f32: row n = row n of L_i^{-1} = column n of R_i^{-1}
-  size_t rcol;      // [G][g][16][g/16] f32: R_i columns interleaved for the back substitution
+  size_t rcol;      // [G][g][g/(16 W)][16][W] f32: R~_i columns in lane chunks (W = min(4, g/16))
   size_t rdinv;     // [G][g] f32: 1 / R_i(l,l)
   size_t rdsq;      // [G][g] f32: R_i(l,l)^2
   size_t hhi;       // [cols][cols] f16: H 2^t, high term
@@ -137,6 +137,8 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
 // not for its outstanding global loads (a __syncthreads would, which drains
 // any prefetch in flight).  The empty asm statements keep the compiler from
 // moving memory accesses across it.
+constexpr int kVmcnt0 = 0x0F70;  // s_waitcnt operand: vmcnt(0), lgkmcnt and expcnt at their maximum
+
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maximum

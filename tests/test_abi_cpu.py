@@ -36,7 +36,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert binding.abi_version() == binding.ABI_VERSION == 2
+    assert binding.abi_version() == binding.ABI_VERSION == 3
     for s in range(6):
         assert binding.status_string(s)
     assert binding.status_string(99) == "unknown status"
@@ -70,6 +70,9 @@ def test_argument_errors_return_before_any_launch(lib):
     assert lib.jarq_prepare(ctypes.byref(p), fake, fake, _vp((1 << 20) + 128), 1 << 30, None) == binding.JARQ_EWORKSPACE
     assert lib.jarq_prepare(ctypes.byref(p), fake, fake, fake, 1024, None) == binding.JARQ_EWORKSPACE
     assert lib.jarq_sweeps(ctypes.byref(p), fake, fake, _vp((1 << 20) + 2), fake, fake, fake, 1 << 30,
+                           None, None) == binding.JARQ_EINVAL
+    # codes are read and written 16 bytes at a time
+    assert lib.jarq_sweeps(ctypes.byref(p), fake, fake, _vp((1 << 20) + 4), fake, fake, fake, 1 << 30,
                            None, None) == binding.JARQ_EINVAL
     assert lib.jarq_code_step(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, 1 << 30, None,
                               None, None) == binding.JARQ_EINVAL

@@ -1,9 +1,14 @@
-// Joint scale solve of the scale update (paper eq. (6), App. E.2): one
-// wavefront per row.
+// Joint scale solve of the scale update (paper eq. (6), App. E.2), in fp64.
 //
 // The G x G Gram matrix (upper triangle from the Gram kernel, symmetrised by
-// construction) and the right-hand side r_a = c_a^T (W H)_a are held in LDS in
-// fp64 and factored by a right-looking Cholesky.  The stabilised branch of
+// construction) and the right-hand side r_a = c_a^T (W H)_a are factored by a
+// right-looking Cholesky.  Two kernels:
+//   solve_reg_kernel (G <= 64): lane i of a row holds row i of the matrix in
+//     registers (two rows per wavefront when G <= 32); the column of each step
+//     is exchanged through LDS, the forward substitution runs inside the
+//     factorisation, the backward one reads L transposed through LDS.
+//   solve_kernel (any G): one wavefront per row with the matrix in LDS.
+// The stabilised branch of
 // App. E.2 (add lambda I and factor again) is taken when an entry is not
 // finite, a pivot is not positive, or the smallest pivot is at most
 // r_cond * max(largest diagonal, 2^-23).  Every Cholesky pivot is a Schur
@@ -196,11 +201,211 @@ __global__ __launch_bounds__(64) void solve_kernel(int rows, int cols, int g,
   for (int a = lane; a < G; a += 64) scales[(size_t)row * G + a] = (float)r[a];
 }
 
+// 1 / sqrt(x) in fp64: the hardware estimate (about 23 bits) and two Newton
+// steps y <- y (3/2 - x y^2 / 2), each of which doubles the correct bits.
+__device__ __forceinline__ double rsqrt_f64(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+  const double h = 0.5 * x;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) y *= fma(-h * y, y, 1.5);
+  return y;
+}
+
+template <int GM, int GS>
+__global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
+                                                       const float* __restrict__ gram,
+                                                       const float* __restrict__ wh,
+                                                       const uint8_t* __restrict__ codes,
+                                                       const int32_t* __restrict__ zeros,
+                                                       float* __restrict__ scales,
+                                                       const uint8_t* __restrict__ active,
+                                                       Counters* __restrict__ cnt,
+                                                       Flags* __restrict__ flags, float lam,
+                                                       float rcond) {
+  constexpr int RPW = 64 / GM;  // rows per wavefront
+  constexpr int g = GS;
+  const int G = cols / g;
+  const int lane = threadIdx.x;
+  const int slot = lane / GM;
+  const int i = lane % GM;      // this lane's row of the G x G system
+  const int row = blockIdx.x * RPW + slot;
+  const bool row_ok = row < rows;
+  const bool act = row_ok && (active == nullptr || active[row] != 0);
+  const bool live = i < G;
+  const int rr = row_ok ? row : 0;  // loads stay unconditional: rows past the edge read row 0
+  const int ic = live ? i : G - 1;
+
+  // column exchange of the factorisation steps and the transposed factor
+  __shared__ double col_a[RPW][GM], col_r[RPW][GM];
+  __shared__ double lt[RPW][GM][GM + 1];
+
+  // ---- right-hand side r_i = sum over group i of (q - z) (W H) ----
+  double r0 = 0.0;
+  {
+    const float* whp = wh + (size_t)rr * cols + (size_t)ic * g;
+    const uint8_t* qp = codes + (size_t)rr * cols + (size_t)ic * g;
+    const double z = (double)zeros[(size_t)rr * G + ic];
+    constexpr int CH = g < 32 ? g : 32;  // columns per batch of loads
+#pragma unroll
+    for (int c0 = 0; c0 < g; c0 += CH) {
+      uint4 qv[CH / 16];
+      f32x4 wv[CH / 4];
+#pragma unroll
+      for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
+#pragma unroll
+      for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
+#pragma unroll
+      for (int u = 0; u < CH / 4; ++u) {
+        const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
+                             : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          r0 = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], r0);
+      }
+    }
+    if (!live) r0 = 0.0;
+  }
+
+  // ---- row i of the Gram matrix (entry (i, j) stored at (min, max)) ----
+  double A[GM];
+  double diag = 0.0;
+  bool finite = isfinite(r0);
+  const float* gr = gram + (size_t)rr * G * G;
+  auto load_rows = [&](double shift) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < GM; ++j) {
+      const bool in = live && j < G;
+      const int idx = in ? (j <= i ? j * G + i : i * G + j) : 0;
+      const float v = gr[idx];
+      if (in) finite &= isfinite(v);
+      if (j == i) diag = in ? (double)v : 1.0;
+      A[j] = in ? (double)v + (j == i ? shift : 0.0) : (j == i ? 1.0 : 0.0);
+    }
+  };
+  load_rows(0.0);
+
+  // ---- factorisation A = L L^T with the forward substitution L y = r ----
+  // Step k: lane k's pivot and r_k reach every lane of the row through LDS
+  // (one wavefront: its LDS accesses complete in order, so no barrier); the
+  // trailing update A_ij -= A_ik A_jk / A_kk and r_i -= A_ik r_k / A_kk run in
+  // every lane (entries above the diagonal are never read).  Afterwards lane
+  // i holds L(i, 0..i), y_i and 1 / L(i, i).
+  double r, dinv = 0.0, minpiv;
+  bool pivots_ok;
+  auto factor = [&]() __attribute__((always_inline)) {
+    r = r0;
+    minpiv = INFINITY;
+    pivots_ok = true;
+#pragma unroll
+    for (int k = 0; k < GM; ++k) {
+      if (k < G) {
+        col_a[slot][i] = A[k];
+        col_r[slot][i] = r;
+        const double piv = col_a[slot][k];
+        const double rk = col_r[slot][k];
+        pivots_ok &= piv > 0.0 && isfinite(piv);
+        minpiv = fmin(minpiv, piv);
+        const double rs = rsqrt_f64(piv);
+        const double li = A[k] * (rs * rs);
+#pragma unroll
+        for (int j = k + 1; j < GM; ++j) A[j] = fma(-li, col_a[slot][j], A[j]);
+        r = i > k ? fma(-li, rk, r) : (i == k ? rk * rs : r);
+        A[k] *= rs;
+        if (i == k) dinv = rs;
+      }
+    }
+  };
+  factor();
+  double dmax = live ? diag : 0.0;
+#pragma unroll
+  for (int off = GM / 2; off >= 1; off >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, off));
+  const unsigned long long bad = __ballot(!finite);
+  const unsigned long long slot_mask = GM == 64 ? ~0ull : (((1ull << GM) - 1) << (slot * GM));
+  const bool all_finite = (bad & slot_mask) == 0;
+  const bool ridge = !all_finite || !pivots_ok ||
+                     !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  bool failed = false;
+  if (__any(ridge)) {
+    // A + lam I from the stored matrix, for the rows that need it (a row that
+    // shares the wavefront and does not keeps its first factorisation)
+    if constexpr (RPW == 1) {
+      load_rows((double)lam);
+      factor();
+      failed = !(pivots_ok && minpiv > 0.0);
+    } else {
+      double keepA[GM];
+      const double keep_r = r, keep_dinv = dinv;
+#pragma unroll
+      for (int j = 0; j < GM; ++j) keepA[j] = A[j];
+      load_rows((double)lam);
+      factor();
+      failed = ridge && !(pivots_ok && minpiv > 0.0);
+      if (!ridge) {
+#pragma unroll
+        for (int j = 0; j < GM; ++j) A[j] = keepA[j];
+        r = keep_r;
+        dinv = keep_dinv;
+      }
+    }
+  }
+
+  // ---- backward substitution L^T s = y: L transposed through LDS ----
+#pragma unroll
+  for (int j = 0; j < GM; ++j) lt[slot][i][j] = A[j];
+#pragma unroll
+  for (int k = GM - 1; k >= 0; --k) {
+    if (k < G) {
+      col_r[slot][i] = r * dinv;
+      const double sk = col_r[slot][k];
+      const double lkj = lt[slot][k][i];
+      r = i < k ? fma(-lkj, sk, r) : (i == k ? sk : r);
+    }
+  }
+
+  if (act && live && !failed) scales[(size_t)row * G + i] = (float)r;
+  if (act && i == 0) {
+    if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
+    if (failed) {
+      atomicAdd(&cnt->solve_failed, 1u);
+      atomicAdd(&flags->solve_failed, 1);
+    }
+  }
+}
+
+template <int GM, int GS>
+static hipError_t launch_solve_reg(hipStream_t st, int rows, int cols, const float* gram,
+                                   const float* wh, const uint8_t* codes, const int32_t* zeros,
+                                   float* scales, const uint8_t* active, Counters* cnt,
+                                   Flags* flags, float lam, float rcond) {
+  constexpr int RPW = 64 / GM;
+  hipLaunchKernelGGL((solve_reg_kernel<GM, GS>), dim3((rows + RPW - 1) / RPW), dim3(64), 0, st,
+                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond);
+  return hipGetLastError();
+}
+
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
                         float lam, float rcond) {
   const int G = cols / g;
+  if (G <= 64) {
+#define JARQ_SOLVE_REG(GM)                                                                        \
+  switch (g) {                                                                                    \
+    case 32: return launch_solve_reg<GM, 32>(st, rows, cols, gram, wh, codes, zeros, scales,      \
+                                             active, cnt, flags, lam, rcond);                     \
+    case 64: return launch_solve_reg<GM, 64>(st, rows, cols, gram, wh, codes, zeros, scales,      \
+                                             active, cnt, flags, lam, rcond);                     \
+    case 128: return launch_solve_reg<GM, 128>(st, rows, cols, gram, wh, codes, zeros, scales,    \
+                                               active, cnt, flags, lam, rcond);                   \
+    default: break;                                                                               \
+  }
+    if (G <= 32) {
+      JARQ_SOLVE_REG(32)
+    } else {
+      JARQ_SOLVE_REG(64)
+    }
+#undef JARQ_SOLVE_REG
+  }
   const size_t lds = ((size_t)G * (G + 1) + 2 * (size_t)G) * sizeof(double);
   hipError_t e = hipFuncSetAttribute((const void*)solve_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -42,7 +42,8 @@ Layout make_layout(int rows, int cols, int g) {
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
-  L.rowflag = take(R);
+  L.plist = take(R * sizeof(int32_t));
+  L.pcount = take((C + 511) / 512 * sizeof(uint32_t));
   L.objpart = take(R * (nt > G ? nt : G) * sizeof(double));  // per-group sweep partials or 64-column slices
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
@@ -135,6 +136,8 @@ hipError_t enqueue_babai(const Ctx& c, const float* H, uint8_t* codes, const flo
                          uint8_t* decision) {
   (void)H;
   const int nb = panel_groups(c.g);
+  hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, (size_t)(c.cols + 511) / 512 * sizeof(uint32_t));
+  if (e0 != hipSuccess) return e0;
   for (int i0 = 0; i0 < c.G; i0 += nb) {
     const int i1 = i0 + nb < c.G ? i0 + nb : c.G;
     hipError_t e = launch_babai(c.st, c.rows, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay,

@@ -175,7 +175,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     const float* __restrict__ rdinv,
     const float* __restrict__ rdsq, uint8_t* __restrict__ codes,
     const float* __restrict__ scales, const uint8_t* __restrict__ active,
-    _Float16* __restrict__ dq, uint8_t* __restrict__ rowflag, uint8_t* __restrict__ cand_out,
+    _Float16* __restrict__ dq, int32_t* __restrict__ plist, uint32_t* __restrict__ pcount,
+    uint8_t* __restrict__ cand_out,
     uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt) {
   constexpr int g = G_SIZE;
   constexpr int RT = 16;                 // rows per work-group
@@ -198,6 +199,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   __shared__ __attribute__((aligned(16))) _Float16 dqp_s[RT * PW];  // accepted changes in the panel
   __shared__ int tacc_s[PG];                         // any row of the tile accepted group
   __shared__ int cnt_s[4];                           // accepted, changed, skipped, blocks
+  __shared__ int racc_s[RT];                         // the row accepted a change in the panel
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -221,6 +223,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 
   if (tid < PG) tacc_s[tid] = 0;
   if (tid < 4) cnt_s[tid] = 0;
+  if (tid < RT) racc_s[tid] = 0;
 
   // Bases of this work-group's 16 rows (wave-uniform); offsets from them fit
   // in 32 bits (16 rows of at most 2^26 columns).
@@ -414,7 +417,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       lds_barrier();  // group i decided: its changes are in dqp_s, tacc_s
       lds_barrier();  // u and R~ of group i + 1 ready
     }
-    if (row_in && cj == 0) rowflag[grow] = any_acc ? 1 : 0;
+    if (row_in && cj == 0) racc_s[crow] = any_acc ? 1 : 0;
   } else {
     // Group i0 + p stages group i0 + p + 1 and applies the changes of groups
     // i0 .. i0 + p to it.  Each position p has its own body, so the
@@ -480,6 +483,18 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     }
   }
 
+  __syncthreads();  // racc_s
+  // ---- rows that accepted a change: appended to the panel's row list (the
+  // panel update folds in only these rows; their order there is immaterial)
+  if (wave == 0) {
+    const bool f = lane < RT && racc_s[lane] != 0;
+    const unsigned long long m = __ballot(f);
+    uint32_t base = 0;
+    if (lane == 0 && m != 0) base = atomicAdd(pcount, (uint32_t)__popcll(m));
+    base = __shfl(base, 0);
+    if (f) plist[base + (uint32_t)__popcll(m & ((1ull << lane) - 1))] = r0 + lane;
+  }
+
   // ---- codes += accepted changes and dq = accepted changes, over the panel's
   // columns: 16 columns per thread and step (16-byte code and 2 x 16-byte dq
   // accesses).  dqp_s is complete since the last barrier.
@@ -532,7 +547,8 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.mrow), (const float*)(ws + lay.rcol),
                      (const float*)(ws + lay.rdinv),
                      (const float*)(ws + lay.rdsq), codes, scales, active,
-                     (_Float16*)(ws + lay.dq), (uint8_t*)(ws + lay.rowflag), cand, decision, cnt);
+                     (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
+                     (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt);
   return hipGetLastError();
 }
 

@@ -74,7 +74,8 @@ struct Layout {
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
   size_t p;         // [rows][cols] f32: (W - What) H
   size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
-  size_t rowflag;   // [rows] u8: the row accepted a change in the last panel of the code update
+  size_t plist;     // [rows] i32: rows that accepted a change in the last panel (any order)
+  size_t pcount;    // [ceil(cols / 512)] u32: length of that list, one counter per panel
   size_t objpart;   // [rows][ceil(cols/64)] f64: partial row objectives
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64
@@ -151,7 +152,8 @@ constexpr int kMaxPanelGroups = 16;
 constexpr int panel_groups_of(int g) { return 512 / g < kMaxPanelGroups ? 512 / g : kMaxPanelGroups; }
 int panel_groups(int g);
 
-// P(:, c1:) -= the accepted changes of the groups in columns [c0, c1).
+// P(:, c1:) -= the accepted changes of the groups in columns [c0, c1) (the
+// panel's rows listed by the code update in plist / pcount[panel]).
 hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0, int c1,
                                const char* ws, const Layout& lay, const float* scales, float* P);
 

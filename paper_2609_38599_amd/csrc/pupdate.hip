@@ -54,7 +54,8 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     int rows, int cols, int g, int c0, int c1, const _Float16* __restrict__ dq,
     const _Float16* __restrict__ Mh, const _Float16* __restrict__ Ml,
     const float* __restrict__ bcol_inv, const float* __restrict__ scales,
-    const uint8_t* __restrict__ rowflag, float* __restrict__ P) {
+    const int32_t* __restrict__ plist, const uint32_t* __restrict__ pcount,
+    float* __restrict__ P) {
   // Three stages in three distinct arrays: the loads of steps k + 1 and k + 2
   // fly while step k computes.
   __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
@@ -72,54 +73,18 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   const int h0 = c0 / g;
   const int ng = (c1 - c0) / g;
 
-  // Only rows that accepted a change in the panel (rowflag) need an update.
-  // Every work-group forms the same compacted list (ascending rows) by a
-  // prefix sum over the flags and takes positions m0 .. m0 + BM - 1 of it;
-  // work-groups past its end have nothing to do.
-  // Scratch for the list lives in the third stage, first loaded after set-up.
-  int* pre_s = (int*)buf2;  // 256
-  int* rl_s = pre_s + 256;  // BM
-  // Flags are 0 or 1; thread t reads words t * wpt .. of the flag array (four
-  // rows a word; the workspace region is padded to 256 bytes, and rows past
-  // the end are masked).
-  const int nw = (rows + 3) / 4;
-  const int wpt = (nw + 255) / 256;  // words per thread
-  const uint32_t* fw = (const uint32_t*)rowflag;
-  auto word = [&](int w) {
-    if (w >= nw) return 0u;
-    const uint32_t x = fw[w] & 0x01010101u;
-    const int valid = rows - 4 * w;  // rows of this word inside the layer
-    return valid >= 4 ? x : (x & ((1u << (8 * valid)) - 1u));
-  };
-  int cntl = 0;
-#pragma unroll 4
-  for (int q = 0; q < wpt; ++q) cntl += __builtin_popcount(word(tid * wpt + q));
-  pre_s[tid] = cntl;
-  __syncthreads();
-  for (int w = 1; w < 256; w <<= 1) {  // inclusive scan (Hillis-Steele)
-    const int v = tid >= w ? pre_s[tid - w] : 0;
-    __syncthreads();
-    pre_s[tid] += v;
-    __syncthreads();
-  }
-  const int total = pre_s[255];
+  // Only rows that accepted a change in the panel need an update: the code
+  // update listed them (plist, pcount entries); this work-group takes list
+  // positions m0 .. m0 + BM - 1, and work-groups past the end have nothing to do.
+  const int total = (int)*pcount;
   if (m0 >= total) return;  // uniform across the work-group
-  {
-    int pos = pre_s[tid] - cntl;  // exclusive prefix
-    for (int q = 0; q < wpt; ++q) {
-      const int w = tid * wpt + q;
-      const uint32_t x = word(w);
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        if ((x >> (8 * b)) & 1u) {
-          if (pos >= m0 && pos < m0 + BM) rl_s[pos - m0] = 4 * w + b;
-          ++pos;
-        }
-      }
-    }
-  }
-  __syncthreads();
   const int nvalid = min(BM, total - m0);
+  // The list lives in the third stage, which is first loaded after every
+  // use of it (set-up, behind the loop's first barrier); a separate array
+  // would push the work-group past half of the LDS (one per CU).
+  int* rl_s = (int*)buf2;
+  if (tid < BM) rl_s[tid] = plist[m0 + (tid < nvalid ? tid : 0)];
+  __syncthreads();
   // Tile row t is row rl_s[t] for t < nvalid; later tile rows repeat a valid row
   // and are never stored.
   auto row_of = [&](int t) { return rl_s[t < nvalid ? t : 0]; };
@@ -278,7 +243,8 @@ hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0
   hipLaunchKernelGGL(panel_update_kernel, grid, dim3(256), 0, st, rows, cols, g, c0, c1,
                      (const _Float16*)(ws + lay.dq), (const _Float16*)(ws + lay.mhi),
                      (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow), scales,
-                     (const uint8_t*)(ws + lay.rowflag), P);
+                     (const int32_t*)(ws + lay.plist),
+                     (const uint32_t*)(ws + lay.pcount) + c0 / (g * panel_groups_of(g)), P);
   return hipGetLastError();
 }
 

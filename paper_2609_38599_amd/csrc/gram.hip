@@ -3,7 +3,7 @@
 // For row j with c_i = q_i - z_i 1 (exact small integers), entry (a, h) of
 // B_j^T B_j is c_a^T H_ah c_h (B_j has columns A_i c_i and H = A^T A).  The
 // matrix is symmetric, so only h >= a is formed.  A work-group takes a tile of
-// 256 rows and a pair of row-groups {p, G-1-p} (so every work-group walks G+1
+// 128 rows and a pair of row-groups {p, G-1-p} (so every work-group walks G+1
 // blocks); for each block h it forms T = H(a-group, h-group) C(rows, h-group)^T
 // on fp16 matrix cores (v_mfma_f32_32x32x16_f16, M = the g weights of group a,
 // N = 32 rows, K = the g weights of group h) with H as its two fp16 planes and
@@ -12,8 +12,10 @@
 // Waves split the a-group into 32-weight blocks and the tile's rows; each H
 // fragment is used for all of a wave's rows.  The codes of block h are staged
 // in LDS as fp16 once per work-group (bit trick: the fp16 with bits
-// 0x6400 | q is 1024 + q) and the next block's codes and H fragments are
-// fetched while the current block runs on the matrix cores.
+// 0x6400 | q is 1024 + q) and the next block's codes are fetched while the
+// current block runs on the matrix cores.  Two work-groups share a CU (LDS and
+// registers sized for it), so one's staging, reduction and H loads overlap
+// the other's matrix work.
 #include "jarq_internal.h"
 
 namespace jarq {
@@ -22,7 +24,7 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 namespace {
-constexpr int RT = 256;  // rows per work-group
+constexpr int RT = 128;  // rows per work-group
 
 // Four codes (one byte each) -> four fp16 values q - z, exactly.
 __device__ __forceinline__ void codes_to_f16(uint32_t q4, f16x2 zz, f16x2* out) {
@@ -35,7 +37,7 @@ __device__ __forceinline__ void codes_to_f16(uint32_t q4, f16x2 zz, f16x2* out) 
 }  // namespace
 
 template <int G_SIZE>
-__global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
+__global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
                                                       const _Float16* __restrict__ Hh,
                                                       const _Float16* __restrict__ Hl,
                                                       const float* __restrict__ h_inv,
@@ -66,31 +68,35 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
   double* red = (double*)(ca_s + RT * LDC);  // NAB x RT
 
   // Stage the codes of column block `blk` of the tile as fp16 (c = q - z):
-  // thread t owns row t of the tile (g bytes, one zero point).
+  // threads 2t and 2t + 1 own the two halves of row t of the tile.
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  u32x4 stq[g / 16];
+  constexpr int TPR = 256 / RT;          // threads per staged row
+  constexpr int CPT = g / TPR;           // codes per thread
+  u32x4 stq[CPT / 16];
   int stz = 0;
-  const int srow = r0 + tid;
+  const int trow = tid / TPR, tpart = tid % TPR;
+  const int srow = r0 + trow;
   // Rows past the edge load row 0 (unconditional loads, so that none is
   // waited for here): each row's Gram entries depend on that row only, and
   // those of rows past the edge are never stored.
   const int lrow = srow < rows ? srow : 0;
   auto fetch_codes = [&](int blk) {
-    const u32x4* src = (const u32x4*)(codes + (size_t)lrow * cols + (size_t)blk * g);
+    const u32x4* src = (const u32x4*)(codes + (size_t)lrow * cols + (size_t)blk * g + tpart * CPT);
 #pragma unroll
-    for (int i = 0; i < g / 16; ++i) stq[i] = src[i];
+    for (int i = 0; i < CPT / 16; ++i) stq[i] = src[i];
     stz = zeros[(size_t)lrow * G + blk];
   };
   auto store_codes = [&](_Float16* dst) {
     const _Float16 zb = (_Float16)(1024 + stz);
     const f16x2 zz = f16x2{zb, zb};
+    _Float16* drow = dst + trow * LDC + tpart * CPT;
 #pragma unroll
-    for (int i = 0; i < g / 16; ++i) {
+    for (int i = 0; i < CPT / 16; ++i) {
       f16x2 v[8];
 #pragma unroll
       for (int w = 0; w < 4; ++w) codes_to_f16(stq[i][w], zz, v + 2 * w);
-      *(f16x8*)(dst + tid * LDC + i * 16) = f16x8{v[0][0], v[0][1], v[1][0], v[1][1], v[2][0], v[2][1], v[3][0], v[3][1]};
-      *(f16x8*)(dst + tid * LDC + i * 16 + 8) = f16x8{v[4][0], v[4][1], v[5][0], v[5][1], v[6][0], v[6][1], v[7][0], v[7][1]};
+      *(f16x8*)(drow + i * 16) = f16x8{v[0][0], v[0][1], v[1][0], v[1][1], v[2][0], v[2][1], v[3][0], v[3][1]};
+      *(f16x8*)(drow + i * 16 + 8) = f16x8{v[4][0], v[4][1], v[5][0], v[5][1], v[6][0], v[6][1], v[7][0], v[7][1]};
     }
   };
   // H fragments of block (a-group ga, column block h) for this wave's a-block.
@@ -114,20 +120,13 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
     fetch_codes(ga);
     store_codes(ca_s);
     fetch_codes(ga);     // block h = ga comes first
-    fetch_h(ga, ga);
     for (int h = ga; h < G; ++h) {
       lds_barrier();   // previous block's reads of ch_s are done
       store_codes(ch_s);
-      f16x8 cur[2][KS];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        cur[0][ks] = hf[0][ks];
-        cur[1][ks] = hf[1][ks];
-      }
-      if (h + 1 < G) {
-        fetch_codes(h + 1);
-        fetch_h(ga, h + 1);
-      }
+      // H fragments of this block (their latency is covered by the other
+      // work-group on the CU), codes of the next one
+      fetch_h(ga, h);
+      if (h + 1 < G) fetch_codes(h + 1);
       lds_barrier();
       f32x16 acc[JB];
 #pragma unroll
@@ -148,8 +147,8 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
         }
 #pragma unroll
         for (int b = 0; b < JB; ++b) {
-          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[0][ks], cf[ks & 1][b], acc[b], 0, 0, 0);
-          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[1][ks], cf[ks & 1][b], acc[b], 0, 0, 0);
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(hf[0][ks], cf[ks & 1][b], acc[b], 0, 0, 0);
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(hf[1][ks], cf[ks & 1][b], acc[b], 0, 0, 0);
         }
       }
       // acc element v of lane l: T(a = ab*32 + 8*(v/4) + 4*kh + v%4, row = rbase + b*32 + l%32).
@@ -169,10 +168,10 @@ __global__ __launch_bounds__(256, 1) void gram_kernel(int rows, int cols,
         if (kh == 0) red[ab * RT + rr] = d;
       }
       lds_barrier();
-      {
+      if (tid < RT) {
         // Thread tid owns row r0 + tid: keep its entries (ga, h) for up to 32
         // consecutive h in registers and store them as one contiguous run.
-        const int rr = tid;  // RT == 256 == blockDim.x
+        const int rr = tid;
         double s = 0.0;
 #pragma unroll
         for (int a = 0; a < NAB; ++a) s += red[a * RT + rr];

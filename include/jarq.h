@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 3
+#define JARQ_ABI_VERSION 4
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
  * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
  * 3 residual product U = E M^T, 4 row objectives and stopping test,
@@ -80,8 +80,13 @@ typedef struct jarq_params {
 } jarq_params;
 
 /* Filled by jarq_sweeps / jarq_refine when a stats pointer is given [host].
- * Per-sweep arrays hold the first JARQ_MAX_RECORDED_SWEEPS sweeps. */
+ * Per-sweep arrays hold the first JARQ_MAX_RECORDED_SWEEPS sweeps.
+ * stage_mask is read, not written: bit s selects stage s for timing (0 = all
+ * stages).  Each timed stage costs a pair of HIP events per sweep, and every
+ * event leaves the GPU idle for a few microseconds between kernels; stages not
+ * selected report 0 ms. */
 typedef struct jarq_stats {
+  uint32_t stage_mask;               /* [in] stages to time, bit s = stage s; 0 = all */
   int32_t sweeps_run;                /* sweeps started (a sweep in which every row had stopped is not run) */
   int32_t rows_active_end;           /* rows still active after the last sweep */
   double objective_after_scales[JARQ_MAX_RECORDED_SWEEPS];  /* sum_j L_j, fp64 */

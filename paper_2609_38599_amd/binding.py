@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libjarq.so")
 MAX_RECORDED_SWEEPS = 64
 NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
 STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
-ABI_VERSION = 3
+ABI_VERSION = 4
 JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
@@ -37,7 +37,8 @@ class Params(ctypes.Structure):
 
 
 class Stats(ctypes.Structure):
-    _fields_ = [("sweeps_run", ctypes.c_int32), ("rows_active_end", ctypes.c_int32),
+    _fields_ = [("stage_mask", ctypes.c_uint32),
+                ("sweeps_run", ctypes.c_int32), ("rows_active_end", ctypes.c_int32),
                 ("objective_after_scales", ctypes.c_double * MAX_RECORDED_SWEEPS),
                 ("accepted_groups", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
                 ("codes_changed", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
@@ -51,6 +52,7 @@ class Stats(ctypes.Structure):
     def to_dict(self):
         n = min(self.sweeps_run, MAX_RECORDED_SWEEPS)
         return {
+            "stage_mask": self.stage_mask,
             "sweeps_run": self.sweeps_run,
             "rows_active_end": self.rows_active_end,
             "objective_after_scales": [self.objective_after_scales[k] for k in range(n)],
@@ -182,9 +184,13 @@ def code_step(p: Params, W, H, codes, scales, zeros, ws, cand=None, decision=Non
                               _ptr(decision, torch.uint8, "decision")), "jarq_code_step")
 
 
-def sweeps(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=True, check=True):
+def sweeps(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=True, check=True,
+           stage_mask=0):
+    """jarq_sweeps; stage_mask selects the stages timed with HIP events (0 = all)."""
     lib = load_library()
     st = Stats() if want_stats else None
+    if st is not None:
+        st.stage_mask = stage_mask
     status = lib.jarq_sweeps(ctypes.byref(p), _ptr(W, torch.float32, "W"),
                              _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
                              _ptr(scales, torch.float32, "scales"),
@@ -196,9 +202,12 @@ def sweeps(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=Tr
     return (st.to_dict() if st is not None else None) if check else (status, st)
 
 
-def refine(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=True, check=True):
+def refine(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=True, check=True,
+           stage_mask=0):
     lib = load_library()
     st = Stats() if want_stats else None
+    if st is not None:
+        st.stage_mask = stage_mask
     status = lib.jarq_refine(ctypes.byref(p), _ptr(W, torch.float32, "W"),
                              _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
                              _ptr(scales, torch.float32, "scales"),

@@ -188,13 +188,23 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   const int K = p->sweeps;
   const int nrec = K < JARQ_MAX_RECORDED_SWEEPS ? K : JARQ_MAX_RECORDED_SWEEPS;
   std::vector<hipEvent_t> ev;
+  // Events at the boundaries of the timed stages only (each one costs an
+  // idle gap between kernels).
+  const uint32_t all_stages = (1u << JARQ_NUM_STAGES) - 1u;
+  const uint32_t tmask = stats == nullptr ? 0u
+                         : (stats->stage_mask & all_stages) ? (stats->stage_mask & all_stages)
+                                                             : all_stages;
+  auto boundary_used = [&](int j) {
+    return ((j > 0 && ((tmask >> (j - 1)) & 1u)) || (j < JARQ_NUM_STAGES && ((tmask >> j) & 1u)));
+  };
   if (stats != nullptr) {
     memset(stats, 0, sizeof(*stats));
+    stats->stage_mask = tmask;
     ev.resize((size_t)nrec * (JARQ_NUM_STAGES + 1));
     for (auto& e : ev) JQ_HIP(hipEventCreate(&e));
   }
   auto mark = [&](int k, int j) -> hipError_t {
-    if (stats == nullptr || k >= nrec) return hipSuccess;
+    if (stats == nullptr || k >= nrec || !boundary_used(j)) return hipSuccess;
     return hipEventRecord(ev[(size_t)k * (JARQ_NUM_STAGES + 1) + j], c.st);
   };
   jarq_status status = JARQ_OK;
@@ -268,7 +278,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
         for (int j = 0; j < JARQ_NUM_STAGES; ++j) {
           float ms = 0.f;
           const size_t b = (size_t)k * (JARQ_NUM_STAGES + 1) + j;
-          hipEventElapsedTime(&ms, ev[b], ev[b + 1]);
+          if ((tmask >> j) & 1u) hipEventElapsedTime(&ms, ev[b], ev[b + 1]);
           stats->stage_ms[k][j] = ms;
         }
       }

@@ -112,6 +112,26 @@ def test_deterministic():
     assert np.array_equal(outs[0][1].view(np.uint32), outs[1][1].view(np.uint32))
 
 
+def test_stage_mask_times_only_the_selected_stages():
+    # Stage timing is instrumentation: the selected stages report time, the
+    # others 0, and the results are bit-identical to a run timing every stage.
+    cfg, W, H, q, s, z = layer(0)
+    res = jq.binding.STAGE_NAMES.index("residual")
+    outs = []
+    for mask in (1 << res, 0):
+        gl = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits, sweeps=3)
+        st = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws, stage_mask=mask)
+        outs.append(gl.state())
+        for k in range(st["sweeps_run"]):
+            for j, ms in enumerate(st["stage_ms"][k]):
+                if mask == 0 or j == res:
+                    assert ms > 0.0, (mask, k, j)
+                else:
+                    assert ms == 0.0, (mask, k, j)
+    assert np.array_equal(outs[0][0], outs[1][0])
+    assert np.array_equal(outs[0][1].view(np.uint32), outs[1][1].view(np.uint32))
+
+
 def test_refine_entry_equals_prepare_plus_sweeps():
     cfg, W, H, q, s, z = layer(0)
     a = GpuLayer(W, H, q, s, z, cfg.group_size, cfg.bits, sweeps=3)

@@ -60,6 +60,17 @@ def stage_work(cfg, rows, corr_blocks):
     }
 
 
+def workload_text(cfg, rows, cols, steps):
+    """The synthetic layer in words (weights, calibration recipe, host)."""
+    wdist = {"normal": "normal", "student_t5": "Student-t(5)"}[cfg.w_dist]
+    xdesc = {"zl": "correlated Gaussian", "ar1": "AR(1)", "silu_gate": "SiLU-gated AR(1)",
+             "block_equi": "block-equicorrelated"}[cfg.x_recipe]
+    outl = f" with {cfg.n_outliers} outlier channels" if cfg.n_outliers else ""
+    return (f"{cfg.name}: W {rows}x{cols} {wdist} std {cfg.w_std}, H from {cfg.n_tokens} "
+            f"{xdesc} tokens{outl}, {cfg.host.upper()} {cfg.bits}-bit host, g {cfg.group_size}, "
+            f"{steps} sweeps from the host state")
+
+
 def traffic_from_profile():
     """Per-launch HBM bytes of the residual product kernel from rocprofv3 counters.
 
@@ -230,9 +241,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: W {rows}x{cols} Student-t(5) std 0.02, H from "
-                               f"{cfg.n_tokens} AR(1) tokens with {cfg.n_outliers} outlier channels, "
-                               f"RTN {bits}-bit host, g {g}, {args.steps} sweeps from the host state",
+        "config": {"workload": workload_text(cfg, rows, cols, args.steps),
                    "rows": rows, "cols": cols, "group_size": g, "bits": bits},
         "rows_per_s": rows / (ms_per_step * 1e-3),
         "prep_ms": prep_ms,

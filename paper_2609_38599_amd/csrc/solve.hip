@@ -7,6 +7,8 @@
 //     registers (two rows per wavefront when G <= 32); the column of each step
 //     is exchanged through LDS, the forward substitution runs inside the
 //     factorisation, the backward one reads L transposed through LDS.
+//   solve_col_kernel (64 < G <= 128): the same with the matrix in LDS,
+//     column-major, one row per work-group of 128 lanes.
 //   solve_kernel (any G): one wavefront per row with the matrix in LDS.
 // The stabilised branch of
 // App. E.2 (add lambda I and factor again) is taken when an entry is not
@@ -372,6 +374,203 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   }
 }
 
+// G in (32, 128]: one row per work-group of 64 or 128 threads; lane i owns
+// row i of the system, which sits in LDS column-major (element (a, b) at
+// b * LD + a), so a lane's own accesses are contiguous across lanes and step
+// k's column (a, k) is a broadcast read.  Column k is left unscaled and
+// 1 / sqrt(pivot k) is kept per k: L(a, k) = A(a, k) rk_s[k].  One barrier
+// per step (the trailing update writes columns > k only).
+template <int GS>
+__global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
+                                                        const float* __restrict__ gram,
+                                                        const float* __restrict__ wh,
+                                                        const uint8_t* __restrict__ codes,
+                                                        const int32_t* __restrict__ zeros,
+                                                        float* __restrict__ scales,
+                                                        const uint8_t* __restrict__ active,
+                                                        Counters* __restrict__ cnt,
+                                                        Flags* __restrict__ flags, float lam,
+                                                        float rcond) {
+  constexpr int g = GS;
+  const int G = cols / g;
+  const int LD = G | 1;  // odd stride (in doubles): rows of a column spread over banks
+  const int row = blockIdx.x;
+  const int i = threadIdx.x;
+  const int nthr = blockDim.x;
+  if (row >= rows) return;
+  if (active != nullptr && !active[row]) return;
+  const bool live = i < G;
+  const int ic = live ? i : G - 1;
+  extern __shared__ double sm[];
+  double* A = sm;               // G columns of LD
+  double* r_s = A + (size_t)G * LD;  // broadcast slot of r / s
+  double* rk_s = r_s + G;       // 1 / sqrt(pivot k)
+  double* red = rk_s + G;       // two wavefronts' partial max / flags
+
+  // right-hand side r_i = sum over group i of (q - z) (W H)
+  double r0 = 0.0;
+  {
+    const float* whp = wh + (size_t)row * cols + (size_t)ic * g;
+    const uint8_t* qp = codes + (size_t)row * cols + (size_t)ic * g;
+    const double z = (double)zeros[(size_t)row * G + ic];
+    constexpr int CH = g < 32 ? g : 32;
+#pragma unroll
+    for (int c0 = 0; c0 < g; c0 += CH) {
+      uint4 qv[CH / 16];
+      f32x4 wv[CH / 4];
+#pragma unroll
+      for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
+#pragma unroll
+      for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
+#pragma unroll
+      for (int u = 0; u < CH / 4; ++u) {
+        const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
+                             : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          r0 = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], r0);
+      }
+    }
+  }
+
+  const float* gr = gram + (size_t)row * G * G;
+  double diag = 0.0;
+  bool finite = !live || isfinite(r0);
+  // column-major copy of the system (+ shift on the diagonal); entry (i, j)
+  // of the Gram matrix is stored at (min, max)
+  // (batches of 8: loads first, from clamped indices, then the LDS stores)
+  auto load = [&](double shift) __attribute__((always_inline)) {
+    if (live) {
+      for (int j0 = 0; j0 < G; j0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = min(j0 + u, G - 1);
+          v[u] = gr[j <= i ? j * G + i : i * G + j];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + u;
+          if (j < G) {
+            finite &= isfinite(v[u]);
+            if (j == i) diag = (double)v[u];
+            A[(size_t)j * LD + i] = (double)v[u] + (j == i ? shift : 0.0);
+          }
+        }
+      }
+    }
+  };
+  // Right-looking factorisation with the forward substitution; returns in r
+  // this lane's y_i.  Pivot k is read by every lane from LDS.
+  double r = 0.0, minpiv = INFINITY;
+  bool pivots_ok = true;
+  auto factor = [&]() __attribute__((always_inline)) {
+    r = r0;
+    minpiv = INFINITY;
+    pivots_ok = true;
+    if (live) r_s[i] = r;
+    __syncthreads();
+    for (int k = 0; k < G; ++k) {
+      const double piv = A[(size_t)k * LD + k];
+      const double rk = r_s[k];
+      pivots_ok &= piv > 0.0 && isfinite(piv);
+      minpiv = fmin(minpiv, piv);
+      const double rs = rsqrt_f64(piv);
+      if (live && i > k) {
+        const double li = A[(size_t)k * LD + i] * (rs * rs);
+        // A(i, j) -= A(i, k) A(j, k) / A(k, k) for k < j <= i, 8 at a time:
+        // reads first (clamped), then the writes
+        for (int j0 = k + 1; j0 <= i; j0 += 8) {
+          double cv[8], av[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int j = min(j0 + u, i);
+            cv[u] = A[(size_t)k * LD + j];
+            av[u] = A[(size_t)j * LD + i];
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (j0 + u <= i) A[(size_t)(j0 + u) * LD + i] = fma(-li, cv[u], av[u]);
+        }
+        r = fma(-li, rk, r);
+        r_s[i] = r;
+      }
+      if (i == k) {
+        r = rk * rs;
+        rk_s[k] = rs;
+      }
+      __syncthreads();
+    }
+  };
+  auto slot_max = [&](double v) {  // over the work-group's live lanes
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+    if ((i & 63) == 0) red[i >> 6] = v;
+    __syncthreads();
+    v = red[0];
+    if (nthr > 64) v = fmax(v, red[1]);
+    __syncthreads();
+    return v;
+  };
+  auto all_true = [&](bool b) {
+    const bool w = __all(b);
+    if ((i & 63) == 0) red[i >> 6] = w ? 1.0 : 0.0;
+    __syncthreads();
+    bool res = red[0] != 0.0 && (nthr <= 64 || red[1] != 0.0);
+    __syncthreads();
+    return res;
+  };
+
+  load(0.0);
+  const double dmax = slot_max(live ? diag : 0.0);
+  const bool all_finite = all_true(finite);
+  factor();
+  const bool ridge = !all_finite || !pivots_ok ||
+                     !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  bool failed = false;
+  if (ridge) {  // uniform: every lane saw the same pivots
+    __syncthreads();
+    load((double)lam);
+    factor();
+    failed = !(pivots_ok && minpiv > 0.0);
+  }
+
+  // backward substitution L^T s = y: L(k, j) = A(k, j) rk_s[j] for j < k
+  for (int k = G - 1; k >= 0; --k) {
+    if (i == k) {
+      r *= rk_s[k];
+      r_s[k] = r;
+    }
+    __syncthreads();
+    if (live && i < k) r = fma(-A[(size_t)i * LD + k] * rk_s[i], r_s[k], r);
+  }
+
+  if (live && !failed) scales[(size_t)row * G + i] = (float)r;
+  if (i == 0) {
+    if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
+    if (failed) {
+      atomicAdd(&cnt->solve_failed, 1u);
+      atomicAdd(&flags->solve_failed, 1);
+    }
+  }
+}
+
+template <int GS>
+static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const float* gram,
+                                   const float* wh, const uint8_t* codes, const int32_t* zeros,
+                                   float* scales, const uint8_t* active, Counters* cnt,
+                                   Flags* flags, float lam, float rcond) {
+  const int G = cols / GS;
+  const int LD = G | 1;
+  const size_t lds = ((size_t)G * LD + 2 * (size_t)G + 2) * sizeof(double);
+  hipError_t e = hipFuncSetAttribute((const void*)solve_col_kernel<GS>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
+                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond);
+  return hipGetLastError();
+}
+
 template <int GM, int GS>
 static hipError_t launch_solve_reg(hipStream_t st, int rows, int cols, const float* gram,
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
@@ -388,6 +587,17 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
                         float lam, float rcond) {
   const int G = cols / g;
+  if (G > 64 && G <= 128) {
+    switch (g) {
+      case 32: return launch_solve_col<32>(st, rows, cols, gram, wh, codes, zeros, scales, active,
+                                           cnt, flags, lam, rcond);
+      case 64: return launch_solve_col<64>(st, rows, cols, gram, wh, codes, zeros, scales, active,
+                                           cnt, flags, lam, rcond);
+      case 128: return launch_solve_col<128>(st, rows, cols, gram, wh, codes, zeros, scales,
+                                             active, cnt, flags, lam, rcond);
+      default: break;
+    }
+  }
   if (G <= 64) {
 #define JARQ_SOLVE_REG(GM)                                                                        \
   switch (g) {                                                                                    \

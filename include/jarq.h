@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 4
+#define JARQ_ABI_VERSION 5
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
  * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
  * 3 residual product U = E M^T, 4 row objectives and stopping test,
@@ -77,6 +77,9 @@ typedef struct jarq_params {
   float tau;             /* early-stopping threshold of App. E.2 (1e-5 there); < 0 disables */
   float ridge_lambda;    /* lambda added on a near-singular Gram matrix (1e-4, App. E.2) */
   float ridge_rcond;     /* r_cond of the near-singularity test (1e-10, App. E.2) */
+  int32_t ridge_accept;  /* 0: keep every ridge solution (App. E.2); 1: keep a ridge solution
+                            only if it does not increase F_j, else the row keeps its
+                            previous scales (the remark on ridge acceptance, App. G.5) */
 } jarq_params;
 
 /* Filled by jarq_sweeps / jarq_refine when a stats pointer is given [host].

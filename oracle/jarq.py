@@ -20,6 +20,8 @@ App. E.2 as "refit all scales of the row, then visit the groups in order"):
   add 1e-4 I when the spectrum is nonfinite, the smallest eigenvalue is at
   most 1e-10 max(|lambda_max|, eps_fp32) or Cholesky fails; a second failure
   is a numerical error.
+  Optionally (the remark on ridge acceptance, App. G.5) a ridge solution is
+  kept only when it does not increase F_j against the previous scales.
 * early stopping (App. E.2, eq. (strict_stopping)), optional.
 * code update (eqs. (7)-(10)): for i = 1..G, the conditional target
   y^(i,k) subtracts the latest contributions of every other group; with
@@ -146,11 +148,32 @@ def _cholesky_or_none(M):
     return L
 
 
-def solve_scales(gram, rhs, lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND):
+def scale_objective_change(gram, rhs, s_new, s_old):
+    """F_j(s_new) - F_j(s_old) at fixed codes, per row.
+
+    F_j(s) = ||y_j - B_j s||^2 = y_j^T y_j - 2 s^T B_j^T y_j + s^T B_j^T B_j s
+    (eq. (5)), so the difference needs only the Gram matrix and the right-hand
+    side: q(s_new) - q(s_old) with q(s) = s^T (B^T B) s - 2 (B^T y)^T s.
+    """
+    gram = _f64(gram)
+    rhs = _f64(rhs)
+    Gs = 0.5 * (gram + np.swapaxes(gram, 1, 2))
+
+    def q(s):
+        s = _f64(s)
+        return np.einsum("ji,jih,jh->j", s, Gs, s) - 2.0 * np.einsum("ji,ji->j", rhs, s)
+
+    return q(s_new) - q(s_old)
+
+
+def solve_scales(gram, rhs, lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND, prev=None):
     """Solve every row's normal equations eq. (6) with the ridge rule of App. E.2.
 
     Returns (scales [rows, G], ridge [rows] bool).  Raises ScaleSolveError if a
-    row's factorisation fails again after adding lam * I.
+    row's factorisation fails again after adding lam * I.  With ``prev`` (the
+    row's previous scales) a ridge solution that would increase F_j is
+    replaced by ``prev`` (ridge acceptance, the remark of App. G.5); the ridge
+    flag stays set either way.
     """
     gram = _f64(gram)
     rhs = _f64(rhs)
@@ -174,13 +197,20 @@ def solve_scales(gram, rhs, lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND):
         s[j] = solve_triangular(L.T, y, lower=False, check_finite=False)
     if failed:
         raise ScaleSolveError(failed)
+    if prev is not None and np.any(ridge):
+        ir = np.nonzero(ridge)[0]
+        worse = scale_objective_change(gram[ir], rhs[ir], s[ir], _f64(prev)[ir]) > 0.0
+        s[ir[worse]] = _f64(prev)[ir[worse]]
     return s, ridge
 
 
-def scale_step(W, H, codes, zeros, g, lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND):
-    """Joint scale update of Sec. 3.3.1: (scales, ridge flags) for the given codes."""
+def scale_step(W, H, codes, zeros, g, lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND, prev=None):
+    """Joint scale update of Sec. 3.3.1: (scales, ridge flags) for the given codes.
+
+    ``prev`` (previous scales) turns on ridge acceptance (see solve_scales).
+    """
     gram, rhs = gram_system(W, H, codes, zeros, g)
-    return solve_scales(gram, rhs, lam, rcond)
+    return solve_scales(gram, rhs, lam, rcond, prev)
 
 
 @dataclasses.dataclass
@@ -272,13 +302,15 @@ class SweepRecord:
 
 
 def refine(W, H, codes, scales, zeros, g, bits, K, tau=None,
-           lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND, R=None):
+           lam=RIDGE_LAMBDA, rcond=RIDGE_RCOND, R=None, ridge_accept=False):
     """Alternate scale and code updates for K iterations (Sec. 3.3, App. E.2).
 
     ``tau`` None disables early stopping; otherwise a row stops before its
     code update at iteration k >= 2 when the decrease of L between consecutive
     scale updates is at most tau, relatively or absolutely, keeping the new
-    scales.  Returns (codes uint8, scales float64, list of SweepRecord).
+    scales.  ``ridge_accept`` keeps a ridge solution only when it does not
+    increase F_j (the remark of App. G.5).  Returns (codes uint8, scales
+    float64, list of SweepRecord).
     """
     W = _f64(W)
     H = _f64(H)
@@ -294,7 +326,8 @@ def refine(W, H, codes, scales, zeros, g, bits, K, tau=None,
         if not np.any(active):
             break
         ia = np.nonzero(active)[0]
-        s_new, ridge_a = scale_step(W[ia], H, q[ia], zeros[ia], g, lam, rcond)
+        s_new, ridge_a = scale_step(W[ia], H, q[ia], zeros[ia], g, lam, rcond,
+                                    prev=s[ia] if ridge_accept else None)
         s[ia] = s_new
         ridge = np.zeros(rows, dtype=bool)
         ridge[ia] = ridge_a

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libjarq.so")
 MAX_RECORDED_SWEEPS = 64
 NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
 STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
-ABI_VERSION = 4
+ABI_VERSION = 5
 JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
@@ -33,7 +33,8 @@ class Params(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int32), ("cols", ctypes.c_int32),
                 ("group_size", ctypes.c_int32), ("bits", ctypes.c_int32),
                 ("sweeps", ctypes.c_int32), ("tau", ctypes.c_float),
-                ("ridge_lambda", ctypes.c_float), ("ridge_rcond", ctypes.c_float)]
+                ("ridge_lambda", ctypes.c_float), ("ridge_rcond", ctypes.c_float),
+                ("ridge_accept", ctypes.c_int32)]
 
 
 class Stats(ctypes.Structure):
@@ -113,9 +114,9 @@ def status_string(status: int) -> str:
 
 
 def make_params(rows, cols, group_size, bits, sweeps=1, tau=-1.0, ridge_lambda=1e-4,
-                ridge_rcond=1e-10) -> Params:
+                ridge_rcond=1e-10, ridge_accept=False) -> Params:
     return Params(int(rows), int(cols), int(group_size), int(bits), int(sweeps), float(tau),
-                  float(ridge_lambda), float(ridge_rcond))
+                  float(ridge_lambda), float(ridge_rcond), int(bool(ridge_accept)))
 
 
 def workspace_bytes(p: Params) -> int:

@@ -72,6 +72,7 @@ bool valid_params(const jarq_params* p) {
   if (!(p->ridge_lambda >= 0.f) || !isfinite(p->ridge_lambda)) return false;
   if (!(p->ridge_rcond >= 0.f) || !isfinite(p->ridge_rcond)) return false;
   if (isnan(p->tau)) return false;
+  if (p->ridge_accept != 0 && p->ridge_accept != 1) return false;
   if ((size_t)p->rows * (size_t)p->cols > ((size_t)1 << 40)) return false;
   return true;
 }
@@ -120,12 +121,12 @@ Ctx make_ctx(const jarq_params* p, void* ws, void* stream) {
 
 hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes, float* scales,
                               const int32_t* zeros, const uint8_t* active, float lam,
-                              float rcond) {
+                              float rcond, int accept) {
   (void)H;
   hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram());
   if (e != hipSuccess) return e;
   return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, active,
-                      c.cnt(), c.flags(), lam, rcond);
+                      c.cnt(), c.flags(), lam, rcond, accept);
 }
 
 // The Gauss-Seidel code update, panel by panel: each panel's groups are
@@ -216,7 +217,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
     if (e == hipSuccess) e = mark(k, 1);
     if (e == hipSuccess)
       e = launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales,
-                       c.active(), c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond);
+                       c.active(), c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond,
+                       p->ridge_accept);
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
       e = launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay);
@@ -320,7 +322,8 @@ jarq_status jarq_scale_step(const jarq_params* p, const float* H, const uint8_t*
   jarq_status s = check_ws(p, workspace, workspace_bytes);
   if (s != JARQ_OK) return s;
   Ctx c = make_ctx(p, workspace, stream);
-  if (enqueue_scale_step(c, H, codes, scales, zeros, nullptr, p->ridge_lambda, p->ridge_rcond) !=
+  if (enqueue_scale_step(c, H, codes, scales, zeros, nullptr, p->ridge_lambda, p->ridge_rcond,
+                         p->ridge_accept) !=
       hipSuccess)
     return JARQ_EHIP;
   return JARQ_OK;

@@ -126,7 +126,7 @@ hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
-                        float lam, float rcond);
+                        float lam, float rcond, int accept);
 
 // Code update of the groups [i0, i1) (one panel).
 hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,

@@ -9,7 +9,6 @@
 //     factorisation, the backward one reads L transposed through LDS.
 //   solve_col_kernel (64 < G <= 128): the same with the matrix in LDS,
 //     column-major, one row per work-group of 128 lanes.
-//   solve_kernel (any G): one wavefront per row with the matrix in LDS.
 // The stabilised branch of
 // App. E.2 (add lambda I and factor again) is taken when an entry is not
 // finite, a pivot is not positive, or the smallest pivot is at most
@@ -21,187 +20,6 @@
 #include "jarq_internal.h"
 
 namespace jarq {
-
-__device__ __forceinline__ double wave_sum(double x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
-  return x;
-}
-
-__device__ __forceinline__ double wave_min(double x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x = fmin(x, __shfl_xor(x, off));
-  return x;
-}
-
-__device__ __forceinline__ double wave_max(double x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x = fmax(x, __shfl_xor(x, off));
-  return x;
-}
-
-// In-place Cholesky of the lower triangle of A (G x G, leading dimension LD),
-// one wavefront.  Step k scales column k, then the trailing triangle's
-// elements are spread over the lanes (independent updates, no dependent chain
-// per lane).  Returns the smallest pivot before the square root (<= 0 or NaN
-// on failure).
-__device__ double chol_lower(double* A, int G, int LD, int lane) {
-  double minpiv = INFINITY;
-  for (int k = 0; k < G; ++k) {
-    const double piv = A[k * LD + k];
-    minpiv = fmin(minpiv, piv);
-    if (!(piv > 0.0) || !isfinite(piv)) return piv > 0.0 ? NAN : piv;
-    const double d = sqrt(piv);
-    __syncthreads();
-    if (lane == 0) A[k * LD + k] = d;
-    const double inv = 1.0 / d;
-    for (int i = k + 1 + lane; i < G; i += 64) A[i * LD + k] *= inv;
-    __syncthreads();
-    const int n = G - k - 1;            // trailing block rows k+1 .. G-1
-    const int ne = n * (n + 1) / 2;     // its lower triangle, row by row
-    for (int e = lane; e < ne; e += 64) {
-      int ii = (int)((sqrtf(8.f * (float)e + 1.f) - 1.f) * 0.5f);
-      if ((ii + 1) * (ii + 2) / 2 <= e) ++ii;  // guard the float estimate
-      if (ii * (ii + 1) / 2 > e) --ii;
-      const int jj = e - ii * (ii + 1) / 2;
-      const int i = k + 1 + ii, j = k + 1 + jj;
-      A[i * LD + j] -= A[i * LD + k] * A[j * LD + k];
-    }
-    __syncthreads();
-  }
-  return minpiv;
-}
-
-__global__ __launch_bounds__(64) void solve_kernel(int rows, int cols, int g,
-                                                   const float* __restrict__ gram,
-                                                   const float* __restrict__ wh,
-                                                   const uint8_t* __restrict__ codes,
-                                                   const int32_t* __restrict__ zeros,
-                                                   float* __restrict__ scales,
-                                                   const uint8_t* __restrict__ active,
-                                                   Counters* __restrict__ cnt,
-                                                   Flags* __restrict__ flags, float lam,
-                                                   float rcond) {
-  const int G = cols / g;
-  const int LD = G + 1;
-  const int row = blockIdx.x;
-  const int lane = threadIdx.x;
-  if (row >= rows) return;
-  if (active != nullptr && !active[row]) return;
-  extern __shared__ double sm[];
-  double* A = sm;              // G x LD: lower = factor, strict upper = original
-  double* diag = A + G * LD;   // original diagonal
-  double* r = diag + G;        // right-hand side, then the solution
-  const float* gr = gram + (size_t)row * G * G;
-  bool finite = true;
-  double dmax = 0.0;
-  // Only the upper triangle of the Gram matrix is stored: entry (i, h) is read
-  // at (min, max).  Loads go in batches of 16 per lane into registers first
-  // (unconditional, from clamped indices), then to LDS.
-  const int GG = G * G;
-  for (int base = 0; base < GG; base += 64 * 16) {
-    float vv[16];
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int e = min(base + lane + 64 * q, GG - 1);
-      const int i = e / G, h = e % G;
-      vv[q] = gr[(i < h ? i : h) * G + (i < h ? h : i)];
-    }
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int e = base + lane + 64 * q;
-      if (e < GG) {
-        const int i = e / G, h = e % G;
-        finite &= isfinite(vv[q]);
-        A[i * LD + h] = (double)vv[q];
-        if (i == h) {
-          diag[i] = (double)vv[q];
-          dmax = fmax(dmax, (double)vv[q]);
-        }
-      }
-    }
-  }
-  // r_a = sum over group a of c * (W H): lane l takes 4 consecutive columns of
-  // every 256 (coalesced), the g / 4 lanes that share a group combine their
-  // sums, and one of them adds the result into r.  Loads of 8 chunks are
-  // issued together (unconditional, clamped), then reduced.
-  for (int a = lane; a < G; a += 64) r[a] = 0.0;
-  __syncthreads();
-  const int lpg = g / 4;  // lanes per group in one 256-column chunk
-  const float* whr = wh + (size_t)row * cols;
-  const uint8_t* qr = codes + (size_t)row * cols;
-  for (int c00 = 0; c00 < cols; c00 += 256 * 8) {
-    f32x4 w4[8];
-    uint32_t q4[8];
-    int zz[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int c = min(c00 + 256 * t + 4 * lane, cols - 4);  // cols is a multiple of 32
-      w4[t] = *(const f32x4*)(whr + c);
-      q4[t] = *(const uint32_t*)(qr + c);
-      zz[t] = zeros[(size_t)row * G + c / g];
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int c = c00 + 256 * t + 4 * lane;
-      double sum = 0.0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        sum = fma((double)((int)((q4[t] >> (8 * i)) & 0xffu) - zz[t]), (double)w4[t][i], sum);
-      if (c >= cols) sum = 0.0;
-      for (int off = lpg / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
-      if (c < cols && (lane % lpg) == 0) r[c / g] += sum;  // one writer per group
-    }
-  }
-  __syncthreads();
-  for (int a = lane; a < G; a += 64) finite &= isfinite(r[a]);
-  const bool all_finite = __all(finite);
-  dmax = wave_max(dmax);
-  __syncthreads();
-
-  bool ridge = !all_finite;
-  double minpiv = 0.0;
-  if (!ridge) {
-    minpiv = chol_lower(A, G, LD, lane);
-    ridge = !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps)) || !isfinite(minpiv);
-  }
-  if (ridge) {
-    __syncthreads();
-    for (int e = lane; e < G * G; e += 64) {
-      const int i = e / G, h = e % G;
-      if (h < i) A[i * LD + h] = A[h * LD + i];
-      if (h == i) A[i * LD + i] = diag[i] + (double)lam;
-    }
-    __syncthreads();
-    minpiv = chol_lower(A, G, LD, lane);
-    if (!(minpiv > 0.0) || !isfinite(minpiv)) {
-      if (lane == 0) {
-        atomicAdd(&cnt->solve_failed, 1u);
-        atomicAdd(&flags->solve_failed, 1);
-        atomicAdd(&cnt->ridge_rows, 1u);
-      }
-      return;  // keep the previous scales of this row
-    }
-    if (lane == 0) atomicAdd(&cnt->ridge_rows, 1u);
-  }
-  __syncthreads();
-  // Forward substitution L y = r, then L^T s = y (right-looking, lanes over rows).
-  for (int k = 0; k < G; ++k) {
-    if (lane == 0) r[k] /= A[k * LD + k];
-    __syncthreads();
-    const double yk = r[k];
-    for (int i = k + 1 + lane; i < G; i += 64) r[i] -= A[i * LD + k] * yk;
-    __syncthreads();
-  }
-  for (int k = G - 1; k >= 0; --k) {
-    if (lane == 0) r[k] /= A[k * LD + k];
-    __syncthreads();
-    const double sk = r[k];
-    for (int i = lane; i < k; i += 64) r[i] -= A[k * LD + i] * sk;
-    __syncthreads();
-  }
-  for (int a = lane; a < G; a += 64) scales[(size_t)row * G + a] = (float)r[a];
-}
 
 // 1 / sqrt(x) in fp64: the hardware estimate (about 23 bits) and two Newton
 // steps y <- y (3/2 - x y^2 / 2), each of which doubles the correct bits.
@@ -223,7 +41,7 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
                                                        const uint8_t* __restrict__ active,
                                                        Counters* __restrict__ cnt,
                                                        Flags* __restrict__ flags, float lam,
-                                                       float rcond) {
+                                                       float rcond, int accept) {
   constexpr int RPW = 64 / GM;  // rows per wavefront
   constexpr int g = GS;
   const int G = cols / g;
@@ -364,7 +182,30 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
     }
   }
 
-  if (act && live && !failed) scales[(size_t)row * G + i] = (float)r;
+  // Ridge acceptance (the remark of App. G.5, optional): a ridge solution is
+  // kept only when it does not increase F_j.  At fixed codes
+  // F_j(s) = const + s^T G s - 2 r^T s, so the change needs the Gram matrix
+  // (reloaded: A holds the factor) and r only.
+  bool keep_old = false;
+  if (accept && __any(ridge && !failed)) {
+    const double s_new = live ? r : 0.0;
+    const double s_old = live ? (double)scales[(size_t)rr * G + i] : 0.0;
+    load_rows(0.0);
+    col_a[slot][i] = s_new;
+    col_r[slot][i] = s_old;
+    double tn = 0.0, to = 0.0;
+#pragma unroll
+    for (int j = 0; j < GM; ++j) {
+      tn = fma(A[j], col_a[slot][j], tn);
+      to = fma(A[j], col_r[slot][j], to);
+    }
+    double dq = live ? (s_new * tn - 2.0 * r0 * s_new) - (s_old * to - 2.0 * r0 * s_old) : 0.0;
+#pragma unroll
+    for (int off = GM / 2; off >= 1; off >>= 1) dq += __shfl_xor(dq, off);
+    keep_old = ridge && !failed && dq > 0.0;
+  }
+
+  if (act && live && !failed && !keep_old) scales[(size_t)row * G + i] = (float)r;
   if (act && i == 0) {
     if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
     if (failed) {
@@ -390,7 +231,7 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
                                                         const uint8_t* __restrict__ active,
                                                         Counters* __restrict__ cnt,
                                                         Flags* __restrict__ flags, float lam,
-                                                        float rcond) {
+                                                        float rcond, int accept) {
   constexpr int g = GS;
   const int G = cols / g;
   const int LD = G | 1;  // odd stride (in doubles): rows of a column spread over banks
@@ -545,7 +386,45 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
     if (live && i < k) r = fma(-A[(size_t)i * LD + k] * rk_s[i], r_s[k], r);
   }
 
-  if (live && !failed) scales[(size_t)row * G + i] = (float)r;
+  // Ridge acceptance (optional), as in solve_reg_kernel; the Gram matrix is
+  // read again from global memory (A holds the factor).
+  bool keep_old = false;
+  if (accept && ridge && !failed) {  // uniform across the work-group
+    const double s_new = live ? r : 0.0;
+    const double s_old = live ? (double)scales[(size_t)row * G + i] : 0.0;
+    __syncthreads();  // the backward substitution's reads of r_s are done
+    if (live) {
+      r_s[i] = s_new;
+      rk_s[i] = s_old;
+    }
+    __syncthreads();
+    double tn = 0.0, to = 0.0;
+    if (live) {
+      for (int j0 = 0; j0 < G; j0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = min(j0 + u, G - 1);
+          v[u] = gr[j <= i ? j * G + i : i * G + j];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (j0 + u < G) {
+            tn = fma((double)v[u], r_s[j0 + u], tn);
+            to = fma((double)v[u], rk_s[j0 + u], to);
+          }
+      }
+    }
+    double dq = live ? (s_new * tn - 2.0 * r0 * s_new) - (s_old * to - 2.0 * r0 * s_old) : 0.0;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) dq += __shfl_xor(dq, off);
+    if ((i & 63) == 0) red[i >> 6] = dq;
+    __syncthreads();
+    dq = nthr > 64 ? red[0] + red[1] : red[0];
+    keep_old = dq > 0.0;
+  }
+
+  if (live && !failed && !keep_old) scales[(size_t)row * G + i] = (float)r;
   if (i == 0) {
     if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
     if (failed) {
@@ -559,7 +438,7 @@ template <int GS>
 static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const float* gram,
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
                                    float* scales, const uint8_t* active, Counters* cnt,
-                                   Flags* flags, float lam, float rcond) {
+                                   Flags* flags, float lam, float rcond, int accept) {
   const int G = cols / GS;
   const int LD = G | 1;
   const size_t lds = ((size_t)G * LD + 2 * (size_t)G + 2) * sizeof(double);
@@ -567,7 +446,7 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
-                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond);
+                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept);
   return hipGetLastError();
 }
 
@@ -575,26 +454,26 @@ template <int GM, int GS>
 static hipError_t launch_solve_reg(hipStream_t st, int rows, int cols, const float* gram,
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
                                    float* scales, const uint8_t* active, Counters* cnt,
-                                   Flags* flags, float lam, float rcond) {
+                                   Flags* flags, float lam, float rcond, int accept) {
   constexpr int RPW = 64 / GM;
   hipLaunchKernelGGL((solve_reg_kernel<GM, GS>), dim3((rows + RPW - 1) / RPW), dim3(64), 0, st,
-                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond);
+                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept);
   return hipGetLastError();
 }
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
-                        float lam, float rcond) {
+                        float lam, float rcond, int accept) {
   const int G = cols / g;
   if (G > 64 && G <= 128) {
     switch (g) {
       case 32: return launch_solve_col<32>(st, rows, cols, gram, wh, codes, zeros, scales, active,
-                                           cnt, flags, lam, rcond);
+                                           cnt, flags, lam, rcond, accept);
       case 64: return launch_solve_col<64>(st, rows, cols, gram, wh, codes, zeros, scales, active,
-                                           cnt, flags, lam, rcond);
+                                           cnt, flags, lam, rcond, accept);
       case 128: return launch_solve_col<128>(st, rows, cols, gram, wh, codes, zeros, scales,
-                                             active, cnt, flags, lam, rcond);
+                                             active, cnt, flags, lam, rcond, accept);
       default: break;
     }
   }
@@ -602,11 +481,11 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
 #define JARQ_SOLVE_REG(GM)                                                                        \
   switch (g) {                                                                                    \
     case 32: return launch_solve_reg<GM, 32>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond);                     \
+                                             active, cnt, flags, lam, rcond, accept);                     \
     case 64: return launch_solve_reg<GM, 64>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond);                     \
+                                             active, cnt, flags, lam, rcond, accept);                     \
     case 128: return launch_solve_reg<GM, 128>(st, rows, cols, gram, wh, codes, zeros, scales,    \
-                                               active, cnt, flags, lam, rcond);                   \
+                                               active, cnt, flags, lam, rcond, accept);                   \
     default: break;                                                                               \
   }
     if (G <= 32) {
@@ -616,13 +495,7 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
     }
 #undef JARQ_SOLVE_REG
   }
-  const size_t lds = ((size_t)G * (G + 1) + 2 * (size_t)G) * sizeof(double);
-  hipError_t e = hipFuncSetAttribute((const void*)solve_kernel,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(solve_kernel, dim3(rows), dim3(64), lds, st, rows, cols, g, gram, wh, codes,
-                     zeros, scales, active, cnt, flags, lam, rcond);
-  return hipGetLastError();
+  return hipErrorInvalidValue;  // G > 128 is rejected by the API
 }
 
 }  // namespace jarq

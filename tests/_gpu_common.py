@@ -67,10 +67,12 @@ def random_layer(rows, cols, g, bits, seed, corr=0.5):
 class GpuLayer:
     """Device copies of one layer plus a prepared workspace."""
 
-    def __init__(self, W, H, q, s, z, g, bits, sweeps=1, tau=-1.0, prepare=True):
+    def __init__(self, W, H, q, s, z, g, bits, sweeps=1, tau=-1.0, prepare=True,
+                 ridge_accept=False):
         self.rows, self.cols = W.shape
         self.g, self.bits = g, bits
-        self.p = jq.make_params(self.rows, self.cols, g, bits, sweeps, tau)
+        self.p = jq.make_params(self.rows, self.cols, g, bits, sweeps, tau,
+                                ridge_accept=ridge_accept)
         self.W = to_dev(W)
         self.H = to_dev(H)
         self.codes = to_dev(q)

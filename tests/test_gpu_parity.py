@@ -218,6 +218,28 @@ def test_ridge_branch_matches_oracle():
     assert st["ridge_rows"][0] == 2
 
 
+@pytest.mark.parametrize("cols,g", [(256, 64), (4608, 64)])
+def test_ridge_acceptance_matches_oracle(cols, g):
+    # Rows 3 and 17 have a group at its zero point (rank-deficient B_j).  With H
+    # scaled by 1e-8 the ridge term dominates and the ridge solution raises F_j:
+    # ridge acceptance keeps those rows' scales; unscaled, it keeps the ridge
+    # solution.  G = 4 and G = 72 cover both solve kernels.
+    W, H, q, s, z = random_layer(40, cols, g, 3, seed=5)
+    q = q.copy()
+    q[3, g:2 * g] = z[3, 1]
+    q[17, 0:g] = z[17, 0]
+    for h_scale, keeps_old in ((1e-8, True), (1.0, False)):
+        Hs = np.ascontiguousarray((H.astype(np.float64) * h_scale).astype(np.float32))
+        gl = GpuLayer(W, Hs, q, s, z, g, 3, ridge_accept=True)
+        gl.scale_step()
+        _, s_gpu = gl.state()
+        s_ref, ridge = jarq.scale_step(W, Hs, q, z, g, prev=s)
+        assert ridge[3] and ridge[17] and ridge.sum() == 2
+        for j in (3, 17):
+            assert np.array_equal(s_gpu[j], s[j]) == keeps_old, (h_scale, j)
+        check_scales(s_gpu, s_ref, f" ridge accept h_scale {h_scale}")
+
+
 def test_small_scale_groups_are_skipped():
     W, H, q, s, z = random_layer(20, 256, 64, 3, seed=6)
     gl = GpuLayer(W, H, q, s, z, 64, 3)

@@ -327,6 +327,74 @@ def test_ridge_branch_on_singular_gram():
     assert np.allclose(s[0], expect, rtol=1e-10)
 
 
+def _ridge_worse_layer(h_scale=1e-8, seed=23):
+    """A layer whose row 0 takes the ridge branch (one group at its zero point,
+    so B_0 is rank deficient).  With H scaled by 1e-8, lambda = 1e-4 dominates
+    the Gram entries (largest eigenvalue ~ 4e-6): the ridge solution shrinks
+    every scale toward zero and raises F_0 above the host's."""
+    rng = np.random.default_rng(seed)
+    g, G = 4, 3
+    H = h_scale * _random_problem(rng, g * G)
+    W = 0.1 * rng.standard_normal((3, g * G))
+    from synth import rtn_quantize
+    codes, scales, zeros = rtn_quantize(W, g, 3)
+    codes[0, g:2 * g] = zeros[0, 1]
+    return W, H, codes, scales.astype(np.float64), zeros, g
+
+
+def test_scale_objective_change_matches_the_objective():
+    """F(s_new) - F(s_old) from the Gram system equals the objective eq. (4) evaluated directly."""
+    rng = np.random.default_rng(29)
+    g, G = 4, 3
+    H = _random_problem(rng, g * G)
+    W = 0.1 * rng.standard_normal((5, g * G))
+    from synth import rtn_quantize
+    codes, scales, zeros = rtn_quantize(W, g, 3)
+    gram, rhs = jarq.gram_system(W, H, codes, zeros, g)
+    s_old = scales.astype(np.float64)
+    s_new = s_old * (1.0 + 0.3 * rng.standard_normal(s_old.shape))
+    got = jarq.scale_objective_change(gram, rhs, s_new, s_old)
+    want = (jarq.objective_rows(W, H, codes, s_new, zeros, g)
+            - jarq.objective_rows(W, H, codes, s_old, zeros, g))
+    assert np.allclose(got, want, rtol=1e-9, atol=1e-14)
+
+
+def test_ridge_acceptance_keeps_previous_scales_when_worse():
+    """Remark of App. G.5: a ridge solution that raises F_j is not kept."""
+    W, H, codes, s_prev, zeros, g = _ridge_worse_layer()
+    s_plain, ridge = jarq.scale_step(W, H, codes, zeros, g)
+    assert ridge[0] and not ridge[1:].any()
+    F = lambda s: jarq.objective_rows(W, H, codes, s, zeros, g)
+    assert F(s_plain)[0] > F(s_prev)[0]                 # the failure the remark describes
+    s_acc, ridge_acc = jarq.scale_step(W, H, codes, zeros, g, prev=s_prev)
+    assert np.array_equal(ridge_acc, ridge)
+    assert np.array_equal(s_acc[0], s_prev[0])          # previous scales retained
+    assert np.array_equal(s_acc[1:], s_plain[1:])       # ordinary solves untouched
+    assert np.all(F(s_acc) <= F(s_prev) * (1 + 1e-12))
+
+
+def test_ridge_acceptance_keeps_a_better_ridge_solution():
+    """On the unscaled problem the ridge solution of the same row lowers F and is kept."""
+    W, H, codes, s_prev, zeros, g = _ridge_worse_layer(h_scale=1.0)
+    s_plain, ridge = jarq.scale_step(W, H, codes, zeros, g)
+    F = lambda s: jarq.objective_rows(W, H, codes, s, zeros, g)
+    assert ridge[0] and F(s_plain)[0] < F(s_prev)[0]
+    s_acc, _ = jarq.scale_step(W, H, codes, zeros, g, prev=s_prev)
+    assert np.array_equal(s_acc, s_plain)
+
+
+def test_ridge_acceptance_makes_the_objective_monotone():
+    """With ridge acceptance L_j^(k) (after each scale update) never increases (Thm. 1 (i))."""
+    W, H, codes, s_prev, zeros, g = _ridge_worse_layer()
+    F0 = jarq.objective_rows(W, H, codes, s_prev, zeros, g)
+    _, _, hist = jarq.refine(W, H, codes, s_prev, zeros, g, 3, 4, ridge_accept=True)
+    L = np.stack([h.L for h in hist])
+    assert np.all(L[0] <= F0 * (1 + 1e-12))
+    assert np.all(np.diff(L, axis=0) <= 1e-12 * np.abs(L[:-1]))
+    _, _, hist_plain = jarq.refine(W, H, codes, s_prev, zeros, g, 3, 1)
+    assert hist_plain[0].L[0] > F0[0]                   # without it the first update goes up
+
+
 def test_ridge_second_failure_raises():
     """A nonfinite coupling block makes the Gram matrix nonfinite: ridge, then failure."""
     g = 2

@@ -135,6 +135,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--tau", type=float, default=-1.0,
+                    help="early-stopping threshold (App. E.2 uses 1e-5); negative = off (default)")
     ap.add_argument("--cpu-rows", type=int, default=4096)
     ap.add_argument("--cpu-sweeps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -177,7 +179,7 @@ def main():
     qh, sh, zd = torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev), torch.from_numpy(z).to(dev)
     rows, cols = W.shape
 
-    p = jq.make_params(rows, cols, g, bits, args.steps)
+    p = jq.make_params(rows, cols, g, bits, args.steps, args.tau)
     ws = jq.alloc_workspace(p, dev)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -187,7 +189,7 @@ def main():
     log(f"[bench] prepare {prep_ms:.2f} ms")
 
     if args.warmup > 0:
-        pw = jq.make_params(rows, cols, g, bits, args.warmup)
+        pw = jq.make_params(rows, cols, g, bits, args.warmup, args.tau)
         qw, sw = qh.clone(), sh.clone()
         jq.sweeps(pw, Wd, Hd, qw, sw, zd, ws)
         del qw, sw
@@ -198,8 +200,10 @@ def main():
     st = jq.sweeps(p, Wd, Hd, qd, sd, zd, ws, stage_mask=1 << res_stage)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3
-    ms_per_step = wall_ms / args.steps
-    log(f"[bench] {args.steps} sweeps in {wall_ms:.2f} ms")
+    # With early stopping a run can end before its budget (every row stopped):
+    # the time is per sweep run.
+    ms_per_step = wall_ms / max(st["sweeps_run"], 1)
+    log(f"[bench] {st['sweeps_run']} sweeps in {wall_ms:.2f} ms")
     n = min(args.steps, len(st["stage_ms"]))
     res_ms = float(np.mean([st["stage_ms"][k][res_stage] for k in range(n)]))
 
@@ -242,12 +246,15 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": workload_text(cfg, rows, cols, args.steps),
-                   "rows": rows, "cols": cols, "group_size": g, "bits": bits},
+                   "rows": rows, "cols": cols, "group_size": g, "bits": bits,
+                   "tau": args.tau if args.tau >= 0 else None},
         "rows_per_s": rows / (ms_per_step * 1e-3),
         "prep_ms": prep_ms,
         "stage_ms": stage_ms,
         "stage_ms_note": "separate untimed run of the same sweeps with HIP events around every stage",
         "accepted_groups": st["accepted_groups"][:n],
+        "rows_active": st["rows_active"][:n],
+        "sweeps_run": st["sweeps_run"],
         "objective_after_scales": st["objective_after_scales"][:n],
         "roofline": roofline,
         "stage_rates_tflops": {name: (work[name] / (stage_ms[name] * 1e-3) / 1e12

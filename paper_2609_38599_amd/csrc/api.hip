@@ -48,6 +48,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
   L.active = take(R);
+  L.rowmap = take(R * sizeof(int32_t));
   L.counters = take(sizeof(Counters));
   L.hist = take(JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord));
   L.flags = take(sizeof(Flags));
@@ -99,6 +100,7 @@ struct Ctx {
   Flags* flags() const { return (Flags*)(ws + lay.flags); }
   SweepRecord* hist() const { return (SweepRecord*)(ws + lay.hist); }
   uint8_t* active() const { return (uint8_t*)(ws + lay.active); }
+  int32_t* rowmap() const { return (int32_t*)(ws + lay.rowmap); }
   float* wh() const { return (float*)(ws + lay.wh); }
   float* gram() const { return (float*)(ws + lay.gram); }
   float* pbuf() const { return (float*)(ws + lay.p); }
@@ -123,29 +125,31 @@ hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes
                               const int32_t* zeros, const uint8_t* active, float lam,
                               float rcond, int accept) {
   (void)H;
-  hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram());
+  hipError_t e =
+      launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(), nullptr);
   if (e != hipSuccess) return e;
   return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, active,
-                      c.cnt(), c.flags(), lam, rcond, accept);
+                      c.cnt(), c.flags(), lam, rcond, accept, nullptr);
 }
 
 // The Gauss-Seidel code update, panel by panel: each panel's groups are
 // decoded in order by the Babai kernel, then their accepted changes are folded
-// into the residual product of every later column.
-hipError_t enqueue_babai(const Ctx& c, const float* H, uint8_t* codes, const float* scales,
-                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
-                         uint8_t* decision) {
+// into the residual product of every later column.  `n` positions of the
+// sweep, position p holding layer row map_row(rowmap, p).
+hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const float* H,
+                         uint8_t* codes, const float* scales, const int32_t* zeros,
+                         const uint8_t* active, uint8_t* cand, uint8_t* decision) {
   (void)H;
   const int nb = panel_groups(c.g);
   hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, (size_t)(c.cols + 511) / 512 * sizeof(uint32_t));
   if (e0 != hipSuccess) return e0;
   for (int i0 = 0; i0 < c.G; i0 += nb) {
     const int i1 = i0 + nb < c.G ? i0 + nb : c.G;
-    hipError_t e = launch_babai(c.st, c.rows, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay,
-                                codes, scales, zeros, active, cand, decision, c.cnt());
+    hipError_t e = launch_babai(c.st, n, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay,
+                                codes, scales, zeros, active, cand, decision, c.cnt(), rowmap);
     if (e != hipSuccess) return e;
-    e = launch_panel_update(c.st, c.rows, c.cols, c.g, i0 * c.g, i1 * c.g, c.ws, c.lay, scales,
-                            c.pbuf());
+    e = launch_panel_update(c.st, n, c.cols, c.g, i0 * c.g, i1 * c.g, c.ws, c.lay, scales,
+                            c.pbuf(), rowmap);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -210,28 +214,35 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   };
   jarq_status status = JARQ_OK;
   int run = 0;
+  // Active-set compaction: a sweep works on the n rows still active when it
+  // starts, in ascending order (rowmap, built once rows have stopped; null
+  // while every row takes part).  Rows stopped in earlier sweeps cost nothing.
+  int n = c.rows;
+  const int32_t* rmap = nullptr;
   for (int k = 0; k < K; ++k) {
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = mark(k, 0);
-    if (e == hipSuccess) e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram());
+    if (e == hipSuccess)
+      e = launch_gram(c.st, n, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(), rmap);
     if (e == hipSuccess) e = mark(k, 1);
     if (e == hipSuccess)
-      e = launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales,
-                       c.active(), c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond,
-                       p->ridge_accept);
+      e = launch_solve(c.st, n, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, c.active(),
+                       c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond, p->ridge_accept,
+                       rmap);
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
-      e = launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay);
+      e = launch_split_e(c.st, n, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay, rmap);
     if (e == hipSuccess) e = mark(k, 3);
-    if (e == hipSuccess) e = launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf());
+    if (e == hipSuccess) e = launch_split_gemm(c.st, n, c.cols, c.ws, c.lay, c.pbuf());
     if (e == hipSuccess) e = mark(k, 4);
     if (e == hipSuccess)
-      e = launch_group_objective(c.st, c.rows, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
+      e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
     if (e == hipSuccess)
-      e = launch_stop_check(c.st, c.rows, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
-                            (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau);
+      e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
+                            (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau, rmap);
     if (e == hipSuccess) e = mark(k, 5);
-    if (e == hipSuccess) e = enqueue_babai(c, H, codes, scales, zeros, c.active(), nullptr, nullptr);
+    if (e == hipSuccess)
+      e = enqueue_babai(c, n, rmap, H, codes, scales, zeros, c.active(), nullptr, nullptr);
     if (e == hipSuccess) e = mark(k, 6);
     if (e == hipSuccess)
       e = launch_record_sweep(c.st, c.rows, (const double*)(c.ws + c.lay.lcur), c.active(),
@@ -254,6 +265,14 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
         break;
       }
       if (rec.active_rows == 0) break;
+      if ((int)rec.active_rows < n) {
+        if (launch_compact_rows(c.st, c.rows, c.active(), c.rowmap()) != hipSuccess) {
+          status = JARQ_EHIP;
+          break;
+        }
+        n = (int)rec.active_rows;
+        rmap = c.rowmap();
+      }
     }
   }
   if (hipStreamSynchronize(c.st) != hipSuccess) status = JARQ_EHIP;
@@ -339,11 +358,12 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
   jarq_status s = check_ws(p, workspace, workspace_bytes);
   if (s != JARQ_OK) return s;
   Ctx c = make_ctx(p, workspace, stream);
-  if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay) !=
-          hipSuccess ||
+  if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay,
+                     nullptr) != hipSuccess ||
       launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf()) != hipSuccess)
     return JARQ_EHIP;
-  if (enqueue_babai(c, H, codes, scales, zeros, nullptr, cand, decision) != hipSuccess)
+  if (enqueue_babai(c, c.rows, nullptr, H, codes, scales, zeros, nullptr, cand, decision) !=
+      hipSuccess)
     return JARQ_EHIP;
   return JARQ_OK;
 }

@@ -177,7 +177,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     const float* __restrict__ scales, const uint8_t* __restrict__ active,
     _Float16* __restrict__ dq, int32_t* __restrict__ plist, uint32_t* __restrict__ pcount,
     uint8_t* __restrict__ cand_out,
-    uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt) {
+    uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt,
+    const int32_t* __restrict__ rowmap) {
   constexpr int g = G_SIZE;
   constexpr int RT = 16;                 // rows per work-group
   constexpr int NT = g / 16;             // positions per lane in the back substitution
@@ -210,9 +211,12 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   // back-substitution role (waves 0-3): 16 lanes per row
   const int crow = (wave & 3) * 4 + (lane >> 4);
   const int cj = lane & 15;
+  // Tile rows are positions of the sweep (P, dq, the panel row list); the
+  // layer row of position p (codes, scales, flags) is map_row(rowmap, p).
   const int grow = r0 + crow;
   const bool row_in = grow < rows;
-  const bool row_act = row_in && (active == nullptr || active[grow] != 0);
+  const int crid = map_row(rowmap, row_in ? grow : 0);
+  const bool row_act = row_in && (active == nullptr || active[crid] != 0);
   // preparation role (waves 4-7): matrix-core lanes, A row / B column = lane & 15,
   // k slice = lane >> 4, output rows 4 (lane >> 4) + v
   const int pw = wave - 4;
@@ -225,14 +229,12 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   if (tid < 4) cnt_s[tid] = 0;
   if (tid < RT) racc_s[tid] = 0;
 
-  // Bases of this work-group's 16 rows (wave-uniform); offsets from them fit
-  // in 32 bits (16 rows of at most 2^26 columns).
+  // Bases of this work-group's 16 positions (wave-uniform); offsets from them
+  // fit in 32 bits (16 rows of at most 2^26 columns).
   const float* __restrict__ P_t = P + (size_t)r0 * cols;
-  uint8_t* __restrict__ codes_t = codes + (size_t)r0 * cols;
   _Float16* __restrict__ dq_t = dq + (size_t)r0 * cols;
-  const float* __restrict__ scales_t = scales + (size_t)r0 * G;
-  // Local row of a lane, or row 0 past the edge (loads stay unconditional;
-  // such values are never used).
+  // Local position of a lane, or position 0 past the edge (loads stay
+  // unconditional; such values are never used).
   auto lrow = [&](int lr) { return (uint32_t)(r0 + lr < rows ? lr : 0); };
   const uint32_t ucols = (uint32_t)cols;
 
@@ -267,6 +269,11 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     float sh[4];
     float cs[BPW];
   };
+  // scales of the layer rows of this lane's 4 output rows (preparation role)
+  const float* sc_rows[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v)
+    sc_rows[v] = scales + (size_t)map_row(rowmap, r0 + (int)lrow(4 * kq + v)) * G;
   auto load_t = [&](int i, int h, TFrag& f) {
     // rows i g .. i g + g - 1 of M (uniform bases), this lane's row n within
     const _Float16* mh_i = Mh + (size_t)i * g * cols;
@@ -283,8 +290,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       f.cs[b] = ld_at(mrow_inv + i * g, (uint32_t)(n * 4));
     }
 #pragma unroll
-    for (int v = 0; v < 4; ++v)
-      f.sh[v] = ld_at(scales_t, (lrow(4 * kq + v) * (uint32_t)G + (uint32_t)h) * 4u);
+    for (int v = 0; v < 4; ++v) f.sh[v] = sc_rows[v][h];
   };
   // uacc -= s_h dq_h M(i-block, h-block)^T (dq_h exact in fp16, M as two fp16
   // terms).  dq_h is zero in every row of the tile unless one of them accepted
@@ -328,16 +334,17 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   // them waits for its data here; row_in is applied where they are used.
   uint32_t nq[NT];
   float nrdinv[NT], nrdsq[NT], ns = 0.f;
-  const uint32_t srow = lrow(crow);
+  const uint8_t* __restrict__ codes_c = codes + (size_t)crid * cols;  // this lane's row
+  const float* __restrict__ scales_c = scales + (size_t)crid * G;
   auto chain_prefetch = [&](int i) {
-    const uint32_t cb = srow * ucols + (uint32_t)(i * g + cj);
+    const uint32_t cb = (uint32_t)(i * g + cj);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      nq[t] = ld_at(codes_t, cb + 16 * t);
+      nq[t] = ld_at(codes_c, cb + 16 * t);
       nrdinv[t] = ld_at(rdinv + i * g, (uint32_t)((cj + 16 * t) * 4));
       nrdsq[t] = ld_at(rdsq + i * g, (uint32_t)((cj + 16 * t) * 4));
     }
-    ns = ld_at(scales_t, (srow * (uint32_t)G + (uint32_t)i) * 4u);
+    ns = scales_c[i];
   };
   // The two roles run separate loops with the same barriers (two per group),
   // so neither role's loop-carried registers are live in the other's code.
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         dqp_s[crow * PW + (i - i0) * g + l] = accept ? (_Float16)cs.d[t] : (_Float16)0.f;
       }
       if (cand_out != nullptr && row_in) {
-        const size_t cbase = (size_t)grow * cols + (size_t)i * g;
+        const size_t cbase = (size_t)crid * cols + (size_t)i * g;
 #pragma unroll
         for (int t = 0; t < NT; ++t)
           cand_out[cbase + cj + 16 * t] =
@@ -405,7 +412,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       if (row_in && cj == 0) {
         if (dec_out != nullptr) {
           uint8_t dd = !row_act ? kDecStopped : (skip ? kDecSkip : (accept ? kDecAccept : kDecReject));
-          dec_out[(size_t)grow * G + i] = dd;
+          dec_out[(size_t)crid * G + i] = dd;
         }
         if (accept) {
           tacc_s[i - i0] = 1;
@@ -505,9 +512,11 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       const int k = (c - r * per_row) * 16;
       if (r0 + r < rows) {
         const uint32_t o = (uint32_t)r * ucols + (uint32_t)(i0 * g + k);
+        uint8_t* codes_r = codes + (size_t)map_row(rowmap, r0 + r) * cols;
+        const uint32_t oq = (uint32_t)(i0 * g + k);
         const f16x8 d0 = *(const f16x8*)(dqp_s + r * PW + k);
         const f16x8 d1 = *(const f16x8*)(dqp_s + r * PW + k + 8);
-        const uint4 qw = ld_at((const uint4*)codes_t, o);
+        const uint4 qw = ld_at((const uint4*)codes_r, oq);
         uint32_t w[4] = {qw.x, qw.y, qw.z, qw.w};
         // Byte b of word b / 4 gains d_b; new codes stay in [0, 2^bits - 1],
         // so the word-wide add never carries into a neighbouring byte.
@@ -516,7 +525,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
           const int dv = (int)(b < 8 ? d0[b] : d1[b - 8]);
           w[b >> 2] += (uint32_t)dv << (8 * (b & 3));
         }
-        st_at((uint4*)codes_t, o, make_uint4(w[0], w[1], w[2], w[3]));
+        st_at((uint4*)codes_r, oq, make_uint4(w[0], w[1], w[2], w[3]));
         st_at((f16x8*)dq_t, 2 * o, d0);
         st_at((f16x8*)dq_t, 2 * o + 16, d1);
       }
@@ -534,7 +543,8 @@ template <int G_SIZE>
 static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, int i0, int i1,
                                  const float* P, const char* ws, const Layout& lay,
                                  uint8_t* codes, const float* scales, const uint8_t* active,
-                                 uint8_t* cand, uint8_t* decision, Counters* cnt) {
+                                 uint8_t* cand, uint8_t* decision, Counters* cnt,
+                                 const int32_t* rowmap) {
   constexpr int g = G_SIZE;
   constexpr int PG = panel_groups_of(g);
   if (i1 - i0 > PG || i0 % PG != 0) return hipErrorInvalidValue;
@@ -548,7 +558,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.rdinv),
                      (const float*)(ws + lay.rdsq), codes, scales, active,
                      (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
-                     (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt);
+                     (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt, rowmap);
   return hipGetLastError();
 }
 
@@ -556,18 +566,18 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
                         const float* P,
                         const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
-                        uint8_t* decision, Counters* cnt) {
+                        uint8_t* decision, Counters* cnt, const int32_t* rowmap) {
   (void)zeros;
   switch (g) {
     case 32:
       return launch_babai_t<32>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt);
+                                cand, decision, cnt, rowmap);
     case 64:
       return launch_babai_t<64>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt);
+                                cand, decision, cnt, rowmap);
     case 128:
       return launch_babai_t<128>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                 cand, decision, cnt);
+                                 cand, decision, cnt, rowmap);
     default:
       return hipErrorInvalidValue;
   }

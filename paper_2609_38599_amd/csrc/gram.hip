@@ -43,7 +43,8 @@ __global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
                                                       const float* __restrict__ h_inv,
                                                       const uint8_t* __restrict__ codes,
                                                       const int32_t* __restrict__ zeros,
-                                                      float* __restrict__ gram) {
+                                                      float* __restrict__ gram,
+                                                      const int32_t* __restrict__ rowmap) {
   constexpr int g = G_SIZE;
   constexpr int NAB = g / 32;            // 32-weight blocks of an a-group
   constexpr int WPA = 4 / NAB;           // waves sharing an a-block
@@ -76,10 +77,11 @@ __global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
   int stz = 0;
   const int trow = tid / TPR, tpart = tid % TPR;
   const int srow = r0 + trow;
-  // Rows past the edge load row 0 (unconditional loads, so that none is
-  // waited for here): each row's Gram entries depend on that row only, and
-  // those of rows past the edge are never stored.
-  const int lrow = srow < rows ? srow : 0;
+  // Tile rows are positions of the sweep (Gram output) holding layer rows
+  // (codes, zero points).  Positions past the edge load position 0
+  // (unconditional loads, so that none is waited for here): each row's Gram
+  // entries depend on that row only, and those past the edge are never stored.
+  const int lrow = map_row(rowmap, srow < rows ? srow : 0);
   auto fetch_codes = [&](int blk) {
     const u32x4* src = (const u32x4*)(codes + (size_t)lrow * cols + (size_t)blk * g + tpart * CPT);
 #pragma unroll
@@ -194,7 +196,7 @@ __global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
 template <int G_SIZE>
 static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* ws,
                                 const Layout& lay, const uint8_t* codes, const int32_t* zeros,
-                                float* gram) {
+                                float* gram, const int32_t* rowmap) {
   constexpr int g = G_SIZE;
   const int G = cols / g;
   const size_t lds = (size_t)2 * RT * (g + 8) * sizeof(_Float16) + (size_t)(g / 32) * RT * sizeof(double);
@@ -204,17 +206,17 @@ static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* 
   dim3 grid((rows + RT - 1) / RT, (G + 1) / 2);
   hipLaunchKernelGGL(gram_kernel<g>, grid, dim3(256), lds, st, rows, cols,
                      (const _Float16*)(ws + lay.hhi), (const _Float16*)(ws + lay.hlo),
-                     (const float*)(ws + lay.hscale), codes, zeros, gram);
+                     (const float*)(ws + lay.hscale), codes, zeros, gram, rowmap);
   return hipGetLastError();
 }
 
 hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,
                        const Layout& lay, const uint8_t* codes, const int32_t* zeros,
-                       float* gram) {
+                       float* gram, const int32_t* rowmap) {
   switch (g) {
-    case 32: return launch_gram_t<32>(st, rows, cols, ws, lay, codes, zeros, gram);
-    case 64: return launch_gram_t<64>(st, rows, cols, ws, lay, codes, zeros, gram);
-    case 128: return launch_gram_t<128>(st, rows, cols, ws, lay, codes, zeros, gram);
+    case 32: return launch_gram_t<32>(st, rows, cols, ws, lay, codes, zeros, gram, rowmap);
+    case 64: return launch_gram_t<64>(st, rows, cols, ws, lay, codes, zeros, gram, rowmap);
+    case 128: return launch_gram_t<128>(st, rows, cols, ws, lay, codes, zeros, gram, rowmap);
     default: return hipErrorInvalidValue;
   }
 }

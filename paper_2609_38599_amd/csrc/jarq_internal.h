@@ -80,6 +80,7 @@ struct Layout {
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64
   size_t active;    // [rows] u8
+  size_t rowmap;    // [rows] i32: row of each position of the sweep (rows still active, ascending)
   size_t counters;  // Counters
   size_t hist;      // [64] SweepRecord
   size_t flags;     // Flags
@@ -106,9 +107,10 @@ hipError_t launch_split_h(hipStream_t st, int cols, const float* H, char* ws, co
 hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char* ws,
                           const Layout& lay);
 
+// `rows` positions of the sweep; position p holds layer row map_row(rowmap, p).
 hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
                           const uint8_t* codes, const float* scales, const int32_t* zeros,
-                          char* ws, const Layout& lay);
+                          char* ws, const Layout& lay, const int32_t* rowmap);
 
 // P = E H from the fp16 planes of E and H in the workspace (three products);
 // objpart as for launch_gemm_ah (may be null).
@@ -121,18 +123,18 @@ hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, con
 // Upper triangles of the grouped Gram matrices from the fp16 planes of H.
 hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,
                        const Layout& lay, const uint8_t* codes, const int32_t* zeros,
-                       float* gram);
+                       float* gram, const int32_t* rowmap);
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
-                        float lam, float rcond, int accept);
+                        float lam, float rcond, int accept, const int32_t* rowmap);
 
 // Code update of the groups [i0, i1) (one panel).
 hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,
                         const float* P, const char* ws, const Layout& lay, uint8_t* codes,
                         const float* scales, const int32_t* zeros, const uint8_t* active,
-                        uint8_t* cand, uint8_t* decision, Counters* cnt);
+                        uint8_t* cand, uint8_t* decision, Counters* cnt, const int32_t* rowmap);
 
 // Work-group barrier for LDS only: waits for this wave's LDS operations,
 // not for its outstanding global loads (a __syncthreads would, which drains
@@ -147,6 +149,18 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Early stopping shrinks the set of rows a sweep works on.  Per-sweep
+// intermediates (Gram matrices, E planes, U, objective partials, dq, the
+// panel row lists) are indexed by position p < n in the sweep's row list; the
+// layer's state (W, codes, scales, zeros, W H, stopping state) by row.  The
+// list is null while every row takes part (position = row).
+__device__ __forceinline__ int map_row(const int32_t* rowmap, int p) {
+  return rowmap != nullptr ? rowmap[p] : p;
+}
+
+// rowmap[0 .. n) = the rows with active[r] != 0, ascending (one work-group).
+hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, int32_t* rowmap);
+
 // Groups per panel of the code update (512 columns, at most 16 groups).
 constexpr int kMaxPanelGroups = 16;
 constexpr int panel_groups_of(int g) { return 512 / g < kMaxPanelGroups ? 512 / g : kMaxPanelGroups; }
@@ -155,14 +169,15 @@ int panel_groups(int g);
 // P(:, c1:) -= the accepted changes of the groups in columns [c0, c1) (the
 // panel's rows listed by the code update in plist / pcount[panel]).
 hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0, int c1,
-                               const char* ws, const Layout& lay, const float* scales, float* P);
+                               const char* ws, const Layout& lay, const float* scales, float* P,
+                               const int32_t* rowmap);
 
 hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
                                 double* out);
 
 hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int sweep,
-                             float tau);
+                             float tau, const int32_t* rowmap);
 
 hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);
 hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n);

@@ -25,14 +25,16 @@ hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* 
 // code update) when (L^(k-1) - L^(k)) / max(|L^(k-1)|, eps) <= tau or
 // |L^(k-1) - L^(k)| <= tau (App. E.2, eq. (strict_stopping)).  The new scales
 // are kept.
-__global__ void stop_check_kernel(int rows, int nt, const double* __restrict__ part,
+__global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part,
                                   double* __restrict__ lcur, double* __restrict__ lprev,
-                                  uint8_t* __restrict__ active, int sweep, float tau) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= rows) return;
+                                  uint8_t* __restrict__ active, int sweep, float tau,
+                                  const int32_t* __restrict__ rowmap) {
+  const int pos = blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos >= n) return;
+  const int r = map_row(rowmap, pos);
   if (!active[r]) return;
   double s = 0.0;
-  for (int t = 0; t < nt; ++t) s += part[(size_t)r * nt + t];
+  for (int t = 0; t < nt; ++t) s += part[(size_t)pos * nt + t];
   lcur[r] = s;
   if (tau >= 0.f && sweep >= 2) {
     const double prev = lprev[r];
@@ -43,11 +45,41 @@ __global__ void stop_check_kernel(int rows, int nt, const double* __restrict__ p
   lprev[r] = s;
 }
 
-hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
+hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int sweep,
-                             float tau) {
-  hipLaunchKernelGGL(stop_check_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, rows, nt,
-                     objpart, lcur, lprev, active, sweep, tau);
+                             float tau, const int32_t* rowmap) {
+  hipLaunchKernelGGL(stop_check_kernel, dim3((n + 255) / 256), dim3(256), 0, st, n, nt,
+                     objpart, lcur, lprev, active, sweep, tau, rowmap);
+  return hipGetLastError();
+}
+
+// Stream compaction of the active flags, one 1024-thread work-group: thread t
+// counts its contiguous chunk of rows, an exclusive scan over the threads
+// gives each chunk's first position, and the chunk is written in order.
+__global__ __launch_bounds__(1024) void compact_rows_kernel(int rows,
+                                                            const uint8_t* __restrict__ active,
+                                                            int32_t* __restrict__ rowmap) {
+  __shared__ int pre_s[1024];
+  const int t = threadIdx.x;
+  const int per = (rows + 1023) / 1024;
+  const int b = min(t * per, rows), e = min(b + per, rows);
+  int c = 0;
+  for (int r = b; r < e; ++r) c += active[r] != 0;
+  pre_s[t] = c;
+  __syncthreads();
+  for (int w = 1; w < 1024; w <<= 1) {  // inclusive scan (Hillis-Steele)
+    const int v = t >= w ? pre_s[t - w] : 0;
+    __syncthreads();
+    pre_s[t] += v;
+    __syncthreads();
+  }
+  int pos = pre_s[t] - c;
+  for (int r = b; r < e; ++r)
+    if (active[r] != 0) rowmap[pos++] = r;
+}
+
+hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, int32_t* rowmap) {
+  hipLaunchKernelGGL(compact_rows_kernel, dim3(1), dim3(1024), 0, st, rows, active, rowmap);
   return hipGetLastError();
 }
 

@@ -55,7 +55,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     const _Float16* __restrict__ Mh, const _Float16* __restrict__ Ml,
     const float* __restrict__ bcol_inv, const float* __restrict__ scales,
     const int32_t* __restrict__ plist, const uint32_t* __restrict__ pcount,
-    float* __restrict__ P) {
+    float* __restrict__ P, const int32_t* __restrict__ rowmap) {
   // Three stages in three distinct arrays: the loads of steps k + 1 and k + 2
   // fly while step k computes.
   __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 
   for (int e = tid; e < BM * ng; e += 256) {
     const int r = e / ng, h = e % ng;
-    sc_s[r][h] = scales[(size_t)row_of(r) * G + h0 + h];
+    sc_s[r][h] = scales[(size_t)map_row(rowmap, row_of(r)) * G + h0 + h];  // list holds positions
   }
   // Rows of this lane's accumulator elements (element v of a 32x32 block is
   // row 8 (v / 4) + 4 (lane / 32) + v % 4), kept for the epilogue.
@@ -236,7 +236,8 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 int panel_groups(int g) { return panel_groups_of(g); }
 
 hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0, int c1,
-                               const char* ws, const Layout& lay, const float* scales, float* P) {
+                               const char* ws, const Layout& lay, const float* scales, float* P,
+                               const int32_t* rowmap) {
   if (c1 >= cols) return hipSuccess;
   if ((c1 - c0) % BK != 0 || (c1 - c0) / g > kMaxPanelGroups) return hipErrorInvalidValue;
   dim3 grid((cols - c1 + BN - 1) / BN, (rows + BM - 1) / BM);
@@ -244,7 +245,7 @@ hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0
                      (const _Float16*)(ws + lay.dq), (const _Float16*)(ws + lay.mhi),
                      (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow), scales,
                      (const int32_t*)(ws + lay.plist),
-                     (const uint32_t*)(ws + lay.pcount) + c0 / (g * panel_groups_of(g)), P);
+                     (const uint32_t*)(ws + lay.pcount) + c0 / (g * panel_groups_of(g)), P, rowmap);
   return hipGetLastError();
 }
 

@@ -41,18 +41,22 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
                                                        const uint8_t* __restrict__ active,
                                                        Counters* __restrict__ cnt,
                                                        Flags* __restrict__ flags, float lam,
-                                                       float rcond, int accept) {
+                                                       float rcond, int accept,
+                                                       const int32_t* __restrict__ rowmap) {
   constexpr int RPW = 64 / GM;  // rows per wavefront
   constexpr int g = GS;
   const int G = cols / g;
   const int lane = threadIdx.x;
   const int slot = lane / GM;
   const int i = lane % GM;      // this lane's row of the G x G system
+  // position `row` of the sweep (Gram matrices) holds layer row `grow`
+  // (everything else)
   const int row = blockIdx.x * RPW + slot;
   const bool row_ok = row < rows;
-  const bool act = row_ok && (active == nullptr || active[row] != 0);
   const bool live = i < G;
-  const int rr = row_ok ? row : 0;  // loads stay unconditional: rows past the edge read row 0
+  const int rr = row_ok ? row : 0;  // loads stay unconditional: positions past the edge read 0
+  const int grow = map_row(rowmap, rr);
+  const bool act = row_ok && (active == nullptr || active[grow] != 0);
   const int ic = live ? i : G - 1;
 
   // column exchange of the factorisation steps and the transposed factor
@@ -62,9 +66,9 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   // ---- right-hand side r_i = sum over group i of (q - z) (W H) ----
   double r0 = 0.0;
   {
-    const float* whp = wh + (size_t)rr * cols + (size_t)ic * g;
-    const uint8_t* qp = codes + (size_t)rr * cols + (size_t)ic * g;
-    const double z = (double)zeros[(size_t)rr * G + ic];
+    const float* whp = wh + (size_t)grow * cols + (size_t)ic * g;
+    const uint8_t* qp = codes + (size_t)grow * cols + (size_t)ic * g;
+    const double z = (double)zeros[(size_t)grow * G + ic];
     constexpr int CH = g < 32 ? g : 32;  // columns per batch of loads
 #pragma unroll
     for (int c0 = 0; c0 < g; c0 += CH) {
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   bool keep_old = false;
   if (accept && __any(ridge && !failed)) {
     const double s_new = live ? r : 0.0;
-    const double s_old = live ? (double)scales[(size_t)rr * G + i] : 0.0;
+    const double s_old = live ? (double)scales[(size_t)grow * G + i] : 0.0;
     load_rows(0.0);
     col_a[slot][i] = s_new;
     col_r[slot][i] = s_old;
@@ -205,7 +209,7 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
     keep_old = ridge && !failed && dq > 0.0;
   }
 
-  if (act && live && !failed && !keep_old) scales[(size_t)row * G + i] = (float)r;
+  if (act && live && !failed && !keep_old) scales[(size_t)grow * G + i] = (float)r;
   if (act && i == 0) {
     if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
     if (failed) {
@@ -231,15 +235,17 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
                                                         const uint8_t* __restrict__ active,
                                                         Counters* __restrict__ cnt,
                                                         Flags* __restrict__ flags, float lam,
-                                                        float rcond, int accept) {
+                                                        float rcond, int accept,
+                                                        const int32_t* __restrict__ rowmap) {
   constexpr int g = GS;
   const int G = cols / g;
   const int LD = G | 1;  // odd stride (in doubles): rows of a column spread over banks
-  const int row = blockIdx.x;
+  const int row = blockIdx.x;  // position of the sweep (Gram); layer row grow
   const int i = threadIdx.x;
   const int nthr = blockDim.x;
   if (row >= rows) return;
-  if (active != nullptr && !active[row]) return;
+  const int grow = map_row(rowmap, row);
+  if (active != nullptr && !active[grow]) return;
   const bool live = i < G;
   const int ic = live ? i : G - 1;
   extern __shared__ double sm[];
@@ -251,9 +257,9 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
   // right-hand side r_i = sum over group i of (q - z) (W H)
   double r0 = 0.0;
   {
-    const float* whp = wh + (size_t)row * cols + (size_t)ic * g;
-    const uint8_t* qp = codes + (size_t)row * cols + (size_t)ic * g;
-    const double z = (double)zeros[(size_t)row * G + ic];
+    const float* whp = wh + (size_t)grow * cols + (size_t)ic * g;
+    const uint8_t* qp = codes + (size_t)grow * cols + (size_t)ic * g;
+    const double z = (double)zeros[(size_t)grow * G + ic];
     constexpr int CH = g < 32 ? g : 32;
 #pragma unroll
     for (int c0 = 0; c0 < g; c0 += CH) {
@@ -391,7 +397,7 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
   bool keep_old = false;
   if (accept && ridge && !failed) {  // uniform across the work-group
     const double s_new = live ? r : 0.0;
-    const double s_old = live ? (double)scales[(size_t)row * G + i] : 0.0;
+    const double s_old = live ? (double)scales[(size_t)grow * G + i] : 0.0;
     __syncthreads();  // the backward substitution's reads of r_s are done
     if (live) {
       r_s[i] = s_new;
@@ -424,7 +430,7 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
     keep_old = dq > 0.0;
   }
 
-  if (live && !failed && !keep_old) scales[(size_t)row * G + i] = (float)r;
+  if (live && !failed && !keep_old) scales[(size_t)grow * G + i] = (float)r;
   if (i == 0) {
     if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
     if (failed) {
@@ -438,7 +444,8 @@ template <int GS>
 static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const float* gram,
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
                                    float* scales, const uint8_t* active, Counters* cnt,
-                                   Flags* flags, float lam, float rcond, int accept) {
+                                   Flags* flags, float lam, float rcond, int accept,
+                                   const int32_t* rowmap) {
   const int G = cols / GS;
   const int LD = G | 1;
   const size_t lds = ((size_t)G * LD + 2 * (size_t)G + 2) * sizeof(double);
@@ -446,7 +453,7 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
-                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept);
+                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap);
   return hipGetLastError();
 }
 
@@ -454,26 +461,27 @@ template <int GM, int GS>
 static hipError_t launch_solve_reg(hipStream_t st, int rows, int cols, const float* gram,
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
                                    float* scales, const uint8_t* active, Counters* cnt,
-                                   Flags* flags, float lam, float rcond, int accept) {
+                                   Flags* flags, float lam, float rcond, int accept,
+                                   const int32_t* rowmap) {
   constexpr int RPW = 64 / GM;
   hipLaunchKernelGGL((solve_reg_kernel<GM, GS>), dim3((rows + RPW - 1) / RPW), dim3(64), 0, st,
-                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept);
+                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap);
   return hipGetLastError();
 }
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
-                        float lam, float rcond, int accept) {
+                        float lam, float rcond, int accept, const int32_t* rowmap) {
   const int G = cols / g;
   if (G > 64 && G <= 128) {
     switch (g) {
       case 32: return launch_solve_col<32>(st, rows, cols, gram, wh, codes, zeros, scales, active,
-                                           cnt, flags, lam, rcond, accept);
+                                           cnt, flags, lam, rcond, accept, rowmap);
       case 64: return launch_solve_col<64>(st, rows, cols, gram, wh, codes, zeros, scales, active,
-                                           cnt, flags, lam, rcond, accept);
+                                           cnt, flags, lam, rcond, accept, rowmap);
       case 128: return launch_solve_col<128>(st, rows, cols, gram, wh, codes, zeros, scales,
-                                             active, cnt, flags, lam, rcond, accept);
+                                             active, cnt, flags, lam, rcond, accept, rowmap);
       default: break;
     }
   }
@@ -481,11 +489,11 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
 #define JARQ_SOLVE_REG(GM)                                                                        \
   switch (g) {                                                                                    \
     case 32: return launch_solve_reg<GM, 32>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond, accept);                     \
+                                             active, cnt, flags, lam, rcond, accept, rowmap);                     \
     case 64: return launch_solve_reg<GM, 64>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond, accept);                     \
+                                             active, cnt, flags, lam, rcond, accept, rowmap);                     \
     case 128: return launch_solve_reg<GM, 128>(st, rows, cols, gram, wh, codes, zeros, scales,    \
-                                               active, cnt, flags, lam, rcond, accept);                   \
+                                               active, cnt, flags, lam, rcond, accept, rowmap);                   \
     default: break;                                                                               \
   }
     if (G <= 32) {

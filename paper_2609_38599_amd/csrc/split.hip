@@ -150,9 +150,12 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
                                                       const int32_t* __restrict__ zeros,
                                                       _Float16* __restrict__ ehi,
                                                       _Float16* __restrict__ elo,
-                                                      float* __restrict__ erow_inv) {
-  const int row = blockIdx.x;
-  if (row >= rows) return;
+                                                      float* __restrict__ erow_inv,
+                                                      const int32_t* __restrict__ rowmap) {
+  // position pos of the sweep (E and its scale) holds layer row `row`
+  const int pos = blockIdx.x;
+  if (pos >= rows) return;
+  const int row = map_row(rowmap, pos);
   const int G = cols / g;
   __shared__ float red[4];
   const float* wr = W + (size_t)row * cols;
@@ -176,9 +179,9 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
   __syncthreads();
   m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const int t = pow2_exponent(m);
-  if (threadIdx.x == 0) erow_inv[row] = ldexpf(1.f, -t);
-  _Float16* hr = ehi + (size_t)row * cols;
-  _Float16* lr = elo + (size_t)row * cols;
+  if (threadIdx.x == 0) erow_inv[pos] = ldexpf(1.f, -t);
+  _Float16* hr = ehi + (size_t)pos * cols;
+  _Float16* lr = elo + (size_t)pos * cols;
   for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
     const f32x4 w = *(const f32x4*)(wr + c);
     const uint32_t q4 = *(const uint32_t*)(qr + c);
@@ -201,10 +204,10 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
 
 hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
                           const uint8_t* codes, const float* scales, const int32_t* zeros,
-                          char* ws, const Layout& lay) {
+                          char* ws, const Layout& lay, const int32_t* rowmap) {
   hipLaunchKernelGGL(split_e_kernel, dim3(rows), dim3(256), 0, st, rows, cols, g, W, codes, scales,
                      zeros, (_Float16*)(ws + lay.ehi), (_Float16*)(ws + lay.elo),
-                     (float*)(ws + lay.erow));
+                     (float*)(ws + lay.erow), rowmap);
   return hipGetLastError();
 }
 

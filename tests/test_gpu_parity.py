@@ -162,6 +162,35 @@ def test_early_stopping_tiny():
     assert rel(F_gpu, F_or) <= 1e-4
 
 
+def test_active_set_compaction_is_exact():
+    # With early stopping each sweep runs on the rows still active, compacted.
+    # Every row's computation depends on that row alone, so running the layer
+    # in three uneven chunks (each compacting at its own times, each row at a
+    # different position) must give bit-identical codes and scales.  Rows stop
+    # at spread-out sweeps here (300 active for three sweeps, 62 at the end).
+    W, H, q, s, z = random_layer(300, 512, 64, 3, seed=7)
+    K, tau = 8, 1e-5
+    full = GpuLayer(W, H, q, s, z, 64, 3, sweeps=K, tau=tau)
+    st = jq.sweeps(full.p, full.W, full.H, full.codes, full.scales, full.zeros, full.ws)
+    qf, sf = full.state()
+    say(f"[compaction] active per sweep {st['rows_active']}")
+    assert st["rows_active"][0] == 300 and st["rows_active"][-1] < 150
+    for lo, hi in ((0, 97), (97, 228), (228, 300)):
+        part = GpuLayer(W[lo:hi], H, q[lo:hi], s[lo:hi], z[lo:hi], 64, 3, sweeps=K, tau=tau)
+        jq.sweeps(part.p, part.W, part.H, part.codes, part.scales, part.zeros, part.ws)
+        qp, sp = part.state()
+        assert np.array_equal(qp, qf[lo:hi]), (lo, hi)
+        assert np.array_equal(sp.view(np.uint32), sf[lo:hi].view(np.uint32)), (lo, hi)
+    qo, so, hist = jarq.refine(W, H, q, s, z, 64, 3, K, tau=tau)
+    act_o = [int(h.active.sum()) for h in hist]
+    say(f"[compaction] oracle active per sweep {act_o}")
+    for k in range(min(len(act_o), st["sweeps_run"])):
+        assert abs(st["rows_active"][k] - act_o[k]) <= 3
+    F_gpu = jarq.objective_rows(W, H, qf, sf, z, 64).sum()
+    F_or = jarq.objective_rows(W, H, qo, so, z, 64).sum()
+    assert rel(F_gpu, F_or) <= 1e-4
+
+
 # --------------------------------------------------------------------------
 # shapes: ragged row tiles, every group size, several bit widths
 # --------------------------------------------------------------------------

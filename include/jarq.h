@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 5
+#define JARQ_ABI_VERSION 6
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
  * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
  * 3 residual product U = E M^T, 4 row objectives and stopping test,
@@ -171,6 +171,46 @@ jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,
                            const uint8_t* codes, const float* scales, const int32_t* zeros,
                            void* workspace, size_t workspace_bytes, void* stream,
                            double* row_objective);
+
+/*
+ * Per-layer set-up from calibration inputs: the Hessian of the layer
+ * objective, H = X~^T X~ + nu^2 I (App. E.1: the Gram matrix of the stacked
+ * design A = [X~; nu I]), accumulated over chunks of tokens.
+ *
+ * jarq_hessian_accumulate adds alpha X^T X to Hacc, for X [m][d] fp32
+ * (m tokens of d input channels, row-major, 16-byte aligned, d a multiple of
+ * 4, 1 <= d <= 32768, 0 <= m < 2^31; m = 0 does nothing and X may then be
+ * NULL) and Hacc [d][d] fp64
+ * in full symmetric storage (8-byte aligned; the caller zeroes it before the
+ * first chunk).  Products are rounded to fp32 and summed in fp32 over at most
+ * 256 tokens; those partial sums are added in fp64.  Hacc stays exactly
+ * symmetric.  Calls on one Hacc must be ordered (same stream).  Asynchronous.
+ */
+jarq_status jarq_hessian_accumulate(const float* X, int64_t m, int32_t d, double alpha,
+                                    double* Hacc, void* stream);
+
+/*
+ * H [d][d] fp32 (16-byte aligned) = Hacc + (damp * mean(diag Hacc) + nu2) I,
+ * rounded once to fp32.  damp = 0, nu2 = nu^2 is App. E.1's regularised
+ * Hessian; damp > 0 adds the relative diagonal damping used by GPTQ-style
+ * pipelines.  damp and nu2 must be finite and >= 0.  H and Hacc must not
+ * overlap.  Asynchronous.
+ */
+jarq_status jarq_hessian_finalize(const double* Hacc, int32_t d, double damp, double nu2,
+                                  float* H, void* stream);
+
+/*
+ * Round-to-nearest host state (S0, Q0, Z) of eq. (1) for W [rows][cols] fp32
+ * (App. A.1: asymmetric group-wise RTN; the min/max reading): per group,
+ * lo = min(min w, 0), hi = max(max w, 0), s = (hi - lo)/(2^b - 1) (s = 1 if
+ * hi == lo) rounded to fp32, z = clip(rint(-lo/s), 0, 2^b - 1) and
+ * q = clip(rint(w/s) + z, 0, 2^b - 1), z and q from the stored s in fp64.
+ * Uses rows, cols, group_size and bits of `p` (which must be valid as a whole).
+ * codes [rows][cols] uint8 (16-byte aligned), scales [rows][G] fp32 and
+ * zeros [rows][G] int32 are written.  Asynchronous.
+ */
+jarq_status jarq_rtn(const jarq_params* p, const float* W, uint8_t* codes, float* scales,
+                     int32_t* zeros, void* stream);
 
 /* Static, NUL-terminated description of a status code. */
 const char* jarq_status_string(jarq_status s);

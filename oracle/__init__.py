@@ -14,8 +14,10 @@ qrform    The paper's own least-squares form with A = [X; nu I], thin QR of
           small layers where X is available to pin the Hessian form.
 replay    Teacher-forced re-evaluation of one code sweep conditioned on the
           decisions of another implementation (parity protocol).
-hosts     GPTQ-style sequential-compensation host used for the wide-MLP
-          layer; written from the GPTQ recursion.
+hosts     Round-to-nearest host, and the GPTQ-style sequential-compensation
+          host used for the wide-MLP layer (written from the GPTQ recursion).
+hessian   The calibration Hessian H = X~^T X~ + nu^2 I (App. E.1) from
+          chunks of tokens, with optional relative damping.
 """
 
-from . import jarq, qrform, replay, hosts  # noqa: F401
+from . import jarq, qrform, replay, hosts, hessian  # noqa: F401

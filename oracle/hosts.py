@@ -1,4 +1,5 @@
-"""GPTQ-style host quantizer for the wide-MLP layer (test oracle side).
+"""Host quantizers: round-to-nearest, and GPTQ-style for the wide-MLP layer
+(test oracle side).
 
 TEST INFRASTRUCTURE ONLY.  It produces the starting state (S0, Q0, Z) of a
 refinement run whose codes come from sequential error compensation rather
@@ -28,6 +29,27 @@ def _grid(wg, qmax):
     s = np.where(hi > lo, (hi - lo) / qmax, 1.0).astype(np.float32).astype(np.float64)
     z = np.clip(np.rint(-lo / s), 0, qmax)
     return s, z
+
+
+def rtn_host(W, g, bits):
+    """Asymmetric group-wise round-to-nearest host (App. A.1; the min/max reading
+    with 0 inside each group's range): every group gets the grid of `_grid` on
+    its own weights and each weight its nearest code, clipped to [0, 2^b - 1].
+    Returns (codes uint8 [rows, cols], scales float32 [rows, G], zeros int32 [rows, G])."""
+    W = np.asarray(W, dtype=np.float64)
+    rows, d = W.shape
+    G = d // g
+    qmax = (1 << bits) - 1
+    codes = np.zeros((rows, d), dtype=np.uint8)
+    scales = np.zeros((rows, G), dtype=np.float32)
+    zeros = np.zeros((rows, G), dtype=np.int32)
+    for i in range(G):
+        wg = W[:, i * g:(i + 1) * g]
+        s, z = _grid(wg, qmax)
+        codes[:, i * g:(i + 1) * g] = np.clip(np.rint(wg / s[:, None]) + z[:, None], 0, qmax)
+        scales[:, i] = s.astype(np.float32)
+        zeros[:, i] = z.astype(np.int32)
+    return codes, scales, zeros
 
 
 def gptq_host(W, H, g, bits):
@@ -61,4 +83,4 @@ def gptq_host(W, H, g, bits):
     return codes, scales, zeros
 
 
-__all__ = ["gptq_host"]
+__all__ = ["rtn_host", "gptq_host"]

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libjarq.so")
 MAX_RECORDED_SWEEPS = 64
 NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
 STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
-ABI_VERSION = 5
+ABI_VERSION = 6
 JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
@@ -82,6 +82,11 @@ _SIGNATURES = {
                                    ctypes.c_size_t, _vp, ctypes.POINTER(Stats)]),
     "jarq_objective": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                       ctypes.c_size_t, _vp, _vp]),
+    "jarq_hessian_accumulate": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
+                                               _vp, _vp]),
+    "jarq_hessian_finalize": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
+                                             _vp, _vp]),
+    "jarq_rtn": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp]),
     "jarq_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "jarq_abi_version": (ctypes.c_int32, []),
 }
@@ -231,6 +236,55 @@ def objective(p: Params, W, H, codes, scales, zeros, ws, out=None, stream=None):
                               _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream),
                               _ptr(out, torch.float64, "row_objective")), "jarq_objective")
     return out
+
+
+def hessian_accumulate(X, Hacc, alpha=1.0, stream=None):
+    """Hacc += alpha X^T X for one chunk X [m, d] fp32 (Hacc [d, d] fp64)."""
+    lib = load_library()
+    if X.dim() != 2 or Hacc.shape != (X.shape[1], X.shape[1]):
+        raise ValueError("X must be [m, d] and Hacc [d, d]")
+    _check(lib.jarq_hessian_accumulate(_ptr(X, torch.float32, "X"), X.shape[0], X.shape[1],
+                                       float(alpha), _ptr(Hacc, torch.float64, "Hacc"),
+                                       _stream(stream)), "jarq_hessian_accumulate")
+
+
+def hessian_finalize(Hacc, damp=0.0, nu2=0.0, out=None, stream=None):
+    """H = Hacc + (damp mean(diag Hacc) + nu2) I as fp32."""
+    lib = load_library()
+    d = Hacc.shape[0]
+    if Hacc.dim() != 2 or Hacc.shape[1] != d:
+        raise ValueError("Hacc must be square")
+    if out is None:
+        out = torch.empty(d, d, dtype=torch.float32, device=Hacc.device)
+    _check(lib.jarq_hessian_finalize(_ptr(Hacc, torch.float64, "Hacc"), d, float(damp),
+                                     float(nu2), _ptr(out, torch.float32, "H"), _stream(stream)),
+           "jarq_hessian_finalize")
+    return out
+
+
+def hessian(chunks, d, alpha=1.0, damp=0.0, nu2=0.0, device=None, stream=None):
+    """The fp32 Hessian of a stream of fp32 device chunks [m_c, d]."""
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device=device or "cuda")
+    for X in chunks:
+        hessian_accumulate(X, Hacc, alpha, stream)
+    return hessian_finalize(Hacc, damp, nu2, stream=stream)
+
+
+def rtn(p: Params, W, codes=None, scales=None, zeros=None, stream=None):
+    """Round-to-nearest host state (codes, scales, zeros) of W."""
+    lib = load_library()
+    G = p.cols // p.group_size
+    dev = W.device
+    if codes is None:
+        codes = torch.empty(p.rows, p.cols, dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty(p.rows, G, dtype=torch.float32, device=dev)
+    if zeros is None:
+        zeros = torch.empty(p.rows, G, dtype=torch.int32, device=dev)
+    _check(lib.jarq_rtn(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                        _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.float32, "scales"),
+                        _ptr(zeros, torch.int32, "zeros"), _stream(stream)), "jarq_rtn")
+    return codes, scales, zeros
 
 
 def abi_version() -> int:

@@ -425,6 +425,42 @@ jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,
   return JARQ_OK;
 }
 
+jarq_status jarq_hessian_accumulate(const float* X, int64_t m, int32_t d, double alpha,
+                                    double* Hacc, void* stream) {
+  if (d < 1 || d > 32768 || d % 4 != 0 || m < 0 || m > INT32_MAX - 64 || !isfinite(alpha) ||
+      !aligned(Hacc, 8))
+    return JARQ_EINVAL;
+  if (m == 0) return JARQ_OK;  // X may be NULL
+  if (!aligned(X, 16)) return JARQ_EINVAL;
+  if (launch_hessian_update((hipStream_t)stream, X, (int)m, d, alpha, Hacc) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_hessian_finalize(const double* Hacc, int32_t d, double damp, double nu2,
+                                  float* H, void* stream) {
+  if (d < 1 || d > 32768 || d % 4 != 0 || !(damp >= 0.0) || !isfinite(damp) || !(nu2 >= 0.0) ||
+      !isfinite(nu2) || !aligned(Hacc, 8) || !aligned(H, 16))
+    return JARQ_EINVAL;
+  const uintptr_t h0 = (uintptr_t)H, h1 = h0 + (size_t)d * d * sizeof(float);
+  const uintptr_t a0 = (uintptr_t)Hacc, a1 = a0 + (size_t)d * d * sizeof(double);
+  if (h0 < a1 && a0 < h1) return JARQ_EINVAL;
+  if (launch_hessian_finalize((hipStream_t)stream, Hacc, d, damp, nu2, H) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_rtn(const jarq_params* p, const float* W, uint8_t* codes, float* scales,
+                     int32_t* zeros, void* stream) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) ||
+      !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  if (launch_rtn((hipStream_t)stream, W, p->rows, p->cols, p->group_size, p->bits, codes, scales,
+                 zeros) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
 const char* jarq_status_string(jarq_status s) {
   switch (s) {
     case JARQ_OK: return "ok";

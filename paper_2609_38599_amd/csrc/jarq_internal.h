@@ -188,4 +188,12 @@ hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
 hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
                            const uint8_t* codes, const int32_t* zeros, Flags* flags);
 
+// Per-layer set-up from calibration inputs and the round-to-nearest host.
+hipError_t launch_hessian_update(hipStream_t st, const float* X, int m, int d, double alpha,
+                                 double* Hacc);
+hipError_t launch_hessian_finalize(hipStream_t st, const double* Hacc, int d, double damp,
+                                   double nu2, float* H);
+hipError_t launch_rtn(hipStream_t st, const float* W, int rows, int cols, int g, int bits,
+                      uint8_t* codes, float* scales, int32_t* zeros);
+
 }  // namespace jarq

@@ -1,0 +1,250 @@
+// Per-layer setup before the refinement path: the calibration Hessian and the
+// round-to-nearest host.
+//
+// Hessian (App. E.1): with A = [X~; nu I], H = A^T A = X~^T X~ + nu^2 I.  The
+// calibration inputs arrive in chunks of tokens.  hessian_syrk_kernel adds
+// alpha X^T X of one chunk (X: m tokens x d channels, row-major) to an fp64
+// accumulator in full symmetric storage.  The products run on fp32 matrix
+// cores (v_mfma_f32_32x32x2_f32); every 256 tokens the fp32 partial sums are
+// added to fp64 registers, so fp32 rounding is confined to sums of 256
+// products.  Only 128 x 128 tiles on or above the diagonal are formed; entry
+// (a, b) with a <= b is computed once and stored at (a, b) and (b, a), so the
+// accumulator stays exactly symmetric.  hessian_finalize_* writes the fp32 H
+// the refinement path reads: Hacc + (damp mean(diag Hacc) + nu^2) I.
+//
+// RTN host (App. A.1 names asymmetric group-wise round-to-nearest without a
+// formula; the min/max reading with 0 forced into the range):
+//   lo = min(min_group, 0), hi = max(max_group, 0), s = (hi - lo) / (2^b - 1)
+//   (s = 1 when hi == lo), z = clip(rint(-lo / s), 0, 2^b - 1),
+//   q = clip(rint(w / s) + z, 0, 2^b - 1),
+// with s rounded to fp32 first and z, q computed on the stored grid in fp64
+// (correctly rounded division and rint), so every code is exact.
+#include "jarq_internal.h"
+
+namespace jarq {
+
+namespace {
+constexpr int HT = 128;     // H tile edge
+constexpr int HK = 32;      // tokens per staged chunk
+constexpr int HFLUSH = 8;   // chunks per fp32 partial sum (256 tokens)
+}  // namespace
+
+// Block blockIdx.x enumerates the tiles (ta, tb), ta <= tb, row by row.  Four
+// waves, each 64 x 64 of the tile as 2 x 2 blocks of 32 x 32.
+__global__ __launch_bounds__(256, 1) void hessian_syrk_kernel(const float* __restrict__ X, int m,
+                                                              int d, double alpha,
+                                                              double* __restrict__ Hacc) {
+  __shared__ float xa_s[2][HK][HT];
+  __shared__ float xb_s[2][HK][HT];
+  const int nt = (d + HT - 1) / HT;
+  int rem = blockIdx.x, ta = 0;
+  while (rem >= nt - ta) {
+    rem -= nt - ta;
+    ++ta;
+  }
+  const int tb = ta + rem;
+  const int a0 = ta * HT, b0 = tb * HT;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, kk = lane >> 5;
+
+  // Staging: float4 e = tid + 256 p (p < 4) of a 32-token x 128-channel chunk
+  // of each operand.  Tokens past m and channels past d load an in-bounds
+  // element and stage 0 (d is a multiple of 4, so a float4 is all in or all out).
+  float4 ra[4], rb[4];
+  auto load_chunk = [&](int t0) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int e = tid + 256 * p;
+      const int t = e >> 5, c = (e & 31) * 4;
+      const bool tin = t0 + t < m;
+      const size_t roff = (size_t)(tin ? t0 + t : m - 1) * d;
+      const bool ina = tin && a0 + c < d, inb = tin && b0 + c < d;
+      const float4 va = *(const float4*)(X + roff + (ina ? a0 + c : 0));
+      const float4 vb = *(const float4*)(X + roff + (inb ? b0 + c : 0));
+      ra[p] = ina ? va : make_float4(0.f, 0.f, 0.f, 0.f);
+      rb[p] = inb ? vb : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto store_chunk = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int e = tid + 256 * p;
+      const int t = e >> 5, c = (e & 31) * 4;
+      *(float4*)&xa_s[buf][t][c] = ra[p];
+      *(float4*)&xb_s[buf][t][c] = rb[p];
+    }
+  };
+
+  f32x16 acc[2][2];
+  double acc64[2][2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = f32x16{};
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc64[i][j][v] = 0.0;
+    }
+  auto flush = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc64[i][j][v] += (double)acc[i][j][v];
+        acc[i][j] = f32x16{};
+      }
+  };
+
+  const int nchunks = (m + HK - 1) / HK;
+  load_chunk(0);
+  store_chunk(0);
+  __syncthreads();
+  for (int q = 0; q < nchunks; ++q) {
+    const int buf = q & 1;
+    if (q + 1 < nchunks) load_chunk((q + 1) * HK);  // in flight during this chunk
+    // A(row a, k) = X[k][a] and B(k, col b) = X[k][b]: lane l supplies row or
+    // column l % 32 at token k + l / 32.
+#pragma unroll
+    for (int k = 0; k < HK; k += 2) {
+      float af[2], bf[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) af[i] = xa_s[buf][k + kk][wm * 64 + i * 32 + l32];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bf[j] = xb_s[buf][k + kk][wn * 64 + j * 32 + l32];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+    if ((q + 1) % HFLUSH == 0) flush();
+    // The other buffer was last read during the previous chunk, before the
+    // barrier that ended it.
+    if (q + 1 < nchunks) store_chunk(buf ^ 1);
+    __syncthreads();
+  }
+  flush();
+
+  // Element v of lane l in a 32 x 32 block is (row 8 (v / 4) + 4 (l / 32) + v % 4,
+  // column l % 32); rows are channels a, columns channels b.  The product
+  // alpha * sum is rounded once and added to both places: no contraction into
+  // an fma on one of them, which would break the symmetry.
+  {
+#pragma clang fp contract(off)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int b = b0 + wn * 64 + j * 32 + l32;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int a = a0 + wm * 64 + i * 32 + 8 * (v / 4) + 4 * kk + (v % 4);
+        if (a <= b && b < d) {
+          const double t = alpha * acc64[i][j][v];
+          Hacc[(size_t)a * d + b] += t;
+          if (a != b) Hacc[(size_t)b * d + a] += t;
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_hessian_update(hipStream_t st, const float* X, int m, int d, double alpha,
+                                 double* Hacc) {
+  const int nt = (d + HT - 1) / HT;
+  hipLaunchKernelGGL(hessian_syrk_kernel, dim3(nt * (nt + 1) / 2), dim3(256), 0, st, X, m, d,
+                     alpha, Hacc);
+  return hipGetLastError();
+}
+
+// Off-diagonal entries: H = (float) Hacc.
+__global__ __launch_bounds__(256) void hessian_finalize_offdiag_kernel(const double* __restrict__ Hacc,
+                                                                       int d,
+                                                                       float* __restrict__ H) {
+  const size_t n = (size_t)d * d;
+  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (size_t)gridDim.x * 256) {
+    if (e % (size_t)(d + 1) != 0) H[e] = (float)Hacc[e];
+  }
+}
+
+// Diagonal: H_ii = (float)(Hacc_ii + damp mean(diag Hacc) + nu2), one work-group.
+__global__ __launch_bounds__(1024) void hessian_finalize_diag_kernel(const double* __restrict__ Hacc,
+                                                                     int d, double damp, double nu2,
+                                                                     float* __restrict__ H) {
+  __shared__ double red[16];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < d; i += 1024) s += Hacc[(size_t)i * (d + 1)];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  double tot = 0.0;
+  for (int w = 0; w < 16; ++w) tot += red[w];
+  const double add = damp * (tot / (double)d) + nu2;
+  for (int i = threadIdx.x; i < d; i += 1024)
+    H[(size_t)i * (d + 1)] = (float)(Hacc[(size_t)i * (d + 1)] + add);
+}
+
+hipError_t launch_hessian_finalize(hipStream_t st, const double* Hacc, int d, double damp,
+                                   double nu2, float* H) {
+  const size_t n = (size_t)d * d;
+  const size_t blocks = (n + 255) / 256 < 8192 ? (n + 255) / 256 : 8192;
+  hipLaunchKernelGGL(hessian_finalize_offdiag_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                     Hacc, d, H);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(hessian_finalize_diag_kernel, dim3(1), dim3(1024), 0, st, Hacc, d, damp, nu2,
+                     H);
+  return hipGetLastError();
+}
+
+// One thread per group.
+__global__ __launch_bounds__(256) void rtn_kernel(const float* __restrict__ W, int rows, int cols,
+                                                  int g, int bits, uint8_t* __restrict__ codes,
+                                                  float* __restrict__ scales,
+                                                  int32_t* __restrict__ zeros) {
+  const int G = cols / g;
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (long long)rows * G) return;
+  const int row = (int)(e / G), grp = (int)(e % G);
+  const float* w = W + (size_t)row * cols + (size_t)grp * g;
+  const double qmax = (double)((1 << bits) - 1);
+  float lo = 0.f, hi = 0.f;  // min and max are exact in fp32
+  for (int c = 0; c < g; c += 4) {
+    const float4 v = *(const float4*)(w + c);
+    lo = fminf(lo, fminf(fminf(v.x, v.y), fminf(v.z, v.w)));
+    hi = fmaxf(hi, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+  }
+  const double s = hi > lo ? ((double)hi - (double)lo) / qmax : 1.0;
+  const float s32 = (float)s;
+  const double s64 = (double)s32;
+  const double z = fmin(fmax(rint(-(double)lo / s64), 0.0), qmax);
+  uint8_t* q = codes + (size_t)row * cols + (size_t)grp * g;
+  for (int c = 0; c < g; c += 4) {
+    const float4 v = *(const float4*)(w + c);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
+    uint32_t packed = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const double qi = fmin(fmax(rint((double)vv[i] / s64) + z, 0.0), qmax);
+      packed |= (uint32_t)qi << (8 * i);
+    }
+    *(uint32_t*)(q + c) = packed;
+  }
+  scales[(size_t)row * G + grp] = s32;
+  zeros[(size_t)row * G + grp] = (int32_t)z;
+}
+
+hipError_t launch_rtn(hipStream_t st, const float* W, int rows, int cols, int g, int bits,
+                      uint8_t* codes, float* scales, int32_t* zeros) {
+  const long long n = (long long)rows * (cols / g);
+  hipLaunchKernelGGL(rtn_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, W, rows,
+                     cols, g, bits, codes, scales, zeros);
+  return hipGetLastError();
+}
+
+}  // namespace jarq

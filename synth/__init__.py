@@ -6,8 +6,9 @@ state (codes, scales, zero points).  It holds none of the refinement
 arithmetic; both the HIP path and the float64 oracle consume what it makes.
 """
 
-from .layers import CONFIGS, LayerConfig, make_layer, make_weights, make_hessian
+from .layers import (CONFIGS, LayerConfig, calibration_chunks, make_hessian, make_layer,
+                     make_weights)
 from .rtn import rtn_quantize
 
-__all__ = ["CONFIGS", "LayerConfig", "make_layer", "make_weights",
+__all__ = ["CONFIGS", "LayerConfig", "calibration_chunks", "make_layer", "make_weights",
            "make_hessian", "rtn_quantize"]

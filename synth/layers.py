@@ -172,6 +172,30 @@ def _tiny_x(cfg: LayerConfig) -> np.ndarray:
     return x
 
 
+def calibration_chunks(cfg: LayerConfig, device: str | None = None,
+                       n_tokens: int | None = None, chunk: int = 8192):
+    """Yield the calibration activations X_c [<= chunk, cols] (float64, on
+    ``device``) whose Gram matrix make_hessian forms: the recipe's tokens with
+    the outlier channels scaled.  sum_c X_c^T X_c / n plus the damping is H."""
+    if cfg.x_recipe == "zl":
+        x = _tiny_x(cfg)
+        n = x.shape[0] if n_tokens is None else int(n_tokens)
+        for t0 in range(0, n, chunk):
+            yield x[t0:min(n, t0 + chunk)]
+        return
+    if torch is None:
+        raise RuntimeError("torch is required for the token-streaming activations")
+    if device is None:
+        device = "cuda" if torch.cuda.is_available() else "cpu"
+    n = cfg.n_tokens if n_tokens is None else int(n_tokens)
+    scale = torch.ones(cfg.cols, dtype=torch.float64, device=device)
+    out = torch.as_tensor(_outlier_channels(cfg), device=device)
+    if out.numel():
+        scale[out] = cfg.outlier_scale
+    for xc in _token_chunks(cfg, n, device, chunk):
+        yield xc * scale[None, :]
+
+
 def make_hessian(cfg: LayerConfig, device: str | None = None,
                  n_tokens: int | None = None, chunk: int = 8192,
                  return_x: bool = False):

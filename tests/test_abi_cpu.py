@@ -36,7 +36,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert binding.abi_version() == binding.ABI_VERSION == 5
+    assert binding.abi_version() == binding.ABI_VERSION == 6
     for s in range(6):
         assert binding.status_string(s)
     assert binding.status_string(99) == "unknown status"
@@ -82,3 +82,24 @@ def test_argument_errors_return_before_any_launch(lib):
                               None) == binding.JARQ_EINVAL
     assert lib.jarq_refine(None, fake, fake, fake, fake, fake, fake, 1 << 30, None, None) == binding.JARQ_EINVAL
     del P
+
+
+def test_setup_entry_points_check_arguments(lib):
+    fake = _vp(1 << 20)
+    st = None
+    acc = lib.jarq_hessian_accumulate
+    assert acc(fake, 10, 130, 1.0, fake, st) == binding.JARQ_EINVAL          # d % 4
+    assert acc(fake, -1, 128, 1.0, fake, st) == binding.JARQ_EINVAL          # m < 0
+    assert acc(_vp((1 << 20) + 4), 10, 128, 1.0, fake, st) == binding.JARQ_EINVAL
+    assert acc(fake, 10, 128, float("nan"), fake, st) == binding.JARQ_EINVAL
+    assert acc(fake, 10, 0, 1.0, fake, st) == binding.JARQ_EINVAL
+    assert acc(fake, 0, 128, 1.0, fake, st) == binding.JARQ_OK              # nothing to do
+    assert acc(None, 0, 128, 1.0, fake, st) == binding.JARQ_OK
+    fin = lib.jarq_hessian_finalize
+    assert fin(fake, 128, -0.1, 0.0, _vp(1 << 30), st) == binding.JARQ_EINVAL
+    assert fin(fake, 128, 0.0, float("inf"), _vp(1 << 30), st) == binding.JARQ_EINVAL
+    assert fin(fake, 128, 0.0, 0.0, _vp((1 << 20) + 64), st) == binding.JARQ_EINVAL  # overlap
+    p = binding.make_params(64, 256, 64, 3, 5)
+    bad = binding.make_params(64, 250, 64, 3, 5)
+    assert lib.jarq_rtn(ctypes.byref(bad), fake, fake, fake, fake, st) == binding.JARQ_EINVAL
+    assert lib.jarq_rtn(ctypes.byref(p), fake, _vp((1 << 20) + 8), fake, fake, st) == binding.JARQ_EINVAL

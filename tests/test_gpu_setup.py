@@ -1,0 +1,163 @@
+"""Per-layer set-up on the GPU vs the float64 oracle (needs an MI355X).
+
+The calibration Hessian (fp32 products on the matrix cores, fp32 sums of at
+most 256 tokens added in fp64) must lie within the fp32 summation bound of the
+exact Hessian of the same fp32 inputs, be exactly symmetric, and be exact when
+every partial sum is an integer below 2^24.  The round-to-nearest host must
+reproduce the oracle's codes, scales and zero points bit for bit.
+"""
+
+import time
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hessian as ohess
+from oracle import hosts
+from synth import CONFIGS, calibration_chunks, make_weights
+from tests._gpu_common import jq, say, to_dev
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+U32 = 2.0 ** -24
+
+
+def _gpu_hessian(chunks, d, alpha, damp=0.0, nu2=0.0):
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    for X in chunks:
+        jq.binding.hessian_accumulate(X, Hacc, alpha)
+    H = jq.binding.hessian_finalize(Hacc, damp, nu2)
+    torch.cuda.synchronize()
+    return Hacc.cpu().numpy(), H.cpu().numpy()
+
+
+def _bound(X32, alpha, Href):
+    """fp32 path bound around the exact Hessian of the fp32 inputs, plus the
+    final rounding to fp32."""
+    ax = np.abs(X32.astype(np.float64))
+    return ohess.fp32_error_bound(ax.T @ ax, alpha) + 2 * U32 * np.abs(Href) + 1e-300
+
+
+@pytest.mark.parametrize("m,d,splits", [(1000, 260, (333,)), (31, 128, ()), (1, 4, ()),
+                                        (600, 516, (64, 65, 300))])
+def test_hessian_integer_inputs_are_exact(m, d, splits):
+    rng = np.random.default_rng(m + d)
+    X = rng.integers(-3, 4, size=(m, d)).astype(np.float32)
+    say(f"[hessian-int] m={m} d={d} splits={splits}")
+    cuts = [0, *splits, m]
+    chunks = [to_dev(X[a:b]) for a, b in zip(cuts[:-1], cuts[1:])]
+    Hacc, H = _gpu_hessian(chunks, d, 0.5)
+    ref = ohess.hessian([X], d, alpha=0.5)
+    assert np.array_equal(Hacc, ref)
+    assert np.array_equal(H, ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("m,d,damp,nu2", [(700, 260, 0.01, 0.0), (257, 516, 0.0, 0.36),
+                                          (2048, 384, 0.01, 0.36), (5, 132, 0.0, 1.0)])
+def test_hessian_matches_oracle_within_fp32_bound(m, d, damp, nu2):
+    rng = np.random.default_rng(d)
+    X = rng.standard_normal((m, d))
+    for c in range(1, d):
+        X[:, c] = 0.6 * X[:, c - 1] + 0.8 * X[:, c]
+    X[:, rng.choice(d, 3, replace=False)] *= 20.0
+    X32 = X.astype(np.float32)
+    say(f"[hessian] m={m} d={d} damp={damp} nu2={nu2}")
+    half = m // 2
+    Hacc, H = _gpu_hessian([to_dev(X32[:half]), to_dev(X32[half:])], d, 1.0 / m, damp, nu2)
+    ref_acc = ohess.hessian([X32], d, alpha=1.0 / m)
+    ref = ohess.finalize(ref_acc, damp, nu2)
+    bound = _bound(X32, 1.0 / m, ref)
+    worst = np.max(np.abs(H - ref) / bound)
+    say(f"[hessian] worst error / bound {worst:.3e}")
+    assert worst <= 1.0
+    assert np.array_equal(H, H.T) and np.array_equal(Hacc, Hacc.T)
+
+
+def test_hessian_zero_tokens_leave_the_accumulator():
+    Hacc = torch.full((8, 8), 2.5, dtype=torch.float64, device="cuda")
+    jq.binding.hessian_accumulate(torch.zeros(0, 8, dtype=torch.float32, device="cuda"), Hacc)
+    torch.cuda.synchronize()
+    assert torch.all(Hacc == 2.5)
+
+
+def test_hessian_full_size_sampled():
+    """4096 channels, 262,144 tokens in chunks of 8192 (the headline layer's
+    calibration set): sampled entries against the oracle's exact dot products
+    of the same fp32 columns, exact symmetry everywhere."""
+    cfg = CONFIGS[1]
+    d, n = cfg.cols, cfg.n_tokens
+    rng = np.random.default_rng(11)
+    idx = np.unique(np.concatenate([rng.choice(d, 40, replace=False), [0, 1, d - 1]]))
+    cols = []
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    say(f"[hessian-full] d={d} n={n}")
+    t_acc = 0.0
+    for c, xc in enumerate(calibration_chunks(cfg, device="cuda", chunk=8192)):
+        X = xc.to(torch.float32).contiguous()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        jq.binding.hessian_accumulate(X, Hacc, 1.0 / n)
+        torch.cuda.synchronize()
+        t_acc += time.perf_counter() - t0
+        cols.append(X[:, torch.as_tensor(idx, device="cuda")].double().cpu().numpy())
+        if c % 8 == 0:
+            say(f"[hessian-full] chunk {c}")
+    H = jq.binding.hessian_finalize(Hacc, cfg.damping, 0.0)
+    torch.cuda.synchronize()
+    say(f"[hessian-full] accumulate {1e3 * t_acc:.1f} ms over {n} tokens")
+    Xs = np.concatenate(cols)
+    Hs = H[torch.as_tensor(idx, device="cuda")][:, torch.as_tensor(idx, device="cuda")].cpu().numpy()
+    assert torch.equal(H, H.T)
+    diag = torch.diagonal(Hacc).double()
+    shift = cfg.damping * float(diag.mean())
+    ref = ohess.finalize(ohess.accumulate(np.zeros((len(idx),) * 2), Xs, 1.0 / n), 0.0, 0.0)
+    ref[np.arange(len(idx)), np.arange(len(idx))] += shift
+    ax = np.abs(Xs)
+    bound = ohess.fp32_error_bound(ax.T @ ax, 1.0 / n) + 2 * U32 * np.abs(ref)
+    worst = np.max(np.abs(Hs - ref) / bound)
+    rel = np.max(np.abs(Hs - ref) / np.sqrt(np.outer(np.diag(ref), np.diag(ref))))
+    say(f"[hessian-full] sampled worst error / bound {worst:.3e}, worst rel {rel:.3e}")
+    assert worst <= 1.0
+
+
+def _edge_weights(rows, cols, g, seed):
+    rng = np.random.default_rng(seed)
+    W = 0.02 * rng.standard_t(5, size=(rows, cols))
+    W[0, :g] = 0.0                        # constant group: s = 1, z = 0
+    W[1, :g] = np.abs(W[1, :g])           # lo = 0
+    W[2, :g] = -np.abs(W[2, :g])          # hi = 0
+    W[3, :g] = 0.01 * np.round(W[3, :g] / 0.01 * 2) / 2   # many ties of w / s
+    W[4, g:2 * g] = 7.0                   # one-signed constant group
+    return W.astype(np.float32)
+
+
+@pytest.mark.parametrize("g", [32, 64, 128])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
+def test_rtn_matches_oracle_exactly(g, bits):
+    rows, cols = 37, 4 * 128
+    W = _edge_weights(rows, cols, g, 100 * g + bits)
+    say(f"[rtn] g={g} bits={bits}")
+    p = jq.binding.make_params(rows, cols, g, bits, 1)
+    q, s, z = jq.binding.rtn(p, to_dev(W))
+    torch.cuda.synchronize()
+    rq, rs, rz = hosts.rtn_host(W, g, bits)
+    assert np.array_equal(q.cpu().numpy(), rq)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+    assert np.array_equal(z.cpu().numpy(), rz)
+
+
+@pytest.mark.parametrize("cfg_id", [1, 2])
+def test_rtn_full_size_exact(cfg_id):
+    cfg = CONFIGS[cfg_id]
+    W = make_weights(cfg)
+    say(f"[rtn-full] config {cfg.name}")
+    p = jq.binding.make_params(cfg.rows, cfg.cols, cfg.group_size, cfg.bits, 1)
+    Wd = to_dev(W)
+    q, s, z = jq.binding.rtn(p, Wd)
+    torch.cuda.synchronize()
+    rq, rs, rz = hosts.rtn_host(W, cfg.group_size, cfg.bits)
+    assert np.array_equal(q.cpu().numpy(), rq)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+    assert np.array_equal(z.cpu().numpy(), rz)

@@ -1,0 +1,143 @@
+"""Pins of the per-layer set-up oracles (CPU): the calibration Hessian and the
+round-to-nearest host."""
+
+import numpy as np
+
+from oracle import hessian, hosts
+from synth import CONFIGS, make_hessian, rtn_quantize
+
+
+# --------------------------------------------------------------------------
+# Hessian H = X~^T X~ + nu^2 I (App. E.1)
+# --------------------------------------------------------------------------
+
+def test_hessian_is_the_sum_of_token_outer_products():
+    rng = np.random.default_rng(3)
+    X = rng.standard_normal((7, 5))
+    brute = np.zeros((5, 5))
+    for t in range(7):
+        for a in range(5):
+            for b in range(5):
+                brute[a, b] += 0.25 * X[t, a] * X[t, b]
+    H = hessian.hessian([X], 5, alpha=0.25)
+    assert np.allclose(H, brute, rtol=0, atol=1e-14)
+
+
+def test_hessian_is_the_gram_matrix_of_the_stacked_design():
+    # A = [X~; nu I] with X~ = sqrt(alpha) X: H = A^T A
+    rng = np.random.default_rng(4)
+    X = rng.standard_normal((40, 12))
+    alpha, nu = 1.0 / 40, 0.6
+    A = np.vstack([np.sqrt(alpha) * X, nu * np.eye(12)])
+    H = hessian.hessian([X], 12, alpha=alpha, nu2=nu * nu)
+    assert np.allclose(H, A.T @ A, rtol=1e-13, atol=1e-14)
+    assert np.all(np.linalg.eigvalsh(H) >= nu * nu * (1 - 1e-12))
+
+
+def test_hessian_does_not_depend_on_chunking():
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((333, 20))
+    whole = hessian.hessian([X], 20, alpha=1 / 333, damp=0.01)
+    parts = hessian.hessian([X[:1], X[1:100], X[100:]], 20, alpha=1 / 333, damp=0.01)
+    assert np.allclose(whole, parts, rtol=1e-13, atol=1e-15)
+    assert np.array_equal(parts, parts.T)
+
+
+def test_hessian_damping_adds_the_stated_diagonal():
+    rng = np.random.default_rng(6)
+    X = rng.standard_normal((50, 8)) * np.arange(1, 9)
+    base = hessian.hessian([X], 8)
+    H = hessian.hessian([X], 8, damp=0.01, nu2=0.36)
+    add = 0.01 * np.trace(X.T @ X) / 8 + 0.36
+    assert np.allclose(np.diag(H) - np.diag(base), add, rtol=1e-14)
+    off = ~np.eye(8, dtype=bool)
+    assert np.array_equal(H[off], base[off])
+    assert np.isclose(np.trace(base), np.sum(X * X), rtol=1e-14)
+
+
+def test_hessian_reproduces_the_tiny_synthetic_layer():
+    cfg = CONFIGS[0]
+    _, X, H64 = make_hessian(cfg, return_x=True)
+    H = hessian.hessian([X[:200], X[200:]], cfg.cols, alpha=1 / X.shape[0], damp=cfg.damping)
+    assert np.allclose(H, H64, rtol=1e-12, atol=1e-14)
+
+
+def test_fp32_error_bound_covers_a_simulated_fp32_path():
+    # products rounded to fp32, fp32 sums of 256, fp64 sum of the partials
+    rng = np.random.default_rng(7)
+    m = 1500
+    x = (rng.standard_normal((m, 2)) * [1.0, 30.0]).astype(np.float32)
+    exact = float(np.dot(x[:, 0].astype(np.float64), x[:, 1].astype(np.float64)))
+    prods = (x[:, 0] * x[:, 1]).astype(np.float32)
+    tot = 0.0
+    for s0 in range(0, m, 256):
+        acc = np.float32(0)
+        for p in prods[s0:s0 + 256]:
+            acc = np.float32(acc + p)
+        tot += float(acc)
+    absg = float(np.dot(np.abs(x[:, 0]).astype(np.float64), np.abs(x[:, 1]).astype(np.float64)))
+    assert abs(tot - exact) <= hessian.fp32_error_bound(absg, 1.0)
+    # the bound is not vacuous: it is far below the size of the terms
+    assert hessian.fp32_error_bound(absg, 1.0) < 1e-4 * absg
+
+
+# --------------------------------------------------------------------------
+# Round-to-nearest host (App. A.1, min/max reading)
+# --------------------------------------------------------------------------
+
+def test_rtn_worked_examples():
+    # b = 2 (codes 0..3), one group of four per row, values worked by hand:
+    # [-1, 0, 0.5, 2]: lo = -1, hi = 2, s = 1, z = 1, q = rint(w) + 1 (0.5 -> 0, half to even)
+    # [0.25, 0.5, 0.75, 1]: lo = 0, hi = 1, s = fp32(1/3) = 0.3333333432674408, z = 0,
+    #   w / s = 0.74999998, 1.49999996, 2.24999993, 2.99999991 -> 1, 1, 2, 3
+    # [0, 0, 0, 0]: hi == lo, s = 1, z = 0, q = 0
+    # [-3, -1, -2, -0.5]: lo = -3, hi = 0, s = 1, z = 3, q = rint(w) + 3 (-0.5 -> -0 -> 3)
+    W = np.array([[-1, 0, 0.5, 2], [0.25, 0.5, 0.75, 1], [0, 0, 0, 0], [-3, -1, -2, -0.5]],
+                 dtype=np.float32)
+    q, s, z = hosts.rtn_host(W, 4, 2)
+    assert q.tolist() == [[0, 1, 1, 3], [1, 1, 2, 3], [0, 0, 0, 0], [0, 2, 1, 3]]
+    assert s[:, 0].tolist() == [1.0, np.float32(1 / 3), 1.0, 1.0]
+    assert z[:, 0].tolist() == [1, 0, 0, 3]
+
+
+def test_rtn_oracle_equals_the_host_generator():
+    # two independent writings of the same rule agree bit for bit
+    rng = np.random.default_rng(8)
+    W = (0.02 * rng.standard_t(5, size=(33, 384))).astype(np.float32)
+    W[0, :32] = 0.0
+    W[1, 32:64] = np.abs(W[1, 32:64])
+    W[2, 64:96] = -np.abs(W[2, 64:96])
+    for g in (32, 64, 128):
+        for bits in (1, 2, 3, 4, 8):
+            a = hosts.rtn_host(W, g, bits)
+            b = rtn_quantize(W, g, bits)
+            for x, y in zip(a, b):
+                assert x.dtype == y.dtype and np.array_equal(x, y), (g, bits)
+
+
+def test_rtn_error_is_at_most_half_a_step_inside_the_range():
+    rng = np.random.default_rng(9)
+    W = (0.03 * rng.standard_normal((20, 256))).astype(np.float32)
+    W[:, 5] = 0.0
+    q, s, z = hosts.rtn_host(W, 64, 3)
+    s64 = np.repeat(s.astype(np.float64), 64, axis=1)
+    z64 = np.repeat(z.astype(np.float64), 64, axis=1)
+    err = np.abs(W - s64 * (q - z64))
+    assert np.all(err <= s64 / 2 * (1 + 1e-6) + 1e-12)
+    # 0 lies in every group's range, so a weight of 0 gets the zero point's
+    # code and is represented exactly
+    assert np.array_equal(q[:, 5].astype(np.int64), z[:, 0].astype(np.int64))
+
+
+def test_calibration_chunks_form_the_synthetic_hessian():
+    # the streamed activations (outlier channels scaled) give make_hessian's H
+    import torch
+    from synth import calibration_chunks
+    cfg = CONFIGS[1]
+    n = 1024
+    chunks = [c.numpy() for c in calibration_chunks(cfg, device="cpu", n_tokens=n, chunk=300)]
+    assert sum(c.shape[0] for c in chunks) == n and chunks[0].shape[1] == cfg.cols
+    H = hessian.hessian(chunks, cfg.cols, alpha=1 / n, damp=cfg.damping)
+    H32 = make_hessian(cfg, device="cpu", n_tokens=n, chunk=300)
+    assert np.max(np.abs(H.astype(np.float32) - H32)) <= 1e-6 * np.max(np.abs(H))
+    del torch

@@ -13,6 +13,11 @@ event leaves the GPU idle for a few microseconds between kernels.  The
 per-stage breakdown comes from a second, untimed call of the same K sweeps
 from the host state with events around every stage.
 
+After the sweeps, a set-up leg (not part of a sweep; --no-setup skips it)
+times the per-layer set-up on the GPU: the Hessian from the layer's 262,144
+calibration tokens (fp32 chunks resident in HBM), its finalisation with the
+layer's damping, and the RTN host.
+
 Prints one JSON line.  --gpus above 1 is refused: the path runs on one GPU.
 --copy-probe runs only a plain device copy of known size (used to calibrate
 the HBM byte counters of rocprofv3) and prints nothing else.
@@ -129,6 +134,47 @@ def copy_probe():
     log(f"[bench] copy probe: 5 copies of {COPY_PROBE_BYTES} bytes")
 
 
+def setup_leg(cfg, jq, H_ref, W_dev):
+    """Per-layer set-up on the GPU, timed with events on the current stream:
+    the calibration Hessian from the layer's full token set (fp32 chunks of
+    8192 tokens resident in HBM), its finalisation with the layer's damping,
+    and the RTN host.  Not part of a sweep."""
+    import torch
+    from synth import calibration_chunks
+    d = cfg.cols
+    chunks = [xc.to(torch.float32).contiguous()
+              for xc in calibration_chunks(cfg, device="cuda", chunk=8192)]
+    n = sum(int(x.shape[0]) for x in chunks)
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    jq.binding.hessian_accumulate(chunks[0], Hacc, 1.0 / n)      # warm-up
+    Hacc.zero_()
+    p = jq.make_params(W_dev.shape[0], d, cfg.group_size, cfg.bits, 1)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for X in chunks:
+        jq.binding.hessian_accumulate(X, Hacc, 1.0 / n)
+    ev[1].record()
+    H = jq.binding.hessian_finalize(Hacc, cfg.damping, 0.0)
+    ev[2].record()
+    jq.binding.rtn(p, W_dev)
+    ev[3].record()
+    torch.cuda.synchronize()
+    t_h, t_f, t_r = (ev[i].elapsed_time(ev[i + 1]) for i in range(3))
+    flops = float(n) * d * (d + 1)                 # the d (d + 1) / 2 distinct entries, 2 n each
+    dg = torch.sqrt(torch.diagonal(H_ref).double())
+    dev_rel = float(((H.double() - H_ref.double()).abs() / torch.outer(dg, dg)).max())
+    del chunks, Hacc, H
+    torch.cuda.empty_cache()
+    tflops = flops / (t_h * 1e-3) / 1e12
+    return {"tokens": n, "chunk_tokens": 8192, "launches": (n + 8191) // 8192,
+            "hessian_ms": t_h, "hessian_tflops": tflops,
+            "hessian_frac_of_fp32_mfma_peak": tflops / PEAK_FP32_MFMA_TFLOPS,
+            "finalize_ms": t_f, "rtn_ms": t_r,
+            "rtn_hbm_gbs": (W_dev.numel() * 5 + 8 * W_dev.numel() // cfg.group_size) / (t_r * 1e-3) / 1e9,
+            "max_rel_dev_from_fp64_build": dev_rel}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,6 +187,8 @@ def main():
     ap.add_argument("--cpu-sweeps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--no-setup", action="store_true",
+                    help="skip the timed per-layer set-up leg (Hessian from tokens, RTN host)")
     ap.add_argument("--inputs", default=None,
                     help="cache file (.npz) of the synthetic layer: loaded if present, else written")
     args = ap.parse_args()
@@ -260,6 +308,9 @@ def main():
         "stage_rates_tflops": {name: (work[name] / (stage_ms[name] * 1e-3) / 1e12
                                       if stage_ms[name] > 0 else None) for name in STAGE_NAMES},
     }
+    if not args.no_setup:
+        log("[bench] per-layer set-up leg (Hessian from calibration tokens, RTN host)")
+        out["setup"] = setup_leg(cfg, jq, Hd, Wd)
     if not args.no_cpu_baseline:
         log("[bench] timing the float64 oracle on the host")
         out["cpu_baseline"] = cpu_baseline(cfg, W, H, q, s, z, args.cpu_rows, args.cpu_sweeps)

@@ -7,7 +7,7 @@
 // accumulator in full symmetric storage.  The products run on fp32 matrix
 // cores (v_mfma_f32_32x32x2_f32); every 256 tokens the fp32 partial sums are
 // added to fp64 registers, so fp32 rounding is confined to sums of 256
-// products.  Only 128 x 128 tiles on or above the diagonal are formed; entry
+// products.  Only 64 x 64 tiles on or above the diagonal are formed; entry
 // (a, b) with a <= b is computed once and stored at (a, b) and (b, a), so the
 // accumulator stays exactly symmetric.  hessian_finalize_* writes the fp32 H
 // the refinement path reads: Hacc + (damp mean(diag Hacc) + nu^2) I.
@@ -24,41 +24,51 @@
 namespace jarq {
 
 namespace {
-constexpr int HT = 128;     // H tile edge
+constexpr int HT = 64;      // H tile edge
 constexpr int HK = 32;      // tokens per staged chunk
 constexpr int HFLUSH = 8;   // chunks per fp32 partial sum (256 tokens)
+
+// First tile index of row stripe ta in the row-by-row enumeration of the
+// upper triangle of an nt x nt tile grid.
+__device__ __forceinline__ long long stripe_start(int ta, int nt) {
+  return (long long)ta * nt - (long long)ta * (ta - 1) / 2;
+}
 }  // namespace
 
-// Block blockIdx.x enumerates the tiles (ta, tb), ta <= tb, row by row.  Four
-// waves, each 64 x 64 of the tile as 2 x 2 blocks of 32 x 32.
-__global__ __launch_bounds__(256, 1) void hessian_syrk_kernel(const float* __restrict__ X, int m,
-                                                              int d, double alpha,
-                                                              double* __restrict__ Hacc) {
+// Block blockIdx.x is tile (ta, tb), ta <= tb, of the upper triangle
+// (64 x 64 tiles: 2080 of them at d = 4096, so the work spreads evenly over
+// 256 compute units).  Four waves, each one 32 x 32 block of the tile.
+__global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restrict__ X, int m,
+                                                           int d, double alpha,
+                                                           double* __restrict__ Hacc) {
   __shared__ float xa_s[2][HK][HT];
   __shared__ float xb_s[2][HK][HT];
   const int nt = (d + HT - 1) / HT;
-  int rem = blockIdx.x, ta = 0;
-  while (rem >= nt - ta) {
-    rem -= nt - ta;
-    ++ta;
-  }
-  const int tb = ta + rem;
+  const long long idx = blockIdx.x;
+  const double bq = 2.0 * nt + 1.0;
+  int ta = (int)floor((bq - sqrt(bq * bq - 8.0 * (double)idx)) * 0.5);
+  ta = ta < 0 ? 0 : (ta > nt - 1 ? nt - 1 : ta);
+  while (ta > 0 && stripe_start(ta, nt) > idx) --ta;
+  while (ta + 1 < nt && stripe_start(ta + 1, nt) <= idx) ++ta;
+  const int tb = ta + (int)(idx - stripe_start(ta, nt));
   const int a0 = ta * HT, b0 = tb * HT;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, kk = lane >> 5;
+  // the lower-left block of a diagonal tile lies below the diagonal
+  const bool idle = ta == tb && wm > wn;
 
-  // Staging: float4 e = tid + 256 p (p < 4) of a 32-token x 128-channel chunk
+  // Staging: float4 e = tid + 256 p (p < 2) of a 32-token x 64-channel chunk
   // of each operand.  Tokens past m and channels past d load an in-bounds
   // element and stage 0 (d is a multiple of 4, so a float4 is all in or all out).
-  float4 ra[4], rb[4];
+  float4 ra[2], rb[2];
   auto load_chunk = [&](int t0) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < 2; ++p) {
       const int e = tid + 256 * p;
-      const int t = e >> 5, c = (e & 31) * 4;
+      const int t = e >> 4, c = (e & 15) * 4;
       const bool tin = t0 + t < m;
       const size_t roff = (size_t)(tin ? t0 + t : m - 1) * d;
       const bool ina = tin && a0 + c < d, inb = tin && b0 + c < d;
@@ -70,33 +80,22 @@ __global__ __launch_bounds__(256, 1) void hessian_syrk_kernel(const float* __res
   };
   auto store_chunk = [&](int buf) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < 2; ++p) {
       const int e = tid + 256 * p;
-      const int t = e >> 5, c = (e & 31) * 4;
+      const int t = e >> 4, c = (e & 15) * 4;
       *(float4*)&xa_s[buf][t][c] = ra[p];
       *(float4*)&xb_s[buf][t][c] = rb[p];
     }
   };
 
-  f32x16 acc[2][2];
-  double acc64[2][2][16];
+  f32x16 acc = f32x16{};
+  double acc64[16];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      acc[i][j] = f32x16{};
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc64[i][j][v] = 0.0;
-    }
+  for (int v = 0; v < 16; ++v) acc64[v] = 0.0;
   auto flush = [&]() {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc64[i][j][v] += (double)acc[i][j][v];
-        acc[i][j] = f32x16{};
-      }
+    for (int v = 0; v < 16; ++v) acc64[v] += (double)acc[v];
+    acc = f32x16{};
   };
 
   const int nchunks = (m + HK - 1) / HK;
@@ -106,27 +105,23 @@ __global__ __launch_bounds__(256, 1) void hessian_syrk_kernel(const float* __res
   for (int q = 0; q < nchunks; ++q) {
     const int buf = q & 1;
     if (q + 1 < nchunks) load_chunk((q + 1) * HK);  // in flight during this chunk
-    // A(row a, k) = X[k][a] and B(k, col b) = X[k][b]: lane l supplies row or
-    // column l % 32 at token k + l / 32.
+    if (!idle) {
+      // A(row a, k) = X[k][a] and B(k, col b) = X[k][b]: lane l supplies row or
+      // column l % 32 at token k + l / 32.
 #pragma unroll
-    for (int k = 0; k < HK; k += 2) {
-      float af[2], bf[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) af[i] = xa_s[buf][k + kk][wm * 64 + i * 32 + l32];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) bf[j] = xb_s[buf][k + kk][wn * 64 + j * 32 + l32];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[j], acc[i][j], 0, 0, 0);
+      for (int k = 0; k < HK; k += 2) {
+        const float af = xa_s[buf][k + kk][wm * 32 + l32];
+        const float bf = xb_s[buf][k + kk][wn * 32 + l32];
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af, bf, acc, 0, 0, 0);
+      }
+      if ((q + 1) % HFLUSH == 0) flush();
     }
-    if ((q + 1) % HFLUSH == 0) flush();
     // The other buffer was last read during the previous chunk, before the
     // barrier that ended it.
     if (q + 1 < nchunks) store_chunk(buf ^ 1);
     __syncthreads();
   }
+  if (idle) return;
   flush();
 
   // Element v of lane l in a 32 x 32 block is (row 8 (v / 4) + 4 (l / 32) + v % 4,
@@ -135,19 +130,14 @@ __global__ __launch_bounds__(256, 1) void hessian_syrk_kernel(const float* __res
   // an fma on one of them, which would break the symmetry.
   {
 #pragma clang fp contract(off)
+    const int b = b0 + wn * 32 + l32;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int b = b0 + wn * 64 + j * 32 + l32;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int a = a0 + wm * 64 + i * 32 + 8 * (v / 4) + 4 * kk + (v % 4);
-        if (a <= b && b < d) {
-          const double t = alpha * acc64[i][j][v];
-          Hacc[(size_t)a * d + b] += t;
-          if (a != b) Hacc[(size_t)b * d + a] += t;
-        }
+    for (int v = 0; v < 16; ++v) {
+      const int a = a0 + wm * 32 + 8 * (v / 4) + 4 * kk + (v % 4);
+      if (a <= b && b < d) {
+        const double t = alpha * acc64[v];
+        Hacc[(size_t)a * d + b] += t;
+        if (a != b) Hacc[(size_t)b * d + a] += t;
       }
     }
   }
@@ -155,9 +145,9 @@ __global__ __launch_bounds__(256, 1) void hessian_syrk_kernel(const float* __res
 
 hipError_t launch_hessian_update(hipStream_t st, const float* X, int m, int d, double alpha,
                                  double* Hacc) {
-  const int nt = (d + HT - 1) / HT;
-  hipLaunchKernelGGL(hessian_syrk_kernel, dim3(nt * (nt + 1) / 2), dim3(256), 0, st, X, m, d,
-                     alpha, Hacc);
+  const long long nt = (d + HT - 1) / HT;
+  hipLaunchKernelGGL(hessian_syrk_kernel, dim3((unsigned)(nt * (nt + 1) / 2)), dim3(256), 0, st,
+                     X, m, d, alpha, Hacc);
   return hipGetLastError();
 }
 

@@ -212,6 +212,28 @@ jarq_status jarq_hessian_finalize(const double* Hacc, int32_t d, double damp, do
 jarq_status jarq_rtn(const jarq_params* p, const float* W, uint8_t* codes, float* scales,
                      int32_t* zeros, void* stream);
 
+/*
+ * GPTQ-style host state (S0, Q0, Z) for W [rows][cols] fp32 and H [cols][cols]
+ * fp32 (symmetric, full storage, positive definite): App. A.1 uses GPTQ as a
+ * host; its sequential error compensation is the nearest-plane relation of
+ * App. G.7.  Columns are visited in their natural order (no activation
+ * ordering, so groups stay contiguous).  At the first column of each group the
+ * group's grid is fixed by the min/max rule of jarq_rtn on the weights
+ * compensated for every earlier column; each column is then rounded on that
+ * grid after compensation for every earlier column, including those of its own
+ * group.  All arithmetic is fp64 (H is factored as J H J = C C^T, J the
+ * order reversal).  codes (16-byte aligned), scales and zeros as for
+ * jarq_rtn.  The workspace (256-byte aligned, jarq_gptq_workspace_bytes(p)
+ * bytes: two cols x cols fp64 matrices, rows x cols fp64 errors and partial
+ * products) is used only during the call.  Synchronises `stream`; returns
+ * JARQ_ENOT_SPD if H is not positive definite (the outputs are then
+ * unspecified).
+ */
+size_t jarq_gptq_workspace_bytes(const jarq_params* p);
+jarq_status jarq_gptq(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
+                      float* scales, int32_t* zeros, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* jarq_status_string(jarq_status s);
 

@@ -52,8 +52,10 @@ def rtn_host(W, g, bits):
     return codes, scales, zeros
 
 
-def gptq_host(W, H, g, bits):
-    """Return (codes uint8 [rows, cols], scales float32 [rows, G], zeros int32 [rows, G])."""
+def gptq_host(W, H, g, bits, return_pre=False):
+    """Return (codes uint8 [rows, cols], scales float32 [rows, G], zeros int32 [rows, G]);
+    with return_pre also the value each code was rounded from (w_k / s + z, float64
+    [rows, cols]) and the value each zero point was rounded from (-lo / s, [rows, G])."""
     W = np.array(W, dtype=np.float64, copy=True)
     H = np.asarray(H, dtype=np.float64)
     rows, d = W.shape
@@ -65,14 +67,18 @@ def gptq_host(W, H, g, bits):
     codes = np.zeros((rows, d), dtype=np.uint8)
     scales = np.zeros((rows, G), dtype=np.float32)
     zeros = np.zeros((rows, G), dtype=np.int32)
+    pre = np.zeros((rows, d))
+    zpre = np.zeros((rows, G))
     for i in range(G):
         b0, b1 = i * g, (i + 1) * g
         s, z = _grid(W[:, b0:b1], qmax)
+        zpre[:, i] = -np.minimum(W[:, b0:b1].min(axis=1), 0.0) / s
         scales[:, i] = s.astype(np.float32)
         zeros[:, i] = z.astype(np.int32)
         err = np.zeros((rows, g))
         for k in range(b0, b1):
             wk = W[:, k]
+            pre[:, k] = wk / s + z
             qk = np.clip(np.rint(wk / s) + z, 0, qmax)
             codes[:, k] = qk.astype(np.uint8)
             e = (wk - s * (qk - z)) / U[k, k]
@@ -80,6 +86,8 @@ def gptq_host(W, H, g, bits):
             err[:, k - b0] = e
         if b1 < d:
             W[:, b1:] -= err @ U[b0:b1, b1:]
+    if return_pre:
+        return codes, scales, zeros, pre, zpre
     return codes, scales, zeros
 
 

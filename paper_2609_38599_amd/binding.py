@@ -87,6 +87,9 @@ _SIGNATURES = {
     "jarq_hessian_finalize": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
                                              _vp, _vp]),
     "jarq_rtn": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp]),
+    "jarq_gptq_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
+    "jarq_gptq": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                 ctypes.c_size_t, _vp]),
     "jarq_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "jarq_abi_version": (ctypes.c_int32, []),
 }
@@ -284,6 +287,31 @@ def rtn(p: Params, W, codes=None, scales=None, zeros=None, stream=None):
     _check(lib.jarq_rtn(ctypes.byref(p), _ptr(W, torch.float32, "W"),
                         _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.float32, "scales"),
                         _ptr(zeros, torch.int32, "zeros"), _stream(stream)), "jarq_rtn")
+    return codes, scales, zeros
+
+
+def gptq(p: Params, W, H, codes=None, scales=None, zeros=None, ws=None, stream=None):
+    """GPTQ-style host state (codes, scales, zeros) of W under H."""
+    lib = load_library()
+    G = p.cols // p.group_size
+    dev = W.device
+    if codes is None:
+        codes = torch.empty(p.rows, p.cols, dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty(p.rows, G, dtype=torch.float32, device=dev)
+    if zeros is None:
+        zeros = torch.empty(p.rows, G, dtype=torch.int32, device=dev)
+    n = int(lib.jarq_gptq_workspace_bytes(ctypes.byref(p)))
+    if n == 0:
+        raise JarqError(JARQ_EINVAL, "jarq_gptq_workspace_bytes")
+    if ws is None:
+        raw = torch.empty(n + 256, dtype=torch.uint8, device=dev)
+        off = (-raw.data_ptr()) % 256
+        ws = raw[off:off + n]
+    _check(lib.jarq_gptq(ctypes.byref(p), _ptr(W, torch.float32, "W"), _ptr(H, torch.float32, "H"),
+                         _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.float32, "scales"),
+                         _ptr(zeros, torch.int32, "zeros"), _ptr(ws, torch.uint8, "workspace"),
+                         ws.numel(), _stream(stream)), "jarq_gptq")
     return codes, scales, zeros
 
 

@@ -461,6 +461,31 @@ jarq_status jarq_rtn(const jarq_params* p, const float* W, uint8_t* codes, float
   return JARQ_OK;
 }
 
+size_t jarq_gptq_workspace_bytes(const jarq_params* p) {
+  if (!valid_params(p)) return 0;
+  return gptq_workspace_bytes(p->rows, p->cols, p->group_size);
+}
+
+jarq_status jarq_gptq(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
+                      float* scales, int32_t* zeros, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 16) ||
+      !aligned(scales, 4) || !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  if (workspace == nullptr || ((uintptr_t)workspace % 256) != 0 ||
+      workspace_bytes < gptq_workspace_bytes(p->rows, p->cols, p->group_size))
+    return JARQ_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  int* flag = nullptr;
+  if (launch_gptq(st, p->rows, p->cols, p->group_size, p->bits, W, H, (char*)workspace, codes,
+                  scales, zeros, &flag) != hipSuccess)
+    return JARQ_EHIP;
+  int f = 0;
+  JQ_HIP(hipMemcpyAsync(&f, flag, sizeof(int), hipMemcpyDeviceToHost, st));
+  JQ_HIP(hipStreamSynchronize(st));
+  return f ? JARQ_ENOT_SPD : JARQ_OK;
+}
+
 const char* jarq_status_string(jarq_status s) {
   switch (s) {
     case JARQ_OK: return "ok";

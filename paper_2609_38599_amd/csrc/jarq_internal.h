@@ -196,4 +196,20 @@ hipError_t launch_hessian_finalize(hipStream_t st, const double* Hacc, int d, do
 hipError_t launch_rtn(hipStream_t st, const float* W, int rows, int cols, int g, int bits,
                       uint8_t* codes, float* scales, int32_t* zeros);
 
+// Dense fp64 building blocks (linalg.hip).
+hipError_t launch_gemm_nt_f64(hipStream_t st, bool lower, int M, int N, int K, int kslice,
+                              double alpha, const double* A, long long lda, const double* B,
+                              long long ldb, double* C, long long ldc, long long cz,
+                              bool accumulate);
+hipError_t launch_potrf_f64(hipStream_t st, double* A, int d, long long lda, double* Linv,
+                            int* flag);
+hipError_t launch_reverse_lower(hipStream_t st, const float* H, int d, double* C);
+hipError_t launch_antitranspose_lower(hipStream_t st, const double* C, int d, double* M);
+
+// GPTQ-style host (gptq.hip).
+size_t gptq_workspace_bytes(int rows, int cols, int g);
+hipError_t launch_gptq(hipStream_t st, int rows, int cols, int g, int bits, const float* W,
+                       const float* H, char* ws, uint8_t* codes, float* scales, int32_t* zeros,
+                       int** flag_out);
+
 }  // namespace jarq

@@ -103,3 +103,17 @@ def test_setup_entry_points_check_arguments(lib):
     bad = binding.make_params(64, 250, 64, 3, 5)
     assert lib.jarq_rtn(ctypes.byref(bad), fake, fake, fake, fake, st) == binding.JARQ_EINVAL
     assert lib.jarq_rtn(ctypes.byref(p), fake, _vp((1 << 20) + 8), fake, fake, st) == binding.JARQ_EINVAL
+
+
+def test_gptq_workspace_and_argument_errors(lib):
+    p = binding.make_params(14336, 4096, 64, 3, 1)
+    n = lib.jarq_gptq_workspace_bytes(ctypes.byref(p))
+    # two 4096^2 fp64 matrices and the 14336 x 4096 fp64 errors dominate
+    assert 2 * 8 * 4096 ** 2 + 8 * 14336 * 4096 < n < 1.2 * (2 * 8 * 4096 ** 2 + 8 * 14336 * 4096) + (64 << 20)
+    assert lib.jarq_gptq_workspace_bytes(ctypes.byref(binding.make_params(64, 250, 64, 3, 1))) == 0
+    fake = _vp(1 << 20)
+    q = binding.make_params(64, 256, 64, 3, 1)
+    assert lib.jarq_gptq(ctypes.byref(q), fake, fake, fake, fake, fake, None, 1 << 30, None) == binding.JARQ_EWORKSPACE
+    assert lib.jarq_gptq(ctypes.byref(q), fake, fake, fake, fake, fake, fake, 1024, None) == binding.JARQ_EWORKSPACE
+    assert lib.jarq_gptq(ctypes.byref(q), _vp((1 << 20) + 4), fake, fake, fake, fake, fake, 1 << 30,
+                         None) == binding.JARQ_EINVAL

@@ -161,3 +161,80 @@ def test_rtn_full_size_exact(cfg_id):
     assert np.array_equal(q.cpu().numpy(), rq)
     assert np.array_equal(s.cpu().numpy().view(np.uint32), rs.view(np.uint32))
     assert np.array_equal(z.cpu().numpy(), rz)
+
+
+def _correlated_hessian(d, seed, rho=0.7, n=None):
+    rng = np.random.default_rng(seed)
+    n = n or 3 * d
+    X = rng.standard_normal((n, d))
+    for c in range(1, d):
+        X[:, c] = rho * X[:, c - 1] + np.sqrt(1 - rho * rho) * X[:, c]
+    H = X.T @ X / n
+    H += 0.01 * np.mean(np.diag(H)) * np.eye(d)
+    return H.astype(np.float32)
+
+
+def _check_gptq(W, H, g, bits, q, s, z, rows_idx=None):
+    """Codes identical except where the oracle's pre-rounding value lies within
+    1e-6 of a rounding boundary (at most 0.1% of codes); scales within 1e-6
+    relative; zero points identical except near-boundary groups."""
+    Wr = W if rows_idx is None else W[rows_idx]
+    rq, rs, rz, pre, zpre = hosts.gptq_host(Wr, H, g, bits, return_pre=True)
+    if rows_idx is not None:
+        q, s, z = q[rows_idx], s[rows_idx], z[rows_idx]
+    dz = z != rz
+    znear = np.abs(zpre - np.floor(zpre) - 0.5) < 1e-6
+    assert np.all(znear[dz]) and dz.mean() <= 1e-3
+    srel = np.abs(s.astype(np.float64) - rs) / np.abs(rs.astype(np.float64))
+    say(f"[gptq] worst scale rel {srel.max():.3e}, zero-point mismatches {int(dz.sum())}")
+    # groups whose grid differs cascade into their codes: judge codes elsewhere
+    ok_groups = np.repeat(~dz & (srel <= 1e-6), g, axis=1)
+    differ = (q != rq) & ok_groups
+    near = np.abs(pre - np.floor(pre) - 0.5) < 1e-6
+    say(f"[gptq] code mismatches {int(differ.sum())} of {q.size}")
+    assert np.all(near[differ]) and differ.mean() <= 1e-3
+    assert np.mean(srel <= 1e-6) >= 1 - 1e-3
+
+
+@pytest.mark.parametrize("rows,cols,g,bits", [(100, 256, 64, 3), (67, 384, 128, 4),
+                                              (130, 320, 32, 2), (64, 128, 128, 8)])
+def test_gptq_matches_oracle(rows, cols, g, bits):
+    rng = np.random.default_rng(rows + cols)
+    W = (0.02 * rng.standard_t(5, size=(rows, cols))).astype(np.float32)
+    H = _correlated_hessian(cols, cols)
+    say(f"[gptq] rows={rows} cols={cols} g={g} bits={bits}")
+    p = jq.binding.make_params(rows, cols, g, bits, 1)
+    q, s, z = jq.binding.gptq(p, to_dev(W), to_dev(H))
+    torch.cuda.synchronize()
+    _check_gptq(W, H, g, bits, q.cpu().numpy(), s.cpu().numpy(), z.cpu().numpy())
+
+
+def test_gptq_full_size_sampled_rows():
+    """The wide-MLP layer (14336 x 4096, g = 64, 3 bits) with its own Hessian:
+    512 sampled rows against the oracle (rows are independent)."""
+    from synth import make_hessian
+    cfg = CONFIGS[4]
+    say(f"[gptq-full] building {cfg.name}")
+    W = make_weights(cfg)
+    H = make_hessian(cfg, device="cuda")
+    p = jq.binding.make_params(cfg.rows, cfg.cols, cfg.group_size, cfg.bits, 1)
+    Wd, Hd = to_dev(W), to_dev(H)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    q, s, z = jq.binding.gptq(p, Wd, Hd)
+    torch.cuda.synchronize()
+    say(f"[gptq-full] GPU host {1e3 * (time.perf_counter() - t0):.1f} ms")
+    idx = np.sort(np.random.default_rng(4).choice(cfg.rows, 512, replace=False))
+    _check_gptq(W, H, cfg.group_size, cfg.bits, q.cpu().numpy(), s.cpu().numpy(),
+                z.cpu().numpy(), rows_idx=idx)
+
+
+def test_gptq_rejects_an_indefinite_hessian():
+    rng = np.random.default_rng(5)
+    W = (0.02 * rng.standard_normal((32, 128))).astype(np.float32)
+    H = _correlated_hessian(128, 3)
+    H[70, 70] = -1.0
+    p = jq.binding.make_params(32, 128, 64, 3, 1)
+    with pytest.raises(jq.binding.JarqError) as ei:
+        jq.binding.gptq(p, to_dev(W), to_dev(H))
+    assert ei.value.status == jq.binding.JARQ_ENOT_SPD

@@ -141,3 +141,80 @@ def test_calibration_chunks_form_the_synthetic_hessian():
     H32 = make_hessian(cfg, device="cpu", n_tokens=n, chunk=300)
     assert np.max(np.abs(H.astype(np.float32) - H32)) <= 1e-6 * np.max(np.abs(H))
     del torch
+
+
+# --------------------------------------------------------------------------
+# GPTQ-style host (App. A.1 host; its recursion is the nearest-plane relation
+# of App. G.7)
+# --------------------------------------------------------------------------
+
+def test_gptq_two_columns_follow_the_optimal_brain_surgeon_update():
+    # One group of two columns: the grid comes from both raw weights; column 0
+    # is rounded as is; column 1 is rounded from the value that minimises the
+    # objective once column 0 is fixed, w_1 + (H_01 / H_11) e_0 (set the
+    # derivative of e^T H e in e_1 to zero).
+    rng = np.random.default_rng(12)
+    for _ in range(50):
+        w = rng.standard_normal((1, 2)).astype(np.float32)
+        B = rng.standard_normal((2, 2))
+        H = B @ B.T + 0.1 * np.eye(2)
+        q, s, z = hosts.gptq_host(w, H, 2, 3)
+        qmax = 7
+        w64 = w.astype(np.float64)
+        lo, hi = min(w64.min(), 0.0), max(w64.max(), 0.0)
+        s0 = np.float64(np.float32((hi - lo) / qmax))
+        z0 = np.clip(np.rint(-lo / s0), 0, qmax)
+        q0 = np.clip(np.rint(w64[0, 0] / s0) + z0, 0, qmax)
+        e0 = w64[0, 0] - s0 * (q0 - z0)
+        x1 = w64[0, 1] + H[0, 1] / H[1, 1] * e0
+        q1 = np.clip(np.rint(x1 / s0) + z0, 0, qmax)
+        assert s[0, 0] == np.float32(s0) and z[0, 0] == z0
+        assert q[0].tolist() == [q0, q1]
+
+
+def test_gptq_with_a_diagonal_hessian_is_rtn():
+    rng = np.random.default_rng(13)
+    W = (0.02 * rng.standard_normal((9, 192))).astype(np.float32)
+    H = np.diag(rng.uniform(0.5, 3.0, 192))
+    for x, y in zip(hosts.gptq_host(W, H, 64, 3), hosts.rtn_host(W, 64, 3)):
+        assert np.array_equal(x, y)
+
+
+def _gptq_lower_factor_form(W, H, g, bits):
+    """The recursion with M lower, M^T M = H (M = J C^T J, J H J = C C^T), no
+    inverse: group grids from w_G + M_GG^{-1} M_GP e_P, columns rounded from
+    w_k + (sum_{i<k} M_ki e_i) / M_kk (the formulation of the GPU host)."""
+    W = np.asarray(W, np.float64)
+    rows, d = W.shape
+    qmax = (1 << bits) - 1
+    J = np.arange(d)[::-1]
+    C = np.linalg.cholesky(np.asarray(H, np.float64)[np.ix_(J, J)])
+    M = C.T[np.ix_(J, J)]
+    E = np.zeros_like(W)
+    q = np.zeros((rows, d), np.uint8)
+    for b0 in range(0, d, g):
+        b1 = b0 + g
+        c = E[:, :b0] @ M[b0:b1, :b0].T
+        y = np.linalg.solve(M[b0:b1, b0:b1], c.T).T
+        lo = np.minimum((W[:, b0:b1] + y).min(axis=1), 0.0)
+        hi = np.maximum((W[:, b0:b1] + y).max(axis=1), 0.0)
+        s = np.where(hi > lo, (hi - lo) / qmax, 1.0).astype(np.float32).astype(np.float64)
+        z = np.clip(np.rint(-lo / s), 0, qmax)
+        for k in range(b0, b1):
+            x = W[:, k] + (E[:, :k] @ M[k, :k]) / M[k, k]
+            qk = np.clip(np.rint(x / s) + z, 0, qmax)
+            q[:, k] = qk
+            E[:, k] = W[:, k] - s * (qk - z)
+    return q
+
+
+def test_gptq_lower_factor_form_equals_the_inverse_factor_recursion():
+    cfg = CONFIGS[0]
+    from synth import make_weights
+    W = make_weights(cfg)
+    H = make_hessian(cfg)
+    q_ref, _, _, pre, _ = hosts.gptq_host(W, H, cfg.group_size, cfg.bits, return_pre=True)
+    q = _gptq_lower_factor_form(W, H, cfg.group_size, cfg.bits)
+    differ = q != q_ref
+    near = np.abs(pre - np.floor(pre) - 0.5) < 1e-6
+    assert np.all(near[differ]) and differ.mean() <= 1e-3

@@ -213,6 +213,40 @@ jarq_status jarq_rtn(const jarq_params* p, const float* W, uint8_t* codes, float
                      int32_t* zeros, void* stream);
 
 /*
+ * Propagation-corrected target (App. E.5, eqs. (mu-target), (w-corr)).  With
+ * X the inputs a layer receives in the full-precision model and X~ those it
+ * receives after the preceding layers were quantized, the mixed target
+ * (1 - mu) X W + mu X~ W (mu in [0, 1]; mu = 1 is the main target) turns the
+ * refinement problem into the main one with W replaced by
+ *     W_corr = W + (1 - mu) (W D^T) H^{-1},   D = X~^T (X - X~)
+ * (rows = output channels; H = X~^T X~ + nu^2 I from jarq_hessian_* on X~),
+ * plus a constant.  Refine W_corr with the usual entry points.
+ *
+ * jarq_cross_accumulate adds alpha X~^T (X - X~) to Dacc [d][d] fp64 (not
+ * symmetric), for Xq = X~ and X [m][d] fp32 (same tokens, same layout and
+ * limits as jarq_hessian_accumulate; X - X~ is formed in fp32, products and
+ * partial sums as there).  Use the alpha of the Hessian so that D and H share
+ * their scale.  Asynchronous.
+ */
+jarq_status jarq_cross_accumulate(const float* Xq, const float* X, int64_t m, int32_t d,
+                                  double alpha, double* Dacc, void* stream);
+
+/*
+ * Wcorr [rows][cols] fp32 (16-byte aligned) = W + (1 - mu) (W D^T) H^{-1} for
+ * W [rows][cols] fp32, H [cols][cols] fp32 (symmetric, full storage, positive
+ * definite; only its lower part is read) and D [cols][cols] fp64, computed in
+ * fp64 (Cholesky of H, two blocked triangular solves) and rounded once.  Uses
+ * rows, cols of `p` (which must be valid as a whole).  The workspace
+ * (256-byte aligned, jarq_qep_workspace_bytes(p) bytes) is used only during
+ * the call.  Synchronises `stream`; JARQ_ENOT_SPD if H is not positive
+ * definite (Wcorr is then unspecified).
+ */
+size_t jarq_qep_workspace_bytes(const jarq_params* p);
+jarq_status jarq_qep_correct(const jarq_params* p, const float* W, const float* H,
+                             const double* D, double mu, float* Wcorr, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/*
  * GPTQ-style host state (S0, Q0, Z) for W [rows][cols] fp32 and H [cols][cols]
  * fp32 (symmetric, full storage, positive definite): App. A.1 uses GPTQ as a
  * host; its sequential error compensation is the nearest-plane relation of

@@ -18,6 +18,7 @@ hosts     Round-to-nearest host, and the GPTQ-style sequential-compensation
           host used for the wide-MLP layer (written from the GPTQ recursion).
 hessian   The calibration Hessian H = X~^T X~ + nu^2 I (App. E.1) from
           chunks of tokens, with optional relative damping.
+qep       The propagation-corrected weights of the mixed target (App. E.5).
 """
 
-from . import jarq, qrform, replay, hosts, hessian  # noqa: F401
+from . import jarq, qrform, replay, hosts, hessian, qep  # noqa: F401

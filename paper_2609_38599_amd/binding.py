@@ -87,6 +87,11 @@ _SIGNATURES = {
     "jarq_hessian_finalize": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
                                              _vp, _vp]),
     "jarq_rtn": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp]),
+    "jarq_cross_accumulate": (ctypes.c_int, [_vp, _vp, ctypes.c_int64, ctypes.c_int32,
+                                             ctypes.c_double, _vp, _vp]),
+    "jarq_qep_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
+    "jarq_qep_correct": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, ctypes.c_double,
+                                        _vp, _vp, ctypes.c_size_t, _vp]),
     "jarq_gptq_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
     "jarq_gptq": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                  ctypes.c_size_t, _vp]),
@@ -288,6 +293,41 @@ def rtn(p: Params, W, codes=None, scales=None, zeros=None, stream=None):
                         _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.float32, "scales"),
                         _ptr(zeros, torch.int32, "zeros"), _stream(stream)), "jarq_rtn")
     return codes, scales, zeros
+
+
+def _scratch(n, dev):
+    raw = torch.empty(n + 256, dtype=torch.uint8, device=dev)
+    off = (-raw.data_ptr()) % 256
+    return raw[off:off + n]
+
+
+def cross_accumulate(Xq, X, Dacc, alpha=1.0, stream=None):
+    """Dacc += alpha Xq^T (X - Xq) for one chunk of tokens (Dacc [d, d] fp64)."""
+    lib = load_library()
+    if Xq.shape != X.shape or Xq.dim() != 2 or Dacc.shape != (X.shape[1], X.shape[1]):
+        raise ValueError("Xq and X must be [m, d] and Dacc [d, d]")
+    _check(lib.jarq_cross_accumulate(_ptr(Xq, torch.float32, "Xq"), _ptr(X, torch.float32, "X"),
+                                     X.shape[0], X.shape[1], float(alpha),
+                                     _ptr(Dacc, torch.float64, "Dacc"), _stream(stream)),
+           "jarq_cross_accumulate")
+
+
+def qep_correct(p: Params, W, H, D, mu, out=None, ws=None, stream=None):
+    """W_corr = W + (1 - mu) (W D^T) H^{-1} (fp32)."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty_like(W)
+    n = int(lib.jarq_qep_workspace_bytes(ctypes.byref(p)))
+    if n == 0:
+        raise JarqError(JARQ_EINVAL, "jarq_qep_workspace_bytes")
+    if ws is None:
+        ws = _scratch(n, W.device)
+    _check(lib.jarq_qep_correct(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                                _ptr(H, torch.float32, "H"), _ptr(D, torch.float64, "D"),
+                                float(mu), _ptr(out, torch.float32, "Wcorr"),
+                                _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream)),
+           "jarq_qep_correct")
+    return out
 
 
 def gptq(p: Params, W, H, codes=None, scales=None, zeros=None, ws=None, stream=None):

@@ -461,6 +461,43 @@ jarq_status jarq_rtn(const jarq_params* p, const float* W, uint8_t* codes, float
   return JARQ_OK;
 }
 
+jarq_status jarq_cross_accumulate(const float* Xq, const float* X, int64_t m, int32_t d,
+                                  double alpha, double* Dacc, void* stream) {
+  if (d < 1 || d > 32768 || d % 4 != 0 || m < 0 || m > INT32_MAX - 64 || !isfinite(alpha) ||
+      !aligned(Dacc, 8))
+    return JARQ_EINVAL;
+  if (m == 0) return JARQ_OK;  // Xq and X may be NULL
+  if (!aligned(Xq, 16) || !aligned(X, 16)) return JARQ_EINVAL;
+  if (launch_cross_update((hipStream_t)stream, Xq, X, (int)m, d, alpha, Dacc) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+size_t jarq_qep_workspace_bytes(const jarq_params* p) {
+  if (!valid_params(p)) return 0;
+  return qep_workspace_bytes(p->rows, p->cols);
+}
+
+jarq_status jarq_qep_correct(const jarq_params* p, const float* W, const float* H,
+                             const double* D, double mu, float* Wcorr, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(D, 8) ||
+      !aligned(Wcorr, 16) || !(mu >= 0.0 && mu <= 1.0))
+    return JARQ_EINVAL;
+  if (workspace == nullptr || ((uintptr_t)workspace % 256) != 0 ||
+      workspace_bytes < qep_workspace_bytes(p->rows, p->cols))
+    return JARQ_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  int* flag = nullptr;
+  if (launch_qep_correct(st, p->rows, p->cols, W, H, D, mu, Wcorr, (char*)workspace, &flag) !=
+      hipSuccess)
+    return JARQ_EHIP;
+  int f = 0;
+  JQ_HIP(hipMemcpyAsync(&f, flag, sizeof(int), hipMemcpyDeviceToHost, st));
+  JQ_HIP(hipStreamSynchronize(st));
+  return f ? JARQ_ENOT_SPD : JARQ_OK;
+}
+
 size_t jarq_gptq_workspace_bytes(const jarq_params* p) {
   if (!valid_params(p)) return 0;
   return gptq_workspace_bytes(p->rows, p->cols, p->group_size);

@@ -132,9 +132,9 @@ hipError_t launch_gptq(hipStream_t st, int rows, int cols, int g, int bits, cons
   *flag_out = flag;
   hipError_t e = launch_zero_bytes(st, flag, sizeof(int));
   if (e != hipSuccess) return e;
-  e = launch_reverse_lower(st, H, cols, Cf);
+  e = launch_copy_lower(st, H, cols, true, Cf);
   if (e != hipSuccess) return e;
-  e = launch_potrf_f64(st, Cf, cols, cols, Linv, flag);
+  e = launch_potrf_f64(st, Cf, cols, cols, Linv, flag, false);
   if (e != hipSuccess) return e;
   e = launch_antitranspose_lower(st, Cf, cols, M);
   if (e != hipSuccess) return e;

@@ -201,10 +201,20 @@ hipError_t launch_gemm_nt_f64(hipStream_t st, bool lower, int M, int N, int K, i
                               double alpha, const double* A, long long lda, const double* B,
                               long long ldb, double* C, long long ldc, long long cz,
                               bool accumulate);
+hipError_t launch_gemm_nn_f64(hipStream_t st, int M, int N, int K, double alpha, const double* A,
+                              long long lda, const double* B, long long ldb, double* C,
+                              long long ldc, bool accumulate);
 hipError_t launch_potrf_f64(hipStream_t st, double* A, int d, long long lda, double* Linv,
-                            int* flag);
-hipError_t launch_reverse_lower(hipStream_t st, const float* H, int d, double* C);
+                            int* flag, bool keep_inverses);
+hipError_t launch_copy_lower(hipStream_t st, const float* H, int d, bool reverse, double* C);
 hipError_t launch_antitranspose_lower(hipStream_t st, const double* C, int d, double* M);
+
+// Propagation-corrected target (setup.hip, qep.hip).
+hipError_t launch_cross_update(hipStream_t st, const float* Xq, const float* X, int m, int d,
+                               double alpha, double* Dacc);
+size_t qep_workspace_bytes(int rows, int cols);
+hipError_t launch_qep_correct(hipStream_t st, int rows, int cols, const float* W, const float* H,
+                              const double* D, double mu, float* Wcorr, char* ws, int** flag_out);
 
 // GPTQ-style host (gptq.hip).
 size_t gptq_workspace_bytes(int rows, int cols, int g);

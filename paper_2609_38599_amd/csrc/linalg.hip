@@ -17,13 +17,14 @@ constexpr int LK = 16;   // k-step of the products
 constexpr int LP = LT + 4;
 }  // namespace
 
-// C[i][j] (+)= alpha sum_{k in slice z} A[i][k] B[j][k] for i < M, j < N, with
+// C[i][j] (+)= alpha sum_{k in slice z} A[i][k] B(j, k) for i < M, j < N, with
+// B(j, k) = B[j][k] (B row-major over j) or, when BK, B[k][j] (row-major over k),
 // the k range split into slices of `kslice` (slice z = blockIdx.z writes
 // C + z * cz).  LOWER: only j <= i is computed and written (tiles wholly above
 // the diagonal exit at once).  A work-group reads rows i0..i0+63 of A and
 // j0..j0+63 of B for its own k range before it writes its tile, so A may
 // alias C when N <= 64 and the tile's k range is all of K (the panel step).
-template <bool LOWER>
+template <bool LOWER, bool BK>
 __global__ __launch_bounds__(256) void gemm_nt_f64_kernel(int M, int N, int K, int kslice,
                                                           double alpha, const double* A,
                                                           long long lda, const double* B,
@@ -53,13 +54,22 @@ __global__ __launch_bounds__(256) void gemm_nt_f64_kernel(int M, int N, int K, i
       const int k = k0 + lk + u;
       const bool kin = k < k_end;
       ra[u] = (kin && i0 + lr < M) ? A[(long long)(i0 + lr) * lda + k] : 0.0;
-      rb[u] = (kin && j0 + lr < N) ? B[(long long)(j0 + lr) * ldb + k] : 0.0;
+      if (BK) {
+        // thread t: k row t / 16, four consecutive j at 4 (t % 16)
+        const int kb = k0 + (tid >> 4), jb = j0 + (tid & 15) * 4 + u;
+        rb[u] = (kb < k_end && jb < N) ? B[(long long)kb * ldb + jb] : 0.0;
+      } else {
+        rb[u] = (kin && j0 + lr < N) ? B[(long long)(j0 + lr) * ldb + k] : 0.0;
+      }
     }
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       as[lk + u][lr] = ra[u];
-      bs[lk + u][lr] = rb[u];
+      if (BK)
+        bs[tid >> 4][(tid & 15) * 4 + u] = rb[u];
+      else
+        bs[lk + u][lr] = rb[u];
     }
     __syncthreads();
 #pragma unroll
@@ -91,21 +101,39 @@ __global__ __launch_bounds__(256) void gemm_nt_f64_kernel(int M, int N, int K, i
   }
 }
 
-hipError_t launch_gemm_nt_f64(hipStream_t st, bool lower, int M, int N, int K, int kslice,
-                              double alpha, const double* A, long long lda, const double* B,
-                              long long ldb, double* C, long long ldc, long long cz,
-                              bool accumulate) {
+static hipError_t launch_gemm_f64(hipStream_t st, bool lower, bool bk, int M, int N, int K,
+                                  int kslice, double alpha, const double* A, long long lda,
+                                  const double* B, long long ldb, double* C, long long ldc,
+                                  long long cz, bool accumulate) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (kslice <= 0) kslice = K > 0 ? K : 1;
   const int nz = K > 0 ? (K + kslice - 1) / kslice : 1;
   dim3 grid((N + LT - 1) / LT, (M + LT - 1) / LT, nz);
   if (lower)
-    hipLaunchKernelGGL(gemm_nt_f64_kernel<true>, grid, dim3(256), 0, st, M, N, K, kslice, alpha,
-                       A, lda, B, ldb, C, ldc, cz, (int)accumulate);
+    hipLaunchKernelGGL((gemm_nt_f64_kernel<true, false>), grid, dim3(256), 0, st, M, N, K, kslice,
+                       alpha, A, lda, B, ldb, C, ldc, cz, (int)accumulate);
+  else if (bk)
+    hipLaunchKernelGGL((gemm_nt_f64_kernel<false, true>), grid, dim3(256), 0, st, M, N, K, kslice,
+                       alpha, A, lda, B, ldb, C, ldc, cz, (int)accumulate);
   else
-    hipLaunchKernelGGL(gemm_nt_f64_kernel<false>, grid, dim3(256), 0, st, M, N, K, kslice, alpha,
-                       A, lda, B, ldb, C, ldc, cz, (int)accumulate);
+    hipLaunchKernelGGL((gemm_nt_f64_kernel<false, false>), grid, dim3(256), 0, st, M, N, K, kslice,
+                       alpha, A, lda, B, ldb, C, ldc, cz, (int)accumulate);
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_nt_f64(hipStream_t st, bool lower, int M, int N, int K, int kslice,
+                              double alpha, const double* A, long long lda, const double* B,
+                              long long ldb, double* C, long long ldc, long long cz,
+                              bool accumulate) {
+  return launch_gemm_f64(st, lower, false, M, N, K, kslice, alpha, A, lda, B, ldb, C, ldc, cz,
+                         accumulate);
+}
+
+hipError_t launch_gemm_nn_f64(hipStream_t st, int M, int N, int K, double alpha, const double* A,
+                              long long lda, const double* B, long long ldb, double* C,
+                              long long ldc, bool accumulate) {
+  return launch_gemm_f64(st, false, true, M, N, K, K, alpha, A, lda, B, ldb, C, ldc, 0,
+                         accumulate);
 }
 
 // Factor the nb x nb diagonal block at A (leading dimension lda, lower part
@@ -164,12 +192,15 @@ __global__ __launch_bounds__(256) void potrf_diag_kernel(double* __restrict__ A,
 }
 
 // In-place lower Cholesky factor of A [d][d] (leading dimension lda; the
-// strict upper part is neither read nor written).  Linv: 64 x 64 fp64 scratch;
-// *flag is set when a pivot is not positive (the caller clears it first).
-hipError_t launch_potrf_f64(hipStream_t st, double* A, int d, long long lda, double* Linv,
-                            int* flag) {
+// strict upper part is neither read nor written).  Linv: 64 x 64 fp64 scratch,
+// or, with keep_inverses, one 64 x 64 block per diagonal block (block b at
+// Linv + 4096 b holds the inverse of the factor's diagonal block b).  *flag is
+// set when a pivot is not positive (the caller clears it first).
+hipError_t launch_potrf_f64(hipStream_t st, double* A, int d, long long lda, double* Linv_base,
+                            int* flag, bool keep_inverses) {
   for (int k0 = 0; k0 < d; k0 += LT) {
     const int nb = min(LT, d - k0);
+    double* Linv = keep_inverses ? Linv_base + (long long)(k0 / LT) * LT * LT : Linv_base;
     double* akk = A + (long long)k0 * lda + k0;
     hipLaunchKernelGGL(potrf_diag_kernel, dim3(1), dim3(256), 0, st, akk, lda, nb, Linv, flag);
     hipError_t e = hipGetLastError();
@@ -190,15 +221,16 @@ hipError_t launch_potrf_f64(hipStream_t st, double* A, int d, long long lda, dou
   return hipSuccess;
 }
 
-// C[i][j] = H[d-1-i][d-1-j] in fp64 (the Hessian with its channel order
-// reversed), lower part only.
-__global__ __launch_bounds__(256) void reverse_lower_kernel(const float* __restrict__ H, int d,
-                                                            double* __restrict__ C) {
+// Lower part of H in fp64: C[i][j] = H[i][j], or with reverse the Hessian
+// with its channel order reversed, C[i][j] = H[d-1-i][d-1-j].
+__global__ __launch_bounds__(256) void copy_lower_kernel(const float* __restrict__ H, int d,
+                                                         int reverse, double* __restrict__ C) {
   const long long n = (long long)d * d;
   for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < n;
        e += (long long)gridDim.x * 256) {
     const int i = (int)(e / d), j = (int)(e % d);
-    if (j <= i) C[e] = (double)H[(long long)(d - 1 - i) * d + (d - 1 - j)];
+    if (j <= i)
+      C[e] = (double)(reverse ? H[(long long)(d - 1 - i) * d + (d - 1 - j)] : H[e]);
   }
 }
 
@@ -223,10 +255,11 @@ __global__ __launch_bounds__(256) void antitranspose_lower_kernel(const double* 
   }
 }
 
-hipError_t launch_reverse_lower(hipStream_t st, const float* H, int d, double* C) {
+hipError_t launch_copy_lower(hipStream_t st, const float* H, int d, bool reverse, double* C) {
   const long long n = (long long)d * d;
   const long long blocks = (n + 255) / 256 < 16384 ? (n + 255) / 256 : 16384;
-  hipLaunchKernelGGL(reverse_lower_kernel, dim3((unsigned)blocks), dim3(256), 0, st, H, d, C);
+  hipLaunchKernelGGL(copy_lower_kernel, dim3((unsigned)blocks), dim3(256), 0, st, H, d,
+                     (int)reverse, C);
   return hipGetLastError();
 }
 

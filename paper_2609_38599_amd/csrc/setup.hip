@@ -35,22 +35,33 @@ __device__ __forceinline__ long long stripe_start(int ta, int nt) {
 }
 }  // namespace
 
-// Block blockIdx.x is tile (ta, tb), ta <= tb, of the upper triangle
-// (64 x 64 tiles: 2080 of them at d = 4096, so the work spreads evenly over
-// 256 compute units).  Four waves, each one 32 x 32 block of the tile.
-__global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restrict__ X, int m,
+// Hessian (CROSS = false): block blockIdx.x is tile (ta, tb), ta <= tb, of
+// the upper triangle (64 x 64 tiles: 2080 of them at d = 4096, so the work
+// spreads evenly over 256 compute units).  Cross product (CROSS = true, the
+// propagation term X~^T (X - X~) of App. E.5): every tile (ta, tb) of the full
+// grid, A = Xq and B = X - Xq formed in fp32 while staging.  Four waves, each
+// one 32 x 32 block of the tile.
+template <bool CROSS>
+__global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restrict__ Xq,
+                                                           const float* __restrict__ X, int m,
                                                            int d, double alpha,
                                                            double* __restrict__ Hacc) {
   __shared__ float xa_s[2][HK][HT];
   __shared__ float xb_s[2][HK][HT];
   const int nt = (d + HT - 1) / HT;
   const long long idx = blockIdx.x;
-  const double bq = 2.0 * nt + 1.0;
-  int ta = (int)floor((bq - sqrt(bq * bq - 8.0 * (double)idx)) * 0.5);
-  ta = ta < 0 ? 0 : (ta > nt - 1 ? nt - 1 : ta);
-  while (ta > 0 && stripe_start(ta, nt) > idx) --ta;
-  while (ta + 1 < nt && stripe_start(ta + 1, nt) <= idx) ++ta;
-  const int tb = ta + (int)(idx - stripe_start(ta, nt));
+  int ta, tb;
+  if (CROSS) {
+    ta = (int)(idx / nt);
+    tb = (int)(idx % nt);
+  } else {
+    const double bq = 2.0 * nt + 1.0;
+    ta = (int)floor((bq - sqrt(bq * bq - 8.0 * (double)idx)) * 0.5);
+    ta = ta < 0 ? 0 : (ta > nt - 1 ? nt - 1 : ta);
+    while (ta > 0 && stripe_start(ta, nt) > idx) --ta;
+    while (ta + 1 < nt && stripe_start(ta + 1, nt) <= idx) ++ta;
+    tb = ta + (int)(idx - stripe_start(ta, nt));
+  }
   const int a0 = ta * HT, b0 = tb * HT;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -58,7 +69,7 @@ __global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restri
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, kk = lane >> 5;
   // the lower-left block of a diagonal tile lies below the diagonal
-  const bool idle = ta == tb && wm > wn;
+  const bool idle = !CROSS && ta == tb && wm > wn;
 
   // Staging: float4 e = tid + 256 p (p < 2) of a 32-token x 64-channel chunk
   // of each operand.  Tokens past m and channels past d load an in-bounds
@@ -72,8 +83,12 @@ __global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restri
       const bool tin = t0 + t < m;
       const size_t roff = (size_t)(tin ? t0 + t : m - 1) * d;
       const bool ina = tin && a0 + c < d, inb = tin && b0 + c < d;
-      const float4 va = *(const float4*)(X + roff + (ina ? a0 + c : 0));
-      const float4 vb = *(const float4*)(X + roff + (inb ? b0 + c : 0));
+      const float4 va = *(const float4*)(Xq + roff + (ina ? a0 + c : 0));
+      float4 vb = *(const float4*)(Xq + roff + (inb ? b0 + c : 0));
+      if (CROSS) {
+        const float4 vx = *(const float4*)(X + roff + (inb ? b0 + c : 0));
+        vb = make_float4(vx.x - vb.x, vx.y - vb.y, vx.z - vb.z, vx.w - vb.w);
+      }
       ra[p] = ina ? va : make_float4(0.f, 0.f, 0.f, 0.f);
       rb[p] = inb ? vb : make_float4(0.f, 0.f, 0.f, 0.f);
     }
@@ -134,7 +149,9 @@ __global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restri
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int a = a0 + wm * 32 + 8 * (v / 4) + 4 * kk + (v % 4);
-      if (a <= b && b < d) {
+      if (CROSS) {
+        if (a < d && b < d) Hacc[(size_t)a * d + b] += alpha * acc64[v];
+      } else if (a <= b && b < d) {
         const double t = alpha * acc64[v];
         Hacc[(size_t)a * d + b] += t;
         if (a != b) Hacc[(size_t)b * d + a] += t;
@@ -146,8 +163,16 @@ __global__ __launch_bounds__(256) void hessian_syrk_kernel(const float* __restri
 hipError_t launch_hessian_update(hipStream_t st, const float* X, int m, int d, double alpha,
                                  double* Hacc) {
   const long long nt = (d + HT - 1) / HT;
-  hipLaunchKernelGGL(hessian_syrk_kernel, dim3((unsigned)(nt * (nt + 1) / 2)), dim3(256), 0, st,
-                     X, m, d, alpha, Hacc);
+  hipLaunchKernelGGL(hessian_syrk_kernel<false>, dim3((unsigned)(nt * (nt + 1) / 2)), dim3(256),
+                     0, st, X, X, m, d, alpha, Hacc);
+  return hipGetLastError();
+}
+
+hipError_t launch_cross_update(hipStream_t st, const float* Xq, const float* X, int m, int d,
+                               double alpha, double* Dacc) {
+  const long long nt = (d + HT - 1) / HT;
+  hipLaunchKernelGGL(hessian_syrk_kernel<true>, dim3((unsigned)(nt * nt)), dim3(256), 0, st, Xq,
+                     X, m, d, alpha, Dacc);
   return hipGetLastError();
 }
 

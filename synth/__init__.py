@@ -7,8 +7,8 @@ arithmetic; both the HIP path and the float64 oracle consume what it makes.
 """
 
 from .layers import (CONFIGS, LayerConfig, calibration_chunks, make_hessian, make_layer,
-                     make_weights)
+                     make_weights, propagated_inputs)
 from .rtn import rtn_quantize
 
 __all__ = ["CONFIGS", "LayerConfig", "calibration_chunks", "make_layer", "make_weights",
-           "make_hessian", "rtn_quantize"]
+           "make_hessian", "propagated_inputs", "rtn_quantize"]

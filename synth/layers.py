@@ -196,6 +196,18 @@ def calibration_chunks(cfg: LayerConfig, device: str | None = None,
         yield xc * scale[None, :]
 
 
+def propagated_inputs(x: np.ndarray, seed: int, rel: float = 0.1, add: float = 0.02):
+    """Stand-in for the inputs a layer receives once the layers before it are
+    quantized: x~ = x (1 + rel xi) + add rms(x) eta, xi and eta independent
+    standard normal (seeded), rms over the whole chunk.  float32 in, float32 out."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([0, 1000 + seed])))
+    x64 = np.asarray(x, np.float64)
+    rms = float(np.sqrt(np.mean(x64 * x64)))
+    xi = rng.standard_normal(x64.shape)
+    eta = rng.standard_normal(x64.shape)
+    return (x64 * (1.0 + rel * xi) + add * rms * eta).astype(np.float32)
+
+
 def make_hessian(cfg: LayerConfig, device: str | None = None,
                  n_tokens: int | None = None, chunk: int = 8192,
                  return_x: bool = False):

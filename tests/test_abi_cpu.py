@@ -117,3 +117,18 @@ def test_gptq_workspace_and_argument_errors(lib):
     assert lib.jarq_gptq(ctypes.byref(q), fake, fake, fake, fake, fake, fake, 1024, None) == binding.JARQ_EWORKSPACE
     assert lib.jarq_gptq(ctypes.byref(q), _vp((1 << 20) + 4), fake, fake, fake, fake, fake, 1 << 30,
                          None) == binding.JARQ_EINVAL
+
+
+def test_qep_entry_points_check_arguments(lib):
+    fake = _vp(1 << 20)
+    acc = lib.jarq_cross_accumulate
+    assert acc(fake, fake, 10, 130, 1.0, fake, None) == binding.JARQ_EINVAL
+    assert acc(None, None, 0, 128, 1.0, fake, None) == binding.JARQ_OK
+    assert acc(fake, _vp((1 << 20) + 4), 10, 128, 1.0, fake, None) == binding.JARQ_EINVAL
+    p = binding.make_params(64, 256, 64, 3, 1)
+    n = lib.jarq_qep_workspace_bytes(ctypes.byref(p))
+    assert n >= 8 * (256 * 256 + 2 * 64 * 256)
+    cor = lib.jarq_qep_correct
+    assert cor(ctypes.byref(p), fake, fake, fake, 1.5, fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
+    assert cor(ctypes.byref(p), fake, fake, fake, float("nan"), fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
+    assert cor(ctypes.byref(p), fake, fake, fake, 0.5, fake, fake, 16, None) == binding.JARQ_EWORKSPACE

@@ -15,7 +15,8 @@ import torch
 
 from oracle import hessian as ohess
 from oracle import hosts
-from synth import CONFIGS, calibration_chunks, make_weights
+from oracle import qep as oqep
+from synth import CONFIGS, calibration_chunks, make_weights, propagated_inputs
 from tests._gpu_common import jq, say, to_dev
 
 pytestmark = [pytest.mark.gpu,
@@ -237,4 +238,112 @@ def test_gptq_rejects_an_indefinite_hessian():
     p = jq.binding.make_params(32, 128, 64, 3, 1)
     with pytest.raises(jq.binding.JarqError) as ei:
         jq.binding.gptq(p, to_dev(W), to_dev(H))
+    assert ei.value.status == jq.binding.JARQ_ENOT_SPD
+
+
+# --------------------------------------------------------------------------
+# Propagation-corrected target (App. E.5)
+# --------------------------------------------------------------------------
+
+def test_cross_integer_inputs_are_exact():
+    rng = np.random.default_rng(21)
+    m, d = 700, 196
+    X = rng.integers(-3, 4, size=(m, d)).astype(np.float32)
+    Xq = (X + rng.integers(-1, 2, size=(m, d))).astype(np.float32)
+    D = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    for a, b in ((0, 300), (300, m)):
+        jq.binding.cross_accumulate(to_dev(Xq[a:b]), to_dev(X[a:b]), D, 0.5)
+    torch.cuda.synchronize()
+    assert np.array_equal(D.cpu().numpy(), oqep.cross([Xq], [X], d, 0.5))
+
+
+@pytest.mark.parametrize("m,d", [(900, 260), (33, 128)])
+def test_cross_matches_oracle_within_fp32_bound(m, d):
+    rng = np.random.default_rng(m)
+    X = rng.standard_normal((m, d)).astype(np.float32)
+    X[:, 3] *= 20.0
+    Xq = propagated_inputs(X, m)
+    D = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    jq.binding.cross_accumulate(to_dev(Xq), to_dev(X), D, 1.0 / m)
+    torch.cuda.synchronize()
+    ref = oqep.cross([Xq], [X], d, 1.0 / m)
+    diff32 = (X - Xq).astype(np.float64)
+    absg = np.abs(Xq.astype(np.float64)).T @ np.abs(diff32)
+    # one more rounding than the Hessian: X - X~ is formed in fp32
+    bound = ohess.fp32_error_bound(absg, 1.0 / m, segment=257) + 1e-300
+    worst = np.max(np.abs(D.cpu().numpy() - ref) / bound)
+    say(f"[cross] m={m} d={d} worst error / bound {worst:.3e}")
+    assert worst <= 1.0
+
+
+def _qep_inputs(rows, d, seed, n=None):
+    rng = np.random.default_rng(seed)
+    n = n or 4 * d
+    X = rng.standard_normal((n, d))
+    for c in range(1, d):
+        X[:, c] = 0.6 * X[:, c - 1] + 0.8 * X[:, c]
+    X = X.astype(np.float32)
+    Xq = propagated_inputs(X, seed)
+    H = ohess.hessian([Xq], d, alpha=1.0 / n, damp=0.01).astype(np.float32)
+    D = oqep.cross([Xq], [X], d, alpha=1.0 / n)
+    W = (0.02 * rng.standard_t(5, size=(rows, d))).astype(np.float32)
+    return W, H, D
+
+
+def _check_qep(Wc, ref, W):
+    corr = np.max(np.abs(ref - W))
+    err = np.abs(Wc.astype(np.float64) - ref)
+    bound = 2.0 ** -24 * np.abs(ref) + 1e-9 * corr
+    say(f"[qep] max |correction| {corr:.3e}, worst error / bound {np.max(err / bound):.3e}")
+    assert np.all(err <= bound)
+
+
+@pytest.mark.parametrize("rows,d,mu", [(100, 256, 0.5), (67, 320, 0.0), (64, 192, 0.25)])
+def test_qep_correct_matches_oracle(rows, d, mu):
+    W, H, D = _qep_inputs(rows, d, rows + d)
+    p = jq.binding.make_params(rows, d, 64, 3, 1)
+    Wc = jq.binding.qep_correct(p, to_dev(W), to_dev(H), to_dev(D), mu)
+    torch.cuda.synchronize()
+    _check_qep(Wc.cpu().numpy(), oqep.corrected_weights(W, H, D, mu), W.astype(np.float64))
+
+
+def test_qep_mu_one_returns_the_weights():
+    W, H, D = _qep_inputs(40, 128, 9)
+    p = jq.binding.make_params(40, 128, 64, 3, 1)
+    Wc = jq.binding.qep_correct(p, to_dev(W), to_dev(H), to_dev(D), 1.0)
+    torch.cuda.synchronize()
+    assert np.array_equal(Wc.cpu().numpy(), W)
+
+
+def test_qep_full_size_sampled_rows():
+    """The 4096 x 4096 attention projection with its Hessian and a cross term
+    from 8192 calibration tokens and their propagated counterparts: 64 sampled
+    rows against the oracle (rows are independent)."""
+    cfg = CONFIGS[1]
+    W = make_weights(cfg)
+    from synth import make_hessian
+    H = make_hessian(cfg, device="cuda")
+    X = next(calibration_chunks(cfg, device="cuda", n_tokens=8192, chunk=8192))
+    X = X.to(torch.float32).cpu().numpy()
+    Xq = propagated_inputs(X, 1)
+    D = oqep.cross([Xq], [X], cfg.cols, alpha=1.0 / X.shape[0])
+    say("[qep-full] inputs ready")
+    p = jq.binding.make_params(cfg.rows, cfg.cols, cfg.group_size, cfg.bits, 1)
+    Wd, Hd, Dd = to_dev(W), to_dev(H), to_dev(D)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    Wc = jq.binding.qep_correct(p, Wd, Hd, Dd, 0.5)
+    torch.cuda.synchronize()
+    say(f"[qep-full] GPU correction {1e3 * (time.perf_counter() - t0):.1f} ms")
+    idx = np.sort(np.random.default_rng(6).choice(cfg.rows, 64, replace=False))
+    ref = oqep.corrected_weights(W[idx], H, D, 0.5)
+    _check_qep(Wc.cpu().numpy()[idx], ref, W[idx].astype(np.float64))
+
+
+def test_qep_rejects_an_indefinite_hessian():
+    W, H, D = _qep_inputs(32, 128, 10)
+    H[5, 5] = -1.0
+    p = jq.binding.make_params(32, 128, 64, 3, 1)
+    with pytest.raises(jq.binding.JarqError) as ei:
+        jq.binding.qep_correct(p, to_dev(W), to_dev(H), to_dev(D), 0.5)
     assert ei.value.status == jq.binding.JARQ_ENOT_SPD

@@ -3,7 +3,7 @@ round-to-nearest host."""
 
 import numpy as np
 
-from oracle import hessian, hosts
+from oracle import hessian, hosts, qep
 from synth import CONFIGS, make_hessian, rtn_quantize
 
 
@@ -218,3 +218,52 @@ def test_gptq_lower_factor_form_equals_the_inverse_factor_recursion():
     differ = q != q_ref
     near = np.abs(pre - np.floor(pre) - 0.5) < 1e-6
     assert np.all(near[differ]) and differ.mean() <= 1e-3
+
+
+# --------------------------------------------------------------------------
+# Propagation-corrected target (App. E.5)
+# --------------------------------------------------------------------------
+
+def _qep_problem(seed, n=60, d=10, dout=7, nu=0.6):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d))
+    Xq = X + 0.1 * rng.standard_normal((n, d))
+    W = rng.standard_normal((dout, d))              # rows = output channels
+    H = Xq.T @ Xq + nu * nu * np.eye(d)
+    D = Xq.T @ (X - Xq)
+    return X, Xq, W, H, D, nu
+
+
+def test_qep_corrected_weights_solve_the_mixed_target():
+    # least squares of Y(mu) = [(1 - mu) X W_p + mu X~ W_p; nu W_p] on A = [X~; nu I]
+    X, Xq, W, H, D, nu = _qep_problem(14)
+    Wp = W.T
+    A = np.vstack([Xq, nu * np.eye(X.shape[1])])
+    for mu in (0.0, 0.3, 0.5, 1.0):
+        Y = np.vstack([(1 - mu) * X @ Wp + mu * Xq @ Wp, nu * Wp])
+        ls = np.linalg.lstsq(A, Y, rcond=None)[0]
+        assert np.allclose(qep.corrected_weights(W, H, D, mu), ls.T, rtol=1e-10, atol=1e-12)
+
+
+def test_qep_objective_splits_into_the_main_problem_plus_a_constant():
+    X, Xq, W, H, D, nu = _qep_problem(15)
+    mu = 0.5
+    Wp = W.T
+    A = np.vstack([Xq, nu * np.eye(X.shape[1])])
+    Y = np.vstack([(1 - mu) * X @ Wp + mu * Xq @ Wp, nu * Wp])
+    Wc = qep.corrected_weights(W, H, D, mu).T
+    const = np.sum((Y - A @ Wc) ** 2)
+    rng = np.random.default_rng(16)
+    for _ in range(5):
+        What = Wp + 0.3 * rng.standard_normal(Wp.shape)
+        lhs = np.sum((Y - A @ What) ** 2)
+        rhs = np.sum((A @ (Wc - What)) ** 2) + const
+        assert np.isclose(lhs, rhs, rtol=1e-11)
+
+
+def test_qep_special_cases():
+    X, Xq, W, H, D, nu = _qep_problem(17)
+    assert np.array_equal(qep.corrected_weights(W, H, D, 1.0), W)
+    assert np.array_equal(qep.corrected_weights(W, H, np.zeros_like(D), 0.0), W)
+    Dc = qep.cross([Xq[:20], Xq[20:]], [X[:20], X[20:]], X.shape[1])
+    assert np.allclose(Dc, D, rtol=1e-13, atol=1e-13)

@@ -268,6 +268,64 @@ jarq_status jarq_gptq(const jarq_params* p, const float* W, const float* H, uint
                       float* scales, int32_t* zeros, void* workspace, size_t workspace_bytes,
                       void* stream);
 
+/*
+ * After refinement.
+ *
+ * jarq_canonicalize (App. E.3, eq. (canonicalization)): every group with
+ * s < 0 becomes s' = -s, q' = (2^b - 1) - q, z' = (2^b - 1) - z, which
+ * represents the same weights (eq. (canonicalization_equivalence)) with
+ * codes in the same range; groups with s >= 0 are left alone.  This changes
+ * Z, so it runs only after refinement, for formats that need positive
+ * scales.  In place; codes 16-byte aligned.  Asynchronous.
+ */
+jarq_status jarq_canonicalize(const jarq_params* p, uint8_t* codes, float* scales,
+                              int32_t* zeros, void* stream);
+
+/* Output dtypes of jarq_dequantize. */
+#define JARQ_F32 0
+#define JARQ_F16 1
+#define JARQ_BF16 2
+
+/*
+ * Dequantized weights out [rows][cols] = s (q - z) of eq. (1), computed in fp32
+ * and rounded once (to nearest even) to dtype JARQ_F32, JARQ_F16 or JARQ_BF16
+ * (the model's floating-point dtype, App. A.1).  perm (nullable, [cols]
+ * int32): the refined layer lives in permuted input coordinates, position k
+ * being original column perm[k] (activation ordering; App. A.1 and E.2 restore
+ * the original coordinates on write-back); out is then in the original order.
+ * perm must be a permutation of 0..cols-1 (entries outside that range are
+ * skipped).  Asynchronous.
+ */
+jarq_status jarq_dequantize(const jarq_params* p, const uint8_t* codes, const float* scales,
+                            const int32_t* zeros, const int32_t* perm, int32_t dtype, void* out,
+                            void* stream);
+
+/*
+ * b-bit codes packed into 32-bit words: row r is one little-endian bit stream
+ * in which code k occupies bits [k b, k b + b); stream bit t is bit t % 32 of
+ * word t / 32 of the row; each row starts on a new word, so packed is
+ * [rows][ceil(cols b / 32)] uint32 (bits past the last code are 0).
+ * jarq_unpack_codes is the inverse.  Asynchronous.
+ */
+jarq_status jarq_pack_codes(const jarq_params* p, const uint8_t* codes, uint32_t* packed,
+                            void* stream);
+jarq_status jarq_unpack_codes(const jarq_params* p, const uint32_t* packed, uint8_t* codes,
+                              void* stream);
+
+/*
+ * Activation ordering of a GPTQ host (App. A.1): perm [d] int32 lists the
+ * input channels by decreasing diag(H), ties by increasing index (H [d][d]
+ * fp32, diagonal not NaN).  jarq_permute gathers the layer into that order:
+ * Wp[r][k] = W[r][perm[k]] ([rows][cols]) and Hp[k][l] = H[perm[k]][perm[l]]
+ * ([cols][cols]), with rows and cols from `p`.  Refinement then runs on
+ * (Wp, Hp) with groups of consecutive permuted columns, and jarq_dequantize
+ * with the same perm writes the weights back in the original order.
+ * Asynchronous.
+ */
+jarq_status jarq_act_order(const float* H, int32_t d, int32_t* perm, void* stream);
+jarq_status jarq_permute(const jarq_params* p, const int32_t* perm, const float* W, const float* H,
+                         float* Wp, float* Hp, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* jarq_status_string(jarq_status s);
 

@@ -19,6 +19,8 @@ hosts     Round-to-nearest host, and the GPTQ-style sequential-compensation
 hessian   The calibration Hessian H = X~^T X~ + nu^2 I (App. E.1) from
           chunks of tokens, with optional relative damping.
 qep       The propagation-corrected weights of the mixed target (App. E.5).
+post      After refinement: canonical positive scales (App. E.3), dequantized
+          weights, packed codes, activation ordering.
 """
 
-from . import jarq, qrform, replay, hosts, hessian, qep  # noqa: F401
+from . import jarq, qrform, replay, hosts, hessian, qep, post  # noqa: F401

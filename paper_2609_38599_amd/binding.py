@@ -92,6 +92,13 @@ _SIGNATURES = {
     "jarq_qep_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
     "jarq_qep_correct": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, ctypes.c_double,
                                         _vp, _vp, ctypes.c_size_t, _vp]),
+    "jarq_canonicalize": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp]),
+    "jarq_dequantize": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, ctypes.c_int32,
+                                       _vp, _vp]),
+    "jarq_pack_codes": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp]),
+    "jarq_unpack_codes": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp]),
+    "jarq_act_order": (ctypes.c_int, [_vp, ctypes.c_int32, _vp, _vp]),
+    "jarq_permute": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp]),
     "jarq_gptq_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
     "jarq_gptq": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                  ctypes.c_size_t, _vp]),
@@ -293,6 +300,76 @@ def rtn(p: Params, W, codes=None, scales=None, zeros=None, stream=None):
                         _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.float32, "scales"),
                         _ptr(zeros, torch.int32, "zeros"), _stream(stream)), "jarq_rtn")
     return codes, scales, zeros
+
+
+DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+
+def canonicalize(p: Params, codes, scales, zeros, stream=None):
+    """In place: groups with a negative scale get s' = -s, q' = qmax - q, z' = qmax - z."""
+    lib = load_library()
+    _check(lib.jarq_canonicalize(ctypes.byref(p), _ptr(codes, torch.uint8, "codes"),
+                                 _ptr(scales, torch.float32, "scales"),
+                                 _ptr(zeros, torch.int32, "zeros"), _stream(stream)),
+           "jarq_canonicalize")
+
+
+def dequantize(p: Params, codes, scales, zeros, dtype=torch.float32, perm=None, out=None,
+               stream=None):
+    """s (q - z) as `dtype`; with perm, written back in the original column order."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty(p.rows, p.cols, dtype=dtype, device=codes.device)
+    _check(lib.jarq_dequantize(ctypes.byref(p), _ptr(codes, torch.uint8, "codes"),
+                               _ptr(scales, torch.float32, "scales"),
+                               _ptr(zeros, torch.int32, "zeros"), _ptr(perm, torch.int32, "perm"),
+                               DTYPES[out.dtype], _ptr(out, out.dtype, "out"), _stream(stream)),
+           "jarq_dequantize")
+    return out
+
+
+def packed_words_per_row(p: Params) -> int:
+    return (p.cols * p.bits + 31) // 32
+
+
+def pack_codes(p: Params, codes, out=None, stream=None):
+    lib = load_library()
+    if out is None:
+        out = torch.empty(p.rows, packed_words_per_row(p), dtype=torch.int32, device=codes.device)
+    _check(lib.jarq_pack_codes(ctypes.byref(p), _ptr(codes, torch.uint8, "codes"),
+                               _ptr(out, torch.int32, "packed"), _stream(stream)),
+           "jarq_pack_codes")
+    return out
+
+
+def unpack_codes(p: Params, packed, out=None, stream=None):
+    lib = load_library()
+    if out is None:
+        out = torch.empty(p.rows, p.cols, dtype=torch.uint8, device=packed.device)
+    _check(lib.jarq_unpack_codes(ctypes.byref(p), _ptr(packed, torch.int32, "packed"),
+                                 _ptr(out, torch.uint8, "codes"), _stream(stream)),
+           "jarq_unpack_codes")
+    return out
+
+
+def act_order(H, out=None, stream=None):
+    lib = load_library()
+    d = H.shape[0]
+    if out is None:
+        out = torch.empty(d, dtype=torch.int32, device=H.device)
+    _check(lib.jarq_act_order(_ptr(H, torch.float32, "H"), d, _ptr(out, torch.int32, "perm"),
+                              _stream(stream)), "jarq_act_order")
+    return out
+
+
+def permute(p: Params, perm, W, H, stream=None):
+    lib = load_library()
+    Wp, Hp = torch.empty_like(W), torch.empty_like(H)
+    _check(lib.jarq_permute(ctypes.byref(p), _ptr(perm, torch.int32, "perm"),
+                            _ptr(W, torch.float32, "W"), _ptr(H, torch.float32, "H"),
+                            _ptr(Wp, torch.float32, "Wp"), _ptr(Hp, torch.float32, "Hp"),
+                            _stream(stream)), "jarq_permute")
+    return Wp, Hp
 
 
 def _scratch(n, dev):

@@ -498,6 +498,61 @@ jarq_status jarq_qep_correct(const jarq_params* p, const float* W, const float* 
   return f ? JARQ_ENOT_SPD : JARQ_OK;
 }
 
+jarq_status jarq_canonicalize(const jarq_params* p, uint8_t* codes, float* scales,
+                              int32_t* zeros, void* stream) {
+  if (!valid_params(p) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  if (launch_canonicalize((hipStream_t)stream, p->rows, p->cols, p->group_size, p->bits, codes,
+                          scales, zeros) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_dequantize(const jarq_params* p, const uint8_t* codes, const float* scales,
+                            const int32_t* zeros, const int32_t* perm, int32_t dtype, void* out,
+                            void* stream) {
+  if (!valid_params(p) || codes == nullptr || !aligned(scales, 4) || !aligned(zeros, 4) ||
+      dtype < JARQ_F32 || dtype > JARQ_BF16 || !aligned(out, dtype == JARQ_F32 ? 4 : 2) ||
+      (perm != nullptr && !aligned(perm, 4)))
+    return JARQ_EINVAL;
+  if (launch_dequantize((hipStream_t)stream, p->rows, p->cols, p->group_size, codes, scales,
+                        zeros, perm, dtype, out) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_pack_codes(const jarq_params* p, const uint8_t* codes, uint32_t* packed,
+                            void* stream) {
+  if (!valid_params(p) || codes == nullptr || !aligned(packed, 4)) return JARQ_EINVAL;
+  if (launch_pack((hipStream_t)stream, p->rows, p->cols, p->bits, codes, packed) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_unpack_codes(const jarq_params* p, const uint32_t* packed, uint8_t* codes,
+                              void* stream) {
+  if (!valid_params(p) || codes == nullptr || !aligned(packed, 4)) return JARQ_EINVAL;
+  if (launch_unpack((hipStream_t)stream, p->rows, p->cols, p->bits, packed, codes) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_act_order(const float* H, int32_t d, int32_t* perm, void* stream) {
+  if (d < 1 || d > 32768 || !aligned(H, 4) || !aligned(perm, 4)) return JARQ_EINVAL;
+  if (launch_act_order((hipStream_t)stream, H, d, perm) != hipSuccess) return JARQ_EHIP;
+  return JARQ_OK;
+}
+
+jarq_status jarq_permute(const jarq_params* p, const int32_t* perm, const float* W, const float* H,
+                         float* Wp, float* Hp, void* stream) {
+  if (!valid_params(p) || !aligned(perm, 4) || !aligned(W, 4) || !aligned(H, 4) ||
+      !aligned(Wp, 4) || !aligned(Hp, 4))
+    return JARQ_EINVAL;
+  if (launch_permute((hipStream_t)stream, p->rows, p->cols, perm, W, H, Wp, Hp) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
 size_t jarq_gptq_workspace_bytes(const jarq_params* p) {
   if (!valid_params(p)) return 0;
   return gptq_workspace_bytes(p->rows, p->cols, p->group_size);

@@ -216,6 +216,20 @@ size_t qep_workspace_bytes(int rows, int cols);
 hipError_t launch_qep_correct(hipStream_t st, int rows, int cols, const float* W, const float* H,
                               const double* D, double mu, float* Wcorr, char* ws, int** flag_out);
 
+// After refinement (post.hip).
+hipError_t launch_canonicalize(hipStream_t st, int rows, int cols, int g, int bits,
+                               uint8_t* codes, float* scales, int32_t* zeros);
+hipError_t launch_dequantize(hipStream_t st, int rows, int cols, int g, const uint8_t* codes,
+                             const float* scales, const int32_t* zeros, const int32_t* perm,
+                             int dtype, void* out);
+hipError_t launch_pack(hipStream_t st, int rows, int cols, int bits, const uint8_t* codes,
+                       uint32_t* packed);
+hipError_t launch_unpack(hipStream_t st, int rows, int cols, int bits, const uint32_t* packed,
+                         uint8_t* codes);
+hipError_t launch_act_order(hipStream_t st, const float* H, int d, int32_t* perm);
+hipError_t launch_permute(hipStream_t st, int rows, int d, const int32_t* perm, const float* W,
+                          const float* H, float* Wp, float* Hp);
+
 // GPTQ-style host (gptq.hip).
 size_t gptq_workspace_bytes(int rows, int cols, int g);
 hipError_t launch_gptq(hipStream_t st, int rows, int cols, int g, int bits, const float* W,

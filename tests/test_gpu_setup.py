@@ -15,6 +15,7 @@ import torch
 
 from oracle import hessian as ohess
 from oracle import hosts
+from oracle import post as opost
 from oracle import qep as oqep
 from synth import CONFIGS, calibration_chunks, make_weights, propagated_inputs
 from tests._gpu_common import jq, say, to_dev
@@ -347,3 +348,88 @@ def test_qep_rejects_an_indefinite_hessian():
     with pytest.raises(jq.binding.JarqError) as ei:
         jq.binding.qep_correct(p, to_dev(W), to_dev(H), to_dev(D), 0.5)
     assert ei.value.status == jq.binding.JARQ_ENOT_SPD
+
+
+# --------------------------------------------------------------------------
+# After refinement: canonical scales, dequantized weights, packed codes,
+# activation ordering
+# --------------------------------------------------------------------------
+
+def _random_state(rows, cols, g, bits, seed):
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(0, 1 << bits, size=(rows, cols)).astype(np.uint8)
+    scales = (rng.standard_normal((rows, cols // g)) * 0.02).astype(np.float32)
+    scales[0, 0] = 0.0
+    zeros = rng.integers(0, 1 << bits, size=(rows, cols // g)).astype(np.int32)
+    return codes, scales, zeros
+
+
+@pytest.mark.parametrize("g,bits", [(32, 2), (64, 3), (128, 4), (64, 8)])
+def test_canonicalize_matches_oracle(g, bits):
+    rows, cols = 45, 384
+    codes, scales, zeros = _random_state(rows, cols, g, bits, g + bits)
+    p = jq.binding.make_params(rows, cols, g, bits, 1)
+    q, s, z = to_dev(codes), to_dev(scales), to_dev(zeros)
+    jq.binding.canonicalize(p, q, s, z)
+    torch.cuda.synchronize()
+    rq, rs, rz = opost.canonicalize(codes, scales, zeros, g, bits)
+    assert np.array_equal(q.cpu().numpy(), rq)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+    assert np.array_equal(z.cpu().numpy(), rz)
+
+
+@pytest.mark.parametrize("dtype,name", [(torch.float32, "f32"), (torch.float16, "f16"),
+                                        (torch.bfloat16, "bf16")])
+def test_dequantize_matches_oracle(dtype, name):
+    rows, cols, g, bits = 37, 256, 64, 4
+    codes, scales, zeros = _random_state(rows, cols, g, bits, 40)
+    scales[3, 1] = 7e4          # overflows fp16
+    p = jq.binding.make_params(rows, cols, g, bits, 1)
+    perm = np.random.default_rng(41).permutation(cols).astype(np.int32)
+    for pm in (None, perm):
+        out = jq.binding.dequantize(p, to_dev(codes), to_dev(scales), to_dev(zeros), dtype,
+                                    None if pm is None else to_dev(pm))
+        torch.cuda.synchronize()
+        ref = opost.dequantize(codes, scales, zeros, g, name, pm)
+        got = out.cpu()
+        got = got.view(torch.int16).numpy().view(np.uint16) if name == "bf16" else got.numpy()
+        assert np.array_equal(got.view(np.uint8), ref.view(np.uint8))
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 6, 7, 8])
+def test_pack_and_unpack_match_oracle(bits):
+    rows, cols = 19, 352
+    codes = np.random.default_rng(bits).integers(0, 1 << bits, size=(rows, cols)).astype(np.uint8)
+    p = jq.binding.make_params(rows, cols, 32, bits, 1)
+    packed = jq.binding.pack_codes(p, to_dev(codes))
+    back = jq.binding.unpack_codes(p, packed)
+    torch.cuda.synchronize()
+    ref = opost.pack(codes, bits)
+    assert np.array_equal(packed.cpu().numpy().view(np.uint32), ref)
+    assert np.array_equal(back.cpu().numpy(), codes)
+
+
+def test_act_order_flow_matches_oracle():
+    """GPTQ with activation ordering: order the channels, gather the layer,
+    build the host in the permuted coordinates, write the weights back."""
+    rows, cols, g, bits = 96, 320, 64, 3
+    rng = np.random.default_rng(50)
+    W = (0.02 * rng.standard_normal((rows, cols))).astype(np.float32)
+    Dg = rng.uniform(0.5, 2.0, cols)
+    H = _correlated_hessian(cols, 51).astype(np.float64) * Dg[:, None] * Dg[None, :]
+    t = max(H[7, 7], H[8, 8])               # a tie, made by raising a diagonal entry
+    H[7, 7] = H[8, 8] = t
+    H = H.astype(np.float32)
+    p = jq.binding.make_params(rows, cols, g, bits, 1)
+    perm = jq.binding.act_order(to_dev(H))
+    Wp, Hp = jq.binding.permute(p, perm, to_dev(W), to_dev(H))
+    q, s, z = jq.binding.gptq(p, Wp, Hp)
+    out = jq.binding.dequantize(p, q, s, z, torch.float32, perm)
+    torch.cuda.synchronize()
+    rperm = opost.act_order(H)
+    assert np.array_equal(perm.cpu().numpy(), rperm)
+    rWp, rHp = opost.permute(W, H, rperm)
+    assert np.array_equal(Wp.cpu().numpy(), rWp) and np.array_equal(Hp.cpu().numpy(), rHp)
+    _check_gptq(rWp, rHp, g, bits, q.cpu().numpy(), s.cpu().numpy(), z.cpu().numpy())
+    rq, rs, rz = (x.cpu().numpy() for x in (q, s, z))
+    assert np.array_equal(out.cpu().numpy(), opost.dequantize(rq, rs, rz, g, "f32", rperm))

@@ -3,7 +3,7 @@ round-to-nearest host."""
 
 import numpy as np
 
-from oracle import hessian, hosts, qep
+from oracle import hessian, hosts, post, qep
 from synth import CONFIGS, make_hessian, rtn_quantize
 
 
@@ -267,3 +267,84 @@ def test_qep_special_cases():
     assert np.array_equal(qep.corrected_weights(W, H, np.zeros_like(D), 0.0), W)
     Dc = qep.cross([Xq[:20], Xq[20:]], [X[:20], X[20:]], X.shape[1])
     assert np.allclose(Dc, D, rtol=1e-13, atol=1e-13)
+
+
+# --------------------------------------------------------------------------
+# After refinement (App. E.3; packing, activation ordering)
+# --------------------------------------------------------------------------
+
+def test_canonicalization_keeps_the_weights_and_makes_scales_positive():
+    rng = np.random.default_rng(30)
+    rows, cols, g, bits = 6, 96, 32, 3
+    codes = rng.integers(0, 8, size=(rows, cols)).astype(np.uint8)
+    scales = (rng.standard_normal((rows, cols // g)) * 0.01).astype(np.float32)
+    zeros = rng.integers(0, 8, size=(rows, cols // g)).astype(np.int32)
+    q, s, z = post.canonicalize(codes, scales, zeros, g, bits)
+    assert np.all(s >= 0) and q.max() <= 7 and z.min() >= 0 and z.max() <= 7
+    # eq. (canonicalization_equivalence), exactly in fp32
+    assert np.array_equal(post.dequantize(q, s, z, g), post.dequantize(codes, scales, zeros, g))
+    # a second pass changes nothing
+    q2, s2, z2 = post.canonicalize(q, s, z, g, bits)
+    assert np.array_equal(q2, q) and np.array_equal(s2, s) and np.array_equal(z2, z)
+    # hand-worked group: s = -0.5, z = 2, q = [0, 7] (3 bits) -> s = 0.5, z = 5, q = [7, 0]
+    q3, s3, z3 = post.canonicalize(np.array([[0, 7]], np.uint8), np.array([[-0.5]], np.float32),
+                                   np.array([[2]], np.int32), 2, 3)
+    assert q3.tolist() == [[7, 0]] and s3.tolist() == [[0.5]] and z3.tolist() == [[5]]
+
+
+def test_dequantize_dtypes():
+    import torch
+    rng = np.random.default_rng(31)
+    codes = rng.integers(0, 16, size=(5, 64)).astype(np.uint8)
+    scales = (rng.standard_normal((5, 2)) * 0.03).astype(np.float32)
+    zeros = rng.integers(0, 16, size=(5, 2)).astype(np.int32)
+    w32 = post.dequantize(codes, scales, zeros, 32)
+    assert w32.dtype == np.float32
+    assert w32[0, 0] == np.float32(scales[0, 0]) * np.float32(int(codes[0, 0]) - int(zeros[0, 0]))
+    # library conversions (round to nearest even) agree with the oracle's
+    assert np.array_equal(post.dequantize(codes, scales, zeros, 32, "f16"), w32.astype(np.float16))
+    ref_bf16 = torch.from_numpy(w32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(post.dequantize(codes, scales, zeros, 32, "bf16"), ref_bf16)
+    # hand-worked bf16 roundings: 1 -> 0x3F80; 1 + 2^-8 (a tie) -> even 0x3F80;
+    # 1 + 3 2^-8 (a tie) -> even 0x3F82; 1 + 2^-8 + 2^-20 -> up 0x3F81
+    x = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 2 ** -8 + 2 ** -20], np.float32)
+    assert post.bf16_bits(x).tolist() == [0x3F80, 0x3F80, 0x3F82, 0x3F81]
+
+
+def test_dequantize_restores_the_original_column_order():
+    rng = np.random.default_rng(32)
+    W = rng.standard_normal((3, 8)).astype(np.float32)
+    perm = np.array([5, 2, 7, 0, 1, 6, 3, 4])
+    codes = np.arange(24, dtype=np.uint8).reshape(3, 8) % 8
+    s = np.ones((3, 1), np.float32)
+    z = np.zeros((3, 1), np.int32)
+    out = post.dequantize(codes, s, z, 8, perm=perm)
+    for k in range(8):
+        assert np.array_equal(out[:, perm[k]], codes[:, k].astype(np.float32))
+    Wp, _ = post.permute(W, np.eye(8), perm)
+    assert np.array_equal(Wp[:, 3], W[:, 0])
+
+
+def test_pack_worked_example_and_round_trip():
+    # 3-bit codes 1..7, 0, 1, 2, 3: code k sits at bits 3k; the last code
+    # (3 = 0b011) straddles the two words: bits 30, 31 of word 0 hold its low
+    # bits (1, 1), bit 0 of word 1 its high bit (0).
+    codes = np.array([[1, 2, 3, 4, 5, 6, 7, 0, 1, 2, 3]], np.uint8)
+    w0 = (1 + (2 << 3) + (3 << 6) + (4 << 9) + (5 << 12) + (6 << 15) + (7 << 18) + (0 << 21)
+          + (1 << 24) + (2 << 27) + (3 << 30)) & 0xFFFFFFFF
+    packed = post.pack(codes, 3)
+    assert packed.shape == (1, 2) and packed[0, 0] == w0 and packed[0, 1] == 0
+    rng = np.random.default_rng(33)
+    for bits in range(1, 9):
+        c = rng.integers(0, 1 << bits, size=(4, 77)).astype(np.uint8)
+        p = post.pack(c, bits)
+        assert p.shape == (4, (77 * bits + 31) // 32)
+        assert np.array_equal(post.unpack(p, 77, bits), c)
+        # every set bit of the stream belongs to some code
+        assert sum(bin(int(v)).count("1") for v in p.ravel()) == \
+            sum(bin(int(v)).count("1") for v in c.ravel())
+
+
+def test_act_order_sorts_the_diagonal_stably():
+    H = np.diag(np.array([2.0, 5.0, 2.0, 7.0, 5.0], np.float32))
+    assert post.act_order(H).tolist() == [3, 1, 4, 0, 2]

@@ -40,6 +40,26 @@ __device__ __forceinline__ void dma16(const _Float16* src, _Float16* lds) {
 // Wait until at most n of this wave's vector-memory operations are in flight
 // (other counters untouched), then meet the other waves.  The empty asm
 // statements keep the compiler from moving LDS accesses across the barrier.
+// LDS reads issued as instructions of their own: the compiler does not treat
+// them as reads that an outstanding direct-to-LDS load might feed, so it adds
+// no wait for those loads; the kernel's own waits (every stage is complete
+// before the barrier that precedes its reads) keep them correct.  The caller
+// waits for the results with lds_wait().
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+__device__ __forceinline__ f16x8 lds_read16(uint32_t a) {
+  f16x8 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a));
+  return r;
+}
+__device__ __forceinline__ float4 lds_read16f(uint32_t a) {
+  float4 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a));
+  return r;
+}
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 template <int N>
 __device__ __forceinline__ void wait_vm_and_barrier() {
   static_assert(N < 16, "vmcnt field");
@@ -61,7 +81,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
   __shared__ __attribute__((aligned(1024))) _Float16 buf1[STAGE];
   __shared__ __attribute__((aligned(1024))) _Float16 buf2[STAGE];
-  __shared__ float sc_s[BM][kMaxPanelGroups];
+  __shared__ __attribute__((aligned(16))) float sc_s[kMaxPanelGroups][BM];
   const int G = cols / g;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -91,7 +111,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 
   for (int e = tid; e < BM * ng; e += 256) {
     const int r = e / ng, h = e % ng;
-    sc_s[r][h] = scales[(size_t)map_row(rowmap, row_of(r)) * G + h0 + h];  // list holds positions
+    sc_s[h][r] = scales[(size_t)map_row(rowmap, row_of(r)) * G + h0 + h];  // list holds positions
   }
   // Rows of this lane's accumulator elements (element v of a 32x32 block is
   // row 8 (v / 4) + 4 (lane / 32) + v % 4), kept for the epilogue.
@@ -131,7 +151,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   };
   auto frag = [&](const _Float16* tile, int r, int ks) {
     const int c = (ks >> 3) + kh;
-    return *(const f16x8*)(tile + r * BK + ((c ^ swz(r)) << 3));
+    return lds_read16(lds_addr(tile + r * BK + ((c ^ swz(r)) << 3)));
   };
 
   f32x16 acc[2][2], seg[2][2];
@@ -155,6 +175,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
         bh[b] = frag(st + A_TILE, r, ks);
         bl[b] = frag(st + A_TILE + B_TILE, r, ks);
       }
+      lds_wait();
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -166,11 +187,19 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     if ((kt + 1) % steps_per_group == 0) {
       // end of group h: acc += s_h (per row) * seg
       const int h = kt / steps_per_group;
+      float4 s4[2][4];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4)   // rows 8 v4 + 4 (lane / 32) + 0..3 of block a
+          s4[a][v4] = lds_read16f(lds_addr(&sc_s[h][wm * 64 + a * 32 + 8 * v4 + 4 * kh]));
+      lds_wait();
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float sv = sc_s[wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4)][h];
+          const float4 q = s4[a][v / 4];
+          const float sv = (v % 4 == 0) ? q.x : (v % 4 == 1) ? q.y : (v % 4 == 2) ? q.z : q.w;
 #pragma unroll
           for (int b = 0; b < 2; ++b) {
             acc[a][b][v] = fmaf(seg[a][b][v], sv, acc[a][b][v]);

@@ -433,3 +433,64 @@ def test_act_order_flow_matches_oracle():
     _check_gptq(rWp, rHp, g, bits, q.cpu().numpy(), s.cpu().numpy(), z.cpu().numpy())
     rq, rs, rz = (x.cpu().numpy() for x in (q, s, z))
     assert np.array_equal(out.cpu().numpy(), opost.dequantize(rq, rs, rz, g, "f32", rperm))
+
+
+# --------------------------------------------------------------------------
+# The widest layer (4096 x 11008, G = 86): set-up entry points at full width
+# --------------------------------------------------------------------------
+
+def _wide_inputs(n_tokens=8192):
+    cfg = CONFIGS[3]
+    X = next(calibration_chunks(cfg, device="cuda", n_tokens=n_tokens, chunk=n_tokens))
+    return cfg, X.to(torch.float32).contiguous()
+
+
+def test_hessian_widest_layer_sampled():
+    cfg, X = _wide_inputs()
+    d, n = cfg.cols, X.shape[0]
+    say(f"[wide-hessian] d={d} n={n}")
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    jq.binding.hessian_accumulate(X[:5000], Hacc, 1.0 / n)
+    jq.binding.hessian_accumulate(X[5000:], Hacc, 1.0 / n)
+    H = jq.binding.hessian_finalize(Hacc, cfg.damping, 0.0)
+    torch.cuda.synchronize()
+    assert torch.equal(H, H.T)
+    idx = np.unique(np.concatenate([np.random.default_rng(3).choice(d, 40, replace=False),
+                                    [0, d - 1]]))
+    ti = torch.as_tensor(idx, device="cuda")
+    Xs = X[:, ti].double().cpu().numpy()
+    ref = ohess.accumulate(np.zeros((len(idx),) * 2), Xs, 1.0 / n)
+    ref[np.arange(len(idx)), np.arange(len(idx))] += cfg.damping * float(torch.diagonal(Hacc).mean())
+    ax = np.abs(Xs)
+    bound = ohess.fp32_error_bound(ax.T @ ax, 1.0 / n) + 2 * U32 * np.abs(ref)
+    Hs = H[ti][:, ti].double().cpu().numpy()
+    worst = np.max(np.abs(Hs - ref) / bound)
+    say(f"[wide-hessian] sampled worst error / bound {worst:.3e}")
+    assert worst <= 1.0
+
+
+def test_gptq_and_qep_widest_layer_sampled_rows():
+    from synth import make_hessian
+    cfg = CONFIGS[3]
+    say(f"[wide] building {cfg.name}")
+    W = make_weights(cfg)
+    H = make_hessian(cfg, device="cuda")
+    p = jq.binding.make_params(cfg.rows, cfg.cols, cfg.group_size, cfg.bits, 1)
+    Wd, Hd = to_dev(W), to_dev(H)
+    t0 = time.perf_counter()
+    q, s, z = jq.binding.gptq(p, Wd, Hd)
+    torch.cuda.synchronize()
+    say(f"[wide] GPTQ host {1e3 * (time.perf_counter() - t0):.1f} ms")
+    idx = np.sort(np.random.default_rng(8).choice(cfg.rows, 32, replace=False))
+    _check_gptq(W, H, cfg.group_size, cfg.bits, q.cpu().numpy(), s.cpu().numpy(),
+                z.cpu().numpy(), rows_idx=idx)
+    _, X = _wide_inputs(4096)
+    Xn = X.cpu().numpy()
+    Xq = propagated_inputs(Xn, 3)
+    D = oqep.cross([Xq], [Xn], cfg.cols, alpha=1.0 / Xn.shape[0])
+    t0 = time.perf_counter()
+    Wc = jq.binding.qep_correct(p, Wd, Hd, to_dev(D), 0.5)
+    torch.cuda.synchronize()
+    say(f"[wide] W_corr {1e3 * (time.perf_counter() - t0):.1f} ms")
+    _check_qep(Wc.cpu().numpy()[idx], oqep.corrected_weights(W[idx], H, D, 0.5),
+               W[idx].astype(np.float64))

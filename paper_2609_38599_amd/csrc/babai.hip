@@ -239,7 +239,9 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   const uint32_t ucols = (uint32_t)cols;
 
   // ---- preparation: u s = L^{-1} (H e) of the next group, this wave's columns ----
-  f32x4 uacc[BPW];
+  // u of the group being prepared, and of the one after it (loaded a
+  // position early: it does not depend on this panel's decisions)
+  f32x4 ua0[BPW], ua1[BPW];
   // R~ of group i into dst: 1 KB pieces, piece j by prep wave j % 4 (lane L
   // copies bytes 16 L .. 16 L + 15 of the piece).  Complete once the issuing
   // wave has passed its next barrier.
@@ -253,13 +255,13 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   };
   // u of group i as the residual product left it (U = E M^T, changes of
   // earlier panels already folded in), this wave's columns.
-  auto u_from_p = [&](int i) {
+  auto u_from_p = [&](int i, f32x4 (&ut)[BPW]) {
 #pragma unroll
     for (int b = 0; b < BPW; ++b) {
       const int n = (pw * BPW + b) * 16 + mr;
 #pragma unroll
       for (int v = 0; v < 4; ++v)
-        uacc[b][v] = ld_at(P_t, (lrow(4 * kq + v) * ucols + (uint32_t)(i * g + n)) * 4u);
+        ut[b][v] = ld_at(P_t, (lrow(4 * kq + v) * ucols + (uint32_t)(i * g + n)) * 4u);
     }
   };
   // Fragments of M(i-block, h-block) = L_i^{-1} H_ih for this wave's columns,
@@ -297,7 +299,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   // group h: then the product can be skipped (may_skip) or computed anyway,
   // which keeps the fragment loads ahead of their use (a use under a branch
   // drags the loads into it).
-  auto apply_t = [&](int h, const TFrag& f, bool may_skip) {
+  auto apply_t = [&](int h, const TFrag& f, bool may_skip, f32x4 (&uacc)[BPW]) {
     const bool any = tacc_s[h - i0] != 0;
     if (may_skip && !any) return;
     if (ptid == 0 && any) cnt_s[3] += 1;
@@ -319,7 +321,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       for (int v = 0; v < 4; ++v) uacc[b][v] = fmaf(-seg[v], f.sh[v] * f.cs[b], uacc[b][v]);
     }
   };
-  auto write_u = [&]() {
+  auto write_u = [&](const f32x4 (&uacc)[BPW]) {
 #pragma unroll
     for (int b = 0; b < BPW; ++b) {
       const int c = (pw * BPW + b) * 16 + mr;
@@ -434,16 +436,21 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     static_assert(PG % 2 == 0, "panels hold an even number of groups");
     stage_rcol(i0, rc0_s);
     if (prep_live) {
-      u_from_p(i0);
-      write_u();
+      u_from_p(i0, ua1);
+      write_u(ua1);
+      if (i0 + 1 < i1) u_from_p(i0 + 1, ua0);
     }
     __syncthreads();  // u and R~ of group i0 staged
     auto prep_at = [&](auto pc) {
       constexpr int p = decltype(pc)::value;
       const int i = i0 + p;
       TFrag fa, fb;
+      // u of group i + 1 is in ua[p % 2] (loaded one position earlier); the
+      // load of group i + 2's goes out now
+      f32x4 (&uc)[BPW] = (p % 2 == 0) ? ua0 : ua1;
+      f32x4 (&un)[BPW] = (p % 2 == 0) ? ua1 : ua0;
       if (prep_live) {
-        u_from_p(i + 1);
+        if (i + 2 < i1) u_from_p(i + 2, un);
         // block h = i0 + k sits in fa for even k, fb for odd k; the next
         // block loads while the current one is applied, and the last one,
         // M(i + 1, i), stays in flight across the barrier
@@ -452,10 +459,10 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
           constexpr int k = decltype(kc)::value;
           if constexpr (k % 2 == 0) {
             load_t(i + 1, i0 + k + 1, fb);
-            apply_t(i0 + k, fa, false);
+            apply_t(i0 + k, fa, false, uc);
           } else {
             load_t(i + 1, i0 + k + 1, fa);
-            apply_t(i0 + k, fb, false);
+            apply_t(i0 + k, fb, false, uc);
           }
         });
       }
@@ -469,10 +476,10 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       lds_barrier();  // group i decided: its changes are in dqp_s, tacc_s
       if (prep_live) {
         if constexpr (p % 2 == 0)
-          apply_t(i, fa, true);
+          apply_t(i, fa, true, uc);
         else
-          apply_t(i, fb, true);
-        write_u();
+          apply_t(i, fb, true, uc);
+        write_u(uc);
       }
       // The direct loads of R~ (i + 1) are complete once this wave's vector
       // memory counter is zero.

@@ -494,3 +494,62 @@ def test_gptq_and_qep_widest_layer_sampled_rows():
     say(f"[wide] W_corr {1e3 * (time.perf_counter() - t0):.1f} ms")
     _check_qep(Wc.cpu().numpy()[idx], oqep.corrected_weights(W[idx], H, D, 0.5),
                W[idx].astype(np.float64))
+
+
+def test_layer_flow_end_to_end():
+    """One layer through every step on the GPU: Hessian from its tokens, RTN
+    host, refinement (App. E.2 early stopping), canonical positive scales,
+    dequantized and packed output.  Canonicalization must leave the weights
+    unchanged bit for bit (eq. (canonicalization_equivalence)); the packed
+    codes must unpack to the canonical codes; the refined objective must not
+    exceed the host's (Cor. 1)."""
+    from oracle import jarq as ojarq
+    cfg = CONFIGS[0]
+    W = make_weights(cfg)
+    from synth import make_hessian
+    _, X, _ = make_hessian(cfg, return_x=True)
+    X32 = to_dev(X.astype(np.float32))
+    H = jq.binding.hessian([X32[:300], X32[300:]], cfg.cols, alpha=1.0 / X.shape[0],
+                           damp=cfg.damping)
+    Wd = to_dev(W)
+    p = jq.binding.make_params(cfg.rows, cfg.cols, cfg.group_size, cfg.bits, 20, tau=1e-5)
+    q, s, z = jq.binding.rtn(p, Wd)
+    q0, s0, z0 = q.clone(), s.clone(), z.clone()
+    ws = jq.binding.alloc_workspace(p)
+    st = jq.binding.refine(p, Wd, H, q, s, z, ws)
+    torch.cuda.synchronize()
+    Hn = H.cpu().numpy()
+    f_host = ojarq.objective_rows(W, Hn, q0.cpu().numpy(), s0.cpu().numpy(), z0.cpu().numpy(),
+                                  cfg.group_size).sum()
+    f_ref = ojarq.objective_rows(W, Hn, q.cpu().numpy(), s.cpu().numpy(), z.cpu().numpy(),
+                                 cfg.group_size).sum()
+    say(f"[flow] sweeps {st['sweeps_run']}, objective {f_host:.6e} -> {f_ref:.6e}")
+    assert f_ref <= f_host
+    # Every other group of the refined state rewritten in its negative-scale
+    # form (s -> -s, q -> qmax - q, z -> qmax - z, the same weights), plus the
+    # groups refinement itself left negative: canonicalization must restore
+    # positive scales without changing a weight.
+    qmax = (1 << cfg.bits) - 1
+    qn, sn, zn = q.cpu().numpy().copy(), s.cpu().numpy().copy(), z.cpu().numpy().copy()
+    flip = (np.arange(sn.size).reshape(sn.shape) % 2 == 0) & (sn > 0)
+    sn[flip] = -sn[flip]
+    zn[flip] = qmax - zn[flip]
+    fc = np.repeat(flip, cfg.group_size, axis=1)
+    qn[fc] = qmax - qn[fc]
+    qd, sd, zd = to_dev(qn), to_dev(sn), to_dev(zn)
+    before = jq.binding.dequantize(p, qd, sd, zd, torch.float32)
+    ref = jq.binding.dequantize(p, q, s, z, torch.float32)
+    jq.binding.canonicalize(p, qd, sd, zd)
+    after = jq.binding.dequantize(p, qd, sd, zd, torch.float32)
+    packed = jq.binding.pack_codes(p, qd)
+    torch.cuda.synchronize()
+    say(f"[flow] groups with negative scales: {int(flip.sum())} planted, "
+        f"{int((s < 0).sum())} from refinement")
+    assert torch.all(sd >= 0)
+    # equal values (a weight of 0 is -0.0 in the negative form: compared by value)
+    assert torch.equal(before, ref)
+    # and after canonicalization equal bit for bit
+    assert torch.equal(after.view(torch.int32), ref.view(torch.int32))
+    pos = (s >= 0)
+    assert torch.equal(sd[pos], s[pos]) and torch.equal(zd[pos], z[pos])
+    assert torch.equal(jq.binding.unpack_codes(p, packed), qd)

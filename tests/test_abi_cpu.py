@@ -132,3 +132,24 @@ def test_qep_entry_points_check_arguments(lib):
     assert cor(ctypes.byref(p), fake, fake, fake, 1.5, fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
     assert cor(ctypes.byref(p), fake, fake, fake, float("nan"), fake, fake, 1 << 30, None) == binding.JARQ_EINVAL
     assert cor(ctypes.byref(p), fake, fake, fake, 0.5, fake, fake, 16, None) == binding.JARQ_EWORKSPACE
+
+
+def test_binding_rejects_host_tensors_and_wrong_types():
+    import torch
+    p = binding.make_params(8, 64, 32, 3, 1)
+    W = torch.zeros(8, 64, dtype=torch.float32)          # host memory
+    with pytest.raises(ValueError):
+        binding.rtn(p, W, codes=torch.zeros(8, 64, dtype=torch.uint8),
+                    scales=torch.zeros(8, 2), zeros=torch.zeros(8, 2, dtype=torch.int32))
+    with pytest.raises(TypeError):
+        binding.rtn(p, W.double(), codes=torch.zeros(8, 64, dtype=torch.uint8),
+                    scales=torch.zeros(8, 2), zeros=torch.zeros(8, 2, dtype=torch.int32))
+    with pytest.raises(ValueError):
+        binding.hessian_accumulate(torch.zeros(5, 8), torch.zeros(4, 4, dtype=torch.float64))
+    with pytest.raises(ValueError):
+        binding.cross_accumulate(torch.zeros(5, 8), torch.zeros(6, 8),
+                                 torch.zeros(8, 8, dtype=torch.float64))
+    with pytest.raises(ValueError):
+        binding.hessian_finalize(torch.zeros(4, 5, dtype=torch.float64))
+    assert binding.packed_words_per_row(binding.make_params(2, 96, 32, 3, 1)) == 9
+    assert binding.DTYPES[torch.bfloat16] == 2

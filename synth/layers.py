@@ -161,7 +161,7 @@ def _token_chunks(cfg: LayerConfig, n_tokens: int, device: str, chunk: int):
 
 
 def _tiny_x(cfg: LayerConfig) -> np.ndarray:
-    """Config-0 activations X = Z L (Z standard normal, L unit lower-triangular)."""
+    """Activations of the tiny 64 x 256 layer: X = Z L (Z standard normal, L unit lower-triangular)."""
     _, x_ss, _, _ = _streams(cfg.cfg_id)
     rng = np.random.Generator(np.random.PCG64(x_ss))
     z = rng.standard_normal((cfg.n_tokens, cfg.cols))
@@ -211,7 +211,7 @@ def propagated_inputs(x: np.ndarray, seed: int, rel: float = 0.1, add: float = 0
 def make_hessian(cfg: LayerConfig, device: str | None = None,
                  n_tokens: int | None = None, chunk: int = 8192,
                  return_x: bool = False):
-    """H [cols, cols] float32 (and, for config 0, X as float64 if asked).
+    """H [cols, cols] float32 (and, for the tiny 64 x 256 layer, X as float64 if asked).
 
     H = X^T X / n with outlier channels of X scaled, plus damping
     0.01 * mean(diag(X^T X / n)) * I.  ``n_tokens`` overrides the token count

@@ -190,6 +190,15 @@ jarq_status jarq_hessian_accumulate(const float* X, int64_t m, int32_t d, double
                                     double* Hacc, void* stream);
 
 /*
+ * The same accumulation for X [m][d] in bf16 (the 16-bit brain float format,
+ * passed as raw 16-bit words; 16-byte aligned, d a multiple of 8, the other
+ * limits as above).  Products of bf16 values are exact in fp32; they are
+ * summed in fp32 over at most 256 tokens and those partial sums in fp64.
+ */
+jarq_status jarq_hessian_accumulate_bf16(const void* X, int64_t m, int32_t d, double alpha,
+                                         double* Hacc, void* stream);
+
+/*
  * H [d][d] fp32 (16-byte aligned) = Hacc + (damp * mean(diag Hacc) + nu2) I,
  * rounded once to fp32.  damp = 0, nu2 = nu^2 is App. E.1's regularised
  * Hessian; damp > 0 adds the relative diagonal damping used by GPTQ-style

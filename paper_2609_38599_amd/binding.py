@@ -84,6 +84,8 @@ _SIGNATURES = {
                                       ctypes.c_size_t, _vp, _vp]),
     "jarq_hessian_accumulate": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
                                                _vp, _vp]),
+    "jarq_hessian_accumulate_bf16": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.c_int32,
+                                                    ctypes.c_double, _vp, _vp]),
     "jarq_hessian_finalize": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
                                              _vp, _vp]),
     "jarq_rtn": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp]),
@@ -254,10 +256,16 @@ def objective(p: Params, W, H, codes, scales, zeros, ws, out=None, stream=None):
 
 
 def hessian_accumulate(X, Hacc, alpha=1.0, stream=None):
-    """Hacc += alpha X^T X for one chunk X [m, d] fp32 (Hacc [d, d] fp64)."""
+    """Hacc += alpha X^T X for one chunk X [m, d] fp32 or bf16 (Hacc [d, d] fp64)."""
     lib = load_library()
     if X.dim() != 2 or Hacc.shape != (X.shape[1], X.shape[1]):
         raise ValueError("X must be [m, d] and Hacc [d, d]")
+    if X.dtype == torch.bfloat16:
+        _check(lib.jarq_hessian_accumulate_bf16(_ptr(X, torch.bfloat16, "X"), X.shape[0],
+                                                X.shape[1], float(alpha),
+                                                _ptr(Hacc, torch.float64, "Hacc"), _stream(stream)),
+               "jarq_hessian_accumulate_bf16")
+        return
     _check(lib.jarq_hessian_accumulate(_ptr(X, torch.float32, "X"), X.shape[0], X.shape[1],
                                        float(alpha), _ptr(Hacc, torch.float64, "Hacc"),
                                        _stream(stream)), "jarq_hessian_accumulate")

@@ -437,6 +437,18 @@ jarq_status jarq_hessian_accumulate(const float* X, int64_t m, int32_t d, double
   return JARQ_OK;
 }
 
+jarq_status jarq_hessian_accumulate_bf16(const void* X, int64_t m, int32_t d, double alpha,
+                                         double* Hacc, void* stream) {
+  if (d < 1 || d > 32768 || d % 8 != 0 || m < 0 || m > INT32_MAX - 128 || !isfinite(alpha) ||
+      !aligned(Hacc, 8))
+    return JARQ_EINVAL;
+  if (m == 0) return JARQ_OK;  // X may be NULL
+  if (!aligned(X, 16)) return JARQ_EINVAL;
+  if (launch_hessian_update_bf16((hipStream_t)stream, X, (int)m, d, alpha, Hacc) != hipSuccess)
+    return JARQ_EHIP;
+  return JARQ_OK;
+}
+
 jarq_status jarq_hessian_finalize(const double* Hacc, int32_t d, double damp, double nu2,
                                   float* H, void* stream) {
   if (d < 1 || d > 32768 || d % 4 != 0 || !(damp >= 0.0) || !isfinite(damp) || !(nu2 >= 0.0) ||

@@ -191,6 +191,8 @@ hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
 // Per-layer set-up from calibration inputs and the round-to-nearest host.
 hipError_t launch_hessian_update(hipStream_t st, const float* X, int m, int d, double alpha,
                                  double* Hacc);
+hipError_t launch_hessian_update_bf16(hipStream_t st, const void* X, int m, int d, double alpha,
+                                      double* Hacc);
 hipError_t launch_hessian_finalize(hipStream_t st, const double* Hacc, int d, double damp,
                                    double nu2, float* H);
 hipError_t launch_rtn(hipStream_t st, const float* W, int rows, int cols, int g, int bits,

@@ -176,6 +176,142 @@ hipError_t launch_cross_update(hipStream_t st, const float* Xq, const float* X, 
   return hipGetLastError();
 }
 
+// The same Hessian from bf16 inputs (the dtype models hold their activations
+// in).  Products of bf16 values are exact in fp32, so
+// v_mfma_f32_32x32x16_bf16 forms them at 16 times the fp32 matrix rate;
+// fp32 sums of at most 256 tokens are added in fp64 as above.  Operands come
+// from a token-major LDS tile through the transposing LDS read
+// (ds_read_b64_tr_b16): in each 16-lane group, lane p points at token
+// base + p / 4, channels 4 (p % 4) .. +3, and lane i receives channel i of
+// tokens base .. base + 3 — the matrix-core operand layout (one row or
+// column per lane, consecutive k), with the same token order in A and B.
+namespace {
+constexpr int BK16 = 64;         // tokens per staged chunk
+constexpr int BLD = HT + 8;      // bf16 row stride of a staged tile (bank spread)
+constexpr int BFLUSH = 4;        // chunks per fp32 partial sum (256 tokens)
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ v4i16 lds_tr16(const __bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(const __attribute__((address_space(3))) void*)p);
+}
+}  // namespace
+
+__global__ __launch_bounds__(256) void hessian_syrk_bf16_kernel(const __bf16* __restrict__ X,
+                                                                int m, int d, double alpha,
+                                                                double* __restrict__ Hacc) {
+  __shared__ __attribute__((aligned(16))) __bf16 xa_s[2][BK16][BLD];
+  __shared__ __attribute__((aligned(16))) __bf16 xb_s[2][BK16][BLD];
+  const int nt = (d + HT - 1) / HT;
+  const long long idx = blockIdx.x;
+  const double bq = 2.0 * nt + 1.0;
+  int ta = (int)floor((bq - sqrt(bq * bq - 8.0 * (double)idx)) * 0.5);
+  ta = ta < 0 ? 0 : (ta > nt - 1 ? nt - 1 : ta);
+  while (ta > 0 && stripe_start(ta, nt) > idx) --ta;
+  while (ta + 1 < nt && stripe_start(ta + 1, nt) <= idx) ++ta;
+  const int tb = ta + (int)(idx - stripe_start(ta, nt));
+  const int a0 = ta * HT, b0 = tb * HT;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, kk = lane >> 5;
+  const bool idle = ta == tb && wm > wn;
+
+  // Staging: 16-byte piece e = tid + 256 p (p < 2) of a 64-token x 64-channel
+  // chunk of each operand: token e / 8, channels 8 (e % 8) .. +7.  Tokens past
+  // m and channels past d load an in-bounds piece and stage 0 (d is a
+  // multiple of 8).
+  uint4 ra[2], rb[2];
+  auto load_chunk = [&](int t0) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int e = tid + 256 * p;
+      const int t = e >> 3, c = (e & 7) * 8;
+      const bool tin = t0 + t < m;
+      const size_t roff = (size_t)(tin ? t0 + t : m - 1) * d;
+      const bool ina = tin && a0 + c < d, inb = tin && b0 + c < d;
+      const uint4 va = *(const uint4*)(X + roff + (ina ? a0 + c : 0));
+      const uint4 vb = *(const uint4*)(X + roff + (inb ? b0 + c : 0));
+      ra[p] = ina ? va : make_uint4(0u, 0u, 0u, 0u);
+      rb[p] = inb ? vb : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto store_chunk = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int e = tid + 256 * p;
+      const int t = e >> 3, c = (e & 7) * 8;
+      *(uint4*)&xa_s[buf][t][c] = ra[p];
+      *(uint4*)&xb_s[buf][t][c] = rb[p];
+    }
+  };
+
+  f32x16 acc = f32x16{};
+  double acc64[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc64[v] = 0.0;
+  auto flush = [&]() {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc64[v] += (double)acc[v];
+    acc = f32x16{};
+  };
+  // transposing-read provider of this lane: token (lane % 16) / 4, channels
+  // 4 (lane % 4) within its 16-channel half; group g = lane / 16 takes the
+  // half g % 2 of the 32-wide block and the 8 tokens 8 (g / 2) .. +7
+  const int gi = lane >> 4, pi = lane & 15;
+  const int ptok = 8 * (gi >> 1) + (pi >> 2);
+  const int pch = 16 * (gi & 1) + 4 * (pi & 3);
+
+  const int nchunks = (m + BK16 - 1) / BK16;
+  load_chunk(0);
+  store_chunk(0);
+  __syncthreads();
+  for (int q = 0; q < nchunks; ++q) {
+    const int buf = q & 1;
+    if (q + 1 < nchunks) load_chunk((q + 1) * BK16);  // in flight during this chunk
+    if (!idle) {
+#pragma unroll
+      for (int ks = 0; ks < BK16; ks += 16) {
+        const __bf16* pa = &xa_s[buf][ks + ptok][wm * 32 + pch];
+        const __bf16* pb = &xb_s[buf][ks + ptok][wn * 32 + pch];
+        const v4i16 a_lo = lds_tr16(pa), a_hi = lds_tr16(pa + 4 * BLD);
+        const v4i16 b_lo = lds_tr16(pb), b_hi = lds_tr16(pb + 4 * BLD);
+        const v4i16 a8[2] = {a_lo, a_hi}, b8[2] = {b_lo, b_hi};
+        const bf16x8 af = __builtin_bit_cast(bf16x8, a8);
+        const bf16x8 bf = __builtin_bit_cast(bf16x8, b8);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf, acc, 0, 0, 0);
+      }
+      if ((q + 1) % BFLUSH == 0) flush();
+    }
+    if (q + 1 < nchunks) store_chunk(buf ^ 1);
+    __syncthreads();
+  }
+  if (idle) return;
+  flush();
+  {
+#pragma clang fp contract(off)
+    const int b = b0 + wn * 32 + l32;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int a = a0 + wm * 32 + 8 * (v / 4) + 4 * kk + (v % 4);
+      if (a <= b && b < d) {
+        const double t = alpha * acc64[v];
+        Hacc[(size_t)a * d + b] += t;
+        if (a != b) Hacc[(size_t)b * d + a] += t;
+      }
+    }
+  }
+}
+
+hipError_t launch_hessian_update_bf16(hipStream_t st, const void* X, int m, int d, double alpha,
+                                      double* Hacc) {
+  const long long nt = (d + HT - 1) / HT;
+  hipLaunchKernelGGL(hessian_syrk_bf16_kernel, dim3((unsigned)(nt * (nt + 1) / 2)), dim3(256), 0,
+                     st, (const __bf16*)X, m, d, alpha, Hacc);
+  return hipGetLastError();
+}
+
 // Off-diagonal entries: H = (float) Hacc.
 __global__ __launch_bounds__(256) void hessian_finalize_offdiag_kernel(const double* __restrict__ Hacc,
                                                                        int d,

@@ -153,3 +153,11 @@ def test_binding_rejects_host_tensors_and_wrong_types():
         binding.hessian_finalize(torch.zeros(4, 5, dtype=torch.float64))
     assert binding.packed_words_per_row(binding.make_params(2, 96, 32, 3, 1)) == 9
     assert binding.DTYPES[torch.bfloat16] == 2
+
+
+def test_bf16_hessian_checks_arguments(lib):
+    fake = _vp(1 << 20)
+    acc = lib.jarq_hessian_accumulate_bf16
+    assert acc(fake, 10, 132, 1.0, fake, None) == binding.JARQ_EINVAL     # d % 8
+    assert acc(_vp((1 << 20) + 8), 10, 128, 1.0, fake, None) == binding.JARQ_EINVAL
+    assert acc(None, 0, 128, 1.0, fake, None) == binding.JARQ_OK

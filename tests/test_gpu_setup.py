@@ -553,3 +553,72 @@ def test_layer_flow_end_to_end():
     pos = (s >= 0)
     assert torch.equal(sd[pos], s[pos]) and torch.equal(zd[pos], z[pos])
     assert torch.equal(jq.binding.unpack_codes(p, packed), qd)
+
+
+# --------------------------------------------------------------------------
+# Hessian from bf16 inputs
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("m,d,splits", [(1000, 264, (333,)), (64, 128, ()), (1, 8, ()),
+                                        (700, 520, (63, 64, 300))])
+def test_hessian_bf16_integer_inputs_are_exact(m, d, splits):
+    rng = np.random.default_rng(m + d + 1)
+    X = rng.integers(-3, 4, size=(m, d)).astype(np.float32)
+    say(f"[hessian-bf16-int] m={m} d={d} splits={splits}")
+    Xb = to_dev(X).to(torch.bfloat16)
+    cuts = [0, *splits, m]
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        jq.binding.hessian_accumulate(Xb[a:b].contiguous(), Hacc, 0.5)
+    torch.cuda.synchronize()
+    assert np.array_equal(Hacc.cpu().numpy(), ohess.hessian([X], d, alpha=0.5))
+
+
+@pytest.mark.parametrize("m,d", [(900, 264), (2048, 384), (33, 128)])
+def test_hessian_bf16_matches_oracle_within_fp32_bound(m, d):
+    rng = np.random.default_rng(d + 7)
+    X = rng.standard_normal((m, d))
+    for c in range(1, d):
+        X[:, c] = 0.6 * X[:, c - 1] + 0.8 * X[:, c]
+    X[:, 5] *= 20.0
+    Xb = to_dev(X.astype(np.float32)).to(torch.bfloat16)
+    Xv = Xb.float().cpu().numpy().astype(np.float64)     # the bf16 values the GPU sees
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    jq.binding.hessian_accumulate(Xb, Hacc, 1.0 / m)
+    torch.cuda.synchronize()
+    H = Hacc.cpu().numpy()
+    ref = ohess.hessian([Xv], d, alpha=1.0 / m)
+    ax = np.abs(Xv)
+    bound = ohess.fp32_error_bound(ax.T @ ax, 1.0 / m) + 1e-300
+    worst = np.max(np.abs(H - ref) / bound)
+    say(f"[hessian-bf16] m={m} d={d} worst error / bound {worst:.3e}")
+    assert worst <= 1.0
+    assert np.array_equal(H, H.T)
+
+
+def test_hessian_bf16_full_size_sampled():
+    cfg = CONFIGS[1]
+    d, n = cfg.cols, cfg.n_tokens
+    rng = np.random.default_rng(12)
+    idx = np.unique(np.concatenate([rng.choice(d, 40, replace=False), [0, d - 1]]))
+    ti = torch.as_tensor(idx, device="cuda")
+    cols = []
+    Hacc = torch.zeros(d, d, dtype=torch.float64, device="cuda")
+    t_acc = 0.0
+    for xc in calibration_chunks(cfg, device="cuda", chunk=8192):
+        X = xc.to(torch.bfloat16).contiguous()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        jq.binding.hessian_accumulate(X, Hacc, 1.0 / n)
+        torch.cuda.synchronize()
+        t_acc += time.perf_counter() - t0
+        cols.append(X[:, ti].double().cpu().numpy())
+    say(f"[hessian-bf16-full] accumulate {1e3 * t_acc:.1f} ms over {n} tokens")
+    Xs = np.concatenate(cols)
+    Hs = Hacc[ti][:, ti].cpu().numpy()
+    ref = ohess.accumulate(np.zeros((len(idx),) * 2), Xs, 1.0 / n)
+    ax = np.abs(Xs)
+    worst = np.max(np.abs(Hs - ref) / (ohess.fp32_error_bound(ax.T @ ax, 1.0 / n) + 1e-300))
+    say(f"[hessian-bf16-full] sampled worst error / bound {worst:.3e}")
+    assert worst <= 1.0
+    assert torch.equal(Hacc, Hacc.T)

@@ -15,8 +15,8 @@ from the host state with events around every stage.
 
 After the sweeps, a set-up leg (not part of a sweep; --no-setup skips it)
 times the per-layer set-up on the GPU: the Hessian from the layer's 262,144
-calibration tokens (fp32 chunks resident in HBM), its finalisation with the
-layer's damping, and the RTN host.
+calibration tokens (fp32 chunks resident in HBM, then the same tokens in
+bf16), its finalisation with the layer's damping, and the RTN host.
 
 Prints one JSON line.  --gpus above 1 is refused: the path runs on one GPU.
 --copy-probe runs only a plain device copy of known size (used to calibrate
@@ -164,7 +164,21 @@ def setup_leg(cfg, jq, H_ref, W_dev):
     flops = float(n) * d * (d + 1)                 # the d (d + 1) / 2 distinct entries, 2 n each
     dg = torch.sqrt(torch.diagonal(H_ref).double())
     dev_rel = float(((H.double() - H_ref.double()).abs() / torch.outer(dg, dg)).max())
-    del chunks, Hacc, H
+    # the same tokens held in bf16 (the dtype a model would capture them in)
+    chunks = [x.to(torch.bfloat16) for x in chunks]
+    Hacc.zero_()
+    jq.binding.hessian_accumulate(chunks[0], Hacc, 1.0 / n)      # warm-up
+    Hacc.zero_()
+    torch.cuda.synchronize()
+    ev[0].record()
+    for X in chunks:
+        jq.binding.hessian_accumulate(X, Hacc, 1.0 / n)
+    ev[1].record()
+    torch.cuda.synchronize()
+    t_b = ev[0].elapsed_time(ev[1])
+    Hb = jq.binding.hessian_finalize(Hacc, cfg.damping, 0.0)
+    dev_rel_b = float(((Hb.double() - H_ref.double()).abs() / torch.outer(dg, dg)).max())
+    del chunks, Hacc, H, Hb
     torch.cuda.empty_cache()
     tflops = flops / (t_h * 1e-3) / 1e12
     return {"tokens": n, "chunk_tokens": 8192, "launches": (n + 8191) // 8192,
@@ -172,7 +186,10 @@ def setup_leg(cfg, jq, H_ref, W_dev):
             "hessian_frac_of_fp32_mfma_peak": tflops / PEAK_FP32_MFMA_TFLOPS,
             "finalize_ms": t_f, "rtn_ms": t_r,
             "rtn_hbm_gbs": (W_dev.numel() * 5 + 8 * W_dev.numel() // cfg.group_size) / (t_r * 1e-3) / 1e9,
-            "max_rel_dev_from_fp64_build": dev_rel}
+            "max_rel_dev_from_fp64_build": dev_rel,
+            "hessian_bf16_ms": t_b, "hessian_bf16_tflops": flops / (t_b * 1e-3) / 1e12,
+            "hessian_bf16_frac_of_bf16_mfma_peak": flops / (t_b * 1e-3) / 1e12 / PEAK_FP16_MFMA_TFLOPS,
+            "bf16_inputs_max_rel_dev_from_fp64_build": dev_rel_b}
 
 
 def main():

@@ -222,8 +222,11 @@ __global__ __launch_bounds__(256) void hessian_syrk_bf16_kernel(const __bf16* __
   // chunk of each operand: token e / 8, channels 8 (e % 8) .. +7.  Tokens past
   // m and channels past d load an in-bounds piece and stage 0 (d is a
   // multiple of 8).
-  uint4 ra[2], rb[2];
-  auto load_chunk = [&](int t0) {
+  // three register sets: chunks q + 1 and q + 2 are in flight while chunk q
+  // computes (a chunk holds little matrix work, so one ahead would leave the
+  // loads' latency exposed)
+  uint4 rs[3][2][2];
+  auto load_chunk = [&](int t0, uint4 (&ra)[2], uint4 (&rb)[2]) {
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const int e = tid + 256 * p;
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(256) void hessian_syrk_bf16_kernel(const __bf16* __
       rb[p] = inb ? vb : make_uint4(0u, 0u, 0u, 0u);
     }
   };
-  auto store_chunk = [&](int buf) {
+  auto store_chunk = [&](int buf, const uint4 (&ra)[2], const uint4 (&rb)[2]) {
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const int e = tid + 256 * p;
@@ -264,12 +267,7 @@ __global__ __launch_bounds__(256) void hessian_syrk_bf16_kernel(const __bf16* __
   const int pch = 16 * (gi & 1) + 4 * (pi & 3);
 
   const int nchunks = (m + BK16 - 1) / BK16;
-  load_chunk(0);
-  store_chunk(0);
-  __syncthreads();
-  for (int q = 0; q < nchunks; ++q) {
-    const int buf = q & 1;
-    if (q + 1 < nchunks) load_chunk((q + 1) * BK16);  // in flight during this chunk
+  auto compute = [&](int buf, int q) {
     if (!idle) {
 #pragma unroll
       for (int ks = 0; ks < BK16; ks += 16) {
@@ -284,8 +282,34 @@ __global__ __launch_bounds__(256) void hessian_syrk_bf16_kernel(const __bf16* __
       }
       if ((q + 1) % BFLUSH == 0) flush();
     }
-    if (q + 1 < nchunks) store_chunk(buf ^ 1);
+  };
+  // Chunk q sits in LDS buffer q % 2 and chunks q + 1, q + 2 in register sets
+  // (q + 1) % 3 and (q + 2) % 3; the loop is unrolled three times so that every
+  // set is chosen at compile time.
+  load_chunk(0, rs[0][0], rs[0][1]);
+  store_chunk(0, rs[0][0], rs[0][1]);
+  if (nchunks > 1) load_chunk(BK16, rs[1][0], rs[1][1]);
+  if (nchunks > 2) load_chunk(2 * BK16, rs[2][0], rs[2][1]);
+  __syncthreads();
+  auto step = [&](int q, int buf, uint4 (&nxt)[2][2], uint4 (&fut)[2][2]) {
+    // nxt holds chunk q + 1, fut receives chunk q + 3
+    compute(buf, q);
+    if (q + 1 < nchunks) store_chunk(buf ^ 1, nxt[0], nxt[1]);
+    if (q + 3 < nchunks) load_chunk((q + 3) * BK16, fut[0], fut[1]);
     __syncthreads();
+  };
+  for (int q = 0; q < nchunks; q += 6) {
+    step(q, 0, rs[1], rs[0]);
+    if (q + 1 >= nchunks) break;
+    step(q + 1, 1, rs[2], rs[1]);
+    if (q + 2 >= nchunks) break;
+    step(q + 2, 0, rs[0], rs[2]);
+    if (q + 3 >= nchunks) break;
+    step(q + 3, 1, rs[1], rs[0]);
+    if (q + 4 >= nchunks) break;
+    step(q + 4, 0, rs[2], rs[1]);
+    if (q + 5 >= nchunks) break;
+    step(q + 5, 1, rs[0], rs[2]);
   }
   if (idle) return;
   flush();

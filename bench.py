@@ -118,7 +118,8 @@ def cpu_baseline(cfg, W, H, q, s, z, rows, sweeps):
     dt = time.perf_counter() - t0
     ms = dt * 1e3 / sweeps * (W.shape[0] / rows)
     return {"value": ms, "unit": "ms/sweep", "cores": int(threads), "kind": "oracle",
-            "sample": f"{sweeps} sweeps (scale update, objective, code update) from the RTN host "
+            "sample": f"{sweeps} sweeps (scale update, objective, code update) from the "
+                      f"{cfg.host.upper()} host "
                       f"over rows 0..{rows - 1} of {W.shape[0]}, float64 NumPy, {dt:.1f} s wall"
                       + ("" if rows == W.shape[0] else ", scaled by rows (rows are independent)")}
 
@@ -236,7 +237,14 @@ def main():
         log(f"[bench] building inputs for {cfg.name}")
         W = make_weights(cfg)
         H = make_hessian(cfg, device="cuda")
-        q, s, z = rtn_quantize(W, g, bits)
+        if cfg.host == "gptq":
+            # the layer's GPTQ-style host state, built by the library on the GPU
+            ph = jq.make_params(W.shape[0], W.shape[1], g, bits, 1)
+            qg, sg, zg = jq.binding.gptq(ph, torch.from_numpy(W).cuda(), torch.from_numpy(H).cuda())
+            q, s, z = qg.cpu().numpy(), sg.cpu().numpy(), zg.cpu().numpy()
+            del qg, sg, zg
+        else:
+            q, s, z = rtn_quantize(W, g, bits)
         if args.inputs:
             np.savez(args.inputs, W=W, H=H, q=q, s=s, z=z)
     dev = torch.device("cuda:0")

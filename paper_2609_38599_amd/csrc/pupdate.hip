@@ -44,7 +44,9 @@ __device__ __forceinline__ void dma16(const _Float16* src, _Float16* lds) {
 // them as reads that an outstanding direct-to-LDS load might feed, so it adds
 // no wait for those loads; the kernel's own waits (every stage is complete
 // before the barrier that precedes its reads) keep them correct.  The caller
-// waits for the results with lds_wait().
+// waits for the results with JARQ_LDS_WAIT(...), whose operands are the values the
+// wait guards: the compiler cannot see that a read's result arrives later, so
+// every use must depend on the wait itself, not only on the read.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)p;
 }
@@ -53,12 +55,13 @@ __device__ __forceinline__ f16x8 lds_read16(uint32_t a) {
   asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a));
   return r;
 }
-__device__ __forceinline__ float4 lds_read16f(uint32_t a) {
-  float4 r;
+__device__ __forceinline__ f32x4 lds_read16f(uint32_t a) {
+  f32x4 r;
   asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a));
   return r;
 }
-__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Operands: "+v"(value) for each value the wait guards.
+#define JARQ_LDS_WAIT(...) asm volatile("s_waitcnt lgkmcnt(0)" : __VA_ARGS__ : : "memory")
 
 template <int N>
 __device__ __forceinline__ void wait_vm_and_barrier() {
@@ -175,7 +178,8 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
         bh[b] = frag(st + A_TILE, r, ks);
         bl[b] = frag(st + A_TILE + B_TILE, r, ks);
       }
-      lds_wait();
+      JARQ_LDS_WAIT("+v"(af[0]), "+v"(af[1]), "+v"(bh[0]), "+v"(bh[1]), "+v"(bl[0]),
+                    "+v"(bl[1]));
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -187,18 +191,19 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     if ((kt + 1) % steps_per_group == 0) {
       // end of group h: acc += s_h (per row) * seg
       const int h = kt / steps_per_group;
-      float4 s4[2][4];
+      f32x4 s4[2][4];
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4)   // rows 8 v4 + 4 (lane / 32) + 0..3 of block a
           s4[a][v4] = lds_read16f(lds_addr(&sc_s[h][wm * 64 + a * 32 + 8 * v4 + 4 * kh]));
-      lds_wait();
+      JARQ_LDS_WAIT("+v"(s4[0][0]), "+v"(s4[0][1]), "+v"(s4[0][2]), "+v"(s4[0][3]),
+                    "+v"(s4[1][0]), "+v"(s4[1][1]), "+v"(s4[1][2]), "+v"(s4[1][3]));
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float4 q = s4[a][v / 4];
+          const f32x4 q = s4[a][v / 4];
           const float sv = (v % 4 == 0) ? q.x : (v % 4 == 1) ? q.y : (v % 4 == 2) ? q.z : q.w;
 #pragma unroll
           for (int b = 0; b < 2; ++b) {

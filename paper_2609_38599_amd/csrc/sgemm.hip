@@ -16,12 +16,14 @@
 // e_i^T (H e)_i in fp64; summed over the groups that is L_j, the objective
 // right after the scale update (App. E.2).
 //
-// Tiling: 256 x BN output tile per 256-thread work-group, 2 x 2 waves of
-// 128 x BN/2, K in steps of 32.  Both planes of both operands go straight from
-// global memory to LDS (global_load_lds_dwordx4, no register staging) into
-// one of two stages (128 KB for BN = 256).  One work-group per CU; a 256 x 256
-// tile gives every k-step 96 matrix instructions per wave, enough to cover
-// the latency of the next step's loads.  Tiles are ordered so that
+// Tiling: 256 x BN output tile per 512-thread work-group, 2 x 4 waves of
+// 128 x BN/4 (two waves per SIMD, so one wave's waits are covered by the
+// other's matrix work), K in steps of 32.  Both planes of both operands go
+// straight from global memory to LDS (global_load_lds_dwordx4, no register
+// staging) into one of two stages (128 KB for BN = 256); the eight loads of
+// the next stage are spread over the first four fragment blocks of the
+// current one.  Fragment reads are software-pipelined one block ahead (see
+// compute).  One work-group per CU.  Tiles are ordered so that
 // each XCD (work-groups are dealt to the 8 XCDs round-robin) works on a
 // compact block of tiles that share A row-tiles and B column-tiles in its L2.
 #include "jarq_internal.h"
@@ -63,12 +65,12 @@ __device__ __forceinline__ void dma16(const _Float16* src, _Float16* lds) {
 }  // namespace
 
 template <int BN, int kMode>
-__global__ __launch_bounds__(256, 1) void split3_kernel(
+__global__ __launch_bounds__(512, 1) void split3_kernel(
     int M, int N, int K, int lda, int ldb, int ldc, const _Float16* __restrict__ Ah,
     const _Float16* __restrict__ Al, const float* __restrict__ arow_inv,
     const _Float16* __restrict__ Bh, const _Float16* __restrict__ Bl,
     const float* __restrict__ bcol_inv, float* __restrict__ C) {
-  constexpr int WN = BN / 2;   // wave tile columns
+  constexpr int WN = BN / 4;   // wave tile columns
   constexpr int NB = WN / 32;  // 32-column blocks per wave
   constexpr int A_PLANE = BM * BK, B_PLANE = BN * BK;  // halves
   constexpr int STAGE = 2 * A_PLANE + 2 * B_PLANE;
@@ -79,7 +81,7 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int lm = lane & 31, kh = lane >> 5;
   const int nbm = (M + BM - 1) / BM, nbn = (N + BN - 1) / BN;
   int tm, tn;
@@ -92,31 +94,44 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
   // chunk (L % 4) ^ swz(row).  Rows past the edge read row 0 instead: their
   // products only reach output rows and columns that are never stored.
   // Element offsets are 32-bit (operands stay below 2^31 elements).
-  constexpr int APW = A_PLANE / 512 / 4;  // 1 KB pieces per wave per A plane
-  constexpr int BPW = B_PLANE / 512 / 4;
+  constexpr int APW = A_PLANE / 512 / 8;  // 1 KB pieces per wave per A plane
+  constexpr int BPW = B_PLANE / 512 / 8;
   unsigned aoff[APW], boff[BPW];
 #pragma unroll
   for (int i = 0; i < APW; ++i) {
-    const int r = 16 * (wave + 4 * i) + (lane >> 2);
+    const int r = 16 * (wave + 8 * i) + (lane >> 2);
     const int gm = m0 + r;
     aoff[i] = (unsigned)(gm < M ? gm : 0) * (unsigned)lda + (unsigned)(((lane & 3) ^ swz(r)) * 8);
   }
 #pragma unroll
   for (int i = 0; i < BPW; ++i) {
-    const int r = 16 * (wave + 4 * i) + (lane >> 2);
+    const int r = 16 * (wave + 8 * i) + (lane >> 2);
     const int gn = n0 + r;
     boff[i] = (unsigned)(gn < N ? gn : 0) * (unsigned)ldb + (unsigned)(((lane & 3) ^ swz(r)) * 8);
   }
+  // Load j of the eight direct loads of a stage: j = 0..3 the A planes
+  // (hi, lo of piece 0, then of piece 1), j = 4..7 the B planes.
+  auto issue_one = [&](int j, int k0, _Float16* stage) {
+    static_assert(APW == 2 && BPW == 2, "eight loads per stage");
+    const int i = (j >> 1) & 1;
+    if (j < 4) {
+      _Float16* dst = stage + (wave + 8 * i) * 512;
+      if (j & 1) dma16(Al + k0 + aoff[i], dst + A_PLANE); else dma16(Ah + k0 + aoff[i], dst);
+    } else {
+      _Float16* dst = stage + 2 * A_PLANE + (wave + 8 * i) * 512;
+      if (j & 1) dma16(Bl + k0 + boff[i], dst + B_PLANE); else dma16(Bh + k0 + boff[i], dst);
+    }
+  };
   auto issue = [&](int k0, _Float16* stage) {
 #pragma unroll
     for (int i = 0; i < APW; ++i) {
-      _Float16* dst = stage + (wave + 4 * i) * 512;
+      _Float16* dst = stage + (wave + 8 * i) * 512;
       dma16(Ah + k0 + aoff[i], dst);
       dma16(Al + k0 + aoff[i], dst + A_PLANE);
     }
 #pragma unroll
     for (int i = 0; i < BPW; ++i) {
-      _Float16* dst = stage + 2 * A_PLANE + (wave + 4 * i) * 512;
+      _Float16* dst = stage + 2 * A_PLANE + (wave + 8 * i) * 512;
       dma16(Bh + k0 + boff[i], dst);
       dma16(Bl + k0 + boff[i], dst + B_PLANE);
     }
@@ -128,35 +143,67 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[a][b] = f32x16{};
 
-  auto frag = [&](const _Float16* plane, int r, int ks) {
+  // Fragment reads are inline asm, paired with explicit waits whose operands
+  // are the fragments they guard (the compiler neither sees when the data
+  // arrives nor can move a use above its wait).  The reads also carry no
+  // dependence on the direct loads, so no drain of those is inserted: every
+  // stage is complete before the barrier that precedes its reads.
+  auto lds_rd = [&](const _Float16* plane, int r, int ks) {
     const int c = (ks >> 3) + kh;
-    return *(const f16x8*)(plane + r * BK + ((c ^ swz(r)) << 3));
+    const uint32_t ad = (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)(
+        plane + r * BK + ((c ^ swz(r)) << 3));
+    f16x8 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(ad));
+    return v;
   };
-  auto compute = [&](const _Float16* base) {
-#pragma unroll
-    for (int ks = 0; ks < BK; ks += 16) {
-      f16x8 bh[NB], bl[NB];
+  // One k-step on stage `base` as eight blocks s (k-slice s / 4, A row block
+  // s % 4).  Block s first issues the reads for block s + 1 (block 1 also those
+  // of the second k-slice's B fragments) and two of the next stage's direct
+  // loads (into `stn` at k0n; none if k0n < 0), then waits only for the reads
+  // issued before this block (LDS returns in order) and runs its 6 products,
+  // so the reads of block s + 1 overlap them.
+  auto compute = [&](const _Float16* base, int k0n, _Float16* stn) {
+    f16x8 bh[2][NB], bl[2][NB], ah[2], al[2];
+    auto loadB = [&](int ks, f16x8 (&h)[NB], f16x8 (&l)[NB]) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const int r = wn * WN + b * 32 + lm;
-        bh[b] = frag(base + 2 * A_PLANE, r, ks);
-        bl[b] = frag(base + 2 * A_PLANE + B_PLANE, r, ks);
+        h[b] = lds_rd(base + 2 * A_PLANE, r, ks);
+        l[b] = lds_rd(base + 2 * A_PLANE + B_PLANE, r, ks);
       }
+    };
+    auto loadA = [&](int ks, int a, f16x8& h, f16x8& l) {
+      const int r = wm * 128 + a * 32 + lm;
+      h = lds_rd(base, r, ks);
+      l = lds_rd(base + A_PLANE, r, ks);
+    };
+    loadB(0, bh[0], bl[0]);
+    loadA(0, 0, ah[0], al[0]);
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int r = wm * 128 + a * 32 + lm;
-        const f16x8 ah = frag(base, r, ks);
-        const f16x8 al = frag(base + A_PLANE, r, ks);
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bh[b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bl[b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, bh[b], acc[a][b], 0, 0, 0);
-        }
+    for (int s = 0; s < 8; ++s) {
+      const int ksl = s >> 2, a = s & 3, c = s & 1;
+      if (s + 1 < 8) loadA(((s + 1) >> 2) * 16, (s + 1) & 3, ah[c ^ 1], al[c ^ 1]);
+      if (s == 1) loadB(16, bh[1], bl[1]);
+      if (k0n >= 0 && s < 4) {
+        issue_one(2 * s, k0n, stn);
+        issue_one(2 * s + 1, k0n, stn);
       }
-      // Keep the fragment loads of the next k-slice from being hoisted here
-      // (register pressure).
-      __builtin_amdgcn_sched_barrier(0);
+      static_assert(NB == 2, "wait operands list two B fragments");
+#define JARQ_WAIT_OPS \
+  "+v"(ah[c]), "+v"(al[c]), "+v"(bh[ksl][0]), "+v"(bh[ksl][1]), "+v"(bl[ksl][0]), "+v"(bl[ksl][1])
+      if (s == 7)
+        asm volatile("s_waitcnt lgkmcnt(0)" : JARQ_WAIT_OPS);
+      else if (s == 1)
+        asm volatile("s_waitcnt lgkmcnt(6)" : JARQ_WAIT_OPS);
+      else
+        asm volatile("s_waitcnt lgkmcnt(2)" : JARQ_WAIT_OPS);
+#undef JARQ_WAIT_OPS
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[c], bh[ksl][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[c], bl[ksl][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[c], bh[ksl][b], acc[a][b], 0, 0, 0);
+      }
     }
   };
 
@@ -168,14 +215,12 @@ __global__ __launch_bounds__(256, 1) void split3_kernel(
   __syncthreads();
   int kt = 0;
   for (; kt + 2 <= nk; kt += 2) {
-    issue((kt + 1) * BK, buf1);
-    compute(buf0);
+    compute(buf0, (kt + 1) * BK, buf1);
     __syncthreads();
-    if (kt + 2 < nk) issue((kt + 2) * BK, buf0);
-    compute(buf1);
+    compute(buf1, kt + 2 < nk ? (kt + 2) * BK : -1, buf0);
     __syncthreads();
   }
-  if (kt < nk) compute(buf0);  // odd step count: the last step sits in buf0
+  if (kt < nk) compute(buf0, -1, buf1);  // odd step count: the last step sits in buf0
 
   // Epilogue.  Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
@@ -303,7 +348,7 @@ static hipError_t launch_split3_t(hipStream_t st, int M, int N, int K, int lda, 
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % BK != 0) return hipErrorInvalidValue;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL((split3_kernel<BN, kMode>), dim3(tiles), dim3(256), 0, st, M, N, K, lda, ldb,
+  hipLaunchKernelGGL((split3_kernel<BN, kMode>), dim3(tiles), dim3(512), 0, st, M, N, K, lda, ldb,
                      ldc, ah, al, arow, bh, bl, bcol, C);
   return hipGetLastError();
 }

@@ -143,6 +143,10 @@ hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char*
 
 // One work-group per row: E = W - s (q - z) in fp32 (as in eq. (1)), its
 // row maximum, then the two fp16 planes and the row's inverse scale 2^-t.
+// With NCH > 0 each thread keeps its NCH chunks of four weights and codes in
+// registers between the two passes (rows of at most 1024 NCH columns), so W
+// and the codes are read from memory once; NCH = 0 reads them twice.
+template <int NCH>
 __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
                                                       const float* __restrict__ W,
                                                       const uint8_t* __restrict__ codes,
@@ -160,17 +164,42 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
   __shared__ float red[4];
   const float* wr = W + (size_t)row * cols;
   const uint8_t* qr = codes + (size_t)row * cols;
+  const float* sr = scales + (size_t)row * G;
+  const int32_t* zr = zeros + (size_t)row * G;
+  auto err = [&](const f32x4& w, uint32_t q4, float s, int z, int i) {
+    return w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z);
+  };
+  constexpr int NR = NCH > 0 ? NCH : 1;
+  f32x4 wv[NR];
+  uint32_t qv[NR];
   float m = 0.f;
-  for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
-    const f32x4 w = *(const f32x4*)(wr + c);
-    const uint32_t q4 = *(const uint32_t*)(qr + c);
-    const int grp = c / g;
-    const float s = scales[(size_t)row * G + grp];
-    const int z = zeros[(size_t)row * G + grp];
+  if (NCH > 0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float e = w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z);
-      m = fmaxf(m, fabsf(e));
+    for (int k = 0; k < NR; ++k) {
+      const int c = (threadIdx.x + 256 * k) * 4;
+      if (c < cols) {
+        wv[k] = *(const f32x4*)(wr + c);
+        qv[k] = *(const uint32_t*)(qr + c);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NR; ++k) {
+      const int c = (threadIdx.x + 256 * k) * 4;
+      if (c < cols) {
+        const float s = sr[c / g];
+        const int z = zr[c / g];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(err(wv[k], qv[k], s, z, i)));
+      }
+    }
+  } else {
+    for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
+      const f32x4 w = *(const f32x4*)(wr + c);
+      const uint32_t q4 = *(const uint32_t*)(qr + c);
+      const float s = sr[c / g];
+      const int z = zr[c / g];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(err(w, q4, s, z, i)));
     }
   }
 #pragma unroll
@@ -182,33 +211,55 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
   if (threadIdx.x == 0) erow_inv[pos] = ldexpf(1.f, -t);
   _Float16* hr = ehi + (size_t)pos * cols;
   _Float16* lr = elo + (size_t)pos * cols;
-  for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
-    const f32x4 w = *(const f32x4*)(wr + c);
-    const uint32_t q4 = *(const uint32_t*)(qr + c);
-    const int grp = c / g;
-    const float s = scales[(size_t)row * G + grp];
-    const int z = zeros[(size_t)row * G + grp];
-    typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+  typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+  auto emit = [&](int c, const f32x4& w, uint32_t q4) {
+    const float s = sr[c / g];
+    const int z = zr[c / g];
     h4 hv, lv;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float e = ldexpf(w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z), t);
+      const float e = ldexpf(err(w, q4, s, z, i), t);
       const _Float16 h = (_Float16)e;
       hv[i] = h;
       lv[i] = (_Float16)(e - (float)h);
     }
     *(h4*)(hr + c) = hv;
     *(h4*)(lr + c) = lv;
+  };
+  if (NCH > 0) {
+#pragma unroll
+    for (int k = 0; k < NR; ++k) {
+      const int c = (threadIdx.x + 256 * k) * 4;
+      if (c < cols) emit(c, wv[k], qv[k]);
+    }
+  } else {
+    for (int c = threadIdx.x * 4; c < cols; c += 256 * 4)
+      emit(c, *(const f32x4*)(wr + c), *(const uint32_t*)(qr + c));
   }
+}
+
+template <int NCH>
+static hipError_t launch_split_e_t(hipStream_t st, int rows, int cols, int g, const float* W,
+                                   const uint8_t* codes, const float* scales,
+                                   const int32_t* zeros, char* ws, const Layout& lay,
+                                   const int32_t* rowmap) {
+  hipLaunchKernelGGL(split_e_kernel<NCH>, dim3(rows), dim3(256), 0, st, rows, cols, g, W, codes,
+                     scales, zeros, (_Float16*)(ws + lay.ehi), (_Float16*)(ws + lay.elo),
+                     (float*)(ws + lay.erow), rowmap);
+  return hipGetLastError();
 }
 
 hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
                           const uint8_t* codes, const float* scales, const int32_t* zeros,
                           char* ws, const Layout& lay, const int32_t* rowmap) {
-  hipLaunchKernelGGL(split_e_kernel, dim3(rows), dim3(256), 0, st, rows, cols, g, W, codes, scales,
-                     zeros, (_Float16*)(ws + lay.ehi), (_Float16*)(ws + lay.elo),
-                     (float*)(ws + lay.erow), rowmap);
-  return hipGetLastError();
+  if (rows <= 0) return hipSuccess;
+  if (cols <= 4096)
+    return launch_split_e_t<4>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+  if (cols <= 12288)
+    return launch_split_e_t<12>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+  if (cols <= 16384)
+    return launch_split_e_t<16>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+  return launch_split_e_t<0>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
 }
 
 }  // namespace jarq

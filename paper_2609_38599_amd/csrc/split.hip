@@ -143,9 +143,9 @@ hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char*
 
 // One work-group per row: E = W - s (q - z) in fp32 (as in eq. (1)), its
 // row maximum, then the two fp16 planes and the row's inverse scale 2^-t.
-// With NCH > 0 each thread keeps its NCH chunks of four weights and codes in
-// registers between the two passes (rows of at most 1024 NCH columns), so W
-// and the codes are read from memory once; NCH = 0 reads them twice.
+// Each thread keeps its NCH chunks of four weights and codes in registers
+// between the two passes (rows of at most 1024 NCH columns), so W and the
+// codes are read from memory once.
 template <int NCH>
 __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
                                                       const float* __restrict__ W,
@@ -169,37 +169,25 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
   auto err = [&](const f32x4& w, uint32_t q4, float s, int z, int i) {
     return w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z);
   };
-  constexpr int NR = NCH > 0 ? NCH : 1;
-  f32x4 wv[NR];
-  uint32_t qv[NR];
+  f32x4 wv[NCH];
+  uint32_t qv[NCH];
   float m = 0.f;
-  if (NCH > 0) {
 #pragma unroll
-    for (int k = 0; k < NR; ++k) {
-      const int c = (threadIdx.x + 256 * k) * 4;
-      if (c < cols) {
-        wv[k] = *(const f32x4*)(wr + c);
-        qv[k] = *(const uint32_t*)(qr + c);
-      }
+  for (int k = 0; k < NCH; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < cols) {
+      wv[k] = *(const f32x4*)(wr + c);
+      qv[k] = *(const uint32_t*)(qr + c);
     }
+  }
 #pragma unroll
-    for (int k = 0; k < NR; ++k) {
-      const int c = (threadIdx.x + 256 * k) * 4;
-      if (c < cols) {
-        const float s = sr[c / g];
-        const int z = zr[c / g];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(err(wv[k], qv[k], s, z, i)));
-      }
-    }
-  } else {
-    for (int c = threadIdx.x * 4; c < cols; c += 256 * 4) {
-      const f32x4 w = *(const f32x4*)(wr + c);
-      const uint32_t q4 = *(const uint32_t*)(qr + c);
+  for (int k = 0; k < NCH; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < cols) {
       const float s = sr[c / g];
       const int z = zr[c / g];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(err(w, q4, s, z, i)));
+      for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(err(wv[k], qv[k], s, z, i)));
     }
   }
 #pragma unroll
@@ -226,15 +214,10 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
     *(h4*)(hr + c) = hv;
     *(h4*)(lr + c) = lv;
   };
-  if (NCH > 0) {
 #pragma unroll
-    for (int k = 0; k < NR; ++k) {
-      const int c = (threadIdx.x + 256 * k) * 4;
-      if (c < cols) emit(c, wv[k], qv[k]);
-    }
-  } else {
-    for (int c = threadIdx.x * 4; c < cols; c += 256 * 4)
-      emit(c, *(const f32x4*)(wr + c), *(const uint32_t*)(qr + c));
+  for (int k = 0; k < NCH; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < cols) emit(c, wv[k], qv[k]);
   }
 }
 
@@ -257,9 +240,9 @@ hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float
     return launch_split_e_t<4>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
   if (cols <= 12288)
     return launch_split_e_t<12>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
-  if (cols <= 16384)
+  if (cols <= 16384)   // the most a layer can have: 128 groups of at most 128
     return launch_split_e_t<16>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
-  return launch_split_e_t<0>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace jarq

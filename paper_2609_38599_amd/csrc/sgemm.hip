@@ -265,8 +265,11 @@ __global__ __launch_bounds__(512, 1) void split3_kernel(
 // Per row j and group i: (R_i e_i) . U_i = e_i^T L_i L_i^{-1} (H e)_i in fp64,
 // with E read from its planes and R_i = L_i^T in fp32.  V = E_i L_i on fp32
 // matrix cores (v_mfma_f32_16x16x4f32; L_i is lower triangular, so output
-// block mb only takes k-blocks kc >= mb).  Work-group: 256 rows x one group,
-// R_i staged once in LDS; wave w takes rows 64 w .. 64 w + 63 in blocks of 16.
+// block mb only takes k-blocks kc >= mb).  Work-group: 64 kDotRowBlocks rows x
+// one group, the part of R_i the products read staged once in LDS; each wave
+// takes kDotRowBlocks blocks of 16 consecutive rows.
+constexpr int kDotRowBlocks = 2;   // 16-row blocks per wave
+
 template <int G_SIZE>
 __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
                                                         const _Float16* __restrict__ Eh,
@@ -277,9 +280,16 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
                                                         double* __restrict__ objpart) {
   constexpr int g = G_SIZE;
   constexpr int NBK = g / 16;
-  constexpr int LDR = g + 4;  // padded row stride of R_i in LDS
+  // R_i in LDS, only what the products read: row m from column 16 (m / 16) on
+  // (the block upper triangle), rows padded by 4 floats, packed one after the
+  // other (about 39 KB at g = 128, so four work-groups fit on a CU).
+  constexpr int RS_SIZE = 16 * (NBK * (g + 4) - 8 * NBK * (NBK - 1));
+  auto roff = [](int m) {
+    const int b = m >> 4;
+    return 16 * (b * (g + 4) - 8 * b * (b - 1)) + (m & 15) * (g - 16 * b + 4);
+  };
   typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-  __shared__ __attribute__((aligned(16))) float rs[g * LDR];
+  __shared__ __attribute__((aligned(16))) float rs[RS_SIZE];
   const int G = cols / g;
   const int i = blockIdx.y;
   const int lane = threadIdx.x & 63;
@@ -288,11 +298,13 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
   const float* Ri = rmat + (size_t)i * g * g;
   for (int e = threadIdx.x; e < g * g / 4; e += 256) {
     const int r = e / (g / 4), c4 = e % (g / 4);
-    *(f32x4*)(rs + r * LDR + 4 * c4) = *(const f32x4*)(Ri + (size_t)r * g + 4 * c4);
+    const int k0 = 16 * (r >> 4);
+    if (4 * c4 >= k0)
+      *(f32x4*)(rs + roff(r) + 4 * c4 - k0) = *(const f32x4*)(Ri + (size_t)r * g + 4 * c4);
   }
   __syncthreads();
-  for (int rb = 0; rb < 4; ++rb) {
-    const int r0 = blockIdx.x * 256 + wave * 64 + rb * 16;
+  for (int rb = 0; rb < kDotRowBlocks; ++rb) {
+    const int r0 = blockIdx.x * (64 * kDotRowBlocks) + wave * (16 * kDotRowBlocks) + rb * 16;
     if (r0 >= rows) break;
     const int arow = r0 + mr;
     const size_t ab = (size_t)(arow < rows ? arow : 0) * cols + (size_t)i * g;
@@ -320,7 +332,7 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
       for (int kc = 0; kc < NBK; ++kc) {
         if (kc < mb) continue;  // zero block of the triangle (constant trip count keeps ea in registers)
         // B(k, m) = L_i(k, m) = R_i(m, k)
-        const f32x4 bv = *(const f32x4*)(rs + m * LDR + kc * 16 + 4 * kq);
+        const f32x4 bv = *(const f32x4*)(rs + roff(m) + (kc - mb) * 16 + 4 * kq);
 #pragma unroll
         for (int t = 0; t < 4; ++t)
           acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ea[kc][t], bv[t], acc, 0, 0, 0);
@@ -356,7 +368,7 @@ static hipError_t launch_split3_t(hipStream_t st, int M, int N, int K, int lda, 
 template <int G_SIZE>
 static hipError_t launch_group_dot_t(hipStream_t st, int rows, int cols, const char* ws,
                                      const Layout& lay, const float* U, double* objpart) {
-  dim3 grid((rows + 255) / 256, cols / G_SIZE);
+  dim3 grid((rows + 64 * kDotRowBlocks - 1) / (64 * kDotRowBlocks), cols / G_SIZE);
   hipLaunchKernelGGL(group_dot_kernel<G_SIZE>, grid, dim3(256), 0, st, rows, cols,
                      (const _Float16*)(ws + lay.ehi), (const _Float16*)(ws + lay.elo),
                      (const float*)(ws + lay.erow), (const float*)(ws + lay.rmat), U, objpart);

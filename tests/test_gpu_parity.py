@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 import torch
 
+from synth import rtn_quantize
 from tests._gpu_common import (CONFIGS, OBJ_RTOL, GpuLayer, check_code_step, check_scales, jarq,
                                jq, layer, random_layer, rel, say)
 
@@ -223,6 +224,45 @@ def test_shapes(rows, cols, g, bits):
     F_gpu = jarq.objective_rows(W, H, qg, sg, z, g).sum()
     F_or = jarq.objective_rows(W, H, qo, so, z, g).sum()
     say(f"[shape e2e] rel {rel(F_gpu, F_or):.2e} agreement {np.mean(qg == qo):.6f}")
+    assert rel(F_gpu, F_or) <= OBJ_RTOL
+
+
+def test_widest_accepted_layer():
+    """The most columns a layer may have: 128 groups of 128 (16384 columns).
+
+    H is the AR(1) covariance 0.5^|i-j| plus damping (closed form, so no token
+    build is needed at this width); 48 rows (a ragged row tile).  One sweep is
+    checked teacher-forced, then two free-running sweeps against the oracle.
+    """
+    from scipy.linalg import toeplitz
+    rows, cols, g, bits = 48, 16384, 128, 3
+    H = toeplitz(0.5 ** np.arange(cols)).astype(np.float32)
+    H += np.float32(0.01) * np.eye(cols, dtype=np.float32)
+    rng = np.random.default_rng(16384)
+    W = (0.02 * rng.standard_normal((rows, cols))).astype(np.float32)
+    q, s, z = rtn_quantize(W, g, bits)
+    say(f"[widest] rows {rows} cols {cols} g {g} bits {bits}")
+    gl = GpuLayer(W, H, q, s, z, g, bits)
+    R = jarq.group_factors(H, g)
+    q0, _ = gl.state()
+    gl.scale_step()
+    q1, s1 = gl.state()
+    assert np.array_equal(q0, q1)
+    s_ref, _ = jarq.scale_step(W, H, q0, z, g)
+    check_scales(s1, s_ref, " widest sweep 1")
+    cand, dec = gl.code_step()
+    check_code_step(W, H, R, q0, s1, z, g, bits, cand, dec, " widest sweep 1")
+    del gl
+    K = 2
+    gk = GpuLayer(W, H, q, s, z, g, bits, sweeps=K)
+    jq.sweeps(gk.p, gk.W, gk.H, gk.codes, gk.scales, gk.zeros, gk.ws)
+    qg, sg = gk.state()
+    del gk
+    torch.cuda.empty_cache()
+    qo, so, _ = jarq.refine(W, H, q, s, z, g, bits, K, R=R)
+    F_gpu = jarq.objective_rows(W, H, qg, sg, z, g).sum()
+    F_or = jarq.objective_rows(W, H, qo, so, z, g).sum()
+    say(f"[widest e2e] rel {rel(F_gpu, F_or):.2e} agreement {np.mean(qg == qo):.6f}")
     assert rel(F_gpu, F_or) <= OBJ_RTOL
 
 

@@ -11,6 +11,11 @@
 namespace jarq {
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+// One row counter per panel of the code update.
+static int pcount_words(int cols, int g) {
+  const int pg = panel_groups_of(g);
+  return (cols / g + pg - 1) / pg;
+}
 
 Layout make_layout(int rows, int cols, int g) {
   Layout L{};
@@ -43,7 +48,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
   L.plist = take(R * sizeof(int32_t));
-  L.pcount = take((C + 511) / 512 * sizeof(uint32_t));
+  L.pcount = take(pcount_words(C, g) * sizeof(uint32_t));
   L.objpart = take(R * (nt > G ? nt : G) * sizeof(double));  // per-group sweep partials or 64-column slices
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
@@ -136,13 +141,18 @@ hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes
 // decoded in order by the Babai kernel, then their accepted changes are folded
 // into the residual product of every later column.  `n` positions of the
 // sweep, position p holding layer row map_row(rowmap, p).
+// The per-panel row counters must be zero when the first Babai launch runs:
+// zeroed here unless the caller's previous launch did (counts_zeroed).
 hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const float* H,
                          uint8_t* codes, const float* scales, const int32_t* zeros,
-                         const uint8_t* active, uint8_t* cand, uint8_t* decision) {
+                         const uint8_t* active, uint8_t* cand, uint8_t* decision,
+                         bool counts_zeroed = false) {
   (void)H;
   const int nb = panel_groups(c.g);
-  hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, (size_t)(c.cols + 511) / 512 * sizeof(uint32_t));
-  if (e0 != hipSuccess) return e0;
+  if (!counts_zeroed) {
+    hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, pcount_words(c.cols, c.g) * sizeof(uint32_t));
+    if (e0 != hipSuccess) return e0;
+  }
   for (int i0 = 0; i0 < c.G; i0 += nb) {
     const int i1 = i0 + nb < c.G ? i0 + nb : c.G;
     hipError_t e = launch_babai(c.st, n, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay,
@@ -239,10 +249,12 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
       e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
     if (e == hipSuccess)
       e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
-                            (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau, rmap);
+                            (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau, rmap,
+                            (uint32_t*)(c.ws + c.lay.pcount), pcount_words(c.cols, c.g));
     if (e == hipSuccess) e = mark(k, 5);
     if (e == hipSuccess)
-      e = enqueue_babai(c, n, rmap, H, codes, scales, zeros, c.active(), nullptr, nullptr);
+      e = enqueue_babai(c, n, rmap, H, codes, scales, zeros, c.active(), nullptr, nullptr,
+                        /*counts_zeroed=*/true);
     if (e == hipSuccess) e = mark(k, 6);
     if (e == hipSuccess)
       e = launch_record_sweep(c.st, c.rows, (const double*)(c.ws + c.lay.lcur), c.active(),

@@ -175,9 +175,11 @@ hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0
 hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
                                 double* out);
 
+// Also zeroes zero_words[0 .. nzero) (nzero <= 256) before any row is handled.
 hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int sweep,
-                             float tau, const int32_t* rowmap);
+                             float tau, const int32_t* rowmap, uint32_t* zero_words,
+                             int nzero);
 
 hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);
 hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n);

@@ -28,7 +28,10 @@ hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* 
 __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part,
                                   double* __restrict__ lcur, double* __restrict__ lprev,
                                   uint8_t* __restrict__ active, int sweep, float tau,
-                                  const int32_t* __restrict__ rowmap) {
+                                  const int32_t* __restrict__ rowmap,
+                                  uint32_t* __restrict__ zero_words, int nzero) {
+  // the code update's per-panel row counters start the sweep at zero
+  if (blockIdx.x == 0 && (int)threadIdx.x < nzero) zero_words[threadIdx.x] = 0u;
   const int pos = blockIdx.x * blockDim.x + threadIdx.x;
   if (pos >= n) return;
   const int r = map_row(rowmap, pos);
@@ -47,9 +50,11 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
 
 hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int sweep,
-                             float tau, const int32_t* rowmap) {
+                             float tau, const int32_t* rowmap, uint32_t* zero_words,
+                             int nzero) {
+  if (n <= 0 || nzero < 0 || nzero > 256) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stop_check_kernel, dim3((n + 255) / 256), dim3(256), 0, st, n, nt,
-                     objpart, lcur, lprev, active, sweep, tau, rowmap);
+                     objpart, lcur, lprev, active, sweep, tau, rowmap, zero_words, nzero);
   return hipGetLastError();
 }
 
@@ -103,22 +108,35 @@ hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n) {
 
 // Sum of L over all rows (a stopped row keeps its last L, which is still its
 // objective) in a fixed order, plus the counters; the counters are then reset.
-__global__ __launch_bounds__(256) void record_sweep_kernel(int rows, const double* __restrict__ lcur,
-                                                           const uint8_t* __restrict__ active,
-                                                           Counters* __restrict__ cnt,
-                                                           SweepRecord* __restrict__ rec) {
-  __shared__ double red[256];
-  __shared__ unsigned int act[256];
+// One 1024-thread work-group; each thread loads four rows before adding them
+// (independent loads in flight), then a fixed-order tree over the threads.
+constexpr int kRecordThreads = 1024;
+__global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
+    int rows, const double* __restrict__ lcur, const uint8_t* __restrict__ active,
+    Counters* __restrict__ cnt, SweepRecord* __restrict__ rec) {
+  __shared__ double red[kRecordThreads];
+  __shared__ unsigned int act[kRecordThreads];
   double s = 0.0;
   unsigned int a = 0;
-  for (int r = threadIdx.x; r < rows; r += 256) {
-    s += lcur[r];
-    a += active[r] ? 1u : 0u;
+  for (int r0 = threadIdx.x; r0 < rows; r0 += 4 * kRecordThreads) {
+    double v[4];
+    unsigned int b[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = r0 + u * kRecordThreads;
+      v[u] = r < rows ? lcur[r] : 0.0;
+      b[u] = r < rows ? (active[r] ? 1u : 0u) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      s += v[u];
+      a += b[u];
+    }
   }
   red[threadIdx.x] = s;
   act[threadIdx.x] = a;
   __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
+  for (int w = kRecordThreads / 2; w >= 1; w >>= 1) {
     if ((int)threadIdx.x < w) {
       red[threadIdx.x] += red[threadIdx.x + w];
       act[threadIdx.x] += act[threadIdx.x + w];
@@ -146,7 +164,8 @@ __global__ __launch_bounds__(256) void record_sweep_kernel(int rows, const doubl
 
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
                                const uint8_t* active, Counters* cnt, SweepRecord* rec) {
-  hipLaunchKernelGGL(record_sweep_kernel, dim3(1), dim3(256), 0, st, rows, lcur, active, cnt, rec);
+  hipLaunchKernelGGL(record_sweep_kernel, dim3(1), dim3(kRecordThreads), 0, st, rows, lcur, active,
+                     cnt, rec);
   return hipGetLastError();
 }
 

@@ -36,6 +36,9 @@ Layout make_layout(int rows, int cols, int g) {
   L.hlo = take(C * C * 2);
   L.hscale = take(2 * sizeof(float));
   L.rmat = take(G * gg * sizeof(float));
+  L.rph = take(G * gg * 2);
+  L.rpl = take(G * gg * 2);
+  L.rrow = take(G * g * sizeof(float));
   L.mhi = take(C * C * 2);
   L.mlo = take(C * C * 2);
   L.mrow = take(C * sizeof(float));
@@ -171,6 +174,7 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
   JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
   JQ_HIP(launch_chol_groups(c.st, c.cols, c.g, H, c.ws, c.lay));
+  JQ_HIP(launch_split_r(c.st, c.cols, c.g, c.ws, c.lay));
   JQ_HIP(launch_split_m(c.st, c.cols, c.g, H, c.ws, c.lay));
   JQ_HIP(launch_split_h(c.st, c.cols, H, c.ws, c.lay));
   JQ_HIP(launch_gemm_ah(c.st, c.rows, c.cols, c.g, false, W, nullptr, nullptr, nullptr, H, c.wh(),

@@ -130,6 +130,47 @@ static hipError_t launch_chol_t(hipStream_t st, int cols, const float* H, char* 
   return hipGetLastError();
 }
 
+// R_i rows as two fp16 terms for the objective's products: row c scaled by
+// 2^t_c (its largest entry in [2^13, 2^14)), hi = fp16(x), lo = fp16(x - hi).
+// One wavefront per row (g <= 128: two entries per lane).
+__global__ __launch_bounds__(256) void split_r_kernel(const float* __restrict__ rmat, int nrows,
+                                                      int g, _Float16* __restrict__ hi,
+                                                      _Float16* __restrict__ lo,
+                                                      float* __restrict__ row_inv) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= nrows) return;
+  const float* x = rmat + (size_t)r * g;
+  const float a = lane < g ? x[lane] : 0.f;
+  const float b = lane + 64 < g ? x[lane + 64] : 0.f;
+  float m = fmaxf(fabsf(a), fabsf(b));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  const int t = (m > 0.f && isfinite(m)) ? 13 - ilogbf(m) : 0;
+  if (lane == 0) row_inv[r] = ldexpf(1.f, -t);
+  if (lane < g) {
+    const float v = ldexpf(a, t);
+    const _Float16 h = (_Float16)v;
+    hi[(size_t)r * g + lane] = h;
+    lo[(size_t)r * g + lane] = (_Float16)(v - (float)h);
+  }
+  if (lane + 64 < g) {
+    const float v = ldexpf(b, t);
+    const _Float16 h = (_Float16)v;
+    hi[(size_t)r * g + lane + 64] = h;
+    lo[(size_t)r * g + lane + 64] = (_Float16)(v - (float)h);
+  }
+}
+
+hipError_t launch_split_r(hipStream_t st, int cols, int g, char* ws, const Layout& lay) {
+  if (g > 128) return hipErrorInvalidValue;
+  const int nrows = cols;  // G groups of g rows
+  hipLaunchKernelGGL(split_r_kernel, dim3((nrows + 3) / 4), dim3(256), 0, st,
+                     (const float*)(ws + lay.rmat), nrows, g, (_Float16*)(ws + lay.rph),
+                     (_Float16*)(ws + lay.rpl), (float*)(ws + lay.rrow));
+  return hipGetLastError();
+}
+
 hipError_t launch_chol_groups(hipStream_t st, int cols, int g, const float* H, char* ws,
                               const Layout& lay) {
   switch (g) {

@@ -63,6 +63,9 @@ struct Layout {
   size_t hlo;       // [cols][cols] f16: H 2^t, low term
   size_t hscale;    // f32[2]: 2^-t, max |H|
   size_t rmat;      // [G][g][g] f32: R_i = L_i^T, row-major
+  size_t rph;       // [G][g][g] f16: R_i row c scaled by 2^t_c, high term
+  size_t rpl;       // [G][g][g] f16: low term
+  size_t rrow;      // [G][g] f32: 2^-t_c of the R rows
   size_t mhi;       // [cols][cols] f16: M = blockdiag(L_i^{-1}) H, row n scaled by 2^t_n, high term
   size_t mlo;       // [cols][cols] f16: low term
   size_t mrow;      // [cols] f32: 2^-t_n
@@ -93,6 +96,8 @@ Layout make_layout(int rows, int cols, int g);
 
 hipError_t launch_chol_groups(hipStream_t st, int cols, int g, const float* H, char* ws,
                               const Layout& lay);
+// R_i rows as two fp16 terms with per-row power-of-two scales (rph, rpl, rrow).
+hipError_t launch_split_r(hipStream_t st, int cols, int g, char* ws, const Layout& lay);
 
 // C = A H with A = W (quant == false) or A = W - What (quant == true).  When
 // objpart is non-null, objpart[row][col/64] receives sum over the 64-column

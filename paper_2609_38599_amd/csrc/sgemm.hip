@@ -262,12 +262,14 @@ __global__ __launch_bounds__(512, 1) void split3_kernel(
   }
 }
 
-// Per row j and group i: (R_i e_i) . U_i = e_i^T L_i L_i^{-1} (H e)_i in fp64,
-// with E read from its planes and R_i = L_i^T in fp32.  V = E_i L_i on fp32
-// matrix cores (v_mfma_f32_16x16x4f32; L_i is lower triangular, so output
-// block mb only takes k-blocks kc >= mb).  Work-group: 64 kDotRowBlocks rows x
-// one group, the part of R_i the products read staged once in LDS; each wave
-// takes kDotRowBlocks blocks of 16 consecutive rows.
+// Per row j and group i: (R_i e_i) . U_i = e_i^T L_i L_i^{-1} (H e)_i, summed
+// in fp64.  V = E_i L_i (V(j, c) = sum_k E(j, k) R_i(c, k)) on fp16 matrix
+// cores (v_mfma_f32_16x16x32_f16) from the two-term planes of E and of the
+// rows of R_i (three products, as in the residual product), scaled back per
+// R row and per E row.  R_i(c, k) = 0 for k < c, so output columns c only take
+// the 32-wide k-chunks from 32 floor(c / 32) on; only those are staged in LDS
+// (rows packed, padded by 8 halves).  Work-group: 64 kDotRowBlocks rows x one
+// group; each wave takes kDotRowBlocks blocks of 16 consecutive rows.
 constexpr int kDotRowBlocks = 2;   // 16-row blocks per wave
 
 template <int G_SIZE>
@@ -275,71 +277,81 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
                                                         const _Float16* __restrict__ Eh,
                                                         const _Float16* __restrict__ El,
                                                         const float* __restrict__ erow_inv,
-                                                        const float* __restrict__ rmat,
+                                                        const _Float16* __restrict__ rph,
+                                                        const _Float16* __restrict__ rpl,
+                                                        const float* __restrict__ rrow,
                                                         const float* __restrict__ U,
                                                         double* __restrict__ objpart) {
   constexpr int g = G_SIZE;
-  constexpr int NBK = g / 16;
-  // R_i in LDS, only what the products read: row m from column 16 (m / 16) on
-  // (the block upper triangle), rows padded by 4 floats, packed one after the
-  // other (about 39 KB at g = 128, so four work-groups fit on a CU).
-  constexpr int RS_SIZE = 16 * (NBK * (g + 4) - 8 * NBK * (NBK - 1));
-  auto roff = [](int m) {
-    const int b = m >> 4;
-    return 16 * (b * (g + 4) - 8 * b * (b - 1)) + (m & 15) * (g - 16 * b + 4);
+  constexpr int NKC = g / 32;   // 32-wide k-chunks
+  constexpr int NMB = g / 16;   // 16-column output blocks
+  constexpr int NB32 = g / 32;  // 32-row bands of R_i
+  // packed rows: band b (rows 32 b .. 32 b + 31) keeps columns 32 b .. g - 1
+  constexpr int PLANE = 32 * (NB32 * (g + 8) - 16 * NB32 * (NB32 - 1));
+  auto roff = [](int c) {
+    const int b = c >> 5;
+    return 32 * (b * (g + 8) - 16 * b * (b - 1)) + (c & 31) * (g - 32 * b + 8);
   };
-  typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-  __shared__ __attribute__((aligned(16))) float rs[RS_SIZE];
+  __shared__ __attribute__((aligned(16))) _Float16 rs_h[PLANE];
+  __shared__ __attribute__((aligned(16))) _Float16 rs_l[PLANE];
   const int G = cols / g;
   const int i = blockIdx.y;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int mr = lane & 15, kq = lane >> 4;
-  const float* Ri = rmat + (size_t)i * g * g;
-  for (int e = threadIdx.x; e < g * g / 4; e += 256) {
-    const int r = e / (g / 4), c4 = e % (g / 4);
-    const int k0 = 16 * (r >> 4);
-    if (4 * c4 >= k0)
-      *(f32x4*)(rs + roff(r) + 4 * c4 - k0) = *(const f32x4*)(Ri + (size_t)r * g + 4 * c4);
+  {
+    const _Float16* Rh = rph + (size_t)i * g * g;
+    const _Float16* Rl = rpl + (size_t)i * g * g;
+    for (int e = threadIdx.x; e < g * g / 8; e += 256) {
+      const int c = e / (g / 8), k0 = 8 * (e % (g / 8));
+      const int kb = 32 * (c >> 5);
+      if (k0 >= kb) {
+        *(f16x8*)(rs_h + roff(c) + k0 - kb) = *(const f16x8*)(Rh + (size_t)c * g + k0);
+        *(f16x8*)(rs_l + roff(c) + k0 - kb) = *(const f16x8*)(Rl + (size_t)c * g + k0);
+      }
+    }
   }
   __syncthreads();
+  const float* rsc = rrow + (size_t)i * g;
   for (int rb = 0; rb < kDotRowBlocks; ++rb) {
     const int r0 = blockIdx.x * (64 * kDotRowBlocks) + wave * (16 * kDotRowBlocks) + rb * 16;
     if (r0 >= rows) break;
+    // A fragments: E(row r0 + mr, k = 32 kc + 8 kq .. + 7); rows past the edge
+    // read row 0 and reach only outputs that are never stored.
     const int arow = r0 + mr;
-    const size_t ab = (size_t)(arow < rows ? arow : 0) * cols + (size_t)i * g;
-    // A fragments: E(row mr, k = 16 kc + 4 kq + t)
-    f32x4 ea[NBK];
+    const size_t ab = (size_t)(arow < rows ? arow : 0) * cols + (size_t)i * g + 8 * kq;
+    f16x8 ah[NKC], al[NKC];
 #pragma unroll
-    for (int kc = 0; kc < NBK; ++kc) {
-      const f16x4 h = *(const f16x4*)(Eh + ab + kc * 16 + 4 * kq);
-      const f16x4 l = *(const f16x4*)(El + ab + kc * 16 + 4 * kq);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) ea[kc][t] = arow < rows ? (float)h[t] + (float)l[t] : 0.f;
+    for (int kc = 0; kc < NKC; ++kc) {
+      ah[kc] = *(const f16x8*)(Eh + ab + kc * 32);
+      al[kc] = *(const f16x8*)(El + ab + kc * 32);
     }
     double part[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int mb = 0; mb < NBK; ++mb) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      const int m = mb * 16 + mr;
+    for (int mb = 0; mb < NMB; ++mb) {
+      const int c = mb * 16 + mr;   // this lane's column of V (and of its B fragment)
       float u[4];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int row = r0 + 4 * kq + v;
-        u[v] = U[(size_t)(row < rows ? row : 0) * cols + (size_t)i * g + m];
+        u[v] = U[(size_t)(row < rows ? row : 0) * cols + (size_t)i * g + c];
       }
+      const float cs = rsc[c];
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kc = 0; kc < NBK; ++kc) {
-        if (kc < mb) continue;  // zero block of the triangle (constant trip count keeps ea in registers)
-        // B(k, m) = L_i(k, m) = R_i(m, k)
-        const f32x4 bv = *(const f32x4*)(rs + roff(m) + (kc - mb) * 16 + 4 * kq);
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ea[kc][t], bv[t], acc, 0, 0, 0);
+      for (int kc = 0; kc < NKC; ++kc) {
+        if (kc < mb / 2) continue;  // chunk left of the diagonal: zero
+        // B(k, c) = R_i(c, k), k = 32 kc + 8 kq .. + 7
+        const int at = roff(c) + (kc - mb / 2) * 32 + 8 * kq;
+        const f16x8 bh = *(const f16x8*)(rs_h + at);
+        const f16x8 bl = *(const f16x8*)(rs_l + at);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[kc], bh, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[kc], bl, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[kc], bh, acc, 0, 0, 0);
       }
       // element v of lane l: (row 4 (l / 16) + v, column l % 16) of the block
 #pragma unroll
-      for (int v = 0; v < 4; ++v) part[v] = fma((double)acc[v], (double)u[v], part[v]);
+      for (int v = 0; v < 4; ++v) part[v] = fma((double)(acc[v] * cs), (double)u[v], part[v]);
     }
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
@@ -371,7 +383,8 @@ static hipError_t launch_group_dot_t(hipStream_t st, int rows, int cols, const c
   dim3 grid((rows + 64 * kDotRowBlocks - 1) / (64 * kDotRowBlocks), cols / G_SIZE);
   hipLaunchKernelGGL(group_dot_kernel<G_SIZE>, grid, dim3(256), 0, st, rows, cols,
                      (const _Float16*)(ws + lay.ehi), (const _Float16*)(ws + lay.elo),
-                     (const float*)(ws + lay.erow), (const float*)(ws + lay.rmat), U, objpart);
+                     (const float*)(ws + lay.erow), (const _Float16*)(ws + lay.rph),
+                     (const _Float16*)(ws + lay.rpl), (const float*)(ws + lay.rrow), U, objpart);
   return hipGetLastError();
 }
 

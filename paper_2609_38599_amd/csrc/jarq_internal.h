@@ -78,7 +78,7 @@ struct Layout {
   size_t p;         // [rows][cols] f32: (W - What) H
   size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
   size_t plist;     // [rows] i32: rows that accepted a change in the last panel (any order)
-  size_t pcount;    // [ceil(cols / 512)] u32: length of that list, one counter per panel
+  size_t pcount;    // [panels] u32: length of that list, one counter per panel
   size_t objpart;   // [rows][ceil(cols/64)] f64: partial row objectives
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64

@@ -161,3 +161,15 @@ def test_bf16_hessian_checks_arguments(lib):
     assert acc(fake, 10, 132, 1.0, fake, None) == binding.JARQ_EINVAL     # d % 8
     assert acc(_vp((1 << 20) + 8), 10, 128, 1.0, fake, None) == binding.JARQ_EINVAL
     assert acc(None, 0, 128, 1.0, fake, None) == binding.JARQ_OK
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark runs on one GPU; asking for more exits with a message."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    res = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode != 0
+    assert "one GPU" in (res.stdout + res.stderr)
+    assert res.stdout.strip() == "" or not res.stdout.strip().startswith("{")

@@ -14,7 +14,7 @@
 // (the group's block of the triangular system restricted to the prefix).  The
 // product M_GP e_P for every row is one fp64 matrix product per group (split
 // over k into partial slices, summed in a fixed order); the triangular parts
-// run per row, one row per thread.
+// run per row, sixteen lanes per row.
 #include "jarq_internal.h"
 
 namespace jarq {
@@ -31,23 +31,26 @@ size_t gptq_workspace_bytes(int rows, int cols, int g) {
   return a(C * C * 8) + a(C * C * 8) + a(R * C * 8) + a(ns * R * g * 8) + a(64 * 64 * 8) + a(4);
 }
 
-// One row per thread; dynamic LDS: cs [g][64] (c = M_GP e_P) and es [g][64]
-// (first y = M_GG^{-1} c, then the group's errors e).
+// Sixteen lanes per row (16 rows per 256-thread work-group): lane j owns the
+// group positions n = j + 16 t (t = 0 .. g/16 - 1) and keeps their values in
+// registers.  Each of the g sequential steps m forms sum_{n<m} M_mn v_n as
+// per-lane partial sums reduced over the row's lanes; the owner of m takes
+// the step.  Pass 1: y = M_GG^{-1} c and the group's grid from w + y (0 forced
+// into the range); pass 2: the columns in order, each rounded from
+// w_m + (c_m + sum_{n<m} M_mn e_n) / M_mm.
 template <int G_SIZE>
-__global__ __launch_bounds__(64) void gptq_group_kernel(int rows, int cols, int bits, int grp,
-                                                        const float* __restrict__ W,
-                                                        const double* __restrict__ M,
-                                                        const double* __restrict__ comp,
-                                                        int nsplit, double* __restrict__ E,
-                                                        uint8_t* __restrict__ codes,
-                                                        float* __restrict__ scales,
-                                                        int32_t* __restrict__ zeros) {
+__global__ __launch_bounds__(256) void gptq_group_kernel(int rows, int cols, int bits, int grp,
+                                                         const float* __restrict__ W,
+                                                         const double* __restrict__ M,
+                                                         const double* __restrict__ comp,
+                                                         int nsplit, double* __restrict__ E,
+                                                         uint8_t* __restrict__ codes,
+                                                         float* __restrict__ scales,
+                                                         int32_t* __restrict__ zeros) {
   constexpr int g = G_SIZE;
-  extern __shared__ double gsm[];
-  double* cs = gsm;
-  double* es = gsm + g * 64;
-  const int tid = threadIdx.x;
-  const int r = blockIdx.x * 64 + tid;
+  constexpr int NT = g / 16;
+  const int j = threadIdx.x & 15;
+  const int r = blockIdx.x * 16 + (threadIdx.x >> 4);
   const bool live = r < rows;
   const int rr = live ? r : rows - 1;
   const int b0 = grp * g;
@@ -56,45 +59,105 @@ __global__ __launch_bounds__(64) void gptq_group_kernel(int rows, int cols, int 
   const double* Mg = M + (long long)b0 * cols + b0;   // M_GG: Mg[m * cols + n], n <= m
   const float* w = W + (long long)rr * cols + b0;
   const long long cstride = (long long)rows * g;
-
-  // y = M_GG^{-1} c and the group's grid from w + y (0 forced into the range).
-  double lo = 0.0, hi = 0.0;
-  for (int m = 0; m < g; ++m) {
+  double cl[NT], wl[NT], vl[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int n = j + 16 * t;
     double c = 0.0;
-    for (int z = 0; z < nsplit; ++z) c += comp[z * cstride + (long long)rr * g + m];
-    cs[m * 64 + tid] = c;
-    double s = c;
-    for (int n = 0; n < m; ++n) s = fma(-Mg[(long long)m * cols + n], es[n * 64 + tid], s);
-    const double y = s / Mg[(long long)m * cols + m];
-    es[m * 64 + tid] = y;
-    const double v = (double)w[m] + y;
-    lo = fmin(lo, v);
-    hi = fmax(hi, v);
+    for (int z = 0; z < nsplit; ++z) c += comp[z * cstride + (long long)rr * g + n];
+    cl[t] = c;
+    wl[t] = (double)w[n];
+    vl[t] = 0.0;
+  }
+  // Row m of M_GG at this lane's positions, loaded one step ahead into the
+  // buffer of the other step parity (no register copies: a copy would wait
+  // for the loads in flight).  The last step reloads row g - 1 (in bounds).
+  double ma[NT], mb[NT];
+  auto load_row = [&](int m, double (&dst)[NT]) __attribute__((always_inline)) {
+    const double* mrow = Mg + (long long)(m < g ? m : g - 1) * cols + j;
+#pragma unroll
+    for (int t2 = 0; t2 < NT; ++t2) dst[t2] = mrow[16 * t2];
+  };
+  // sum_{n < m} M_mn v_n over the row's lanes (positions of earlier blocks, and
+  // of block t those before m), with mrow = row m at this lane's positions
+  auto row_dot = [&](int t, int i, const double (&mrow)[NT]) __attribute__((always_inline)) {
+    double part = 0.0;
+#pragma unroll
+    for (int t2 = 0; t2 < NT; ++t2)
+      if (t2 < t) part = fma(mrow[t2], vl[t2], part);
+    if (j < i) part = fma(mrow[t], vl[t], part);
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) part += __shfl_xor(part, off);
+    return part;
+  };
+
+  // pass 1: y = M_GG^{-1} c, grid from w + y
+  double lo = 0.0, hi = 0.0;
+  auto step1 = [&](int t, int i, const double (&mrow)[NT]) __attribute__((always_inline)) {
+    const double part = row_dot(t, i, mrow);
+    if (j == i) {
+      const double y = (cl[t] - part) / mrow[t];   // the owner's mrow[t] is M_mm
+      vl[t] = y;
+      const double v = wl[t] + y;
+      lo = fmin(lo, v);
+      hi = fmax(hi, v);
+    }
+  };
+  load_row(0, ma);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    for (int i = 0; i < 16; i += 2) {
+      load_row(16 * t + i + 1, mb);
+      step1(t, i, ma);
+      load_row(16 * t + i + 2, ma);
+      step1(t, i + 1, mb);
+    }
+  }
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) {
+    lo = fmin(lo, __shfl_xor(lo, off));
+    hi = fmax(hi, __shfl_xor(hi, off));
   }
   const double s = hi > lo ? (hi - lo) / qmax : 1.0;
   const float s32 = (float)s;
   const double s64 = (double)s32;
   const double zp = fmin(fmax(rint(-lo / s64), 0.0), qmax);
 
-  // Columns in order: round w_k + (c_k + sum_{n<k} M_kn e_n) / M_kk.
-  uint8_t* q_out = codes + (long long)rr * cols + b0;
-  double* e_out = E + (long long)rr * cols + b0;
-  for (int m = 0; m < g; ++m) {
-    double t = cs[m * 64 + tid];
-    for (int n = 0; n < m; ++n) t = fma(Mg[(long long)m * cols + n], es[n * 64 + tid], t);
-    const double wk = (double)w[m];
-    const double x = wk + t / Mg[(long long)m * cols + m];
-    const double q = fmin(fmax(rint(x / s64) + zp, 0.0), qmax);
-    const double e = wk - s64 * (q - zp);
-    es[m * 64 + tid] = e;
-    if (live) {
-      e_out[m] = e;
-      q_out[m] = (uint8_t)q;
+  // pass 2: the columns in order (vl now takes the errors e = w - s (q - z))
+  uint8_t ql[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) ql[t] = 0;
+  auto step2 = [&](int t, int i, const double (&mrow)[NT]) __attribute__((always_inline)) {
+    const double part = row_dot(t, i, mrow);
+    if (j == i) {
+      const double x = wl[t] + (cl[t] + part) / mrow[t];
+      const double q = fmin(fmax(rint(x / s64) + zp, 0.0), qmax);
+      vl[t] = wl[t] - s64 * (q - zp);
+      ql[t] = (uint8_t)q;
+    }
+  };
+  load_row(0, ma);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    for (int i = 0; i < 16; i += 2) {
+      load_row(16 * t + i + 1, mb);
+      step2(t, i, ma);
+      load_row(16 * t + i + 2, ma);
+      step2(t, i + 1, mb);
     }
   }
   if (live) {
-    scales[(long long)r * G + grp] = s32;
-    zeros[(long long)r * G + grp] = (int32_t)zp;
+    uint8_t* q_out = codes + (long long)r * cols + b0;
+    double* e_out = E + (long long)r * cols + b0;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      q_out[j + 16 * t] = ql[t];
+      e_out[j + 16 * t] = vl[t];
+    }
+    if (j == 0) {
+      scales[(long long)r * G + grp] = s32;
+      zeros[(long long)r * G + grp] = (int32_t)zp;
+    }
   }
 }
 
@@ -103,11 +166,7 @@ static hipError_t launch_gptq_group_t(hipStream_t st, int rows, int cols, int bi
                                       const float* W, const double* M, const double* comp,
                                       int nsplit, double* E, uint8_t* codes, float* scales,
                                       int32_t* zeros) {
-  const size_t lds = (size_t)2 * G_SIZE * 64 * sizeof(double);
-  hipError_t e = hipFuncSetAttribute((const void*)gptq_group_kernel<G_SIZE>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(gptq_group_kernel<G_SIZE>, dim3((rows + 63) / 64), dim3(64), lds, st, rows,
+  hipLaunchKernelGGL(gptq_group_kernel<G_SIZE>, dim3((rows + 15) / 16), dim3(256), 0, st, rows,
                      cols, bits, grp, W, M, comp, nsplit, E, codes, scales, zeros);
   return hipGetLastError();
 }

@@ -151,6 +151,9 @@ __global__ __launch_bounds__(256) void potrf_diag_kernel(double* __restrict__ A,
     L[i][j] = (i < nb && j <= i) ? A[(long long)i * lda + j] : 0.0;
   }
   __syncthreads();
+  // Trailing updates on a 16 x 16 thread grid: thread (ty, tx) owns rows
+  // ty + 16 a and columns tx + 16 b of the block (no index division).
+  const int tx = tid & 15, ty = tid >> 4;
   for (int j = 0; j < nb; ++j) {
     double piv = L[j][j];
     const bool bad = !(piv > 0.0) || !isfinite(piv);
@@ -160,12 +163,19 @@ __global__ __launch_bounds__(256) void potrf_diag_kernel(double* __restrict__ A,
       L[j][j] = dj;
       if (bad) *flag = 1;
     }
-    for (int i = j + 1 + tid; i < nb; i += 256) L[i][j] /= dj;
+    if (tid > j && tid < nb) L[tid][j] /= dj;
     __syncthreads();
-    const int n = nb - j - 1;
-    for (int e = tid; e < n * n; e += 256) {
-      const int i = j + 1 + e / n, k = j + 1 + e % n;
-      if (k <= i) L[i][k] = fma(-L[i][j], L[k][j], L[i][k]);
+#pragma unroll
+    for (int a = 0; a < LT / 16; ++a) {
+      const int i = ty + 16 * a;
+      if (i > j && i < nb) {
+        const double lij = L[i][j];
+#pragma unroll
+        for (int b = 0; b < LT / 16; ++b) {
+          const int k = tx + 16 * b;
+          if (k > j && k <= i) L[i][k] = fma(-lij, L[k][j], L[i][k]);
+        }
+      }
     }
     __syncthreads();
   }
@@ -173,18 +183,24 @@ __global__ __launch_bounds__(256) void potrf_diag_kernel(double* __restrict__ A,
     const int i = e / nb, j = e % nb;
     if (j <= i) A[(long long)i * lda + j] = L[i][j];
   }
-  // Column c of L^{-1} by forward substitution (thread c).
-  if (tid < nb) {
-    const int c = tid;
-    for (int i = 0; i < c; ++i) X[i][c] = 0.0;
-    X[c][c] = 1.0 / L[c][c];
-    for (int i = c + 1; i < nb; ++i) {
+  // L^{-1} row by row: X[i][i] = 1 / L[i][i] and, for c < i,
+  // X[i][c] = -(sum_{t=c}^{i-1} L[i][t] X[t][c]) / L[i][i].  Thread 4 c + q
+  // takes column c and every fourth t from c + q; the four partial sums are
+  // added across the four adjacent lanes.
+  {
+    const int c = tid >> 2, q = tid & 3;
+    if (q == 0 && c < nb) X[c][c] = 1.0 / L[c][c];
+    __syncthreads();
+    for (int i = 1; i < nb; ++i) {
       double s = 0.0;
-      for (int t = c; t < i; ++t) s = fma(L[i][t], X[t][c], s);
-      X[i][c] = -s / L[i][i];
+      if (c < i)
+        for (int t = c + q; t < i; t += 4) s = fma(L[i][t], X[t][c], s);
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      if (c < i && q == 0) X[i][c] = -s / L[i][i];
+      __syncthreads();
     }
   }
-  __syncthreads();
   for (int e = tid; e < LT * LT; e += 256) {
     const int i = e / LT, j = e % LT;
     Linv[e] = (i < nb && j < nb && j <= i) ? X[i][j] : 0.0;

@@ -210,6 +210,11 @@ hipError_t launch_gemm_nt_f64(hipStream_t st, bool lower, int M, int N, int K, i
                               double alpha, const double* A, long long lda, const double* B,
                               long long ldb, double* C, long long ldc, long long cz,
                               bool accumulate);
+// C_z = alpha A B over k-slice z (B k-major [K][N]), slice z stored at C + z cz.
+hipError_t launch_gemm_nn_f64_sliced(hipStream_t st, int M, int N, int K, int kslice,
+                                     double alpha, const double* A, long long lda,
+                                     const double* B, long long ldb, double* C, long long ldc,
+                                     long long cz);
 hipError_t launch_gemm_nn_f64(hipStream_t st, int M, int N, int K, double alpha, const double* A,
                               long long lda, const double* B, long long ldb, double* C,
                               long long ldc, bool accumulate);

@@ -129,6 +129,14 @@ hipError_t launch_gemm_nt_f64(hipStream_t st, bool lower, int M, int N, int K, i
                          accumulate);
 }
 
+hipError_t launch_gemm_nn_f64_sliced(hipStream_t st, int M, int N, int K, int kslice,
+                                     double alpha, const double* A, long long lda,
+                                     const double* B, long long ldb, double* C, long long ldc,
+                                     long long cz) {
+  return launch_gemm_f64(st, false, true, M, N, K, kslice, alpha, A, lda, B, ldb, C, ldc, cz,
+                         false);
+}
+
 hipError_t launch_gemm_nn_f64(hipStream_t st, int M, int N, int K, double alpha, const double* A,
                               long long lda, const double* B, long long ldb, double* C,
                               long long ldc, bool accumulate) {

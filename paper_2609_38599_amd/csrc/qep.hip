@@ -17,12 +17,35 @@ namespace jarq {
 
 namespace {
 constexpr int QB = 64;
+constexpr int kMaxSlices = 8;   // k-slices of the off-diagonal updates of the solves
 size_t al(size_t x) { return (x + 255) & ~size_t(255); }
+// k-slice length for a K-long update: at most kMaxSlices slices, 16-aligned
+int slice_of(int K) {
+  const int s = (K + kMaxSlices - 1) / kMaxSlices;
+  return ((s + 15) / 16) * 16;
+}
 }  // namespace
 
 size_t qep_workspace_bytes(int rows, int cols) {
   const size_t R = rows, C = cols, nb = (C + QB - 1) / QB;
-  return al(C * C * 8) + al(nb * QB * QB * 8) + al(R * C * 8) + al(R * C * 8) + al(4);
+  return al(C * C * 8) + al(nb * QB * QB * 8) + al(R * C * 8) + al(R * C * 8) + al(4) +
+         al((size_t)kMaxSlices * R * QB * 8);
+}
+
+// T[r][c] += sum_z P[z][r][c] (z in order) for the nb columns of one block.
+__global__ __launch_bounds__(256) void add_slices_kernel(double* __restrict__ T, long long ldt,
+                                                         int rows, int nb,
+                                                         const double* __restrict__ P, int nz,
+                                                         long long pz) {
+  const long long n = (long long)rows * nb;
+  for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < n;
+       e += (long long)gridDim.x * 256) {
+    const long long r = e / nb;
+    const int c = (int)(e % nb);
+    double s = T[r * ldt + c];
+    for (int z = 0; z < nz; ++z) s += P[z * pz + r * nb + c];
+    T[r * ldt + c] = s;
+  }
 }
 
 __global__ __launch_bounds__(256) void to_f64_kernel(const float* __restrict__ x, long long n,
@@ -55,6 +78,8 @@ hipError_t launch_qep_correct(hipStream_t st, int rows, int cols, const float* W
   double* W64 = (double*)((char*)Linv + al(nblk * QB * QB * 8));
   double* T = (double*)((char*)W64 + al(R * C * 8));
   int* flag = (int*)((char*)T + al(R * C * 8));
+  double* P = (double*)((char*)flag + al(4));   // [kMaxSlices][rows][nb] partial updates
+  const long long pz = (long long)rows * QB;
   *flag_out = flag;
   const long long n = (long long)rows * cols;
   const long long d = cols;
@@ -73,9 +98,14 @@ hipError_t launch_qep_correct(hipStream_t st, int rows, int cols, const float* W
   for (int k0 = 0; k0 < cols; k0 += QB) {
     const int nb = min(QB, cols - k0);
     if (k0 > 0) {
-      e = launch_gemm_nt_f64(st, false, rows, nb, k0, k0, -1.0, T, d, L + (long long)k0 * d, d,
-                             T + k0, d, 0, true);
+      // T_k -= Y_{<k} L_{k,<k}^T, the k range split into slices summed in order
+      const int ks = slice_of(k0);
+      e = launch_gemm_nt_f64(st, false, rows, nb, k0, ks, -1.0, T, d, L + (long long)k0 * d, d,
+                             P, nb, pz, false);
       if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(add_slices_kernel, dim3(grid_for((long long)rows * nb)), dim3(256), 0, st,
+                         T + k0, d, rows, nb, P, (k0 + ks - 1) / ks, pz);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     e = launch_gemm_nt_f64(st, false, rows, nb, nb, nb, 1.0, T + k0, d,
                            Linv + (long long)(k0 / QB) * QB * QB, QB, T + k0, d, 0, false);
@@ -86,9 +116,14 @@ hipError_t launch_qep_correct(hipStream_t st, int rows, int cols, const float* W
     const int nb = min(QB, cols - k0);
     const int rest = cols - k0 - nb;
     if (rest > 0) {
-      e = launch_gemm_nn_f64(st, rows, nb, rest, -1.0, T + k0 + nb, d,
-                             L + (long long)(k0 + nb) * d + k0, d, T + k0, d, true);
+      // T_k -= Z_{>k} L_{>k,k}, sliced as in the forward pass
+      const int ks = slice_of(rest);
+      e = launch_gemm_nn_f64_sliced(st, rows, nb, rest, ks, -1.0, T + k0 + nb, d,
+                                    L + (long long)(k0 + nb) * d + k0, d, P, nb, pz);
       if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(add_slices_kernel, dim3(grid_for((long long)rows * nb)), dim3(256), 0, st,
+                         T + k0, d, rows, nb, P, (rest + ks - 1) / ks, pz);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     e = launch_gemm_nn_f64(st, rows, nb, nb, 1.0, T + k0, d,
                            Linv + (long long)(k0 / QB) * QB * QB, QB, T + k0, d, false);

@@ -291,6 +291,24 @@ def code_step(W, H, R, codes, scales, zeros, g, bits, record=False):
     return (q8, tr) if record else q8
 
 
+def stop_rows(L_prev, L, tau):
+    """Early-stopping test of eq. (strict_stopping), App. E.2, per row.
+
+    L_prev holds L_j^(k-1) and L holds L_j^(k), the objective right after the
+    scale updates of two consecutive iterations k - 1 and k (k >= 2; there is
+    no test at k = 1).  A row stops when its decrease L^(k-1) - L^(k) is at
+    most tau relative to max(|L^(k-1)|, eps_fp32), or at most tau in absolute
+    value.  A negative decrease (the objective went up, e.g. after a ridge
+    solve) therefore always stops the row.  The stopped row keeps the new
+    scales s^(k) and skips the code update of iteration k.
+    """
+    L_prev = _f64(L_prev)
+    L = _f64(L)
+    dec = L_prev - L
+    rel = dec / np.maximum(np.abs(L_prev), FP32_EPS)
+    return (rel <= tau) | (np.abs(dec) <= tau)
+
+
 @dataclasses.dataclass
 class SweepRecord:
     L: np.ndarray            # objective right after the scale update, per row
@@ -334,9 +352,7 @@ def refine(W, H, codes, scales, zeros, g, bits, K, tau=None,
         L = np.full(rows, np.nan)
         L[ia] = objective_rows(W[ia], H, q[ia], s[ia], zeros[ia], g)
         if tau is not None and k >= 2:
-            dec = L_prev[ia] - L[ia]
-            rel = dec / np.maximum(np.abs(L_prev[ia]), FP32_EPS)
-            stop = (rel <= tau) | (np.abs(dec) <= tau)
+            stop = stop_rows(L_prev[ia], L[ia], tau)
             active[ia[stop]] = False
             ia = np.nonzero(active)[0]
         if L_prev is None:

@@ -16,7 +16,7 @@ from tests import test_oracle_pins as pins
 
 _ORIG = {name: getattr(jarq, name) for name in
          ("babai_group", "code_step", "gram_system", "solve_scales",
-          "group_factors", "objective_rows", "dequantize")}
+          "group_factors", "objective_rows", "dequantize", "refine")}
 
 
 def _battery():
@@ -40,6 +40,9 @@ def _battery():
         ("qr_form", lambda: pins.test_qr_form_equals_hessian_form(tl)),
         ("monotone", lambda: pins.test_monotone_descent_and_host_bound(tl)),
         ("babai_bound", lambda: pins.test_unclipped_babai_residual_bound(tl)),
+        ("stop_sequences", pins.test_stopping_rule_on_hand_built_sequences),
+        ("stop_counts", pins.test_stopping_rule_active_counts),
+        ("stop_idle_rows", lambda: pins.test_row_without_accepts_stops_at_the_next_iteration(tl)),
     ]
     failed = []
     for name, fn in checks:
@@ -153,6 +156,61 @@ def _dequantize_no_zero(codes, scales, zeros, g):
     return _ORIG["dequantize"](codes, scales, np.zeros_like(zeros), g)
 
 
+def _refine_factory(and_not_or=False, first_k=2, keep_old_scales=False, denom_current=False):
+    """refine() with a planted mistake in the early-stopping rule.
+
+    and_not_or: both tests of eq. (strict_stopping) must hold; first_k = 1:
+    the test also runs at k = 1, against the host state's objective;
+    keep_old_scales: a stopped row goes back to its previous scales;
+    denom_current: the relative decrease is divided by L^(k), not L^(k-1).
+    """
+    def refine(W, H, codes, scales, zeros, g, bits, K, tau=None, lam=jarq.RIDGE_LAMBDA,
+               rcond=jarq.RIDGE_RCOND, R=None, ridge_accept=False):
+        W = np.asarray(W, dtype=np.float64)
+        H = np.asarray(H, dtype=np.float64)
+        if R is None:
+            R = jarq.group_factors(H, g)
+        q = np.asarray(codes).astype(np.uint8).copy()
+        s = np.asarray(scales, dtype=np.float64).copy()
+        rows = W.shape[0]
+        active = np.ones(rows, dtype=bool)
+        L_prev = jarq.objective_rows(W, H, q, s, zeros, g) if first_k == 1 else None
+        history = []
+        for k in range(1, K + 1):
+            if not np.any(active):
+                break
+            ia = np.nonzero(active)[0]
+            s_old = s.copy()
+            s_new, ridge_a = jarq.scale_step(W[ia], H, q[ia], zeros[ia], g, lam, rcond)
+            s[ia] = s_new
+            L = np.full(rows, np.nan)
+            L[ia] = jarq.objective_rows(W[ia], H, q[ia], s[ia], zeros[ia], g)
+            if tau is not None and k >= first_k:
+                dec = L_prev[ia] - L[ia]
+                base = np.abs(L[ia]) if denom_current else np.abs(L_prev[ia])
+                rel = dec / np.maximum(base, jarq.FP32_EPS)
+                stop = ((rel <= tau) & (np.abs(dec) <= tau)) if and_not_or else \
+                    ((rel <= tau) | (np.abs(dec) <= tau))
+                active[ia[stop]] = False
+                if keep_old_scales:
+                    s[ia[stop]] = s_old[ia[stop]]
+                ia = np.nonzero(active)[0]
+            L_prev = L.copy() if L_prev is None else np.where(np.isnan(L), L_prev, L)
+            q_old = q.copy()
+            accepted = 0
+            if ia.size:
+                q_new, tr = jarq.code_step(W[ia], H, R, q[ia], s[ia], zeros[ia], g, bits, record=True)
+                q[ia] = q_new
+                accepted = int(np.sum(tr.decision == jarq.DEC_ACCEPT))
+            F_after = np.full(rows, np.nan)
+            if ia.size:
+                F_after[ia] = jarq.objective_rows(W[ia], H, q[ia], s[ia], zeros[ia], g)
+            history.append(jarq.SweepRecord(L, F_after, np.zeros(rows, bool), accepted,
+                                            int(np.sum(q != q_old)), active.copy()))
+        return q, s, history
+    return refine
+
+
 MUTATIONS = {
     "babai_tail_transposed": ("babai_group", _babai_factory(tail_transposed=True)),
     "babai_drops_zero_point": ("babai_group", _babai_factory(drop_zero=True)),
@@ -170,7 +228,17 @@ MUTATIONS = {
     "factor_lower_not_upper": ("group_factors", _factors_lower),
     "objective_without_hessian": ("objective_rows", _objective_without_h),
     "dequantize_drops_zero_point": ("dequantize", _dequantize_no_zero),
+    "stop_and_not_or": ("refine", _refine_factory(and_not_or=True)),
+    "stop_from_first_iteration": ("refine", _refine_factory(first_k=1)),
+    "stop_keeps_old_scales": ("refine", _refine_factory(keep_old_scales=True)),
+    "stop_relative_to_current": ("refine", _refine_factory(denom_current=True)),
 }
+
+
+def test_refine_factory_without_mistakes_passes_the_stopping_pins(monkeypatch):
+    # the mutated copies differ from the oracle only in the planted mistake
+    monkeypatch.setattr(jarq, "refine", _refine_factory())
+    assert _battery() == []
 
 
 @pytest.mark.parametrize("name", sorted(MUTATIONS))

@@ -580,3 +580,152 @@ def test_code_step_two_forms_agree(tiny_layer):
         assert np.all(np.abs(dF - (tr.err_new[:, i] - tr.err_old[:, i])) <= 1e-9 * scale)
         acc = tr.decision[:, i] == jarq.DEC_ACCEPT
         q_cur[acc, blk] = tr.cand[acc, blk]
+
+
+# ---------------------------------------------------------------------------
+# Early stopping, eq. (strict_stopping) of App. E.2
+# ---------------------------------------------------------------------------
+#
+# The stopping rule is pinned on hand-built objective sequences: the scale
+# step, the objective and the code step are replaced by scripted stand-ins so
+# that L_j^(k) (the objective right after the scale update of iteration k)
+# follows a table chosen per row, and refine() decides when each row stops.
+# tau = 2^-16 keeps every quotient below exact.
+
+STOP_TAU_EXACT = 2.0 ** -16
+_BIG = 2.0 ** 20
+# rows x (host, k = 1..4); the host column is what a row's objective is at
+# the host state (the scripted objective of scales marked 0)
+STOP_TABLE = np.array([
+    [2 * _BIG, _BIG, _BIG - 16.0, _BIG - 8.0, _BIG - 4.0],      # relative decrease exactly tau at k = 2
+    [2 * _BIG, _BIG, _BIG - 32.0, _BIG - 64.0, _BIG - 96.0],    # relative decrease 2 tau: never stops
+    [2.0 ** -9, 2.0 ** -10, 2.0 ** -10 - STOP_TAU_EXACT, 0.0, 0.0],  # absolute decrease exactly tau at k = 2
+    [4.0, 1.0, 1.5, 1.0, 0.5],                                  # the objective went up at k = 2
+    [_BIG, _BIG, _BIG / 2, _BIG / 4, _BIG / 8],                 # no decrease at k = 1: k = 1 never stops
+    [8.0, 4.0, 2.0, 1.0, 1.0 - 2.0 ** -20],                     # stops at k = 4 on L^(3) - L^(4)
+    [3 * _BIG, 3 * _BIG / 4, 3 * _BIG / 4 - 12.0, 0.0, 0.0],    # relative exactly tau of L^(k-1) (not of L^(k))
+])
+STOP_EXPECT = [2, None, 2, 2, None, 4, 2]     # iteration at which each row stops (None: never)
+
+
+class _Scripted:
+    """Scripted scale step, objective and code step for refine().
+
+    Row r of W carries r in column 0.  The scale step of iteration k (its k-th
+    call) returns scales equal to k; the objective returns STOP_TABLE[r, k] for scales equal
+    to k (k = 0 is the host); the code step writes k into column 1 of the codes
+    of the rows it updates.
+    """
+
+    def __init__(self, table):
+        self.table = table
+        self.k = 0
+        self.saved = {}
+
+    def scale_step(self, W, H, codes, zeros, g, lam=None, rcond=None, prev=None):
+        self.k += 1
+        return np.full((W.shape[0], zeros.shape[1]), float(self.k)), np.zeros(W.shape[0], bool)
+
+    def objective_rows(self, W, H, codes, scales, zeros, g):
+        r = np.asarray(W[:, 0], dtype=np.int64)
+        k = np.asarray(scales[:, 0], dtype=np.int64)
+        return self.table[r, k].astype(np.float64)
+
+    def code_step(self, W, H, R, codes, scales, zeros, g, bits, record=False):
+        q = np.asarray(codes).copy()
+        q[:, 1] = np.asarray(scales[:, 0], dtype=np.uint8)
+        G = zeros.shape[1]
+        tr = jarq.CodeTrace(None, None, np.full((q.shape[0], G), jarq.DEC_REJECT, np.uint8), None, None)
+        return (q, tr) if record else q
+
+    def __enter__(self):
+        for name in ("scale_step", "objective_rows", "code_step"):
+            self.saved[name] = getattr(jarq, name)
+            setattr(jarq, name, getattr(self, name))
+        return self
+
+    def __exit__(self, *exc):
+        for name, fn in self.saved.items():
+            setattr(jarq, name, fn)
+        return False
+
+
+def _run_scripted(table, K, tau):
+    rows = table.shape[0]
+    W = np.zeros((rows, 4))
+    W[:, 0] = np.arange(rows)
+    codes = np.zeros((rows, 4), dtype=np.uint8)
+    scales = np.zeros((rows, 2))
+    zeros = np.zeros((rows, 2), dtype=np.int32)
+    with _Scripted(table):
+        q, s, hist = jarq.refine(W, np.eye(4), codes, scales, zeros, 2, 3, K, tau=tau,
+                                 R=np.zeros((2, 2, 2)))
+    return q, s, hist
+
+
+def stopping_sweeps(hist, rows):
+    """Iteration at which each row stopped (None if it never did)."""
+    out = [None] * rows
+    was = np.ones(rows, dtype=bool)
+    for k, h in enumerate(hist, start=1):
+        for r in np.nonzero(was & ~h.active)[0]:
+            out[r] = k
+        was = h.active.copy()
+    return out
+
+
+def test_stopping_rule_on_hand_built_sequences():
+    q, s, hist = _run_scripted(STOP_TABLE, 4, STOP_TAU_EXACT)
+    assert stopping_sweeps(hist, STOP_TABLE.shape[0]) == STOP_EXPECT
+    for r, k_stop in enumerate(STOP_EXPECT):
+        k_last = 4 if k_stop is None else k_stop
+        # a stopped row keeps the scales of the iteration that stopped it and
+        # the codes of the iteration before (its code update is skipped)
+        assert np.all(s[r] == k_last), (r, s[r])
+        assert q[r, 1] == (4 if k_stop is None else k_stop - 1), (r, q[r])
+
+
+def test_stopping_rule_active_counts():
+    _, _, hist = _run_scripted(STOP_TABLE, 4, STOP_TAU_EXACT)
+    expect = [sum(1 for e in STOP_EXPECT if e is None or e > k) for k in range(1, 5)]
+    assert [int(h.active.sum()) for h in hist] == expect == [7, 3, 3, 2]
+
+
+def test_stop_rows_branches():
+    t = STOP_TAU_EXACT
+    # relative branch at exactly tau, and just above it (absolute branch silent)
+    assert jarq.stop_rows([_BIG], [_BIG - 16.0], t)[0]
+    assert not jarq.stop_rows([_BIG], [_BIG - 17.0], t)[0]
+    # absolute branch at exactly tau, relative decrease large
+    assert jarq.stop_rows([2.0 ** -10], [2.0 ** -10 - t], t)[0]
+    assert not jarq.stop_rows([2.0 ** -10], [2.0 ** -10 - 2 * t], t)[0]
+    # an increase stops; tau = 0 stops exactly on no decrease
+    assert jarq.stop_rows([1.0], [1.25], t)[0]
+    assert jarq.stop_rows([1.0], [1.0], 0.0)[0]
+    assert not jarq.stop_rows([1.0], [1.0 - 2.0 ** -40], 0.0)[0]
+
+
+def test_row_without_accepts_stops_at_the_next_iteration(tiny_layer):
+    """After an iteration that changes no code, L^(k) = L^(k-1) and the rule
+    stops the row (the remark after the proof of Theorem 1); with tau = 0 a
+    row stops exactly then, since every accepted proposal lowers F strictly."""
+    cfg, W, H32, H64, A, codes, scales, zeros = tiny_layer
+    g, bits, K = cfg.group_size, cfg.bits, 8
+    H = H32.astype(np.float64)
+    R = jarq.group_factors(H, g)
+    # the changes of every sweep without stopping
+    q, s = codes.copy(), scales.copy()
+    first_idle = [None] * cfg.rows
+    for k in range(1, K + 1):
+        s, _ = jarq.scale_step(W, H, q, zeros, g)
+        q_new = jarq.code_step(W, H, R, q, s, zeros, g, bits)
+        idle = np.all(q_new == q, axis=1)
+        for r in np.nonzero(idle)[0]:
+            if first_idle[r] is None:
+                first_idle[r] = k
+        q = q_new
+    _, _, hist = jarq.refine(W, H, codes, scales, zeros, g, bits, K, tau=0.0, R=R)
+    got = stopping_sweeps(hist, cfg.rows)
+    expect = [None if f is None or f + 1 > K else f + 1 for f in first_idle]
+    assert any(e is not None for e in expect)
+    assert got == expect

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 6
+#define JARQ_ABI_VERSION 7
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
  * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
  * 3 residual product U = E M^T, 4 row objectives and stopping test,
@@ -154,6 +154,18 @@ jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H,
                         uint8_t* codes, float* scales, const int32_t* zeros,
                         void* workspace, size_t workspace_bytes, void* stream,
                         jarq_stats* stats);
+
+/*
+ * Per-row outcome of the early-stopping rule (App. E.2, eq. (strict_stopping))
+ * in the last jarq_sweeps / jarq_refine call on this workspace: stop_sweep
+ * [rows] int32 (device, 4-byte aligned) receives, for every row, the
+ * iteration k >= 2 whose stopping test stopped it (the row kept that
+ * iteration's scales and skipped its code update), or 0 if the row ran every
+ * iteration (always 0 when tau < 0).  `p` must describe the same layer as that
+ * call.  Asynchronous (a device-to-device copy on `stream`).
+ */
+jarq_status jarq_stop_sweeps(const jarq_params* p, const void* workspace, size_t workspace_bytes,
+                             int32_t* stop_sweep, void* stream);
 
 /* jarq_prepare followed by jarq_sweeps. */
 jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H,

@@ -9,12 +9,12 @@ from .binding import (DEC_ACCEPT, DEC_REJECT, DEC_SKIP, DEC_STOPPED, EXPORTED, J
                       JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EWORKSPACE, JARQ_OK,
                       LIB_PATH, MAX_RECORDED_SWEEPS, JarqError, Params, Stats, abi_version,
                       alloc_workspace, code_step, load_library, make_params, objective, prepare,
-                      refine, scale_step, status_string, sweeps, workspace_bytes)
+                      refine, scale_step, status_string, stop_sweeps, sweeps, workspace_bytes)
 
 __all__ = [
     "DEC_ACCEPT", "DEC_REJECT", "DEC_SKIP", "DEC_STOPPED", "EXPORTED", "JARQ_EHIP",
     "JARQ_EINVAL", "JARQ_ENOT_SPD", "JARQ_ESCALE_SOLVE", "JARQ_EWORKSPACE", "JARQ_OK",
     "LIB_PATH", "MAX_RECORDED_SWEEPS", "JarqError", "Params", "Stats", "abi_version",
     "alloc_workspace", "code_step", "load_library", "make_params", "objective", "prepare",
-    "refine", "scale_step", "status_string", "sweeps", "workspace_bytes",
+    "refine", "scale_step", "status_string", "stop_sweeps", "sweeps", "workspace_bytes",
 ]

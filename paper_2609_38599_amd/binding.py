@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libjarq.so")
 MAX_RECORDED_SWEEPS = 64
 NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
 STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
-ABI_VERSION = 6
+ABI_VERSION = 7
 JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
@@ -82,6 +82,7 @@ _SIGNATURES = {
                                    ctypes.c_size_t, _vp, ctypes.POINTER(Stats)]),
     "jarq_objective": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                       ctypes.c_size_t, _vp, _vp]),
+    "jarq_stop_sweeps": (ctypes.c_int, [ctypes.POINTER(Params), _vp, ctypes.c_size_t, _vp, _vp]),
     "jarq_hessian_accumulate": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
                                                _vp, _vp]),
     "jarq_hessian_accumulate_bf16": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.c_int32,
@@ -252,6 +253,17 @@ def objective(p: Params, W, H, codes, scales, zeros, ws, out=None, stream=None):
                               _ptr(zeros, torch.int32, "zeros"),
                               _ptr(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream),
                               _ptr(out, torch.float64, "row_objective")), "jarq_objective")
+    return out
+
+
+def stop_sweeps(p: Params, ws, out=None, stream=None):
+    """Per row, the iteration at which the last sweeps call stopped it (0 = never)."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty(p.rows, dtype=torch.int32, device=ws.device)
+    _check(lib.jarq_stop_sweeps(ctypes.byref(p), _ptr(ws, torch.uint8, "workspace"), ws.numel(),
+                                _ptr(out, torch.int32, "stop_sweep"), _stream(stream)),
+           "jarq_stop_sweeps")
     return out
 
 

@@ -56,6 +56,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
   L.active = take(R);
+  L.stopat = take(R * sizeof(int32_t));
   L.rowmap = take(R * sizeof(int32_t));
   L.counters = take(sizeof(Counters));
   L.hist = take(JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord));
@@ -186,9 +187,10 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   return JARQ_OK;
 }
 
+// time_stages = false: no HIP events are created and stage_ms stays 0.
 jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
                         float* scales, const int32_t* zeros, void* ws, void* stream,
-                        jarq_stats* stats) {
+                        jarq_stats* stats, bool time_stages = true) {
   Ctx c = make_ctx(p, ws, stream);
   // Device-side input checks (codes in range, |zero point| <= 1024).
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
@@ -199,6 +201,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   if (f.bad_codes || f.bad_zeros) return JARQ_EINVAL;
 
   JQ_HIP(launch_fill_u8(c.st, c.active(), (size_t)c.rows, 1));
+  JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.stopat, (size_t)c.rows * sizeof(int32_t)));
   JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lcur, (size_t)c.rows * sizeof(double)));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lprev, (size_t)c.rows * sizeof(double)));
@@ -206,11 +209,11 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
 
   const int K = p->sweeps;
   const int nrec = K < JARQ_MAX_RECORDED_SWEEPS ? K : JARQ_MAX_RECORDED_SWEEPS;
-  std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t> ev;  // empty unless stages are timed
   // Events at the boundaries of the timed stages only (each one costs an
   // idle gap between kernels).
   const uint32_t all_stages = (1u << JARQ_NUM_STAGES) - 1u;
-  const uint32_t tmask = stats == nullptr ? 0u
+  const uint32_t tmask = (stats == nullptr || !time_stages) ? 0u
                          : (stats->stage_mask & all_stages) ? (stats->stage_mask & all_stages)
                                                              : all_stages;
   auto boundary_used = [&](int j) {
@@ -219,11 +222,13 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   if (stats != nullptr) {
     memset(stats, 0, sizeof(*stats));
     stats->stage_mask = tmask;
-    ev.resize((size_t)nrec * (JARQ_NUM_STAGES + 1));
-    for (auto& e : ev) JQ_HIP(hipEventCreate(&e));
+    if (tmask != 0u) {
+      ev.resize((size_t)nrec * (JARQ_NUM_STAGES + 1));
+      for (auto& e : ev) JQ_HIP(hipEventCreate(&e));
+    }
   }
   auto mark = [&](int k, int j) -> hipError_t {
-    if (stats == nullptr || k >= nrec || !boundary_used(j)) return hipSuccess;
+    if (tmask == 0u || k >= nrec || !boundary_used(j)) return hipSuccess;
     return hipEventRecord(ev[(size_t)k * (JARQ_NUM_STAGES + 1) + j], c.st);
   };
   jarq_status status = JARQ_OK;
@@ -253,7 +258,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
       e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
     if (e == hipSuccess)
       e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
-                            (double*)(c.ws + c.lay.lprev), c.active(), k + 1, p->tau, rmap,
+                            (double*)(c.ws + c.lay.lprev), c.active(),
+                            (int32_t*)(c.ws + c.lay.stopat), k + 1, p->tau, rmap,
                             (uint32_t*)(c.ws + c.lay.pcount), pcount_words(c.cols, c.g));
     if (e == hipSuccess) e = mark(k, 5);
     if (e == hipSuccess)
@@ -300,9 +306,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   }
   if (stats != nullptr) {
     stats->sweeps_run = run;
-    std::vector<SweepRecord> hist(JARQ_MAX_RECORDED_SWEEPS);
-    if (hipMemcpy(hist.data(), c.hist(), hist.size() * sizeof(SweepRecord),
-                  hipMemcpyDeviceToHost) == hipSuccess) {
+    SweepRecord hist[JARQ_MAX_RECORDED_SWEEPS];
+    if (hipMemcpy(hist, c.hist(), sizeof(hist), hipMemcpyDeviceToHost) == hipSuccess) {
       const int n = run < nrec ? run : nrec;
       for (int k = 0; k < n; ++k) {
         stats->objective_after_scales[k] = hist[k].objective_after_scales;
@@ -421,6 +426,18 @@ jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H, ui
   s = sweeps_impl(p, W, H, codes, scales, zeros, workspace, stream, stats);
   if (stats != nullptr) stats->prep_ms = prep_ms;
   return s;
+}
+
+jarq_status jarq_stop_sweeps(const jarq_params* p, const void* workspace, size_t workspace_bytes,
+                             int32_t* stop_sweep, void* stream) {
+  if (!valid_params(p) || !aligned(stop_sweep, 4)) return JARQ_EINVAL;
+  jarq_status s = check_ws(p, workspace, workspace_bytes);
+  if (s != JARQ_OK) return s;
+  const Layout lay = make_layout(p->rows, p->cols, p->group_size);
+  JQ_HIP(hipMemcpyAsync(stop_sweep, (const char*)workspace + lay.stopat,
+                        (size_t)p->rows * sizeof(int32_t), hipMemcpyDeviceToDevice,
+                        (hipStream_t)stream));
+  return JARQ_OK;
 }
 
 jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,

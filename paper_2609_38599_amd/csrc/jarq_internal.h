@@ -83,6 +83,7 @@ struct Layout {
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64
   size_t active;    // [rows] u8
+  size_t stopat;    // [rows] i32: iteration at which the row stopped, 0 while it has not
   size_t rowmap;    // [rows] i32: row of each position of the sweep (rows still active, ascending)
   size_t counters;  // Counters
   size_t hist;      // [64] SweepRecord
@@ -181,9 +182,10 @@ hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* 
                                 double* out);
 
 // Also zeroes zero_words[0 .. nzero) (nzero <= 256) before any row is handled.
+// A row that stops gets stopat[row] = sweep.
 hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
-                             double* lcur, double* lprev, uint8_t* active, int sweep,
-                             float tau, const int32_t* rowmap, uint32_t* zero_words,
+                             double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
+                             int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
                              int nzero);
 
 hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);

@@ -24,10 +24,11 @@ hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* 
 // L_j^(k) = sum of the partials; at k >= 2 an active row stops (before its
 // code update) when (L^(k-1) - L^(k)) / max(|L^(k-1)|, eps) <= tau or
 // |L^(k-1) - L^(k)| <= tau (App. E.2, eq. (strict_stopping)).  The new scales
-// are kept.
+// are kept, and the iteration is recorded in stopat.
 __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part,
                                   double* __restrict__ lcur, double* __restrict__ lprev,
-                                  uint8_t* __restrict__ active, int sweep, float tau,
+                                  uint8_t* __restrict__ active, int32_t* __restrict__ stopat,
+                                  int sweep, float tau,
                                   const int32_t* __restrict__ rowmap,
                                   uint32_t* __restrict__ zero_words, int nzero) {
   // the code update's per-panel row counters start the sweep at zero
@@ -43,18 +44,21 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
     const double prev = lprev[r];
     const double dec = prev - s;
     const double rel = dec / fmax(fabs(prev), (double)kFp32Eps);
-    if (rel <= (double)tau || fabs(dec) <= (double)tau) active[r] = 0;
+    if (rel <= (double)tau || fabs(dec) <= (double)tau) {
+      active[r] = 0;
+      stopat[r] = sweep;
+    }
   }
   lprev[r] = s;
 }
 
 hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpart,
-                             double* lcur, double* lprev, uint8_t* active, int sweep,
-                             float tau, const int32_t* rowmap, uint32_t* zero_words,
+                             double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
+                             int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
                              int nzero) {
   if (n <= 0 || nzero < 0 || nzero > 256) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stop_check_kernel, dim3((n + 255) / 256), dim3(256), 0, st, n, nt,
-                     objpart, lcur, lprev, active, sweep, tau, rowmap, zero_words, nzero);
+                     objpart, lcur, lprev, active, stopat, sweep, tau, rowmap, zero_words, nzero);
   return hipGetLastError();
 }
 

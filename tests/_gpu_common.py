@@ -10,7 +10,7 @@ import torch
 
 import paper_2609_38599_amd as jq
 from oracle import hosts, jarq
-from oracle.replay import replay_code_step
+from oracle.replay import forced_refine, replay_code_step
 from synth import CONFIGS, make_hessian, make_weights, rtn_quantize
 
 SCALE_RTOL = 1e-4          # scales within 1e-4 relative (parity bar)
@@ -134,5 +134,54 @@ def rel(a, b):
     return abs(a - b) / max(abs(b), 1e-300)
 
 
+def traced_sweeps(gl, K, rows=None):
+    """K sweeps of the step entry points on a GpuLayer, with traces.
+
+    Returns per sweep the proposals and decisions (restricted to `rows` if
+    given) and the state (codes, scales) after every sweep, states[0] being
+    the start.  The step entry points run the same kernels as jarq_sweeps
+    with every row active."""
+    sel = slice(None) if rows is None else rows
+    cands, decs = [], []
+    q, s = gl.state()
+    states = [(q[sel].copy(), s[sel].copy())]
+    for _ in range(K):
+        gl.scale_step()
+        cand, dec = gl.code_step()
+        cands.append(cand[sel].copy())
+        decs.append(dec[sel].copy())
+        q, s = gl.state()
+        states.append((q[sel].copy(), s[sel].copy()))
+    return cands, decs, states
+
+
+def check_forced(W, H, R, q0, s0, z, g, bits, K, cands, decs, q_gpu, s_gpu, label="",
+                 tau=None, stop_at=None, rows_active=None):
+    """The oracle's own K iterations, deferring to the GPU only inside the bands
+    (oracle.replay.forced_refine), must reach the GPU's codes exactly and each
+    row's final objective within OBJ_RTOL; at most EXEMPT_FRAC of the proposal
+    positions may be deferred."""
+    qf, sf, rep = forced_refine(W, H, q0, s0, z, g, bits, K, cands, decs, tau=tau,
+                                stop_at=stop_at, R=R)
+    F_gpu = jarq.objective_rows(W, H, q_gpu, s_gpu, z, g)
+    F_f = jarq.objective_rows(W, H, qf, sf, z, g)
+    row_rel = np.abs(F_gpu - F_f) / np.maximum(np.abs(F_f), 1e-300)
+    forced = rep.code_forced + rep.decision_forced + rep.stop_forced
+    say(f"[forced{label}] {rep.sweeps} sweeps, positions {rep.n_codes}: deferred codes "
+        f"{rep.code_forced} decisions {rep.decision_forced} stops {rep.stop_forced} of {rep.n_stops}; "
+        f"mismatches codes {rep.code_mismatch} decisions {rep.decision_mismatch} "
+        f"skips {rep.skip_mismatch} stops {rep.stop_mismatch}; codes equal "
+        f"{np.array_equal(qf, q_gpu)}; F rel total {rel(F_gpu.sum(), F_f.sum()):.2e} "
+        f"worst row {float(np.max(row_rel)):.2e}")
+    assert rep.ok, rep
+    assert forced <= max(1, EXEMPT_FRAC * rep.n_codes), rep
+    assert np.array_equal(qf, q_gpu)
+    assert np.all(row_rel <= OBJ_RTOL), float(np.max(row_rel))
+    if rows_active is not None:
+        assert [int(a.sum()) for a in rep.active][:len(rows_active)] == list(rows_active)
+    return rep
+
+
 __all__ = ["jq", "jarq", "torch", "np", "CONFIGS", "layer", "random_layer", "GpuLayer",
-           "check_scales", "check_code_step", "rel", "say", "OBJ_RTOL", "to_dev"]
+           "check_scales", "check_code_step", "check_forced", "traced_sweeps", "rel", "say",
+           "OBJ_RTOL", "to_dev"]

@@ -3,10 +3,15 @@
 Per stage: the objective, the scale step (scales within 1e-4 relative) and the
 code step checked decision by decision against the oracle conditioned on the
 GPU's earlier decisions (codes identical except within 1e-4 of a rounding
-boundary, at most 0.1% of codes).  End to end: K free-running sweeps, final
-objective within 1e-5 relative.  Shapes cover several tiles with ragged
-tails, every group size and bit width, the degenerate cases of the method,
-and the full-size layers (checked on sampled rows, rows being independent).
+boundary, at most 0.1% of codes).  End to end: K sweeps, final objective
+within 1e-5 relative; on the small layers against the free-running oracle, on
+the full-size layers and with early stopping against the oracle's own K
+iterations that defer to the GPU only at decisions inside those bands (a
+single near-boundary split changes every later decision of a row, so the
+free-running comparison there is reported, not asserted).  Shapes cover
+several tiles with ragged tails, every group size and bit width, the
+degenerate cases of the method, and the full-size layers (checked on sampled
+rows, rows being independent).
 """
 
 import numpy as np
@@ -14,8 +19,9 @@ import pytest
 import torch
 
 from synth import rtn_quantize
-from tests._gpu_common import (CONFIGS, OBJ_RTOL, GpuLayer, check_code_step, check_scales, jarq,
-                               jq, layer, random_layer, rel, say)
+from tests._gpu_common import (CONFIGS, OBJ_RTOL, GpuLayer, check_code_step, check_forced,
+                               check_scales, jarq, jq, layer, random_layer, rel, say,
+                               traced_sweeps)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -145,22 +151,44 @@ def test_refine_entry_equals_prepare_plus_sweeps():
     assert np.array_equal(qa, qb) and np.array_equal(sa, sb)
 
 
-def test_early_stopping_tiny():
-    cfg, W, H, q, s, z = layer(0)
-    g, bits = cfg.group_size, cfg.bits
-    tau = 1e-5
-    gl = GpuLayer(W, H, q, s, z, g, bits, sweeps=12, tau=tau)
+def _check_stopping_run(W, H, q, s, z, g, bits, K, tau, label):
+    """Early stopping on the GPU against the oracle.
+
+    A row that stops at iteration k holds the scales of iteration k and the
+    codes of iteration k - 1, and rows are independent, so each row of the
+    stopping run (jarq_sweeps) must equal, bit for bit, the same row of a run
+    without stopping (the traced step entry points) cut at the iteration
+    jarq_stop_sweeps reports.  The oracle then runs its own K iterations with
+    the stopping rule, deferring to the GPU only inside the bands: its codes
+    must equal the GPU's, every row's objective must agree within 1e-5, and
+    the number of active rows must agree in every sweep."""
+    rows = W.shape[0]
+    R = jarq.group_factors(H, g)
+    tr = GpuLayer(W, H, q, s, z, g, bits)
+    cands, decs, states = traced_sweeps(tr, K)
+    del tr
+    gl = GpuLayer(W, H, q, s, z, g, bits, sweeps=K, tau=tau)
     st = jq.sweeps(gl.p, gl.W, gl.H, gl.codes, gl.scales, gl.zeros, gl.ws)
     qg, sg = gl.state()
-    qo, so, hist = jarq.refine(W, H, q, s, z, g, bits, 12, tau=tau)
-    act_o = [int(h.active.sum()) for h in hist]
-    say(f"[early stop] gpu active {st['rows_active']} oracle {act_o}")
-    n = min(len(act_o), st["sweeps_run"])
-    for k in range(n):
-        assert abs(st["rows_active"][k] - act_o[k]) <= 2
-    F_gpu = jarq.objective_rows(W, H, qg, sg, z, g).sum()
-    F_or = jarq.objective_rows(W, H, qo, so, z, g).sum()
-    assert rel(F_gpu, F_or) <= 1e-4
+    stop_at = jq.stop_sweeps(gl.p, gl.ws).cpu().numpy()
+    say(f"[stopping{label}] gpu active per sweep {st['rows_active']}, stopped rows "
+        f"{int(np.count_nonzero(stop_at))} of {rows}")
+    assert np.all((stop_at == 0) | ((stop_at >= 2) & (stop_at <= st["sweeps_run"])))
+    for r in range(rows):
+        k = int(stop_at[r])
+        qk = states[k - 1][0][r] if k else states[K][0][r]
+        sk = states[k][1][r] if k else states[K][1][r]
+        assert np.array_equal(qg[r], qk), (r, k)
+        assert np.array_equal(sg[r].view(np.uint32), sk.view(np.uint32)), (r, k)
+    check_forced(W, H, R, q, s, z, g, bits, K, cands, decs, qg, sg, label, tau=tau,
+                 stop_at=stop_at, rows_active=st["rows_active"])
+    return st, qg, sg
+
+
+def test_early_stopping_tiny():
+    cfg, W, H, q, s, z = layer(0)
+    st, _, _ = _check_stopping_run(W, H, q, s, z, cfg.group_size, cfg.bits, 12, 1e-5, " tiny")
+    assert st["rows_active_end"] < cfg.rows
 
 
 def test_active_set_compaction_is_exact():
@@ -171,10 +199,7 @@ def test_active_set_compaction_is_exact():
     # at spread-out sweeps here (300 active for three sweeps, 62 at the end).
     W, H, q, s, z = random_layer(300, 512, 64, 3, seed=7)
     K, tau = 8, 1e-5
-    full = GpuLayer(W, H, q, s, z, 64, 3, sweeps=K, tau=tau)
-    st = jq.sweeps(full.p, full.W, full.H, full.codes, full.scales, full.zeros, full.ws)
-    qf, sf = full.state()
-    say(f"[compaction] active per sweep {st['rows_active']}")
+    st, qf, sf = _check_stopping_run(W, H, q, s, z, 64, 3, K, tau, " compaction")
     assert st["rows_active"][0] == 300 and st["rows_active"][-1] < 150
     for lo, hi in ((0, 97), (97, 228), (228, 300)):
         part = GpuLayer(W[lo:hi], H, q[lo:hi], s[lo:hi], z[lo:hi], 64, 3, sweeps=K, tau=tau)
@@ -182,14 +207,6 @@ def test_active_set_compaction_is_exact():
         qp, sp = part.state()
         assert np.array_equal(qp, qf[lo:hi]), (lo, hi)
         assert np.array_equal(sp.view(np.uint32), sf[lo:hi].view(np.uint32)), (lo, hi)
-    qo, so, hist = jarq.refine(W, H, q, s, z, 64, 3, K, tau=tau)
-    act_o = [int(h.active.sum()) for h in hist]
-    say(f"[compaction] oracle active per sweep {act_o}")
-    for k in range(min(len(act_o), st["sweeps_run"])):
-        assert abs(st["rows_active"][k] - act_o[k]) <= 3
-    F_gpu = jarq.objective_rows(W, H, qf, sf, z, 64).sum()
-    F_or = jarq.objective_rows(W, H, qo, so, z, 64).sum()
-    assert rel(F_gpu, F_or) <= 1e-4
 
 
 # --------------------------------------------------------------------------
@@ -369,10 +386,12 @@ def test_full_size_layer(cfg_id):
     (the same kernels as jarq_sweeps).  For the sampled rows, each sweep's
     scales are compared with the oracle's scale step on the GPU's codes and each
     sweep's decisions are replayed by the oracle conditioned on the GPU's
-    earlier decisions.  A row whose free-running trajectory leaves the
-    oracle's does so at a decision within the rounding band, which the replay
-    allows; the objective bar is applied to rows whose trajectories agree, and
-    the total difference is reported.
+    earlier decisions.  End to end, the oracle runs its own K iterations from
+    the host state and defers to the GPU only at decisions inside the rounding
+    and accept bands: it must reach the GPU's codes exactly and every sampled
+    row's final objective within 1e-5 relative.  The free-running oracle
+    (which leaves the GPU's trajectory at the first such decision) is
+    reported for information.
     """
     cfg, W, H, q, s, z = layer(cfg_id)
     g, bits, K = cfg.group_size, cfg.bits, cfg.sweeps
@@ -381,6 +400,7 @@ def test_full_size_layer(cfg_id):
     R = jarq.group_factors(H, g)
     gl = GpuLayer(W, H, q, s, z, g, bits, sweeps=1)
     exempt = positions = 0
+    cands, decs = [], []
     for k in range(K):
         qk, _ = gl.state()
         gl.scale_step()
@@ -391,6 +411,8 @@ def test_full_size_layer(cfg_id):
         cand, dec = gl.code_step()
         rep = check_code_step(W[wide], H, R, qk[wide], sk[wide], z[wide], g, bits, cand[wide],
                               dec[wide], f" cfg{cfg_id} sweep {k + 1}")
+        cands.append(cand[wide].copy())
+        decs.append(dec[wide].copy())
         exempt += rep.code_exempt + rep.decision_exempt
         positions += rep.n_codes
     qt, st_ = gl.state()
@@ -406,18 +428,19 @@ def test_full_size_layer(cfg_id):
     say(f"[cfg{cfg_id}] accepted {st['accepted_groups']} stage ms {st['stage_ms'][-1]}")
     del gk
     torch.cuda.empty_cache()
-    # free-running oracle on the same rows
-    qo, so, _ = jarq.refine(W[wide], H, q[wide], s[wide], z[wide], g, bits, K, R=R)
+    # end to end on the GPU's trajectory: the oracle deferring only inside the bands
+    check_forced(W[wide], H, R, q[wide], s[wide], z[wide], g, bits, K, cands, decs,
+                 qg[wide], sg[wide], f" cfg{cfg_id}")
     F_gpu = jarq.objective_rows(W[wide], H, qg[wide], sg[wide], z[wide], g)
+    # free-running oracle on the same rows, for information
+    qo, so, _ = jarq.refine(W[wide], H, q[wide], s[wide], z[wide], g, bits, K, R=R)
     F_or = jarq.objective_rows(W[wide], H, qo, so, z[wide], g)
     same = np.all(qg[wide] == qo, axis=1)
-    say(f"[cfg{cfg_id}] {wide.size} rows, {int((~same).sum())} on another trajectory "
-        f"(band exemptions over the {K} sweeps: {exempt} of {positions} positions); "
+    say(f"[cfg{cfg_id}] free-running oracle: {wide.size} rows, {int((~same).sum())} on another "
+        f"trajectory (band exemptions over the {K} sweeps: {exempt} of {positions} positions); "
         f"F rel all rows {rel(F_gpu.sum(), F_or.sum()):.2e} "
         f"(gpu {'lower' if F_gpu.sum() <= F_or.sum() else 'higher'}), "
         f"agreeing rows {rel(F_gpu[same].sum(), F_or[same].sum()):.2e}")
-    assert same.sum() >= 0.8 * wide.size
-    assert rel(F_gpu[same].sum(), F_or[same].sum()) <= OBJ_RTOL
     assert np.all(np.abs(F_dev[wide] - F_gpu) <= OBJ_RTOL * F_gpu)
     L = st["objective_after_scales"]
     assert all(L[k + 1] <= L[k] * (1 + 1e-6) for k in range(len(L) - 1))

@@ -64,7 +64,9 @@ typedef enum jarq_status {
   JARQ_ENOT_SPD = 2,      /* some diagonal block H_ii is not positive definite (eq. (9)) */
   JARQ_ESCALE_SOLVE = 3,  /* a row's Gram matrix failed Cholesky after the ridge (App. E.2) */
   JARQ_EHIP = 4,          /* a HIP runtime call or kernel launch failed */
-  JARQ_EWORKSPACE = 5     /* workspace missing, too small or misaligned */
+  JARQ_EWORKSPACE = 5,    /* workspace missing, too small or misaligned */
+  JARQ_ESTATIC_LIMIT = 6  /* jarq_refine_static: the layer needs more than
+                             JARQ_STATIC_WORKSPACE_BYTES of workspace */
 } jarq_status;
 
 /* Problem description.  Sizes are those of eq. (1). */
@@ -172,6 +174,28 @@ jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H,
                         uint8_t* codes, float* scales, const int32_t* zeros,
                         void* workspace, size_t workspace_bytes, void* stream,
                         jarq_stats* stats);
+
+/*
+ * jarq_refine without a workspace argument, for callers that cannot allocate
+ * device memory (code under graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same kernels run on a workspace that the
+ * library holds in a static device array of JARQ_STATIC_WORKSPACE_BYTES
+ * (384 MiB; enough for a 4096 x 4096 layer at g = 128), created on each GPU
+ * the library runs on and held until the process ends.  The call allocates
+ * nothing: no hipMalloc, no hipFree, no HIP event.  Layers whose
+ * jarq_workspace_bytes exceeds the limit are rejected with
+ * JARQ_ESTATIC_LIMIT before anything is enqueued.  Results are those of
+ * jarq_refine on the same inputs; stats (nullable) is filled the same way
+ * except that no stage is timed (stage_ms and prep_ms are 0).  Every call on
+ * one GPU uses that GPU's single array, which keeps the previous call's
+ * contents (each call overwrites what it reads): calls that overlap on one
+ * GPU, from any stream or thread, race and must be serialised by the caller.
+ * Synchronises `stream`.
+ */
+#define JARQ_STATIC_WORKSPACE_BYTES (384u << 20)
+jarq_status jarq_refine_static(const jarq_params* p, const float* W, const float* H,
+                               uint8_t* codes, float* scales, const int32_t* zeros, void* stream,
+                               jarq_stats* stats);
 
 /*
  * Layer objective eq. (4) in the Hessian form for the given state:

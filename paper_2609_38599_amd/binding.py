@@ -19,7 +19,9 @@ MAX_RECORDED_SWEEPS = 64
 NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
 STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
 ABI_VERSION = 7
-JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE = range(6)
+(JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE,
+ JARQ_ESTATIC_LIMIT) = range(7)
+STATIC_WORKSPACE_BYTES = 384 << 20
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
 
@@ -80,6 +82,8 @@ _SIGNATURES = {
                                    ctypes.c_size_t, _vp, ctypes.POINTER(Stats)]),
     "jarq_refine": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                    ctypes.c_size_t, _vp, ctypes.POINTER(Stats)]),
+    "jarq_refine_static": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                          ctypes.POINTER(Stats)]),
     "jarq_objective": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                       ctypes.c_size_t, _vp, _vp]),
     "jarq_stop_sweeps": (ctypes.c_int, [ctypes.POINTER(Params), _vp, ctypes.c_size_t, _vp, _vp]),
@@ -240,6 +244,21 @@ def refine(p: Params, W, H, codes, scales, zeros, ws, stream=None, want_stats=Tr
                              ctypes.byref(st) if st is not None else None)
     if check:
         _check(status, "jarq_refine")
+    return (st.to_dict() if st is not None else None) if check else (status, st)
+
+
+def refine_static(p: Params, W, H, codes, scales, zeros, stream=None, want_stats=True,
+                  check=True):
+    """jarq_refine_static: jarq_refine on the library's static workspace (no allocation)."""
+    lib = load_library()
+    st = Stats() if want_stats else None
+    status = lib.jarq_refine_static(ctypes.byref(p), _ptr(W, torch.float32, "W"),
+                                    _ptr(H, torch.float32, "H"), _ptr(codes, torch.uint8, "codes"),
+                                    _ptr(scales, torch.float32, "scales"),
+                                    _ptr(zeros, torch.int32, "zeros"), _stream(stream),
+                                    ctypes.byref(st) if st is not None else None)
+    if check:
+        _check(status, "jarq_refine_static")
     return (st.to_dict() if st is not None else None) if check else (status, st)
 
 

@@ -3,6 +3,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "jarq.h"
@@ -338,6 +339,35 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
 
 }  // namespace
 
+// ---- workspace for callers that cannot allocate (jarq_refine_static) ----
+// One array per GPU, created with the code object on each device and held
+// until the process ends.  Host code never uses the array's name as an
+// address: the device address comes from hipGetSymbolAddress, once per
+// device, with that device current.
+static __device__ __align__(256) unsigned char scratch[JARQ_STATIC_WORKSPACE_BYTES];
+
+namespace {
+
+constexpr int kMaxStaticDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxStaticDevices];
+
+jarq_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxStaticDevices) return JARQ_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr)
+      return JARQ_EHIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return JARQ_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t jarq_workspace_bytes(const jarq_params* p) {
@@ -438,6 +468,22 @@ jarq_status jarq_stop_sweeps(const jarq_params* p, const void* workspace, size_t
                         (size_t)p->rows * sizeof(int32_t), hipMemcpyDeviceToDevice,
                         (hipStream_t)stream));
   return JARQ_OK;
+}
+
+jarq_status jarq_refine_static(const jarq_params* p, const float* W, const float* H,
+                               uint8_t* codes, float* scales, const int32_t* zeros, void* stream,
+                               jarq_stats* stats) {
+  if (!valid_params(p) || !aligned(W, 16) || !aligned(H, 16) || !aligned(codes, 16) ||
+      !aligned(scales, 16) || !aligned(zeros, 4))
+    return JARQ_EINVAL;
+  if (make_layout(p->rows, p->cols, p->group_size).total > (size_t)JARQ_STATIC_WORKSPACE_BYTES)
+    return JARQ_ESTATIC_LIMIT;
+  void* ws = nullptr;
+  jarq_status s = static_scratch(&ws);
+  if (s != JARQ_OK) return s;
+  s = prepare_impl(p, W, H, ws, stream);
+  if (s != JARQ_OK) return s;
+  return sweeps_impl(p, W, H, codes, scales, zeros, ws, stream, stats, /*time_stages=*/false);
 }
 
 jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,
@@ -631,6 +677,8 @@ const char* jarq_status_string(jarq_status s) {
     case JARQ_ESCALE_SOLVE: return "a scale solve failed after the ridge";
     case JARQ_EHIP: return "HIP runtime error";
     case JARQ_EWORKSPACE: return "workspace missing, too small or misaligned";
+    case JARQ_ESTATIC_LIMIT:
+      return "layer needs more workspace than the static scratch of jarq_refine_static";
     default: return "unknown status";
   }
 }

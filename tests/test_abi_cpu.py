@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_abi_version_and_status_strings(lib):
     assert binding.abi_version() == binding.ABI_VERSION == 7
-    for s in range(6):
+    for s in range(7):
         assert binding.status_string(s)
     assert binding.status_string(99) == "unknown status"
 
@@ -82,6 +82,23 @@ def test_argument_errors_return_before_any_launch(lib):
                               None) == binding.JARQ_EINVAL
     assert lib.jarq_refine(None, fake, fake, fake, fake, fake, fake, 1 << 30, None, None) == binding.JARQ_EINVAL
     del P
+
+
+def test_static_refine_rejects_before_any_launch(lib):
+    fake = _vp(1 << 20)          # aligned, never dereferenced
+    big = binding.make_params(4096, 11008, 128, 3, 10)
+    assert binding.workspace_bytes(big) > binding.STATIC_WORKSPACE_BYTES
+    assert lib.jarq_refine_static(ctypes.byref(big), fake, fake, fake, fake, fake, None,
+                                  None) == binding.JARQ_ESTATIC_LIMIT
+    bad = binding.make_params(64, 250, 64, 3, 5)
+    assert lib.jarq_refine_static(ctypes.byref(bad), fake, fake, fake, fake, fake, None,
+                                  None) == binding.JARQ_EINVAL
+    p = binding.make_params(64, 256, 64, 3, 5)
+    assert lib.jarq_refine_static(ctypes.byref(p), fake, fake, _vp((1 << 20) + 4), fake, fake,
+                                  None, None) == binding.JARQ_EINVAL
+    # the headline layer fits
+    assert binding.workspace_bytes(binding.make_params(4096, 4096, 128, 3, 10)) <= \
+        binding.STATIC_WORKSPACE_BYTES
 
 
 def test_setup_entry_points_check_arguments(lib):

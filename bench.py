@@ -71,7 +71,8 @@ def stage_work(cfg, rows, corr_blocks):
         "esplit": 0.0,
         "residual": 3 * 2.0 * rows * d * d,                 # three fp16 products of U = E M^T
         "objective": 2.0 * rows * d * g / 2.0,              # (R_i e_i) per group, triangular
-        "code": 2.0 * rows * d * g + 2.0 * 16 * g * g * 2 * corr_blocks,
+        "babai": 2.0 * rows * d * g + 2.0 * 16 * g * g * 2 * corr_blocks,
+        "panel": 0.0,                                       # in proportion to the rows that changed
     }
 
 
@@ -410,6 +411,9 @@ def main():
         "prep_ms": prep_ms,
         "stage_ms": stage_ms,
         "stage_ms_note": "separate untimed run of the same sweeps with HIP events around every stage",
+        "stage_ms_per_sweep": {name: [round(stb["stage_ms"][k][j], 5) for k in range(n)]
+                               for j, name in enumerate(STAGE_NAMES)},
+        "gram_listed": stb["gram_listed"][:n],
         "accepted_groups": st["accepted_groups"][:n],
         "rows_active": st["rows_active"][:n],
         "sweeps_run": st["sweeps_run"],

@@ -50,12 +50,14 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 7
+#define JARQ_ABI_VERSION 8
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
  * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
  * 3 residual product U = E M^T, 4 row objectives and stopping test,
- * 5 code update (Babai kernels and panel updates). */
-#define JARQ_NUM_STAGES 6
+ * 5 code update: the Babai kernels (one per panel of groups), 6 code update:
+ * the panel updates between them.  Stages 5 and 6 interleave; each of their
+ * launches is timed on its own. */
+#define JARQ_NUM_STAGES 7
 #define JARQ_MAX_RECORDED_SWEEPS 64
 
 typedef enum jarq_status {
@@ -101,6 +103,8 @@ typedef struct jarq_stats {
   int32_t ridge_rows[JARQ_MAX_RECORDED_SWEEPS];              /* stabilised scale solves */
   int32_t rows_active[JARQ_MAX_RECORDED_SWEEPS];             /* rows that ran the code update */
   int64_t correction_blocks[JARQ_MAX_RECORDED_SWEEPS];      /* 16-row x g x g correction products run */
+  int32_t gram_listed[JARQ_MAX_RECORDED_SWEEPS];            /* 1: only the Gram entries of groups the
+                                                               last code update changed were formed */
   float stage_ms[JARQ_MAX_RECORDED_SWEEPS][JARQ_NUM_STAGES]; /* HIP-event ms per stage, see JARQ_NUM_STAGES */
   float prep_ms;                                             /* jarq_refine only */
 } jarq_stats;
@@ -151,6 +155,12 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
  * changed).  Synchronises `stream` before returning.  `stats` [host] may be
  * NULL.  Returns JARQ_ESCALE_SOLVE if any row's solve failed after the ridge
  * (that row keeps its previous scales).
+ * From the second sweep on, the Gram matrices of (b) are formed only for the
+ * groups whose codes the previous sweep changed when that is cheaper (entry
+ * (a, h) depends on the codes of groups a and h alone, eq. (5)); the entries
+ * are bit-identical to a full build.  With early stopping the set of active
+ * rows stays on the device; the host looks at it every fourth sweep and stops
+ * launching once no row is left.
  */
 jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H,
                         uint8_t* codes, float* scales, const int32_t* zeros,

@@ -16,9 +16,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libjarq.so")
 
 MAX_RECORDED_SWEEPS = 64
-NUM_STAGES = 6           # Gram, scale solve, E split, residual product, objective, code update
-STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "code")
-ABI_VERSION = 7
+NUM_STAGES = 7           # Gram, scale solve, E split, residual product, objective, Babai, panel update
+STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "babai", "panel")
+ABI_VERSION = 8
 (JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE,
  JARQ_ESTATIC_LIMIT) = range(7)
 STATIC_WORKSPACE_BYTES = 384 << 20
@@ -49,6 +49,7 @@ class Stats(ctypes.Structure):
                 ("ridge_rows", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
                 ("rows_active", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
                 ("correction_blocks", ctypes.c_int64 * MAX_RECORDED_SWEEPS),
+                ("gram_listed", ctypes.c_int32 * MAX_RECORDED_SWEEPS),
                 ("stage_ms", (ctypes.c_float * NUM_STAGES) * MAX_RECORDED_SWEEPS),
                 ("prep_ms", ctypes.c_float)]
 
@@ -65,6 +66,7 @@ class Stats(ctypes.Structure):
             "ridge_rows": [self.ridge_rows[k] for k in range(n)],
             "rows_active": [self.rows_active[k] for k in range(n)],
             "correction_blocks": [self.correction_blocks[k] for k in range(n)],
+            "gram_listed": [self.gram_listed[k] for k in range(n)],
             "stage_ms": [list(self.stage_ms[k]) for k in range(n)],
             "prep_ms": self.prep_ms,
         }

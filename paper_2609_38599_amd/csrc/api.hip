@@ -58,6 +58,11 @@ Layout make_layout(int rows, int cols, int g) {
   L.lprev = take(R * sizeof(double));
   L.active = take(R);
   L.stopat = take(R * sizeof(int32_t));
+  L.chg = take(R * G);
+  L.glist = take(G * R * sizeof(int32_t));
+  L.gcount = take(G * sizeof(uint32_t));
+  L.gctl = take(sizeof(GramCtl));
+  L.sctl = take(sizeof(SweepCtl));
   L.rowmap = take(R * sizeof(int32_t));
   L.counters = take(sizeof(Counters));
   L.hist = take(JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord));
@@ -115,7 +120,12 @@ struct Ctx {
   float* gram() const { return (float*)(ws + lay.gram); }
   float* pbuf() const { return (float*)(ws + lay.p); }
   double* objpart() const { return (double*)(ws + lay.objpart); }
+  uint8_t* chg() const { return (uint8_t*)(ws + lay.chg); }
+  GramCtl* gctl() const { return (GramCtl*)(ws + lay.gctl); }
+  SweepCtl* sctl() const { return (SweepCtl*)(ws + lay.sctl); }
+  uint32_t* gcount() const { return (uint32_t*)(ws + lay.gcount); }
   int nt() const { return (cols + kObjTile - 1) / kObjTile; }
+  int panels() const { return pcount_words(cols, g); }
 };
 
 Ctx make_ctx(const jarq_params* p, void* ws, void* stream) {
@@ -135,36 +145,49 @@ hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes
                               const int32_t* zeros, const uint8_t* active, float lam,
                               float rcond, int accept) {
   (void)H;
-  hipError_t e =
-      launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(), nullptr);
+  hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(),
+                             nullptr, nullptr, /*incremental=*/false);
   if (e != hipSuccess) return e;
   return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, active,
-                      c.cnt(), c.flags(), lam, rcond, accept, nullptr);
+                      c.cnt(), c.flags(), lam, rcond, accept, nullptr, nullptr);
 }
+
+struct NoHook {
+  hipError_t operator()(int, int, int) const { return hipSuccess; }
+};
 
 // The Gauss-Seidel code update, panel by panel: each panel's groups are
 // decoded in order by the Babai kernel, then their accepted changes are folded
 // into the residual product of every later column.  `n` positions of the
-// sweep, position p holding layer row map_row(rowmap, p).
-// The per-panel row counters must be zero when the first Babai launch runs:
-// zeroed here unless the caller's previous launch did (counts_zeroed).
-hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const float* H,
+// sweep at most (the current count in *n_dev when it is not null), position p
+// holding layer row map_row(rowmap, p).  The per-panel row counters must be
+// zero when the first Babai launch runs: zeroed here unless the caller's
+// previous launch did (counts_zeroed).  hook(kind, panel, phase) runs before
+// (phase 0) and after (phase 1) each launch: kind 0 Babai, 1 panel update.
+template <typename Hook = NoHook>
+hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const int* n_dev,
                          uint8_t* codes, const float* scales, const int32_t* zeros,
                          const uint8_t* active, uint8_t* cand, uint8_t* decision,
-                         bool counts_zeroed = false) {
-  (void)H;
+                         bool counts_zeroed = false, Hook hook = Hook()) {
   const int nb = panel_groups(c.g);
   if (!counts_zeroed) {
-    hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, pcount_words(c.cols, c.g) * sizeof(uint32_t));
+    hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, c.panels() * sizeof(uint32_t));
     if (e0 != hipSuccess) return e0;
   }
-  for (int i0 = 0; i0 < c.G; i0 += nb) {
+  for (int i0 = 0, q = 0; i0 < c.G; i0 += nb, ++q) {
     const int i1 = i0 + nb < c.G ? i0 + nb : c.G;
-    hipError_t e = launch_babai(c.st, n, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay,
-                                codes, scales, zeros, active, cand, decision, c.cnt(), rowmap);
+    hipError_t e = hook(0, q, 0);
+    if (e == hipSuccess)
+      e = launch_babai(c.st, n, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay, codes,
+                       scales, zeros, active, cand, decision, c.cnt(), rowmap, n_dev, c.chg());
+    if (e == hipSuccess) e = hook(0, q, 1);
     if (e != hipSuccess) return e;
-    e = launch_panel_update(c.st, n, c.cols, c.g, i0 * c.g, i1 * c.g, c.ws, c.lay, scales,
-                            c.pbuf(), rowmap);
+    if (i1 * c.g >= c.cols) break;  // no later columns to update
+    e = hook(1, q, 0);
+    if (e == hipSuccess)
+      e = launch_panel_update(c.st, n, c.cols, c.g, i0 * c.g, i1 * c.g, c.ws, c.lay, scales,
+                              c.pbuf(), rowmap);
+    if (e == hipSuccess) e = hook(1, q, 1);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -188,10 +211,16 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   return JARQ_OK;
 }
 
+// Stage boundaries with a HIP event each (stages 0-4 are consecutive runs of
+// kernels), and the code update's launches with a pair each (stage 5: the
+// Babai kernels, stage 6: the panel updates, which alternate).
+constexpr int kBoundaries = 6;
+
 // time_stages = false: no HIP events are created and stage_ms stays 0.
 jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
                         float* scales, const int32_t* zeros, void* ws, void* stream,
                         jarq_stats* stats, bool time_stages = true) {
+  (void)H;
   Ctx c = make_ctx(p, ws, stream);
   // Device-side input checks (codes in range, |zero point| <= 1024).
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
@@ -207,110 +236,124 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lcur, (size_t)c.rows * sizeof(double)));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lprev, (size_t)c.rows * sizeof(double)));
   JQ_HIP(launch_zero_bytes(c.st, c.hist(), JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord)));
+  JQ_HIP(launch_zero_bytes(c.st, c.gctl(), sizeof(GramCtl)));
+  JQ_HIP(launch_zero_bytes(c.st, c.sctl(), sizeof(SweepCtl)));
+  JQ_HIP(launch_zero_bytes(c.st, c.gcount(), (size_t)c.G * sizeof(uint32_t)));
+  // every row active: rowmap = 0 .. rows - 1, sctl->n = rows
+  JQ_HIP(launch_compact_rows(c.st, c.rows, c.active(), c.rowmap(), c.sctl()));
+
+  // Active-set compaction (early stopping on): a sweep works on the rows still
+  // active when it starts, in ascending order (rowmap), n of them (sctl->n).
+  // Both stay on the device: every per-row kernel is sized for all rows and
+  // reads n itself, so no sweep waits for the host.  Without early stopping
+  // every row takes part in every sweep (no list).
+  const bool stopping = p->tau >= 0.f;
+  const int* n_dev = stopping ? &c.sctl()->n : nullptr;
+  const int32_t* rmap = stopping ? c.rowmap() : nullptr;
+  const int n = c.rows;
 
   const int K = p->sweeps;
   const int nrec = K < JARQ_MAX_RECORDED_SWEEPS ? K : JARQ_MAX_RECORDED_SWEEPS;
+  const int npan = c.panels();
+  const int per_sweep = kBoundaries + 4 * npan;  // boundaries + a pair per code-update launch
   std::vector<hipEvent_t> ev;  // empty unless stages are timed
-  // Events at the boundaries of the timed stages only (each one costs an
-  // idle gap between kernels).
   const uint32_t all_stages = (1u << JARQ_NUM_STAGES) - 1u;
   const uint32_t tmask = (stats == nullptr || !time_stages) ? 0u
                          : (stats->stage_mask & all_stages) ? (stats->stage_mask & all_stages)
                                                              : all_stages;
+  // Boundary j is used when stage j - 1 or stage j (j < 5) is timed.
   auto boundary_used = [&](int j) {
-    return ((j > 0 && ((tmask >> (j - 1)) & 1u)) || (j < JARQ_NUM_STAGES && ((tmask >> j) & 1u)));
+    return (j > 0 && ((tmask >> (j - 1)) & 1u)) || (j < kBoundaries - 1 && ((tmask >> j) & 1u));
   };
   if (stats != nullptr) {
     memset(stats, 0, sizeof(*stats));
     stats->stage_mask = tmask;
     if (tmask != 0u) {
-      ev.resize((size_t)nrec * (JARQ_NUM_STAGES + 1));
+      ev.resize((size_t)nrec * per_sweep);
       for (auto& e : ev) JQ_HIP(hipEventCreate(&e));
     }
   }
   auto mark = [&](int k, int j) -> hipError_t {
     if (tmask == 0u || k >= nrec || !boundary_used(j)) return hipSuccess;
-    return hipEventRecord(ev[(size_t)k * (JARQ_NUM_STAGES + 1) + j], c.st);
+    return hipEventRecord(ev[(size_t)k * per_sweep + j], c.st);
   };
   jarq_status status = JARQ_OK;
-  int run = 0;
-  // Active-set compaction: a sweep works on the n rows still active when it
-  // starts, in ascending order (rowmap, built once rows have stopped; null
-  // while every row takes part).  Rows stopped in earlier sweeps cost nothing.
-  int n = c.rows;
-  const int32_t* rmap = nullptr;
   for (int k = 0; k < K; ++k) {
-    hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = mark(k, 0);
+    // launches of the code update timed with a pair of events each
+    auto hook = [&](int kind, int q, int phase) -> hipError_t {
+      if (k >= nrec || !((tmask >> (5 + kind)) & 1u)) return hipSuccess;
+      const size_t at = (size_t)k * per_sweep + kBoundaries + 2 * (kind * npan + q) + phase;
+      return hipEventRecord(ev[at], c.st);
+    };
+    hipError_t e = mark(k, 0);
     if (e == hipSuccess)
-      e = launch_gram(c.st, n, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(), rmap);
+      e = launch_gram(c.st, n, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(), rmap, n_dev,
+                      /*incremental=*/true);
     if (e == hipSuccess) e = mark(k, 1);
     if (e == hipSuccess)
       e = launch_solve(c.st, n, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, c.active(),
                        c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond, p->ridge_accept,
-                       rmap);
+                       rmap, n_dev);
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
-      e = launch_split_e(c.st, n, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay, rmap);
+      e = launch_split_e(c.st, n, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay, rmap, n_dev);
     if (e == hipSuccess) e = mark(k, 3);
-    if (e == hipSuccess) e = launch_split_gemm(c.st, n, c.cols, c.ws, c.lay, c.pbuf());
+    if (e == hipSuccess) e = launch_split_gemm(c.st, n, c.cols, c.ws, c.lay, c.pbuf(), n_dev);
     if (e == hipSuccess) e = mark(k, 4);
     if (e == hipSuccess)
-      e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart());
+      e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart(), n_dev);
     if (e == hipSuccess)
       e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(),
                             (int32_t*)(c.ws + c.lay.stopat), k + 1, p->tau, rmap,
-                            (uint32_t*)(c.ws + c.lay.pcount), pcount_words(c.cols, c.g));
+                            (uint32_t*)(c.ws + c.lay.pcount), npan, n_dev);
     if (e == hipSuccess) e = mark(k, 5);
     if (e == hipSuccess)
-      e = enqueue_babai(c, n, rmap, H, codes, scales, zeros, c.active(), nullptr, nullptr,
-                        /*counts_zeroed=*/true);
-    if (e == hipSuccess) e = mark(k, 6);
+      e = enqueue_babai(c, n, rmap, n_dev, codes, scales, zeros, c.active(), nullptr, nullptr,
+                        /*counts_zeroed=*/true, hook);
     if (e == hipSuccess)
       e = launch_record_sweep(c.st, c.rows, (const double*)(c.ws + c.lay.lcur), c.active(),
                               c.cnt(),
                               c.hist() + (k < JARQ_MAX_RECORDED_SWEEPS ? k
-                                                                        : JARQ_MAX_RECORDED_SWEEPS - 1));
+                                                                        : JARQ_MAX_RECORDED_SWEEPS - 1),
+                              c.sctl(), c.gctl(), c.gcount(), c.G);
+    // the rows still active after this sweep's stopping test, for the next one
+    if (e == hipSuccess && stopping)
+      e = launch_compact_rows(c.st, c.rows, c.active(), c.rowmap(), c.sctl());
     if (e != hipSuccess) {
       status = JARQ_EHIP;
       break;
     }
-    ++run;
-    if (p->tau >= 0.f) {
-      // With early stopping on, stop launching once every row has stopped.
-      SweepRecord rec{};
-      const int slot = k < JARQ_MAX_RECORDED_SWEEPS ? k : JARQ_MAX_RECORDED_SWEEPS - 1;
-      if (hipMemcpyAsync(&rec, c.hist() + slot, sizeof(rec), hipMemcpyDeviceToHost, c.st) !=
-              hipSuccess ||
+    if (stopping && (k + 1) % 4 == 0 && k + 1 < K) {
+      // Every fourth sweep the host looks whether any row is left (the
+      // sweeps in between run without waiting; one with no row left costs
+      // its launches only).
+      SweepCtl sc{};
+      if (hipMemcpyAsync(&sc, c.sctl(), sizeof(sc), hipMemcpyDeviceToHost, c.st) != hipSuccess ||
           hipStreamSynchronize(c.st) != hipSuccess) {
         status = JARQ_EHIP;
         break;
       }
-      if (rec.active_rows == 0) break;
-      if ((int)rec.active_rows < n) {
-        if (launch_compact_rows(c.st, c.rows, c.active(), c.rowmap()) != hipSuccess) {
-          status = JARQ_EHIP;
-          break;
-        }
-        n = (int)rec.active_rows;
-        rmap = c.rowmap();
-      }
+      if (sc.n == 0) break;
     }
   }
   if (hipStreamSynchronize(c.st) != hipSuccess) status = JARQ_EHIP;
+  SweepCtl sc{};
   if (status == JARQ_OK) {
-    if (hipMemcpy(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost) != hipSuccess)
+    if (hipMemcpy(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost) != hipSuccess ||
+        hipMemcpy(&sc, c.sctl(), sizeof(sc), hipMemcpyDeviceToHost) != hipSuccess)
       status = JARQ_EHIP;
     else if (f.solve_failed)
       status = JARQ_ESCALE_SOLVE;
   }
   if (stats != nullptr) {
+    // sweeps that started with at least one active row
+    const int run = sc.started;
     stats->sweeps_run = run;
     SweepRecord hist[JARQ_MAX_RECORDED_SWEEPS];
     if (hipMemcpy(hist, c.hist(), sizeof(hist), hipMemcpyDeviceToHost) == hipSuccess) {
-      const int n = run < nrec ? run : nrec;
-      for (int k = 0; k < n; ++k) {
+      const int nk = run < nrec ? run : nrec;
+      for (int k = 0; k < nk; ++k) {
         stats->objective_after_scales[k] = hist[k].objective_after_scales;
         stats->accepted_groups[k] = (int64_t)hist[k].accepted;
         stats->codes_changed[k] = (int64_t)hist[k].changed;
@@ -318,11 +361,24 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
         stats->ridge_rows[k] = (int32_t)hist[k].ridge_rows;
         stats->rows_active[k] = (int32_t)hist[k].active_rows;
         stats->correction_blocks[k] = (int64_t)hist[k].corr_blocks;
-        for (int j = 0; j < JARQ_NUM_STAGES; ++j) {
+        stats->gram_listed[k] = (int32_t)hist[k].gram_listed;
+        const size_t b = (size_t)k * per_sweep;
+        for (int j = 0; j < kBoundaries - 1; ++j) {
           float ms = 0.f;
-          const size_t b = (size_t)k * (JARQ_NUM_STAGES + 1) + j;
-          if ((tmask >> j) & 1u) hipEventElapsedTime(&ms, ev[b], ev[b + 1]);
+          if ((tmask >> j) & 1u) hipEventElapsedTime(&ms, ev[b + j], ev[b + j + 1]);
           stats->stage_ms[k][j] = ms;
+        }
+        for (int kind = 0; kind < 2; ++kind) {
+          float tot = 0.f;
+          if ((tmask >> (5 + kind)) & 1u) {
+            for (int q = 0; q < npan - kind; ++q) {
+              float ms = 0.f;
+              const size_t at = b + kBoundaries + 2 * (kind * npan + q);
+              hipEventElapsedTime(&ms, ev[at], ev[at + 1]);
+              tot += ms;
+            }
+          }
+          stats->stage_ms[k][5 + kind] = tot;
         }
       }
       if (run > 0) {
@@ -409,11 +465,11 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
   jarq_status s = check_ws(p, workspace, workspace_bytes);
   if (s != JARQ_OK) return s;
   Ctx c = make_ctx(p, workspace, stream);
-  if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay,
+  if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay, nullptr,
                      nullptr) != hipSuccess ||
-      launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf()) != hipSuccess)
+      launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf(), nullptr) != hipSuccess)
     return JARQ_EHIP;
-  if (enqueue_babai(c, c.rows, nullptr, H, codes, scales, zeros, nullptr, cand, decision) !=
+  if (enqueue_babai(c, c.rows, nullptr, nullptr, codes, scales, zeros, nullptr, cand, decision) !=
       hipSuccess)
     return JARQ_EHIP;
   return JARQ_OK;

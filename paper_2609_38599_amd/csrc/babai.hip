@@ -178,7 +178,10 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     _Float16* __restrict__ dq, int32_t* __restrict__ plist, uint32_t* __restrict__ pcount,
     uint8_t* __restrict__ cand_out,
     uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt,
-    const int32_t* __restrict__ rowmap) {
+    const int32_t* __restrict__ rowmap, const int* __restrict__ n_dev,
+    uint8_t* __restrict__ chg) {
+  if (n_dev != nullptr) rows = *n_dev;
+  if ((int)blockIdx.x * 16 >= rows) return;  // the whole work-group: no row here
   constexpr int g = G_SIZE;
   constexpr int RT = 16;                 // rows per work-group
   constexpr int NT = g / 16;             // positions per lane in the back substitution
@@ -411,6 +414,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
               (uint8_t)(do_row ? fminf(fmaxf(qold[t] + cs.d[t], 0.f), qmax) : qold[t]);
       }
       any_acc |= accept;
+      if (chg != nullptr && row_in && cj == 0) chg[(size_t)crid * G + i] = accept ? 1 : 0;
       if (row_in && cj == 0) {
         if (dec_out != nullptr) {
           uint8_t dd = !row_act ? kDecStopped : (skip ? kDecSkip : (accept ? kDecAccept : kDecReject));
@@ -551,7 +555,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                                  const float* P, const char* ws, const Layout& lay,
                                  uint8_t* codes, const float* scales, const uint8_t* active,
                                  uint8_t* cand, uint8_t* decision, Counters* cnt,
-                                 const int32_t* rowmap) {
+                                 const int32_t* rowmap, const int* n_dev, uint8_t* chg) {
   constexpr int g = G_SIZE;
   constexpr int PG = panel_groups_of(g);
   if (i1 - i0 > PG || i0 % PG != 0) return hipErrorInvalidValue;
@@ -565,7 +569,8 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.rdinv),
                      (const float*)(ws + lay.rdsq), codes, scales, active,
                      (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
-                     (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt, rowmap);
+                     (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt, rowmap, n_dev,
+                     chg);
   return hipGetLastError();
 }
 
@@ -573,18 +578,19 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
                         const float* P,
                         const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
-                        uint8_t* decision, Counters* cnt, const int32_t* rowmap) {
+                        uint8_t* decision, Counters* cnt, const int32_t* rowmap, const int* n_dev,
+                        uint8_t* chg) {
   (void)zeros;
   switch (g) {
     case 32:
       return launch_babai_t<32>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt, rowmap);
+                                cand, decision, cnt, rowmap, n_dev, chg);
     case 64:
       return launch_babai_t<64>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt, rowmap);
+                                cand, decision, cnt, rowmap, n_dev, chg);
     case 128:
       return launch_babai_t<128>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                 cand, decision, cnt, rowmap);
+                                 cand, decision, cnt, rowmap, n_dev, chg);
     default:
       return hipErrorInvalidValue;
   }

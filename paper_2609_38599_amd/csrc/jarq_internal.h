@@ -39,8 +39,24 @@ struct SweepRecord {
   unsigned long long corr_blocks;
   unsigned int ridge_rows;
   unsigned int solve_failed;
-  unsigned int active_rows;
+  unsigned int active_rows;   // rows that ran the code update
+  unsigned int started_rows;  // rows the sweep started with
+  unsigned int gram_listed;   // the Gram matrices were rebuilt from the row lists
   unsigned int pad;
+};
+
+// State of the incremental Gram build (gram.hip).
+struct GramCtl {
+  int valid;   // every active row's matrix matches its codes before the last code update
+  int listed;  // the last build used the row lists
+  int pad[2];
+};
+
+// Rows a sweep works on, kept on the device when early stopping is on.
+struct SweepCtl {
+  int n;        // rows active at the start of the sweep (the list in rowmap)
+  int started;  // sweeps that started with at least one row
+  int pad[2];
 };
 
 // Status words written by device checks and read by the host.
@@ -84,6 +100,11 @@ struct Layout {
   size_t lprev;     // [rows] f64
   size_t active;    // [rows] u8
   size_t stopat;    // [rows] i32: iteration at which the row stopped, 0 while it has not
+  size_t chg;       // [rows][G] u8: the last code update changed group (row, i)
+  size_t glist;     // [G][rows] i32: rows that changed group i (incremental Gram build)
+  size_t gcount;    // [G] u32: length of each list
+  size_t gctl;      // GramCtl
+  size_t sctl;      // SweepCtl
   size_t rowmap;    // [rows] i32: row of each position of the sweep (rows still active, ascending)
   size_t counters;  // Counters
   size_t hist;      // [64] SweepRecord
@@ -116,31 +137,42 @@ hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char*
 // `rows` positions of the sweep; position p holds layer row map_row(rowmap, p).
 hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
                           const uint8_t* codes, const float* scales, const int32_t* zeros,
-                          char* ws, const Layout& lay, const int32_t* rowmap);
+                          char* ws, const Layout& lay, const int32_t* rowmap, const int* n_dev);
 
-// P = E H from the fp16 planes of E and H in the workspace (three products);
-// objpart as for launch_gemm_ah (may be null).
+// P = E H from the fp16 planes of E and H in the workspace (three products).
 hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
-                             const Layout& lay, float* C);
+                             const Layout& lay, float* C, const int* n_dev);
 // Per row and group, (R_i e_i) . U_i = e_i^T (H e)_i (fp64) into objpart[row][group].
 hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, const char* ws,
-                                  const Layout& lay, const float* C, double* objpart);
+                                  const Layout& lay, const float* C, double* objpart,
+                                  const int* n_dev);
 
-// Upper triangles of the grouped Gram matrices from the fp16 planes of H.
+// Row counts on the device: every per-row kernel of a sweep takes the number
+// of positions n as `rows` (the most it may be, which sizes the grid) and,
+// when n_dev is not null, reads the current n from *n_dev; work-groups past it
+// return at once.
+
+// Upper triangles of the grouped Gram matrices from the fp16 planes of H,
+// stored by layer row.  incremental: build from the rows listed per changed
+// group when that is cheaper and the matrices of the last sweep are complete
+// (the code update marks the changed groups in chg; GramCtl in the workspace).
 hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,
                        const Layout& lay, const uint8_t* codes, const int32_t* zeros,
-                       float* gram, const int32_t* rowmap);
+                       float* gram, const int32_t* rowmap, const int* n_dev, bool incremental);
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
-                        float lam, float rcond, int accept, const int32_t* rowmap);
+                        float lam, float rcond, int accept, const int32_t* rowmap,
+                        const int* n_dev);
 
-// Code update of the groups [i0, i1) (one panel).
+// Code update of the groups [i0, i1) (one panel).  chg[row][i] (nullable) is
+// set to whether the update changed group i of the row.
 hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,
                         const float* P, const char* ws, const Layout& lay, uint8_t* codes,
                         const float* scales, const int32_t* zeros, const uint8_t* active,
-                        uint8_t* cand, uint8_t* decision, Counters* cnt, const int32_t* rowmap);
+                        uint8_t* cand, uint8_t* decision, Counters* cnt, const int32_t* rowmap,
+                        const int* n_dev, uint8_t* chg);
 
 // Work-group barrier for LDS only: waits for this wave's LDS operations,
 // not for its outstanding global loads (a __syncthreads would, which drains
@@ -164,8 +196,10 @@ __device__ __forceinline__ int map_row(const int32_t* rowmap, int p) {
   return rowmap != nullptr ? rowmap[p] : p;
 }
 
-// rowmap[0 .. n) = the rows with active[r] != 0, ascending (one work-group).
-hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, int32_t* rowmap);
+// rowmap[0 .. n) = the rows with active[r] != 0, ascending, and sctl->n = n
+// (one work-group).
+hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, int32_t* rowmap,
+                               SweepCtl* sctl);
 
 // Groups per panel of the code update (512 columns, at most 16 groups).
 constexpr int kMaxPanelGroups = 16;
@@ -186,13 +220,16 @@ hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* 
 hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
                              int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
-                             int nzero);
+                             int nzero, const int* n_dev);
 
 hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);
 hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n);
 
+// Also: gram->valid = 1 (every active row's matrix now exists), gcount[0..G)
+// zeroed for the next sweep's lists, sctl->started counted.
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
-                               const uint8_t* active, Counters* cnt, SweepRecord* rec);
+                               const uint8_t* active, Counters* cnt, SweepRecord* rec,
+                               SweepCtl* sctl, GramCtl* gctl, uint32_t* gcount, int G);
 
 hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
                            const uint8_t* codes, const int32_t* zeros, Flags* flags);

@@ -30,9 +30,11 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
                                   uint8_t* __restrict__ active, int32_t* __restrict__ stopat,
                                   int sweep, float tau,
                                   const int32_t* __restrict__ rowmap,
-                                  uint32_t* __restrict__ zero_words, int nzero) {
+                                  uint32_t* __restrict__ zero_words, int nzero,
+                                  const int* __restrict__ n_dev) {
   // the code update's per-panel row counters start the sweep at zero
   if (blockIdx.x == 0 && (int)threadIdx.x < nzero) zero_words[threadIdx.x] = 0u;
+  if (n_dev != nullptr) n = *n_dev;
   const int pos = blockIdx.x * blockDim.x + threadIdx.x;
   if (pos >= n) return;
   const int r = map_row(rowmap, pos);
@@ -55,10 +57,11 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
 hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
                              int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
-                             int nzero) {
+                             int nzero, const int* n_dev) {
   if (n <= 0 || nzero < 0 || nzero > 256) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stop_check_kernel, dim3((n + 255) / 256), dim3(256), 0, st, n, nt,
-                     objpart, lcur, lprev, active, stopat, sweep, tau, rowmap, zero_words, nzero);
+                     objpart, lcur, lprev, active, stopat, sweep, tau, rowmap, zero_words, nzero,
+                     n_dev);
   return hipGetLastError();
 }
 
@@ -67,7 +70,8 @@ hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpar
 // gives each chunk's first position, and the chunk is written in order.
 __global__ __launch_bounds__(1024) void compact_rows_kernel(int rows,
                                                             const uint8_t* __restrict__ active,
-                                                            int32_t* __restrict__ rowmap) {
+                                                            int32_t* __restrict__ rowmap,
+                                                            SweepCtl* __restrict__ sctl) {
   __shared__ int pre_s[1024];
   const int t = threadIdx.x;
   const int per = (rows + 1023) / 1024;
@@ -85,10 +89,12 @@ __global__ __launch_bounds__(1024) void compact_rows_kernel(int rows,
   int pos = pre_s[t] - c;
   for (int r = b; r < e; ++r)
     if (active[r] != 0) rowmap[pos++] = r;
+  if (t == 1023) sctl->n = pre_s[1023];
 }
 
-hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, int32_t* rowmap) {
-  hipLaunchKernelGGL(compact_rows_kernel, dim3(1), dim3(1024), 0, st, rows, active, rowmap);
+hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, int32_t* rowmap,
+                               SweepCtl* sctl) {
+  hipLaunchKernelGGL(compact_rows_kernel, dim3(1), dim3(1024), 0, st, rows, active, rowmap, sctl);
   return hipGetLastError();
 }
 
@@ -117,7 +123,10 @@ hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n) {
 constexpr int kRecordThreads = 1024;
 __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     int rows, const double* __restrict__ lcur, const uint8_t* __restrict__ active,
-    Counters* __restrict__ cnt, SweepRecord* __restrict__ rec) {
+    Counters* __restrict__ cnt, SweepRecord* __restrict__ rec, SweepCtl* __restrict__ sctl,
+    GramCtl* __restrict__ gctl, uint32_t* __restrict__ gcount, int G) {
+  // the next sweep's Gram row lists start empty
+  for (int x = threadIdx.x; x < G; x += kRecordThreads) gcount[x] = 0u;
   __shared__ double red[kRecordThreads];
   __shared__ unsigned int act[kRecordThreads];
   double s = 0.0;
@@ -156,6 +165,13 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     rec->ridge_rows = cnt->ridge_rows;
     rec->solve_failed = cnt->solve_failed;
     rec->active_rows = act[0];
+    const int started = sctl->n;
+    rec->started_rows = (unsigned int)started;
+    rec->gram_listed = (unsigned int)gctl->listed;
+    if (started > 0) {
+      sctl->started += 1;
+      gctl->valid = 1;  // every row that took part has its matrix built
+    }
     cnt->accepted = 0;
     cnt->changed = 0;
     cnt->skipped = 0;
@@ -167,9 +183,10 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
 }
 
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
-                               const uint8_t* active, Counters* cnt, SweepRecord* rec) {
+                               const uint8_t* active, Counters* cnt, SweepRecord* rec,
+                               SweepCtl* sctl, GramCtl* gctl, uint32_t* gcount, int G) {
   hipLaunchKernelGGL(record_sweep_kernel, dim3(1), dim3(kRecordThreads), 0, st, rows, lcur, active,
-                     cnt, rec);
+                     cnt, rec, sctl, gctl, gcount, G);
   return hipGetLastError();
 }
 

@@ -26,7 +26,10 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
                                                         const _Float16* __restrict__ rpl,
                                                         const float* __restrict__ rrow,
                                                         const float* __restrict__ U,
-                                                        double* __restrict__ objpart) {
+                                                        double* __restrict__ objpart,
+                                                        const int* __restrict__ n_dev) {
+  if (n_dev != nullptr) rows = *n_dev;
+  if (blockIdx.x * (64 * kDotRowBlocks) >= rows) return;  // uniform: nothing to do here
   constexpr int g = G_SIZE;
   constexpr int NKC = g / 32;   // 32-wide k-chunks
   constexpr int NMB = g / 16;   // 16-column output blocks
@@ -111,22 +114,25 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
 
 template <int G_SIZE>
 static hipError_t launch_group_dot_t(hipStream_t st, int rows, int cols, const char* ws,
-                                     const Layout& lay, const float* U, double* objpart) {
+                                     const Layout& lay, const float* U, double* objpart,
+                                     const int* n_dev) {
   dim3 grid((rows + 64 * kDotRowBlocks - 1) / (64 * kDotRowBlocks), cols / G_SIZE);
   hipLaunchKernelGGL(group_dot_kernel<G_SIZE>, grid, dim3(256), 0, st, rows, cols,
                      (const _Float16*)(ws + lay.ehi), (const _Float16*)(ws + lay.elo),
                      (const float*)(ws + lay.erow), (const _Float16*)(ws + lay.rph),
-                     (const _Float16*)(ws + lay.rpl), (const float*)(ws + lay.rrow), U, objpart);
+                     (const _Float16*)(ws + lay.rpl), (const float*)(ws + lay.rrow), U, objpart,
+                     n_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, const char* ws,
-                                  const Layout& lay, const float* C, double* objpart) {
+                                  const Layout& lay, const float* C, double* objpart,
+                                  const int* n_dev) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
   switch (g) {
-    case 32: return launch_group_dot_t<32>(st, rows, cols, ws, lay, C, objpart);
-    case 64: return launch_group_dot_t<64>(st, rows, cols, ws, lay, C, objpart);
-    case 128: return launch_group_dot_t<128>(st, rows, cols, ws, lay, C, objpart);
+    case 32: return launch_group_dot_t<32>(st, rows, cols, ws, lay, C, objpart, n_dev);
+    case 64: return launch_group_dot_t<64>(st, rows, cols, ws, lay, C, objpart, n_dev);
+    case 128: return launch_group_dot_t<128>(st, rows, cols, ws, lay, C, objpart, n_dev);
     default: return hipErrorInvalidValue;
   }
 }

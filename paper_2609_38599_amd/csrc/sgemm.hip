@@ -33,10 +33,13 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 namespace {
 constexpr int BM = 256, BK = 32;
 
-__device__ __forceinline__ void tile_of(int wid, int nbm, int nbn, int& tm, int& tn) {
+// Tile of work-group wid; false when wid has none (the grid may be sized for
+// more rows than the sweep has).
+__device__ __forceinline__ bool tile_of(int wid, int nbm, int nbn, int& tm, int& tn) {
   const int total = nbm * nbn;
   const int q = total / 8, r = total % 8;
   const int x = wid % 8, loc = wid / 8;
+  if (loc >= q + (x < r ? 1 : 0)) return false;  // this XCD's share is taken
   const int id = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + loc;
   constexpr int GM = 4;  // tile-rows per band
   const int band = id / (GM * nbn);
@@ -45,6 +48,7 @@ __device__ __forceinline__ void tile_of(int wid, int nbm, int nbn, int& tm, int&
   const int within = id - band * GM * nbn;
   tm = first + within % gsz;
   tn = within / gsz;
+  return true;
 }
 
 // LDS holds each plane tile as rows of 32 halves (four 16-byte chunks); chunk
@@ -67,7 +71,8 @@ __global__ __launch_bounds__(512, 1) void split3_kernel(
     int M, int N, int K, int lda, int ldb, int ldc, const _Float16* __restrict__ Ah,
     const _Float16* __restrict__ Al, const float* __restrict__ arow_inv,
     const _Float16* __restrict__ Bh, const _Float16* __restrict__ Bl,
-    const float* __restrict__ bcol_inv, float* __restrict__ C) {
+    const float* __restrict__ bcol_inv, float* __restrict__ C, const int* __restrict__ m_dev) {
+  if (m_dev != nullptr) M = *m_dev;
   constexpr int WN = BN / 4;   // wave tile columns
   constexpr int NB = WN / 32;  // 32-column blocks per wave
   constexpr int A_PLANE = BM * BK, B_PLANE = BN * BK;  // halves
@@ -83,7 +88,7 @@ __global__ __launch_bounds__(512, 1) void split3_kernel(
   const int lm = lane & 31, kh = lane >> 5;
   const int nbm = (M + BM - 1) / BM, nbn = (N + BN - 1) / BN;
   int tm, tn;
-  tile_of(blockIdx.x, nbm, nbn, tm, tn);
+  if (M <= 0 || !tile_of(blockIdx.x, nbm, nbn, tm, tn)) return;  // uniform across the work-group
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Direct global -> LDS loads, 16 bytes per lane: one instruction fills 1 KB
@@ -264,17 +269,17 @@ template <int BN, int kMode>
 static hipError_t launch_split3_t(hipStream_t st, int M, int N, int K, int lda, int ldb,
                                   int ldc, const _Float16* ah, const _Float16* al,
                                   const float* arow, const _Float16* bh, const _Float16* bl,
-                                  const float* bcol, float* C) {
+                                  const float* bcol, float* C, const int* m_dev) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % BK != 0) return hipErrorInvalidValue;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   hipLaunchKernelGGL((split3_kernel<BN, kMode>), dim3(tiles), dim3(512), 0, st, M, N, K, lda, ldb,
-                     ldc, ah, al, arow, bh, bl, bcol, C);
+                     ldc, ah, al, arow, bh, bl, bcol, C, m_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
-                             const Layout& lay, float* C) {
+                             const Layout& lay, float* C, const int* n_dev) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
   const _Float16* ah = (const _Float16*)(ws + lay.ehi);
   const _Float16* al = (const _Float16*)(ws + lay.elo);
@@ -283,7 +288,7 @@ hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
   const float* ar = (const float*)(ws + lay.erow);
   const float* bc = (const float*)(ws + lay.mrow);
   return launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, ah, al, ar, bh, bl, bc,
-                                 C);
+                                 C, n_dev);
 }
 
 }  // namespace jarq

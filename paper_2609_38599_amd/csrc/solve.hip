@@ -42,8 +42,11 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
                                                        Counters* __restrict__ cnt,
                                                        Flags* __restrict__ flags, float lam,
                                                        float rcond, int accept,
-                                                       const int32_t* __restrict__ rowmap) {
+                                                       const int32_t* __restrict__ rowmap,
+                                                       const int* __restrict__ n_dev) {
   constexpr int RPW = 64 / GM;  // rows per wavefront
+  if (n_dev != nullptr) rows = *n_dev;
+  if ((int)blockIdx.x * RPW >= rows) return;  // the whole wavefront: no row here
   constexpr int g = GS;
   const int G = cols / g;
   const int lane = threadIdx.x;
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   double A[GM];
   double diag = 0.0;
   bool finite = isfinite(r0);
-  const float* gr = gram + (size_t)rr * G * G;
+  const float* gr = gram + (size_t)grow * G * G;  // stored by layer row
   auto load_rows = [&](double shift) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < GM; ++j) {
@@ -236,13 +239,15 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
                                                         Counters* __restrict__ cnt,
                                                         Flags* __restrict__ flags, float lam,
                                                         float rcond, int accept,
-                                                        const int32_t* __restrict__ rowmap) {
+                                                        const int32_t* __restrict__ rowmap,
+                                                        const int* __restrict__ n_dev) {
   constexpr int g = GS;
   const int G = cols / g;
   const int LD = G | 1;  // odd stride (in doubles): rows of a column spread over banks
-  const int row = blockIdx.x;  // position of the sweep (Gram); layer row grow
+  const int row = blockIdx.x;  // position of the sweep; layer row grow
   const int i = threadIdx.x;
   const int nthr = blockDim.x;
+  if (n_dev != nullptr) rows = *n_dev;
   if (row >= rows) return;
   const int grow = map_row(rowmap, row);
   if (active != nullptr && !active[grow]) return;
@@ -280,7 +285,7 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
     }
   }
 
-  const float* gr = gram + (size_t)row * G * G;
+  const float* gr = gram + (size_t)grow * G * G;  // stored by layer row
   double diag = 0.0;
   bool finite = !live || isfinite(r0);
   // column-major copy of the system (+ shift on the diagonal); entry (i, j)
@@ -445,7 +450,7 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
                                    float* scales, const uint8_t* active, Counters* cnt,
                                    Flags* flags, float lam, float rcond, int accept,
-                                   const int32_t* rowmap) {
+                                   const int32_t* rowmap, const int* n_dev) {
   const int G = cols / GS;
   const int LD = G | 1;
   const size_t lds = ((size_t)G * LD + 2 * (size_t)G + 2) * sizeof(double);
@@ -453,7 +458,7 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
-                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap);
+                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
   return hipGetLastError();
 }
 
@@ -462,26 +467,27 @@ static hipError_t launch_solve_reg(hipStream_t st, int rows, int cols, const flo
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
                                    float* scales, const uint8_t* active, Counters* cnt,
                                    Flags* flags, float lam, float rcond, int accept,
-                                   const int32_t* rowmap) {
+                                   const int32_t* rowmap, const int* n_dev) {
   constexpr int RPW = 64 / GM;
   hipLaunchKernelGGL((solve_reg_kernel<GM, GS>), dim3((rows + RPW - 1) / RPW), dim3(64), 0, st,
-                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap);
+                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
-                        float lam, float rcond, int accept, const int32_t* rowmap) {
+                        float lam, float rcond, int accept, const int32_t* rowmap,
+                        const int* n_dev) {
   const int G = cols / g;
   if (G > 64 && G <= 128) {
     switch (g) {
       case 32: return launch_solve_col<32>(st, rows, cols, gram, wh, codes, zeros, scales, active,
-                                           cnt, flags, lam, rcond, accept, rowmap);
+                                           cnt, flags, lam, rcond, accept, rowmap, n_dev);
       case 64: return launch_solve_col<64>(st, rows, cols, gram, wh, codes, zeros, scales, active,
-                                           cnt, flags, lam, rcond, accept, rowmap);
+                                           cnt, flags, lam, rcond, accept, rowmap, n_dev);
       case 128: return launch_solve_col<128>(st, rows, cols, gram, wh, codes, zeros, scales,
-                                             active, cnt, flags, lam, rcond, accept, rowmap);
+                                             active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
       default: break;
     }
   }
@@ -489,11 +495,11 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
 #define JARQ_SOLVE_REG(GM)                                                                        \
   switch (g) {                                                                                    \
     case 32: return launch_solve_reg<GM, 32>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond, accept, rowmap);                     \
+                                             active, cnt, flags, lam, rcond, accept, rowmap, n_dev);                     \
     case 64: return launch_solve_reg<GM, 64>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond, accept, rowmap);                     \
+                                             active, cnt, flags, lam, rcond, accept, rowmap, n_dev);                     \
     case 128: return launch_solve_reg<GM, 128>(st, rows, cols, gram, wh, codes, zeros, scales,    \
-                                               active, cnt, flags, lam, rcond, accept, rowmap);                   \
+                                               active, cnt, flags, lam, rcond, accept, rowmap, n_dev);                   \
     default: break;                                                                               \
   }
     if (G <= 32) {

@@ -155,10 +155,11 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
                                                       _Float16* __restrict__ ehi,
                                                       _Float16* __restrict__ elo,
                                                       float* __restrict__ erow_inv,
-                                                      const int32_t* __restrict__ rowmap) {
+                                                      const int32_t* __restrict__ rowmap,
+                                                      const int* __restrict__ n_dev) {
   // position pos of the sweep (E and its scale) holds layer row `row`
   const int pos = blockIdx.x;
-  if (pos >= rows) return;
+  if (pos >= (n_dev != nullptr ? *n_dev : rows)) return;
   const int row = map_row(rowmap, pos);
   const int G = cols / g;
   __shared__ float red[4];
@@ -225,23 +226,24 @@ template <int NCH>
 static hipError_t launch_split_e_t(hipStream_t st, int rows, int cols, int g, const float* W,
                                    const uint8_t* codes, const float* scales,
                                    const int32_t* zeros, char* ws, const Layout& lay,
-                                   const int32_t* rowmap) {
+                                   const int32_t* rowmap, const int* n_dev) {
   hipLaunchKernelGGL(split_e_kernel<NCH>, dim3(rows), dim3(256), 0, st, rows, cols, g, W, codes,
                      scales, zeros, (_Float16*)(ws + lay.ehi), (_Float16*)(ws + lay.elo),
-                     (float*)(ws + lay.erow), rowmap);
+                     (float*)(ws + lay.erow), rowmap, n_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
                           const uint8_t* codes, const float* scales, const int32_t* zeros,
-                          char* ws, const Layout& lay, const int32_t* rowmap) {
+                          char* ws, const Layout& lay, const int32_t* rowmap,
+                          const int* n_dev) {
   if (rows <= 0) return hipSuccess;
   if (cols <= 4096)
-    return launch_split_e_t<4>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+    return launch_split_e_t<4>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap, n_dev);
   if (cols <= 12288)
-    return launch_split_e_t<12>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+    return launch_split_e_t<12>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap, n_dev);
   if (cols <= 16384)   // the most a layer can have: 128 groups of at most 128
-    return launch_split_e_t<16>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap);
+    return launch_split_e_t<16>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap, n_dev);
   return hipErrorInvalidValue;
 }
 

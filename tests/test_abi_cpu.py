@@ -36,7 +36,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert binding.abi_version() == binding.ABI_VERSION == 7
+    assert binding.abi_version() == binding.ABI_VERSION == 8
     for s in range(7):
         assert binding.status_string(s)
     assert binding.status_string(99) == "unknown status"

@@ -120,8 +120,8 @@ static hipError_t launch_chol_t(hipStream_t st, int cols, const float* H, char* 
                                 const Layout& lay) {
   const int G = cols / G_SIZE;
   const size_t lds = (size_t)G_SIZE * (G_SIZE + 1) * sizeof(double);
-  hipError_t e = hipFuncSetAttribute((const void*)chol_groups_kernel<G_SIZE>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static std::atomic<unsigned long long> lds_set{0};
+  hipError_t e = allow_dynamic_lds((const void*)chol_groups_kernel<G_SIZE>, lds, lds_set);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(chol_groups_kernel<G_SIZE>, dim3(G), dim3(256), lds, st, H, cols,
                      (double*)(ws + lay.lfac), (float*)(ws + lay.rinv), (float*)(ws + lay.rcol),

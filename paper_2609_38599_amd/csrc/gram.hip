@@ -440,11 +440,10 @@ static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* 
   GramCtl* ctl = incremental ? (GramCtl*)(ws + lay.gctl) : nullptr;
   const int32_t* glist = (const int32_t*)(ws + lay.glist);
   const uint32_t* gcount = (const uint32_t*)(ws + lay.gcount);
-  hipError_t e = hipFuncSetAttribute((const void*)gram_kernel<g>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static std::atomic<unsigned long long> full_set{0}, listed_set{0};
+  hipError_t e = allow_dynamic_lds((const void*)gram_kernel<g>, lds, full_set);
   if (e == hipSuccess && incremental)
-    e = hipFuncSetAttribute((const void*)gram_listed_kernel<g>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    e = allow_dynamic_lds((const void*)gram_listed_kernel<g>, lds, listed_set);
   if (e != hipSuccess) return e;
   if (incremental)
     hipLaunchKernelGGL(gram_lists_kernel, dim3((rows + 255) / 256, G), dim3(256), 0, st, rows, G,

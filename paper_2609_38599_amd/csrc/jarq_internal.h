@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace jarq {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -67,6 +69,23 @@ struct Flags {
   int solve_failed;    // rows whose scale solve failed after the ridge (all sweeps)
   int pad[4];
 };
+
+// hipFuncSetAttribute(MaxDynamicSharedMemorySize, bytes) once per kernel and
+// device (bit d of `done` for device d < 64): the attribute belongs to the
+// function, and setting it again on every launch costs host time that the GPU
+// spends idle between short kernels.  `bytes` is the most any launch of the
+// kernel asks for.
+inline hipError_t allow_dynamic_lds(const void* fn, size_t bytes,
+                                    std::atomic<unsigned long long>& done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+  const unsigned long long bit = (dev >= 0 && dev < 64) ? 1ull << dev : 0ull;
+  if (bit != 0 && (done.load(std::memory_order_acquire) & bit) != 0) return hipSuccess;
+  const hipError_t e =
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess && bit != 0) done.fetch_or(bit, std::memory_order_release);
+  return e;
+}
 
 // Offsets (bytes) of the workspace regions for one problem size.
 struct Layout {

@@ -2,13 +2,15 @@
 //
 // The G x G Gram matrix (upper triangle from the Gram kernel, symmetrised by
 // construction) and the right-hand side r_a = c_a^T (W H)_a are factored by a
-// right-looking Cholesky.  Two kernels:
-//   solve_reg_kernel (G <= 64): lane i of a row holds row i of the matrix in
-//     registers (two rows per wavefront when G <= 32); the column of each step
-//     is exchanged through LDS, the forward substitution runs inside the
-//     factorisation, the backward one reads L transposed through LDS.
-//   solve_col_kernel (64 < G <= 128): the same with the matrix in LDS,
-//     column-major, one row per work-group of 128 lanes.
+// right-looking Cholesky.  Three kernels:
+//   solve_reg_kernel (G <= 32): lane i of a row holds row i of the matrix in
+//     registers, two rows per wavefront; the column of each step is exchanged
+//     through LDS, the forward substitution runs inside the factorisation, the
+//     backward one reads L transposed through LDS.
+//   solve_tile_kernel (32 < G <= 108): one row per wavefront, the lower
+//     triangle in 4 x 4 register tiles spread over the lanes (see there).
+//   solve_col_kernel (108 < G <= 128): the matrix in LDS, column-major, one
+//     row per work-group of 128 lanes.
 // The stabilised branch of
 // App. E.2 (add lambda I and factor again) is taken when an entry is not
 // finite, a pivot is not positive, or the smallest pivot is at most
@@ -445,6 +447,320 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
   }
 }
 
+// One wavefront per row for every G up to 108: the lower triangle of the
+// G x G system in 4 x 4 tiles held in registers, tile t (numbered column by
+// column: tiles of column-block 0 first) in lane t % 64, slot t / 64.  Step k
+// of the right-looking factorisation publishes column k of the Schur
+// complement in LDS (the lanes holding it write it; a barrier, which for one
+// wavefront only orders the accesses, precedes every read), every lane forms
+// 1/sqrt(pivot) from it itself (same bits everywhere) and scales what it
+// reads, and every tile with columns right of k subtracts l_rk l_ck from its
+// entries.  Tiles of finished column blocks drop out (the slot is skipped once
+// every lane's tile in it is finished).  The forward substitution L y = r runs
+// along (r_i in lane i % 64, slot i / 64; y_k broadcast by a cross-lane
+// shuffle), and the published columns stay in LDS (packed column-major lower
+// triangle) for the backward one.
+// f(IntC<0>), ..., f(IntC<3>): a loop of four steps with a static index
+template <int V>
+struct StepC {
+  static constexpr int value = V;
+};
+template <typename F>
+__device__ __forceinline__ void Unroll4(F&& f) {
+  f(StepC<0>{});
+  f(StepC<1>{});
+  f(StepC<2>{});
+  f(StepC<3>{});
+}
+
+template <int TPL, int GS>
+__global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
+                                                        const float* __restrict__ gram,
+                                                        const float* __restrict__ wh,
+                                                        const uint8_t* __restrict__ codes,
+                                                        const int32_t* __restrict__ zeros,
+                                                        float* __restrict__ scales,
+                                                        const uint8_t* __restrict__ active,
+                                                        Counters* __restrict__ cnt,
+                                                        Flags* __restrict__ flags, float lam,
+                                                        float rcond, int accept,
+                                                        const int32_t* __restrict__ rowmap,
+                                                        const int* __restrict__ n_dev) {
+  constexpr int g = GS;
+  const int G = cols / g;
+  if (n_dev != nullptr) rows = *n_dev;
+  const int row = blockIdx.x;  // position of the sweep; layer row grow
+  if (row >= rows) return;
+  const int grow = map_row(rowmap, row);
+  if (active != nullptr && !active[grow]) return;
+  const int lane = threadIdx.x;
+  const int T = (G + 3) >> 2;            // tile rows (and columns)
+  const int NT = T * (T + 1) / 2;        // tiles of the lower triangle
+  extern __shared__ double sm[];
+  double* colbuf = sm;                         // column k of L: rows k .. G - 1
+  double* rsb = colbuf + G * (G + 1) / 2;      // ridge acceptance: previous scales
+  double* vb = rsb + G;                        // ridge acceptance: new scales
+  auto cstart = [&](int k) { return k * G - k * (k - 1) / 2; };
+
+  // ---- right-hand side r_i = sum over group i of (q - z) (W H), i = lane, lane + 64 ----
+  double r0[2] = {0.0, 0.0};
+  bool finite = true;
+#pragma unroll
+  for (int sl = 0; sl < 2; ++sl) {
+    const int i = lane + 64 * sl;
+    if (i < G) {
+      const float* whp = wh + (size_t)grow * cols + (size_t)i * g;
+      const uint8_t* qp = codes + (size_t)grow * cols + (size_t)i * g;
+      const double z = (double)zeros[(size_t)grow * G + i];
+      double acc = 0.0;
+      constexpr int CH = g < 32 ? g : 32;
+#pragma unroll
+      for (int c0 = 0; c0 < g; c0 += CH) {
+        uint4 qv[CH / 16];
+        f32x4 wv[CH / 4];
+#pragma unroll
+        for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
+#pragma unroll
+        for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
+#pragma unroll
+        for (int u = 0; u < CH / 4; ++u) {
+          const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
+                               : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], acc);
+        }
+      }
+      r0[sl] = acc;
+      finite &= isfinite(acc);
+    }
+  }
+
+  // ---- this lane's tiles ----
+  double ta[TPL][4][4];
+  int ttr[TPL], ttc[TPL];
+  bool tvalid[TPL];
+#pragma unroll
+  for (int m = 0; m < TPL; ++m) {
+    int id = lane + 64 * m, tc = 0;
+    tvalid[m] = id < NT;
+    while (tc < T && id >= T - tc) {  // column-block tc holds T - tc tiles
+      id -= T - tc;
+      ++tc;
+    }
+    ttc[m] = tc;
+    ttr[m] = tc + id;
+  }
+  // last step at which slot m still has columns to update, over the wavefront
+  int kend[TPL];
+#pragma unroll
+  for (int m = 0; m < TPL; ++m) {
+    int e = tvalid[m] ? 4 * ttc[m] + 3 : -1;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) e = max(e, __shfl_xor(e, off));
+    kend[m] = e;
+  }
+  const float* gr = gram + (size_t)grow * G * G;  // upper triangle, stored by layer row
+  double diag = 0.0;
+  auto load = [&](double shift) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < TPL; ++m) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int r = 4 * ttr[m] + a, c = 4 * ttc[m] + b;
+          const bool in = tvalid[m] && r < G && c <= r;
+          const float v = in ? gr[(size_t)c * G + r] : 0.f;
+          if (in) finite &= isfinite(v);
+          if (in && r == c) diag = fmax(diag, (double)v);
+          ta[m][a][b] = (double)v + (in && r == c ? shift : 0.0);
+        }
+      }
+      // one tile's loads in flight at a time (registers)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // The column published at step k is the Schur complement's column k
+  // (unscaled); every lane forms 1/sqrt(pivot) from it, and reads scale by it.
+  double rr[2], rs_own[2] = {0.0, 0.0}, minpiv = INFINITY;
+  bool pivots_ok = true;
+  auto factor = [&]() __attribute__((always_inline)) {
+    rr[0] = r0[0];
+    rr[1] = r0[1];
+    minpiv = INFINITY;
+    pivots_ok = true;
+    for (int kc = 0; kc < T; ++kc) {
+      // four steps per column block, unrolled: the tile column j is static
+      Unroll4([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        const int k = 4 * kc + j;
+        if (k >= G) return;  // uniform
+        // column k of the packed store, indexed by row: colk[r] for r >= k
+        double* colk = colbuf + (cstart(k) - k);
+        // publish column k (rows k .. G - 1) from the tiles of column-block kc
+#pragma unroll
+        for (int m = 0; m < TPL; ++m) {
+          if (tvalid[m] && ttc[m] == kc) {
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+              const int r = 4 * ttr[m] + a;
+              if (r >= k && r < G) colk[4 * ttr[m] + a] = ta[m][a][j];
+            }
+          }
+        }
+        __syncthreads();  // one wavefront: orders the LDS writes before the reads
+        const double piv = colk[k];
+        pivots_ok &= piv > 0.0 && isfinite(piv);
+        minpiv = fmin(minpiv, piv);
+        const double rs = rsqrt_f64(piv);
+        const double rs2 = rs * rs;
+        // forward substitution: y_k = r_k / l_kk, r_i -= l_ik y_k for i > k
+        const double yk = __shfl(k >> 6 ? rr[1] : rr[0], k & 63) * rs;
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+          const int i = lane + 64 * sl;
+          if (i > k && i < G) rr[sl] = fma(-(colk[i] * rs), yk, rr[sl]);
+          if (i == k) {
+            rr[sl] = yk;
+            rs_own[sl] = rs;
+          }
+        }
+        // Trailing update of the tiles with columns right of k, unmasked:
+        // an entry (r, c) with r > k and c > k (r, c < G) reads its column
+        // values from column k; every other entry of a tile is finished or
+        // padding, is never read again, and may take any value.  Rows below
+        // k and past G read inside the allocation (column k - 1's tail, the
+        // scratch after the last column).
+#pragma unroll
+        for (int m = 0; m < TPL; ++m) {
+          if (k < kend[m]) {
+            const double* pr = colk + 4 * ttr[m];
+            const double* pc = colk + 4 * ttc[m];
+            double lr[4], lc[4];
+#pragma unroll
+            for (int a = 0; a < 4; ++a) lr[a] = pr[a] * rs2;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) lc[b] = pc[b];
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+              for (int b = 0; b < 4; ++b) ta[m][a][b] = fma(-lr[a], lc[b], ta[m][a][b]);
+          }
+          // one tile's column values live at a time (registers)
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+    }
+  };
+
+  load(0.0);
+  double dmax = diag;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, off));
+  const bool all_finite = __all(finite);
+  factor();
+  const bool ridge = !all_finite || !pivots_ok ||
+                     !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  bool failed = false;
+  if (ridge) {  // uniform: every lane saw the same pivots
+    __syncthreads();  // the last step's reads are done before the columns are rewritten
+    load((double)lam);
+    factor();
+    failed = !(pivots_ok && minpiv > 0.0);
+  }
+
+  // ---- backward substitution L^T s = y: s_k = y_k / l_kk, y_i -= l_ki s_k ----
+  // l_ki = (column i as published) / sqrt(pivot i); lane i keeps 1/sqrt(pivot i).
+  for (int k = G - 1; k >= 0; --k) {
+    const double sk = __shfl(k >> 6 ? rr[1] * rs_own[1] : rr[0] * rs_own[0], k & 63);
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl) {
+      const int i = lane + 64 * sl;
+      if (i < k) rr[sl] = fma(-(colbuf[cstart(i) + k - i] * rs_own[sl]), sk, rr[sl]);
+      if (i == k) rr[sl] = sk;
+    }
+  }
+
+  // Ridge acceptance (optional; the remark of App. G.5): keep the ridge
+  // solution only when it does not increase F_j, from the Gram matrix
+  // (reloaded: the tiles hold the factor) and the right-hand side:
+  // dq = s'^T G s' - s^T G s - 2 r^T (s' - s).
+  bool keep_old = false;
+  if (accept && ridge && !failed) {  // uniform
+    double s_old[2];
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl) {
+      const int i = lane + 64 * sl;
+      s_old[sl] = i < G ? (double)scales[(size_t)grow * G + i] : 0.0;
+      if (i < G) {
+        vb[i] = rr[sl];       // s' (new)
+        rsb[i] = s_old[sl];   // s (previous)
+      }
+    }
+    __syncthreads();  // the writes before every lane's reads
+    load(0.0);
+    double dq = 0.0;
+#pragma unroll
+    for (int m = 0; m < TPL; ++m) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int r = 4 * ttr[m] + a, c = 4 * ttc[m] + b;
+          if (tvalid[m] && r < G && c <= r) {
+            const double w = r == c ? 1.0 : 2.0;
+            dq += w * ta[m][a][b] * (vb[r] * vb[c] - rsb[r] * rsb[c]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl)
+      if (lane + 64 * sl < G) dq -= 2.0 * r0[sl] * (rr[sl] - s_old[sl]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) dq += __shfl_xor(dq, off);
+    keep_old = dq > 0.0;
+  }
+
+  if (!failed && !keep_old) {
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl) {
+      const int i = lane + 64 * sl;
+      if (i < G) scales[(size_t)grow * G + i] = (float)rr[sl];
+    }
+  }
+  if (lane == 0) {
+    if (ridge) atomicAdd(&cnt->ridge_rows, 1u);
+    if (failed) {
+      atomicAdd(&cnt->solve_failed, 1u);
+      atomicAdd(&flags->solve_failed, 1);
+    }
+  }
+}
+
+template <int TPL, int GS>
+static hipError_t launch_solve_tile(hipStream_t st, int rows, int cols, const float* gram,
+                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
+                                    float* scales, const uint8_t* active, Counters* cnt,
+                                    Flags* flags, float lam, float rcond, int accept,
+                                    const int32_t* rowmap, const int* n_dev) {
+  const int G = cols / GS;
+  const size_t lds = ((size_t)G * (G + 1) / 2 + 2 * (size_t)G) * sizeof(double);
+  // the most any system of this tile count needs (T (T + 1) / 2 <= 64 TPL tiles of 4)
+  constexpr int kGmax = TPL == 1 ? 40 : TPL == 2 ? 60 : TPL == 3 ? 76 : TPL == 4 ? 88 : 108;
+  static std::atomic<unsigned long long> lds_set{0};
+  hipError_t e = allow_dynamic_lds((const void*)solve_tile_kernel<TPL, GS>,
+                                   ((size_t)kGmax * (kGmax + 1) / 2 + 2 * kGmax) * sizeof(double),
+                                   lds_set);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((solve_tile_kernel<TPL, GS>), dim3(rows), dim3(64), lds, st, rows, cols,
+                     gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept,
+                     rowmap, n_dev);
+  return hipGetLastError();
+}
+
 template <int GS>
 static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const float* gram,
                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
@@ -454,8 +770,10 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
   const int G = cols / GS;
   const int LD = G | 1;
   const size_t lds = ((size_t)G * LD + 2 * (size_t)G + 2) * sizeof(double);
-  hipError_t e = hipFuncSetAttribute((const void*)solve_col_kernel<GS>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static std::atomic<unsigned long long> lds_set{0};
+  // the widest layer: G = 128 (odd stride 129)
+  hipError_t e = allow_dynamic_lds((const void*)solve_col_kernel<GS>,
+                                   ((size_t)128 * 129 + 2 * 128 + 2) * sizeof(double), lds_set);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
                      cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
@@ -480,7 +798,40 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                         float lam, float rcond, int accept, const int32_t* rowmap,
                         const int* n_dev) {
   const int G = cols / g;
-  if (G > 64 && G <= 128) {
+  const int T = (G + 3) / 4, NT = T * (T + 1) / 2;  // 4 x 4 tiles of the lower triangle
+#define JARQ_SOLVE_TILE(TPL)                                                                     \
+  switch (g) {                                                                                   \
+    case 32: return launch_solve_tile<TPL, 32>(st, rows, cols, gram, wh, codes, zeros, scales,   \
+                                               active, cnt, flags, lam, rcond, accept, rowmap,   \
+                                               n_dev);                                           \
+    case 64: return launch_solve_tile<TPL, 64>(st, rows, cols, gram, wh, codes, zeros, scales,   \
+                                               active, cnt, flags, lam, rcond, accept, rowmap,   \
+                                               n_dev);                                           \
+    case 128: return launch_solve_tile<TPL, 128>(st, rows, cols, gram, wh, codes, zeros, scales, \
+                                                 active, cnt, flags, lam, rcond, accept, rowmap, \
+                                                 n_dev);                                         \
+    default: return hipErrorInvalidValue;                                                        \
+  }
+  if (G <= 32) {  // two systems per wavefront, a row of the system per lane
+    switch (g) {
+      case 32: return launch_solve_reg<32, 32>(st, rows, cols, gram, wh, codes, zeros, scales,
+                                               active, cnt, flags, lam, rcond, accept, rowmap,
+                                               n_dev);
+      case 64: return launch_solve_reg<32, 64>(st, rows, cols, gram, wh, codes, zeros, scales,
+                                               active, cnt, flags, lam, rcond, accept, rowmap,
+                                               n_dev);
+      case 128: return launch_solve_reg<32, 128>(st, rows, cols, gram, wh, codes, zeros, scales,
+                                                 active, cnt, flags, lam, rcond, accept, rowmap,
+                                                 n_dev);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (NT <= 128) { JARQ_SOLVE_TILE(2) }
+  if (NT <= 192) { JARQ_SOLVE_TILE(3) }
+  if (NT <= 256) { JARQ_SOLVE_TILE(4) }
+  if (NT <= 384) { JARQ_SOLVE_TILE(6) }
+#undef JARQ_SOLVE_TILE
+  if (G <= 128) {  // the widest layers: the system in LDS, one work-group per row
     switch (g) {
       case 32: return launch_solve_col<32>(st, rows, cols, gram, wh, codes, zeros, scales, active,
                                            cnt, flags, lam, rcond, accept, rowmap, n_dev);
@@ -490,24 +841,6 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                                              active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
       default: break;
     }
-  }
-  if (G <= 64) {
-#define JARQ_SOLVE_REG(GM)                                                                        \
-  switch (g) {                                                                                    \
-    case 32: return launch_solve_reg<GM, 32>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond, accept, rowmap, n_dev);                     \
-    case 64: return launch_solve_reg<GM, 64>(st, rows, cols, gram, wh, codes, zeros, scales,      \
-                                             active, cnt, flags, lam, rcond, accept, rowmap, n_dev);                     \
-    case 128: return launch_solve_reg<GM, 128>(st, rows, cols, gram, wh, codes, zeros, scales,    \
-                                               active, cnt, flags, lam, rcond, accept, rowmap, n_dev);                   \
-    default: break;                                                                               \
-  }
-    if (G <= 32) {
-      JARQ_SOLVE_REG(32)
-    } else {
-      JARQ_SOLVE_REG(64)
-    }
-#undef JARQ_SOLVE_REG
   }
   return hipErrorInvalidValue;  // G > 128 is rejected by the API
 }

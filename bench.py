@@ -30,7 +30,9 @@ bf16), its finalisation with the layer's damping, and the RTN host.
 
 Prints one JSON line.  --gpus above 1 is refused: the path runs on one GPU.
 --copy-probe runs only a plain device copy of known size (used to calibrate
-the HBM byte counters of rocprofv3) and prints nothing else.
+the HBM byte counters of rocprofv3) and prints nothing else; --lds-probe runs
+only the library's LDS calibration kernel (known LDS bytes, for the LDS
+counters) and logs the rate it reaches.
 """
 
 from __future__ import annotations
@@ -52,8 +54,13 @@ PEAK_FP16_MFMA_TFLOPS = 2500.0   # dense
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_FP64_TFLOPS = 78.6
 PEAK_HBM_GBS = 8000.0
+# LDS: 256 CUs x 256 bytes per clock x 2.4 GHz (the library's LDS probe reads
+# 124 TB/s, above the 78.6 TB/s that 128 bytes per clock would allow)
+PEAK_LDS_GBS = 256 * 256 * 2.4
 COPY_PROBE_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_residual_product_4096x4096.txt")
+STAGE_COUNTERS_FILE = os.path.join(ROOT, "profiles",
+                                   "stage_counters_attn_proj_4096x4096_first_sweep.txt")
 
 
 def log(msg):
@@ -142,6 +149,72 @@ def _oracle_sweeps(jarq, cfg, H, R, Ws, qs, ss, zs, sweeps):
     return time.perf_counter() - t0
 
 
+def stage_counters():
+    """Per-dispatch HBM and LDS bytes of the sweep's kernels in the first sweep
+    of a run, from rocprofv3 counters (the committed summary); a kernel whose
+    source has changed since is left out."""
+    if not os.path.exists(STAGE_COUNTERS_FILE):
+        return {}
+    kv = {}
+    for line in open(STAGE_COUNTERS_FILE):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    out = {}
+    for key in kv:
+        if not key.endswith(".source"):
+            continue
+        name = key[:-len(".source")]
+        try:
+            digest = hashlib.sha256(open(os.path.join(ROOT, kv[key]), "rb").read()).hexdigest()
+            if digest != kv[name + ".source_sha256"]:
+                continue
+            out[name] = {f: float(kv[f"{name}.{f}"]) for f in
+                         ("hbm_fetch_bytes", "hbm_write_bytes", "lds_read_bytes", "lds_write_bytes",
+                          "lds_bank_conflict_cycles")}
+        except (OSError, KeyError, ValueError):
+            continue
+    return out
+
+
+def stage_rooflines(cfg, rows, stb, npan):
+    """HBM and LDS rates of the Gram, Babai and panel-update kernels in the
+    first sweep (full Gram build, every row changes), from the per-launch
+    time of that sweep (HIP events) and the counted bytes per dispatch."""
+    from paper_2609_38599_amd.binding import STAGE_NAMES
+    d, g = cfg.cols, cfg.group_size
+    G, pg = d // g, min(512 // g, 16)
+    sm = stb["stage_ms"][0]
+    launch = {"gram_kernel": sm[STAGE_NAMES.index("gram")],
+              "babai_kernel": sm[STAGE_NAMES.index("babai")] / npan,
+              "panel_update_kernel": sm[STAGE_NAMES.index("panel")] / max(npan - 1, 1)}
+    # the method's own work per launch (FLOP as in the residual product's
+    # roofline: fp32-equivalent, against the fp16 peak the kernel runs on)
+    flop = {"gram_kernel": float(rows) * (d * d + d * g),
+            "babai_kernel": 2.0 * rows * pg * g * g,
+            "panel_update_kernel": None}
+    counted = stage_counters()
+    out = {}
+    for k, ms in launch.items():
+        e = {"launch_ms": ms, "scope": "first sweep of a run"}
+        c = counted.get(k)
+        if c is not None and ms > 0:
+            hbm = c["hbm_fetch_bytes"] + c["hbm_write_bytes"]
+            lds = c["lds_read_bytes"] + c["lds_write_bytes"]
+            e.update({"hbm_bytes": hbm, "hbm_gbs": hbm / (ms * 1e-3) / 1e9,
+                      "hbm_frac": hbm / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                      "lds_bytes": lds, "lds_gbs": lds / (ms * 1e-3) / 1e9,
+                      "lds_frac": lds / (ms * 1e-3) / 1e9 / PEAK_LDS_GBS,
+                      "lds_bank_conflict_cycles": c["lds_bank_conflict_cycles"]})
+        else:
+            e.update({"hbm_bytes": None, "lds_bytes": None})
+        if flop[k] is not None and ms > 0:
+            e["algorithmic_flop"] = flop[k]
+            e["frac_of_fp16_peak"] = flop[k] / (ms * 1e-3) / 1e12 / PEAK_FP16_MFMA_TFLOPS
+        out[k] = e
+    return out
+
+
 def cpu_baseline(cfg, W, H, q, s, z, rows, sweeps, st_rows=256):
     """The float64 oracle on the host cores, over a bounded sample of the workload,
     with every BLAS thread, then on one thread over a smaller sample."""
@@ -173,6 +246,25 @@ def cpu_baseline(cfg, W, H, q, s, z, rows, sweeps, st_rows=256):
                                 "sample": f"1 sweep over rows 0..{st_rows - 1}, one BLAS thread, "
                                           f"{dt1:.1f} s wall, scaled by rows"}
     return out
+
+
+def lds_probe(workgroups=4096, passes=128, reps=5):
+    import torch
+    import paper_2609_38599_amd as jq
+    out = torch.empty(workgroups * 256, dtype=torch.float32, device="cuda")
+    for _ in range(2):
+        jq.binding.lds_probe(workgroups, passes, out)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        n, _ = jq.binding.lds_probe(workgroups, passes, out)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    log(f"[bench] LDS probe: {workgroups} work-groups x {passes} passes, {n} LDS bytes per dispatch "
+        f"({workgroups * 32768} written, {workgroups * 32768 * passes} read), {ms:.4f} ms, "
+        f"{n / (ms * 1e-3) / 1e12:.2f} TB/s")
 
 
 def copy_probe():
@@ -251,6 +343,8 @@ def main():
                     help="sweeps per timed run (default: the layer's own sweep count)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--reps", type=int, default=5, help="timed runs of --steps sweeps")
+    ap.add_argument("--no-own-k", action="store_true",
+                    help="do not also time the layer's own sweep count when --steps differs")
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--tau", type=float, default=-1.0,
                     help="early-stopping threshold (App. E.2 uses 1e-5); negative = off (default)")
@@ -258,6 +352,7 @@ def main():
     ap.add_argument("--cpu-sweeps", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--lds-probe", action="store_true")
     ap.add_argument("--no-setup", action="store_true",
                     help="skip the timed per-layer set-up leg (Hessian from tokens, RTN host)")
     ap.add_argument("--inputs", default=None,
@@ -270,6 +365,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe()
+        return
+    if args.lds_probe:
+        lds_probe()
         return
 
     import torch
@@ -351,7 +449,7 @@ def main():
     res_ms = float(np.mean([r[1]["stage_ms"][k][res_stage] for r in runs
                             for k in range(min(r[1]["sweeps_run"], len(r[1]["stage_ms"])))]))
     own_k = None
-    if args.steps != cfg.sweeps:
+    if args.steps != cfg.sweeps and not args.no_own_k:
         own = np.array([r[0] for r in timed_runs(cfg.sweeps, args.reps)])
         own_k = {"sweeps": cfg.sweeps, "ms_per_sweep_median": float(np.median(own)),
                  "ms_per_sweep_iqr": [float(v) for v in np.percentile(own, [25, 75])]}
@@ -421,6 +519,10 @@ def main():
         "roofline": roofline,
         "stage_rates_tflops": {name: (work[name] / (stage_ms[name] * 1e-3) / 1e12
                                       if stage_ms[name] > 0 else None) for name in STAGE_NAMES},
+        "stage_rooflines": stage_rooflines(cfg, rows, stb, (cols // g + min(512 // g, 16) - 1)
+                                           // min(512 // g, 16)),
+        "peaks": {"fp16_mfma_tflops": PEAK_FP16_MFMA_TFLOPS, "hbm_gbs": PEAK_HBM_GBS,
+                  "lds_gbs": PEAK_LDS_GBS},
     }
     if not args.no_setup:
         log("[bench] per-layer set-up leg (Hessian from calibration tokens, RTN host)")

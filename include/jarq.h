@@ -381,6 +381,18 @@ jarq_status jarq_act_order(const float* H, int32_t d, int32_t* perm, void* strea
 jarq_status jarq_permute(const jarq_params* p, const int32_t* perm, const float* W, const float* H,
                          float* Wp, float* Hp, void* stream);
 
+/*
+ * Measurement aid (not part of refinement): a kernel that moves a known
+ * number of bytes through the local data share (LDS), used to scale LDS
+ * profiler counters to bytes and to see the rate the LDS sustains for a
+ * streaming reader.  `workgroups` work-groups of 256 threads each write 32 KB
+ * of LDS once and read it `passes` times (16-byte reads, no bank conflict),
+ * then write one float per thread to out [workgroups * 256] (device, 4-byte
+ * aligned).  Returns the LDS bytes moved (writes + reads), or -1 on a bad
+ * argument or a failed launch.  Asynchronous.
+ */
+int64_t jarq_lds_probe(int32_t workgroups, int32_t passes, float* out, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* jarq_status_string(jarq_status s);
 

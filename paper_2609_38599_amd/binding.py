@@ -111,6 +111,7 @@ _SIGNATURES = {
     "jarq_gptq_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Params)]),
     "jarq_gptq": (ctypes.c_int, [ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
                                  ctypes.c_size_t, _vp]),
+    "jarq_lds_probe": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32, _vp, _vp]),
     "jarq_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "jarq_abi_version": (ctypes.c_int32, []),
 }
@@ -471,6 +472,18 @@ def gptq(p: Params, W, H, codes=None, scales=None, zeros=None, ws=None, stream=N
                          _ptr(zeros, torch.int32, "zeros"), _ptr(ws, torch.uint8, "workspace"),
                          ws.numel(), _stream(stream)), "jarq_gptq")
     return codes, scales, zeros
+
+
+def lds_probe(workgroups, passes, out=None, stream=None):
+    """Run the LDS calibration kernel; returns (LDS bytes moved, out)."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty(workgroups * 256, dtype=torch.float32, device="cuda")
+    n = int(lib.jarq_lds_probe(int(workgroups), int(passes), _ptr(out, torch.float32, "out"),
+                               _stream(stream)))
+    if n < 0:
+        raise JarqError(JARQ_EINVAL, "jarq_lds_probe")
+    return n, out
 
 
 def abi_version() -> int:

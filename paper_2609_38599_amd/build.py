@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "jarq")
 LIB = os.path.join(HERE, "libjarq.so")
-SOURCES = ["chol.hip", "split.hip", "sgemm.hip", "objective.hip", "gemm.hip", "gram.hip", "solve.hip", "babai.hip", "pupdate.hip", "misc.hip", "setup.hip", "linalg.hip", "gptq.hip", "qep.hip", "post.hip", "api.hip"]
+SOURCES = ["chol.hip", "split.hip", "sgemm.hip", "objective.hip", "gemm.hip", "gram.hip", "solve.hip", "babai.hip", "pupdate.hip", "misc.hip", "setup.hip", "linalg.hip", "gptq.hip", "qep.hip", "post.hip", "probe.hip", "api.hip"]
 ARCH = "gfx950"
 
 

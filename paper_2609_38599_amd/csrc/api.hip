@@ -58,7 +58,6 @@ Layout make_layout(int rows, int cols, int g) {
   L.lprev = take(R * sizeof(double));
   L.active = take(R);
   L.stopat = take(R * sizeof(int32_t));
-  L.chg = take(R * G);
   L.glist = take(G * R * sizeof(int32_t));
   L.gcount = take(G * sizeof(uint32_t));
   L.gctl = take(sizeof(GramCtl));
@@ -120,7 +119,6 @@ struct Ctx {
   float* gram() const { return (float*)(ws + lay.gram); }
   float* pbuf() const { return (float*)(ws + lay.p); }
   double* objpart() const { return (double*)(ws + lay.objpart); }
-  uint8_t* chg() const { return (uint8_t*)(ws + lay.chg); }
   GramCtl* gctl() const { return (GramCtl*)(ws + lay.gctl); }
   SweepCtl* sctl() const { return (SweepCtl*)(ws + lay.sctl); }
   uint32_t* gcount() const { return (uint32_t*)(ws + lay.gcount); }
@@ -162,13 +160,15 @@ struct NoHook {
 // sweep at most (the current count in *n_dev when it is not null), position p
 // holding layer row map_row(rowmap, p).  The per-panel row counters must be
 // zero when the first Babai launch runs: zeroed here unless the caller's
-// previous launch did (counts_zeroed).  hook(kind, panel, phase) runs before
+// previous launch did (counts_zeroed).  With `lists` the Babai launches also
+// append each row that accepted group i to the group's list (glist, gcount),
+// whose counters the caller has zeroed.  hook(kind, panel, phase) runs before
 // (phase 0) and after (phase 1) each launch: kind 0 Babai, 1 panel update.
 template <typename Hook = NoHook>
 hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const int* n_dev,
                          uint8_t* codes, const float* scales, const int32_t* zeros,
                          const uint8_t* active, uint8_t* cand, uint8_t* decision,
-                         bool counts_zeroed = false, Hook hook = Hook()) {
+                         bool counts_zeroed = false, bool lists = false, Hook hook = Hook()) {
   const int nb = panel_groups(c.g);
   if (!counts_zeroed) {
     hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, c.panels() * sizeof(uint32_t));
@@ -179,7 +179,9 @@ hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const int* 
     hipError_t e = hook(0, q, 0);
     if (e == hipSuccess)
       e = launch_babai(c.st, n, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay, codes,
-                       scales, zeros, active, cand, decision, c.cnt(), rowmap, n_dev, c.chg());
+                       scales, zeros, active, cand, decision, c.cnt(), rowmap, n_dev,
+                       lists ? (int32_t*)(c.ws + c.lay.glist) : nullptr,
+                       lists ? c.gcount() : nullptr, c.rows);
     if (e == hipSuccess) e = hook(0, q, 1);
     if (e != hipSuccess) return e;
     if (i1 * c.g >= c.cols) break;  // no later columns to update
@@ -306,17 +308,17 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
       e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(),
                             (int32_t*)(c.ws + c.lay.stopat), k + 1, p->tau, rmap,
-                            (uint32_t*)(c.ws + c.lay.pcount), npan, n_dev);
+                            (uint32_t*)(c.ws + c.lay.pcount), npan, c.gcount(), c.G, n_dev);
     if (e == hipSuccess) e = mark(k, 5);
     if (e == hipSuccess)
       e = enqueue_babai(c, n, rmap, n_dev, codes, scales, zeros, c.active(), nullptr, nullptr,
-                        /*counts_zeroed=*/true, hook);
+                        /*counts_zeroed=*/true, /*lists=*/true, hook);
     if (e == hipSuccess)
       e = launch_record_sweep(c.st, c.rows, (const double*)(c.ws + c.lay.lcur), c.active(),
                               c.cnt(),
                               c.hist() + (k < JARQ_MAX_RECORDED_SWEEPS ? k
                                                                         : JARQ_MAX_RECORDED_SWEEPS - 1),
-                              c.sctl(), c.gctl(), c.gcount(), c.G);
+                              c.sctl(), c.gctl());
     // the rows still active after this sweep's stopping test, for the next one
     if (e == hipSuccess && stopping)
       e = launch_compact_rows(c.st, c.rows, c.active(), c.rowmap(), c.sctl());

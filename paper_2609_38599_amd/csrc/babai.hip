@@ -179,7 +179,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     uint8_t* __restrict__ cand_out,
     uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt,
     const int32_t* __restrict__ rowmap, const int* __restrict__ n_dev,
-    uint8_t* __restrict__ chg) {
+    int32_t* __restrict__ glist, uint32_t* __restrict__ gcount, int list_stride) {
   if (n_dev != nullptr) rows = *n_dev;
   if ((int)blockIdx.x * 16 >= rows) return;  // the whole work-group: no row here
   constexpr int g = G_SIZE;
@@ -203,7 +203,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   __shared__ __attribute__((aligned(16))) _Float16 dqp_s[RT * PW];  // accepted changes in the panel
   __shared__ int tacc_s[PG];                         // any row of the tile accepted group
   __shared__ int cnt_s[4];                           // accepted, changed, skipped, blocks
-  __shared__ int racc_s[RT];                         // the row accepted a change in the panel
+  __shared__ int racc_s[RT];                         // bit i - i0: the row accepted group i
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -357,7 +357,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   // across them.
   if (chain_wave) {
     chain_prefetch(i0);
-    bool any_acc = false;  // this row accepted a change in the panel
+    int acc_bits = 0;  // bit i - i0: this row accepted group i
     __syncthreads();       // u and R~ of group i0 staged
     for (int i = i0; i < i1; ++i) {
       // ---- back substitution of group i, 16 lanes per row ----
@@ -413,8 +413,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
           cand_out[cbase + cj + 16 * t] =
               (uint8_t)(do_row ? fminf(fmaxf(qold[t] + cs.d[t], 0.f), qmax) : qold[t]);
       }
-      any_acc |= accept;
-      if (chg != nullptr && row_in && cj == 0) chg[(size_t)crid * G + i] = accept ? 1 : 0;
+      acc_bits |= accept ? 1 << (i - i0) : 0;
       if (row_in && cj == 0) {
         if (dec_out != nullptr) {
           uint8_t dd = !row_act ? kDecStopped : (skip ? kDecSkip : (accept ? kDecAccept : kDecReject));
@@ -430,7 +429,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       lds_barrier();  // group i decided: its changes are in dqp_s, tacc_s
       lds_barrier();  // u and R~ of group i + 1 ready
     }
-    if (row_in && cj == 0) racc_s[crow] = any_acc ? 1 : 0;
+    if (row_in && cj == 0) racc_s[crow] = acc_bits;
   } else {
     // Group i0 + p stages group i0 + p + 1 and applies the changes of groups
     // i0 .. i0 + p to it.  Each position p has its own body, so the
@@ -511,6 +510,34 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     if (lane == 0 && m != 0) base = atomicAdd(pcount, (uint32_t)__popcll(m));
     base = __shfl(base, 0);
     if (f) plist[base + (uint32_t)__popcll(m & ((1ull << lane) - 1))] = r0 + lane;
+  } else if (wave == 1 && glist != nullptr) {
+    // ---- and, per group of the panel, to that group's list of changed rows
+    // (the next sweep forms the Gram entries of only those): lane p reserves
+    // room for group i0 + p, every lane r then writes row r's entries
+    const int ng = i1 - i0;
+    int mask = 0;  // rows of the tile that accepted group i0 + lane
+    if (lane < ng) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) mask |= ((racc_s[r] >> lane) & 1) << r;
+    }
+    uint32_t base = 0;
+    if (lane < ng && mask != 0) base = atomicAdd(&gcount[i0 + lane], (uint32_t)__popc(mask));
+    if (lane < RT && r0 + lane < rows) {
+      const int bits = racc_s[lane];
+      const int lrow_r = map_row(rowmap, r0 + lane);
+      for (int p = 0; p < ng; ++p) {
+        const int mp = __shfl(mask, p);
+        const uint32_t bp = __shfl(base, p);
+        if ((bits >> p) & 1)
+          glist[(size_t)(i0 + p) * list_stride + bp + (uint32_t)__popc(mp & ((1 << lane) - 1))] =
+              lrow_r;
+      }
+    } else {
+      for (int p = 0; p < ng; ++p) {  // the shuffles need every lane
+        (void)__shfl(mask, p);
+        (void)__shfl(base, p);
+      }
+    }
   }
 
   // ---- codes += accepted changes and dq = accepted changes, over the panel's
@@ -555,7 +582,8 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                                  const float* P, const char* ws, const Layout& lay,
                                  uint8_t* codes, const float* scales, const uint8_t* active,
                                  uint8_t* cand, uint8_t* decision, Counters* cnt,
-                                 const int32_t* rowmap, const int* n_dev, uint8_t* chg) {
+                                 const int32_t* rowmap, const int* n_dev, int32_t* glist,
+                                 uint32_t* gcount, int list_stride) {
   constexpr int g = G_SIZE;
   constexpr int PG = panel_groups_of(g);
   if (i1 - i0 > PG || i0 % PG != 0) return hipErrorInvalidValue;
@@ -570,7 +598,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.rdsq), codes, scales, active,
                      (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
                      (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt, rowmap, n_dev,
-                     chg);
+                     glist, gcount, list_stride);
   return hipGetLastError();
 }
 
@@ -579,18 +607,18 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
                         const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
                         uint8_t* decision, Counters* cnt, const int32_t* rowmap, const int* n_dev,
-                        uint8_t* chg) {
+                        int32_t* glist, uint32_t* gcount, int list_stride) {
   (void)zeros;
   switch (g) {
     case 32:
       return launch_babai_t<32>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt, rowmap, n_dev, chg);
+                                cand, decision, cnt, rowmap, n_dev, glist, gcount, list_stride);
     case 64:
       return launch_babai_t<64>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt, rowmap, n_dev, chg);
+                                cand, decision, cnt, rowmap, n_dev, glist, gcount, list_stride);
     case 128:
       return launch_babai_t<128>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                 cand, decision, cnt, rowmap, n_dev, chg);
+                                 cand, decision, cnt, rowmap, n_dev, glist, gcount, list_stride);
     default:
       return hipErrorInvalidValue;
   }

@@ -13,8 +13,8 @@
 //
 // Incremental build: entry (a, h) depends on the codes of groups a and h
 // only, so after a code update only the entries of groups whose codes changed
-// need forming.  The code update marks, per row, the groups it changed; the
-// rows that changed group x are listed per x, and a work-group takes a tile of
+// need forming.  The code update lists, per group x, the rows whose group x
+// it changed (in any order), and a work-group takes a tile of
 // 128 listed rows of one x and forms the G entries of row and column x of
 // their matrices, (a, x) for a < x and (x, h) for h >= x, with the same
 // block_entries arithmetic, so every entry is bit-identical to the full
@@ -74,33 +74,6 @@ __device__ __forceinline__ bool gram_use_lists(const GramCtl* ctl, const uint32_
   return 3 * listed * G < 2 * full;
 }
 }  // namespace
-
-// Rows of the sweep's positions [0, n) whose code update changed group x are
-// appended to glist[x]: a work-group takes 256 positions and one group x
-// (blockIdx.y), each wavefront reserves room for its listed rows with one
-// atomic and writes them in lane order (the order within a list is
-// immaterial).  Nothing is listed while the matrices are incomplete.
-__global__ __launch_bounds__(256) void gram_lists_kernel(int rows, int G,
-                                                         const int* __restrict__ n_dev,
-                                                         const int32_t* __restrict__ rowmap,
-                                                         const uint8_t* __restrict__ chg,
-                                                         const GramCtl* __restrict__ ctl,
-                                                         int32_t* __restrict__ glist,
-                                                         uint32_t* __restrict__ gcount) {
-  if (ctl->valid == 0) return;
-  const int n = n_dev != nullptr ? *n_dev : rows;
-  const int x = blockIdx.y;
-  const int p = blockIdx.x * 256 + threadIdx.x;
-  if ((int)blockIdx.x * 256 >= n) return;  // uniform
-  const int row = map_row(rowmap, p < n ? p : 0);
-  const bool listed = p < n && chg[(size_t)row * G + x] != 0;
-  const unsigned long long m = __ballot(listed);
-  const int lane = threadIdx.x & 63;
-  uint32_t base = 0;
-  if (lane == 0 && m != 0) base = atomicAdd(&gcount[x], (uint32_t)__popcll(m));
-  base = __shfl(base, 0);
-  if (listed) glist[(size_t)x * rows + base + (uint32_t)__popcll(m & ((1ull << lane) - 1))] = row;
-}
 
 // ---- pieces shared by both builds (so every entry has one arithmetic) ----
 
@@ -445,10 +418,6 @@ static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* 
   if (e == hipSuccess && incremental)
     e = allow_dynamic_lds((const void*)gram_listed_kernel<g>, lds, listed_set);
   if (e != hipSuccess) return e;
-  if (incremental)
-    hipLaunchKernelGGL(gram_lists_kernel, dim3((rows + 255) / 256, G), dim3(256), 0, st, rows, G,
-                       n_dev, rowmap, (const uint8_t*)(ws + lay.chg), ctl,
-                       (int32_t*)(ws + lay.glist), (uint32_t*)(ws + lay.gcount));
   hipLaunchKernelGGL((gram_kernel<g>), dim3((rows + RT - 1) / RT, (G + 1) / 2), dim3(256), lds,
                      st, rows, cols, (const _Float16*)(ws + lay.hhi),
                      (const _Float16*)(ws + lay.hlo), (const float*)(ws + lay.hscale), codes,

@@ -119,7 +119,6 @@ struct Layout {
   size_t lprev;     // [rows] f64
   size_t active;    // [rows] u8
   size_t stopat;    // [rows] i32: iteration at which the row stopped, 0 while it has not
-  size_t chg;       // [rows][G] u8: the last code update changed group (row, i)
   size_t glist;     // [G][rows] i32: rows that changed group i (incremental Gram build)
   size_t gcount;    // [G] u32: length of each list
   size_t gctl;      // GramCtl
@@ -174,7 +173,8 @@ hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, con
 // Upper triangles of the grouped Gram matrices from the fp16 planes of H,
 // stored by layer row.  incremental: build from the rows listed per changed
 // group when that is cheaper and the matrices of the last sweep are complete
-// (the code update marks the changed groups in chg; GramCtl in the workspace).
+// (the code update lists the rows it changed per group in glist / gcount;
+// GramCtl in the workspace).
 hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws,
                        const Layout& lay, const uint8_t* codes, const int32_t* zeros,
                        float* gram, const int32_t* rowmap, const int* n_dev, bool incremental);
@@ -185,13 +185,15 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                         float lam, float rcond, int accept, const int32_t* rowmap,
                         const int* n_dev);
 
-// Code update of the groups [i0, i1) (one panel).  chg[row][i] (nullable) is
-// set to whether the update changed group i of the row.
+// Code update of the groups [i0, i1) (one panel).  With glist not null, every
+// row whose group i the update changed is appended (as its layer row, in any
+// order) to glist[i * list_stride ...], gcount[i] counting the entries; the
+// counters are zeroed before the sweep's first panel.
 hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,
                         const float* P, const char* ws, const Layout& lay, uint8_t* codes,
                         const float* scales, const int32_t* zeros, const uint8_t* active,
                         uint8_t* cand, uint8_t* decision, Counters* cnt, const int32_t* rowmap,
-                        const int* n_dev, uint8_t* chg);
+                        const int* n_dev, int32_t* glist, uint32_t* gcount, int list_stride);
 
 // Work-group barrier for LDS only: waits for this wave's LDS operations,
 // not for its outstanding global loads (a __syncthreads would, which drains
@@ -239,16 +241,16 @@ hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* 
 hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
                              int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
-                             int nzero, const int* n_dev);
+                             int nzero, uint32_t* zero_words2, int nzero2, const int* n_dev);
 
 hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);
 hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n);
 
-// Also: gram->valid = 1 (every active row's matrix now exists), gcount[0..G)
-// zeroed for the next sweep's lists, sctl->started counted.
+// Also: gram->valid = 1 (every active row's matrix now exists),
+// sctl->started counted.
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
                                const uint8_t* active, Counters* cnt, SweepRecord* rec,
-                               SweepCtl* sctl, GramCtl* gctl, uint32_t* gcount, int G);
+                               SweepCtl* sctl, GramCtl* gctl);
 
 hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
                            const uint8_t* codes, const int32_t* zeros, Flags* flags);

@@ -31,9 +31,14 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
                                   int sweep, float tau,
                                   const int32_t* __restrict__ rowmap,
                                   uint32_t* __restrict__ zero_words, int nzero,
+                                  uint32_t* __restrict__ zero_words2, int nzero2,
                                   const int* __restrict__ n_dev) {
-  // the code update's per-panel row counters start the sweep at zero
-  if (blockIdx.x == 0 && (int)threadIdx.x < nzero) zero_words[threadIdx.x] = 0u;
+  // counters the code update appends to start it at zero (its per-panel and
+  // per-group row lists)
+  if (blockIdx.x == 0) {
+    if ((int)threadIdx.x < nzero) zero_words[threadIdx.x] = 0u;
+    for (int t = threadIdx.x; t < nzero2; t += blockDim.x) zero_words2[t] = 0u;
+  }
   if (n_dev != nullptr) n = *n_dev;
   const int pos = blockIdx.x * blockDim.x + threadIdx.x;
   if (pos >= n) return;
@@ -57,11 +62,11 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
 hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
                              int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
-                             int nzero, const int* n_dev) {
-  if (n <= 0 || nzero < 0 || nzero > 256) return hipErrorInvalidValue;
+                             int nzero, uint32_t* zero_words2, int nzero2, const int* n_dev) {
+  if (n <= 0 || nzero < 0 || nzero > 256 || nzero2 < 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stop_check_kernel, dim3((n + 255) / 256), dim3(256), 0, st, n, nt,
                      objpart, lcur, lprev, active, stopat, sweep, tau, rowmap, zero_words, nzero,
-                     n_dev);
+                     zero_words2, nzero2, n_dev);
   return hipGetLastError();
 }
 
@@ -124,9 +129,7 @@ constexpr int kRecordThreads = 1024;
 __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     int rows, const double* __restrict__ lcur, const uint8_t* __restrict__ active,
     Counters* __restrict__ cnt, SweepRecord* __restrict__ rec, SweepCtl* __restrict__ sctl,
-    GramCtl* __restrict__ gctl, uint32_t* __restrict__ gcount, int G) {
-  // the next sweep's Gram row lists start empty
-  for (int x = threadIdx.x; x < G; x += kRecordThreads) gcount[x] = 0u;
+    GramCtl* __restrict__ gctl) {
   __shared__ double red[kRecordThreads];
   __shared__ unsigned int act[kRecordThreads];
   double s = 0.0;
@@ -184,9 +187,9 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
 
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
                                const uint8_t* active, Counters* cnt, SweepRecord* rec,
-                               SweepCtl* sctl, GramCtl* gctl, uint32_t* gcount, int G) {
+                               SweepCtl* sctl, GramCtl* gctl) {
   hipLaunchKernelGGL(record_sweep_kernel, dim3(1), dim3(kRecordThreads), 0, st, rows, lcur, active,
-                     cnt, rec, sctl, gctl, gcount, G);
+                     cnt, rec, sctl, gctl);
   return hipGetLastError();
 }
 

@@ -11,6 +11,17 @@
         bytes for a plain device copy of N bytes; prints key = value lines for
         the named kernel (read by bench.py) and a table for every kernel.
 
+    python3 -m paper_2609_38599_amd.profiling counters --fetch F.csv --write W.csv \
+        --copy-fetch CF.csv --copy-write CW.csv --copy-bytes N \
+        --lds L.csv --probe-lds PL.csv --probe-read-bytes R --probe-write-bytes S \
+        --kernel gram_kernel=paper_2609_38599_amd/csrc/gram.hip [--kernel ...]
+        per named kernel and dispatch: HBM bytes (FETCH_SIZE / WRITE_SIZE scaled
+        by the plain copy) and LDS bytes (SQ_INSTS_LDS_LOAD_BANDWIDTH /
+        SQ_INSTS_LDS_STORE_BANDWIDTH, 64-byte units, scaled so that the LDS
+        probe kernel reads R and writes S bytes per dispatch), with the LDS
+        bank-conflict cycles; key = value lines (read by bench.py) keyed by
+        the kernel source's sha256.
+
 Reads CSV written by rocprofv3 --output-format csv; nothing here touches the GPU.
 """
 
@@ -55,11 +66,21 @@ def stats(path: str, sweeps: int) -> str:
     return "\n".join(out)
 
 
-def per_kernel_mean(path: str) -> dict:
+def per_kernel_mean(path: str, counter: str = None) -> dict:
+    """Mean counter value per dispatch for each kernel (one counter name, or
+    the only one the file holds)."""
     acc = collections.defaultdict(list)
     for r in csv.DictReader(open(path)):
+        if counter is not None and r.get("Counter_Name") != counter:
+            continue
         acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
     return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def _find(means: dict, name: str):
+    """The kernel whose name contains `name` (the first by sorted name)."""
+    keys = sorted(k for k in means if name in k)
+    return keys[0] if keys else None
 
 
 def copy_factor(path: str, nbytes: int) -> float:
@@ -100,6 +121,50 @@ def traffic(a) -> str:
     return "\n".join(kv + lines)
 
 
+def counters(a) -> str:
+    ff = copy_factor(a.copy_fetch, a.copy_bytes)
+    fw = copy_factor(a.copy_write, a.copy_bytes)
+    fetch, write = per_kernel_mean(a.fetch), per_kernel_mean(a.write)
+    ld = per_kernel_mean(a.lds, "SQ_INSTS_LDS_LOAD_BANDWIDTH")
+    st = per_kernel_mean(a.lds, "SQ_INSTS_LDS_STORE_BANDWIDTH")
+    bank = per_kernel_mean(a.lds, "SQ_LDS_BANK_CONFLICT")
+    active = per_kernel_mean(a.lds, "SQ_LDS_IDX_ACTIVE")
+    pld = per_kernel_mean(a.probe_lds, "SQ_INSTS_LDS_LOAD_BANDWIDTH")
+    pst = per_kernel_mean(a.probe_lds, "SQ_INSTS_LDS_STORE_BANDWIDTH")
+    probe = _find(pld, "lds_probe")
+    if probe is None:
+        raise SystemExit(f"lds_probe_kernel not in {a.probe_lds}")
+    fl = a.probe_read_bytes / (64.0 * pld[probe])
+    fs = a.probe_write_bytes / (64.0 * pst[probe])
+    lines = [f"# FETCH_SIZE scale {ff:.4f}, WRITE_SIZE scale {fw:.4f} (plain copy of {a.copy_bytes} bytes)",
+             f"# LDS load scale {fl:.4f}, store scale {fs:.4f} (probe: {a.probe_read_bytes} bytes "
+             f"read, {a.probe_write_bytes} written per dispatch; counters in 64-byte units)"]
+    kv = [f"fetch_scale = {ff:.4f}", f"write_scale = {fw:.4f}",
+          f"lds_load_scale = {fl:.4f}", f"lds_store_scale = {fs:.4f}"]
+    lines.append(f"# {'kernel':30s} {'fetch MiB':>10s} {'write MiB':>10s} {'LDS rd MiB':>11s} "
+                 f"{'LDS wr MiB':>11s} {'bank confl':>11s} {'LDS active':>11s}   per dispatch")
+    for spec in a.kernel:
+        name, src = spec.split("=", 1)
+        k = _find(fetch, name)
+        kl = _find(ld, name)
+        if k is None or kl is None:
+            raise SystemExit(f"kernel {name} missing from the counter files")
+        fb = fetch[k] * ff * 1024
+        wb = write.get(_find(write, name), 0.0) * fw * 1024
+        lr = ld[kl] * 64.0 * fl
+        lw = st.get(_find(st, name), 0.0) * 64.0 * fs
+        digest = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
+        kv += [f"{name}.source = {src}", f"{name}.source_sha256 = {digest}",
+               f"{name}.hbm_fetch_bytes = {fb:.0f}", f"{name}.hbm_write_bytes = {wb:.0f}",
+               f"{name}.lds_read_bytes = {lr:.0f}", f"{name}.lds_write_bytes = {lw:.0f}",
+               f"{name}.lds_bank_conflict_cycles = {bank.get(_find(bank, name), 0.0):.0f}",
+               f"{name}.lds_idx_active_cycles = {active.get(_find(active, name), 0.0):.0f}"]
+        lines.append(f"# {short_name(k):30s} {fb / 2**20:10.2f} {wb / 2**20:10.2f} {lr / 2**20:11.2f} "
+                     f"{lw / 2**20:11.2f} {bank.get(_find(bank, name), 0.0):11.0f} "
+                     f"{active.get(_find(active, name), 0.0):11.0f}")
+    return "\n".join(kv + lines)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -111,8 +176,21 @@ def main(argv=None):
     for name in ("fetch", "write", "copy_fetch", "copy_write", "kernel", "source"):
         t.add_argument("--" + name.replace("_", "-"), dest=name, required=True)
     t.add_argument("--copy-bytes", dest="copy_bytes", type=int, required=True)
+    c = sub.add_parser("counters")
+    for name in ("fetch", "write", "copy_fetch", "copy_write", "lds", "probe_lds"):
+        c.add_argument("--" + name.replace("_", "-"), dest=name, required=True)
+    c.add_argument("--copy-bytes", dest="copy_bytes", type=int, required=True)
+    c.add_argument("--probe-read-bytes", dest="probe_read_bytes", type=float, required=True)
+    c.add_argument("--probe-write-bytes", dest="probe_write_bytes", type=float, required=True)
+    c.add_argument("--kernel", action="append", required=True,
+                   help="name=source: a kernel (substring of its name) and its source file")
     a = ap.parse_args(argv)
-    print(stats(a.csv, a.sweeps) if a.cmd == "stats" else traffic(a))
+    if a.cmd == "stats":
+        print(stats(a.csv, a.sweeps))
+    elif a.cmd == "traffic":
+        print(traffic(a))
+    else:
+        print(counters(a))
 
 
 if __name__ == "__main__":

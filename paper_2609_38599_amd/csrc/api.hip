@@ -12,7 +12,7 @@
 namespace jarq {
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
-// One row counter per panel of the code update.
+// Panels of the code update (each has kSubLists row counters).
 static int pcount_words(int cols, int g) {
   const int pg = panel_groups_of(g);
   return (cols / g + pg - 1) / pg;
@@ -51,19 +51,21 @@ Layout make_layout(int rows, int cols, int g) {
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
-  L.plist = take(R * sizeof(int32_t));
-  L.pcount = take(pcount_words(C, g) * sizeof(uint32_t));
+  const size_t cap = (size_t)sublist_cap(rows);
+  L.plist = take(kSubLists * cap * sizeof(int32_t));
+  L.pcount = take(pcount_words(C, g) * kSubLists * kCtrStride * sizeof(uint32_t));
   L.objpart = take(R * (nt > G ? nt : G) * sizeof(double));  // per-group sweep partials or 64-column slices
   L.lcur = take(R * sizeof(double));
   L.lprev = take(R * sizeof(double));
   L.active = take(R);
   L.stopat = take(R * sizeof(int32_t));
-  L.glist = take(G * R * sizeof(int32_t));
-  L.gcount = take(G * sizeof(uint32_t));
+  L.glist = take(G * kSubLists * cap * sizeof(int32_t));
+  L.gcount = take(G * kSubLists * kCtrStride * sizeof(uint32_t));
+  L.gpre = take(G * (kSubLists + 1) * sizeof(int32_t));
   L.gctl = take(sizeof(GramCtl));
   L.sctl = take(sizeof(SweepCtl));
   L.rowmap = take(R * sizeof(int32_t));
-  L.counters = take(sizeof(Counters));
+  L.counters = take(kSubLists * sizeof(Counters));
   L.hist = take(JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord));
   L.flags = take(sizeof(Flags));
   L.total = off;
@@ -171,7 +173,8 @@ hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const int* 
                          bool counts_zeroed = false, bool lists = false, Hook hook = Hook()) {
   const int nb = panel_groups(c.g);
   if (!counts_zeroed) {
-    hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount, c.panels() * sizeof(uint32_t));
+    hipError_t e0 = launch_zero_bytes(c.st, c.ws + c.lay.pcount,
+                                      (size_t)c.panels() * kSubLists * kCtrStride * sizeof(uint32_t));
     if (e0 != hipSuccess) return e0;
   }
   for (int i0 = 0, q = 0; i0 < c.G; i0 += nb, ++q) {
@@ -181,7 +184,7 @@ hipError_t enqueue_babai(const Ctx& c, int n, const int32_t* rowmap, const int* 
       e = launch_babai(c.st, n, c.cols, c.g, c.bits, i0, i1, c.pbuf(), c.ws, c.lay, codes,
                        scales, zeros, active, cand, decision, c.cnt(), rowmap, n_dev,
                        lists ? (int32_t*)(c.ws + c.lay.glist) : nullptr,
-                       lists ? c.gcount() : nullptr, c.rows);
+                       lists ? c.gcount() : nullptr, sublist_cap(c.rows));
     if (e == hipSuccess) e = hook(0, q, 1);
     if (e != hipSuccess) return e;
     if (i1 * c.g >= c.cols) break;  // no later columns to update
@@ -199,7 +202,7 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
                          void* stream) {
   Ctx c = make_ctx(p, ws, stream);
   JQ_HIP(launch_zero_bytes(c.st, c.flags(), sizeof(Flags)));
-  JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
+  JQ_HIP(launch_zero_bytes(c.st, c.cnt(), kSubLists * sizeof(Counters)));
   JQ_HIP(launch_chol_groups(c.st, c.cols, c.g, H, c.ws, c.lay));
   JQ_HIP(launch_split_r(c.st, c.cols, c.g, c.ws, c.lay));
   JQ_HIP(launch_split_m(c.st, c.cols, c.g, H, c.ws, c.lay));
@@ -234,13 +237,13 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
 
   JQ_HIP(launch_fill_u8(c.st, c.active(), (size_t)c.rows, 1));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.stopat, (size_t)c.rows * sizeof(int32_t)));
-  JQ_HIP(launch_zero_bytes(c.st, c.cnt(), sizeof(Counters)));
+  JQ_HIP(launch_zero_bytes(c.st, c.cnt(), kSubLists * sizeof(Counters)));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lcur, (size_t)c.rows * sizeof(double)));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.lprev, (size_t)c.rows * sizeof(double)));
   JQ_HIP(launch_zero_bytes(c.st, c.hist(), JARQ_MAX_RECORDED_SWEEPS * sizeof(SweepRecord)));
   JQ_HIP(launch_zero_bytes(c.st, c.gctl(), sizeof(GramCtl)));
   JQ_HIP(launch_zero_bytes(c.st, c.sctl(), sizeof(SweepCtl)));
-  JQ_HIP(launch_zero_bytes(c.st, c.gcount(), (size_t)c.G * sizeof(uint32_t)));
+  JQ_HIP(launch_zero_bytes(c.st, c.gcount(), (size_t)c.G * kSubLists * kCtrStride * sizeof(uint32_t)));
   // every row active: rowmap = 0 .. rows - 1, sctl->n = rows
   JQ_HIP(launch_compact_rows(c.st, c.rows, c.active(), c.rowmap(), c.sctl()));
 
@@ -308,7 +311,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
       e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(),
                             (int32_t*)(c.ws + c.lay.stopat), k + 1, p->tau, rmap,
-                            (uint32_t*)(c.ws + c.lay.pcount), npan, c.gcount(), c.G, n_dev);
+                            (uint32_t*)(c.ws + c.lay.pcount), npan * kSubLists, c.gcount(),
+                            c.G * kSubLists, n_dev);
     if (e == hipSuccess) e = mark(k, 5);
     if (e == hipSuccess)
       e = enqueue_babai(c, n, rmap, n_dev, codes, scales, zeros, c.active(), nullptr, nullptr,
@@ -318,7 +322,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
                               c.cnt(),
                               c.hist() + (k < JARQ_MAX_RECORDED_SWEEPS ? k
                                                                         : JARQ_MAX_RECORDED_SWEEPS - 1),
-                              c.sctl(), c.gctl());
+                              c.sctl(), c.gctl(), c.gcount(), (int32_t*)(c.ws + c.lay.gpre),
+                              c.G);
     // the rows still active after this sweep's stopping test, for the next one
     if (e == hipSuccess && stopping)
       e = launch_compact_rows(c.st, c.rows, c.active(), c.rowmap(), c.sctl());

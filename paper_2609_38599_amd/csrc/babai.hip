@@ -179,7 +179,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     uint8_t* __restrict__ cand_out,
     uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt,
     const int32_t* __restrict__ rowmap, const int* __restrict__ n_dev,
-    int32_t* __restrict__ glist, uint32_t* __restrict__ gcount, int list_stride) {
+    int32_t* __restrict__ glist, uint32_t* __restrict__ gcount, int list_cap) {
   if (n_dev != nullptr) rows = *n_dev;
   if ((int)blockIdx.x * 16 >= rows) return;  // the whole work-group: no row here
   constexpr int g = G_SIZE;
@@ -502,14 +502,17 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 
   __syncthreads();  // racc_s
   // ---- rows that accepted a change: appended to the panel's row list (the
-  // panel update folds in only these rows; their order there is immaterial)
+  // panel update folds in only these rows; their order there is immaterial),
+  // this work-group's sub-list
+  const int sub = (int)blockIdx.x % kSubLists;
   if (wave == 0) {
     const bool f = lane < RT && racc_s[lane] != 0;
     const unsigned long long m = __ballot(f);
     uint32_t base = 0;
-    if (lane == 0 && m != 0) base = atomicAdd(pcount, (uint32_t)__popcll(m));
+    if (lane == 0 && m != 0) base = atomicAdd(&pcount[sub * kCtrStride], (uint32_t)__popcll(m));
     base = __shfl(base, 0);
-    if (f) plist[base + (uint32_t)__popcll(m & ((1ull << lane) - 1))] = r0 + lane;
+    if (f)
+      plist[(size_t)sub * list_cap + base + (uint32_t)__popcll(m & ((1ull << lane) - 1))] = r0 + lane;
   } else if (wave == 1 && glist != nullptr) {
     // ---- and, per group of the panel, to that group's list of changed rows
     // (the next sweep forms the Gram entries of only those): lane p reserves
@@ -521,7 +524,9 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       for (int r = 0; r < RT; ++r) mask |= ((racc_s[r] >> lane) & 1) << r;
     }
     uint32_t base = 0;
-    if (lane < ng && mask != 0) base = atomicAdd(&gcount[i0 + lane], (uint32_t)__popc(mask));
+    if (lane < ng && mask != 0)
+      base = atomicAdd(&gcount[((size_t)(i0 + lane) * kSubLists + sub) * kCtrStride],
+                       (uint32_t)__popc(mask));
     if (lane < RT && r0 + lane < rows) {
       const int bits = racc_s[lane];
       const int lrow_r = map_row(rowmap, r0 + lane);
@@ -529,8 +534,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         const int mp = __shfl(mask, p);
         const uint32_t bp = __shfl(base, p);
         if ((bits >> p) & 1)
-          glist[(size_t)(i0 + p) * list_stride + bp + (uint32_t)__popc(mp & ((1 << lane) - 1))] =
-              lrow_r;
+          glist[((size_t)(i0 + p) * kSubLists + sub) * list_cap + bp +
+                (uint32_t)__popc(mp & ((1 << lane) - 1))] = lrow_r;
       }
     } else {
       for (int p = 0; p < ng; ++p) {  // the shuffles need every lane
@@ -570,10 +575,11 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     }
   }
   if (tid == 0) {
-    if (cnt_s[0]) atomicAdd(&cnt->accepted, (unsigned long long)cnt_s[0]);
-    if (cnt_s[1]) atomicAdd(&cnt->changed, (unsigned long long)cnt_s[1]);
-    if (cnt_s[2]) atomicAdd(&cnt->skipped, (unsigned long long)cnt_s[2]);
-    if (cnt_s[3]) atomicAdd(&cnt->corr_blocks, (unsigned long long)cnt_s[3]);
+    Counters* c = cnt + sub;
+    if (cnt_s[0]) atomicAdd(&c->accepted, (unsigned long long)cnt_s[0]);
+    if (cnt_s[1]) atomicAdd(&c->changed, (unsigned long long)cnt_s[1]);
+    if (cnt_s[2]) atomicAdd(&c->skipped, (unsigned long long)cnt_s[2]);
+    if (cnt_s[3]) atomicAdd(&c->corr_blocks, (unsigned long long)cnt_s[3]);
   }
 }
 
@@ -583,7 +589,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                                  uint8_t* codes, const float* scales, const uint8_t* active,
                                  uint8_t* cand, uint8_t* decision, Counters* cnt,
                                  const int32_t* rowmap, const int* n_dev, int32_t* glist,
-                                 uint32_t* gcount, int list_stride) {
+                                 uint32_t* gcount, int list_cap) {
   constexpr int g = G_SIZE;
   constexpr int PG = panel_groups_of(g);
   if (i1 - i0 > PG || i0 % PG != 0) return hipErrorInvalidValue;
@@ -597,8 +603,8 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.rdinv),
                      (const float*)(ws + lay.rdsq), codes, scales, active,
                      (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
-                     (uint32_t*)(ws + lay.pcount) + i0 / PG, cand, decision, cnt, rowmap, n_dev,
-                     glist, gcount, list_stride);
+                     (uint32_t*)(ws + lay.pcount) + (size_t)(i0 / PG) * kSubLists * kCtrStride,
+                     cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap);
   return hipGetLastError();
 }
 
@@ -607,18 +613,18 @@ hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int
                         const char* ws, const Layout& lay, uint8_t* codes, const float* scales,
                         const int32_t* zeros, const uint8_t* active, uint8_t* cand,
                         uint8_t* decision, Counters* cnt, const int32_t* rowmap, const int* n_dev,
-                        int32_t* glist, uint32_t* gcount, int list_stride) {
+                        int32_t* glist, uint32_t* gcount, int list_cap) {
   (void)zeros;
   switch (g) {
     case 32:
       return launch_babai_t<32>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt, rowmap, n_dev, glist, gcount, list_stride);
+                                cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap);
     case 64:
       return launch_babai_t<64>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                cand, decision, cnt, rowmap, n_dev, glist, gcount, list_stride);
+                                cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap);
     case 128:
       return launch_babai_t<128>(st, rows, cols, bits, i0, i1, P, ws, lay, codes, scales, active,
-                                 cand, decision, cnt, rowmap, n_dev, glist, gcount, list_stride);
+                                 cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap);
     default:
       return hipErrorInvalidValue;
   }

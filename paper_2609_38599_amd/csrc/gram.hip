@@ -57,16 +57,19 @@ __device__ __forceinline__ void codes_to_f16(uint32_t q4, f16x2 zz, f16x2* out) 
 // blocks than the full build (tiles of 128 rows x G blocks per changed group,
 // against pairs of a-groups x (G + 1) blocks per tile of the n rows; a listed
 // block costs more, its work-group stages the codes of two groups).
-// Evaluated by whole wavefronts: lane l reads the counts of groups l and l + 64
-// (a layer has at most 128 groups), and a reduction over the lanes gives
-// every lane the same answer.
-__device__ __forceinline__ bool gram_use_lists(const GramCtl* ctl, const uint32_t* gcount, int G,
+// Evaluated by whole wavefronts: lane l reads the lengths of the lists of
+// groups l and l + 64 (a layer has at most 128 groups), and a reduction over
+// the lanes gives every lane the same answer.
+__device__ __forceinline__ int list_length(const int32_t* gpre, int x) {
+  return gpre[x * (kSubLists + 1) + kSubLists];
+}
+__device__ __forceinline__ bool gram_use_lists(const GramCtl* ctl, const int32_t* gpre, int G,
                                                int n) {
   if (ctl == nullptr || ctl->valid == 0) return false;
   const int lane = threadIdx.x & 63;
   int tiles = 0;
-  if (lane < G) tiles += ((int)gcount[lane] + RT - 1) / RT;
-  if (lane + 64 < G) tiles += ((int)gcount[lane + 64] + RT - 1) / RT;
+  if (lane < G) tiles += (list_length(gpre, lane) + RT - 1) / RT;
+  if (lane + 64 < G) tiles += (list_length(gpre, lane + 64) + RT - 1) / RT;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) tiles += __shfl_xor(tiles, off);
   const long long listed = tiles;
@@ -217,12 +220,12 @@ __global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
                                                       const int32_t* __restrict__ rowmap,
                                                       const int* __restrict__ n_dev,
                                                       GramCtl* __restrict__ ctl,
-                                                      const uint32_t* __restrict__ gcount) {
+                                                      const int32_t* __restrict__ gpre) {
   using S = GramShape<G_SIZE>;
   const int G = cols / S::g;
   const int n = n_dev != nullptr ? *n_dev : rows;
   // every work-group takes the same branch (same counts, same n)
-  const bool lists = gram_use_lists(ctl, gcount, G, n);
+  const bool lists = gram_use_lists(ctl, gpre, G, n);
   if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && ctl != nullptr)
     ctl->listed = lists ? 1 : 0;
   if (lists) return;
@@ -296,11 +299,11 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
     const float* __restrict__ h_inv, const uint8_t* __restrict__ codes,
     const int32_t* __restrict__ zeros, float* __restrict__ gram, const int* __restrict__ n_dev,
     const GramCtl* __restrict__ ctl, const int32_t* __restrict__ glist,
-    const uint32_t* __restrict__ gcount) {
+    const int32_t* __restrict__ gpre, int list_cap) {
   using S = GramShape<G_SIZE>;
   const int G = cols / S::g;
   const int n = n_dev != nullptr ? *n_dev : rows;
-  if (!gram_use_lists(ctl, gcount, G, n)) return;  // uniform
+  if (!gram_use_lists(ctl, gpre, G, n)) return;  // uniform
   const int nch = (G + kChunk - 1) / kChunk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
   const float hinv = *h_inv;
@@ -312,7 +315,8 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
   // counts over the groups, Hillis-Steele over 128 + 1 entries)
   __shared__ int first_s[kMaxGramGroups + 1];
   __shared__ int scan_s[kMaxGramGroups];
-  if (tid < kMaxGramGroups) scan_s[tid] = tid < G ? (int)((gcount[tid] + RT - 1) / RT) * nch : 0;
+  if (tid < kMaxGramGroups)
+    scan_s[tid] = tid < G ? ((list_length(gpre, tid) + RT - 1) / RT) * nch : 0;
   __syncthreads();
   for (int w = 1; w < kMaxGramGroups; w <<= 1) {
     const int v = (tid < kMaxGramGroups && tid >= w) ? scan_s[tid - w] : 0;
@@ -329,8 +333,16 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
   // Item geometry; the codes of x and of the item's first block are fetched
   // one item ahead (during the previous item's last block).
   struct Item {
-    int x, b0, b1, r0, ntile, lrow;
-    const int* lst;
+    int x, b0, b1, r0, ntile, lrow, orow;
+  };
+  // Layer row at position k of group x's list (the concatenation of its
+  // sub-lists): k lies in the last sub-list that starts at or before it.
+  auto list_row = [&](int x, int k) {
+    const int32_t* pr = gpre + x * (kSubLists + 1);
+    int s = 0;
+#pragma unroll
+    for (int q = 1; q < kSubLists; ++q) s = pr[q] <= k ? q : s;
+    return glist[((size_t)x * kSubLists + s) * list_cap + (k - pr[s])];
   };
   auto locate = [&](int item) {
     Item it;
@@ -343,13 +355,15 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
     }
     const int x = lo;
     const int local = item - first_s[x];
-    const int tiles = (int)((gcount[x] + RT - 1) / RT);
+    const int len = list_length(gpre, x);
+    const int tiles = (len + RT - 1) / RT;
     const int c = local / tiles, t = local - c * tiles;
     it.x = x;
     it.r0 = t * RT;
-    it.ntile = (int)gcount[x];
-    it.lst = glist + (size_t)x * rows;
-    it.lrow = it.lst[it.r0 + (it.r0 + trow < it.ntile ? trow : 0)];
+    it.ntile = len;
+    it.lrow = list_row(x, it.r0 + (it.r0 + trow < len ? trow : 0));
+    // the output row of thread tid < RT
+    it.orow = list_row(x, it.r0 + (tid < RT && it.r0 + tid < len ? tid : 0));
     it.b0 = c * kChunk;
     it.b1 = min(it.b0 + kChunk, G);
     return it;
@@ -370,7 +384,7 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
   while (true) {
     const int x = it.x;
     const bool store = tid < RT && it.r0 + tid < it.ntile;
-    float* grow_out = gram + (size_t)it.lst[it.r0 + (store ? tid : 0)] * G * G;
+    float* grow_out = gram + (size_t)it.orow * G * G;
     const int next = item + gridDim.x;
     Item nt = it;
     lds_barrier();  // the previous item's reads are done
@@ -412,7 +426,7 @@ static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* 
   const size_t lds = GramShape<g>::lds_bytes();
   GramCtl* ctl = incremental ? (GramCtl*)(ws + lay.gctl) : nullptr;
   const int32_t* glist = (const int32_t*)(ws + lay.glist);
-  const uint32_t* gcount = (const uint32_t*)(ws + lay.gcount);
+  const int32_t* gpre = (const int32_t*)(ws + lay.gpre);
   static std::atomic<unsigned long long> full_set{0}, listed_set{0};
   hipError_t e = allow_dynamic_lds((const void*)gram_kernel<g>, lds, full_set);
   if (e == hipSuccess && incremental)
@@ -421,7 +435,7 @@ static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* 
   hipLaunchKernelGGL((gram_kernel<g>), dim3((rows + RT - 1) / RT, (G + 1) / 2), dim3(256), lds,
                      st, rows, cols, (const _Float16*)(ws + lay.hhi),
                      (const _Float16*)(ws + lay.hlo), (const float*)(ws + lay.hscale), codes,
-                     zeros, gram, rowmap, n_dev, ctl, gcount);
+                     zeros, gram, rowmap, n_dev, ctl, gpre);
   if (incremental) {
     // two resident work-groups per CU, each looping over the listed items
     int dev = 0, ncu = 256;
@@ -431,7 +445,7 @@ static hipError_t launch_gram_t(hipStream_t st, int rows, int cols, const char* 
     hipLaunchKernelGGL((gram_listed_kernel<g>), dim3(wgs), dim3(256), lds, st, rows, cols,
                        (const _Float16*)(ws + lay.hhi), (const _Float16*)(ws + lay.hlo),
                        (const float*)(ws + lay.hscale), codes, zeros, gram, n_dev, ctl, glist,
-                       gcount);
+                       gpre, sublist_cap(rows));
   }
   return hipGetLastError();
 }

@@ -21,6 +21,10 @@ enum : uint8_t { kDecReject = 0, kDecAccept = 1, kDecSkip = 2, kDecStopped = 3 }
 
 // Device-side counters of one sweep.  Integer atomics only, so totals do not
 // depend on scheduling.
+// Counts of one sweep.  The workspace holds kSubLists copies, one cache line
+// each: work-group b of the code update adds into copy b % kSubLists (a
+// single copy would serialise every work-group's atomics); the sweep record
+// sums them.
 struct Counters {
   unsigned long long accepted;
   unsigned long long changed;
@@ -30,7 +34,20 @@ struct Counters {
   unsigned int solve_failed;
   unsigned int active_rows;
   unsigned int pad;
+  unsigned char line_pad[80];      // one 128-byte line per copy
 };
+
+// Row lists that every work-group of a launch appends to are split into
+// kSubLists sub-lists: work-group b appends to sub-list b % kSubLists, whose
+// counter sits kCtrStride words (one cache line) away from the next one's.
+// A list is the concatenation of its sub-lists; each sub-list has room for
+// sublist_cap(rows) entries.
+constexpr int kSubLists = 16;
+constexpr int kCtrStride = 32;
+__host__ __device__ inline int sublist_cap(int rows) {
+  const int tiles = (rows + 15) / 16;
+  return 16 * ((tiles + kSubLists - 1) / kSubLists);
+}
 
 // One recorded sweep.
 struct SweepRecord {
@@ -112,15 +129,16 @@ struct Layout {
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
   size_t p;         // [rows][cols] f32: (W - What) H
   size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
-  size_t plist;     // [rows] i32: rows that accepted a change in the last panel (any order)
-  size_t pcount;    // [panels] u32: length of that list, one counter per panel
+  size_t plist;     // [kSubLists][cap] i32: rows that accepted a change in the last panel (any order)
+  size_t pcount;    // [panels][kSubLists] u32 kCtrStride apart: lengths of the sub-lists
   size_t objpart;   // [rows][ceil(cols/64)] f64: partial row objectives
   size_t lcur;      // [rows] f64
   size_t lprev;     // [rows] f64
   size_t active;    // [rows] u8
   size_t stopat;    // [rows] i32: iteration at which the row stopped, 0 while it has not
-  size_t glist;     // [G][rows] i32: rows that changed group i (incremental Gram build)
-  size_t gcount;    // [G] u32: length of each list
+  size_t glist;     // [G][kSubLists][cap] i32: rows that changed group i (incremental Gram build)
+  size_t gcount;    // [G][kSubLists] u32 kCtrStride apart: lengths of the sub-lists
+  size_t gpre;      // [G][kSubLists + 1] i32: their exclusive prefix sums (last: list length)
   size_t gctl;      // GramCtl
   size_t sctl;      // SweepCtl
   size_t rowmap;    // [rows] i32: row of each position of the sweep (rows still active, ascending)
@@ -185,15 +203,17 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
                         float lam, float rcond, int accept, const int32_t* rowmap,
                         const int* n_dev);
 
-// Code update of the groups [i0, i1) (one panel).  With glist not null, every
-// row whose group i the update changed is appended (as its layer row, in any
-// order) to glist[i * list_stride ...], gcount[i] counting the entries; the
-// counters are zeroed before the sweep's first panel.
+// Code update of the groups [i0, i1) (one panel).  The positions of the rows
+// that accepted a change go to the panel's row list (plist, pcount).  With
+// glist not null, every row whose group i the update changed is appended (as
+// its layer row, in any order) to group i's list (glist, gcount); the
+// counters are zeroed before the sweep's first panel.  list_cap =
+// sublist_cap(rows of the layer).
 hipError_t launch_babai(hipStream_t st, int rows, int cols, int g, int bits, int i0, int i1,
                         const float* P, const char* ws, const Layout& lay, uint8_t* codes,
                         const float* scales, const int32_t* zeros, const uint8_t* active,
                         uint8_t* cand, uint8_t* decision, Counters* cnt, const int32_t* rowmap,
-                        const int* n_dev, int32_t* glist, uint32_t* gcount, int list_stride);
+                        const int* n_dev, int32_t* glist, uint32_t* gcount, int list_cap);
 
 // Work-group barrier for LDS only: waits for this wave's LDS operations,
 // not for its outstanding global loads (a __syncthreads would, which drains
@@ -228,7 +248,8 @@ constexpr int panel_groups_of(int g) { return 512 / g < kMaxPanelGroups ? 512 / 
 int panel_groups(int g);
 
 // P(:, c1:) -= the accepted changes of the groups in columns [c0, c1) (the
-// panel's rows listed by the code update in plist / pcount[panel]).
+// panel's rows listed by the code update in the panel's plist / pcount
+// sub-lists; rows = the layer's rows).
 hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0, int c1,
                                const char* ws, const Layout& lay, const float* scales, float* P,
                                const int32_t* rowmap);
@@ -236,21 +257,23 @@ hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0
 hipError_t launch_row_objective(hipStream_t st, int rows, int nt, const double* objpart,
                                 double* out);
 
-// Also zeroes zero_words[0 .. nzero) (nzero <= 256) before any row is handled.
+// Also zeroes the counters zero_ctr[t * kCtrStride], t < nzero, and likewise
+// zero_ctr2 (the code update's list counters) before any row is handled.
 // A row that stops gets stopat[row] = sweep.
 hipError_t launch_stop_check(hipStream_t st, int rows, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
-                             int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
-                             int nzero, uint32_t* zero_words2, int nzero2, const int* n_dev);
+                             int sweep, float tau, const int32_t* rowmap, uint32_t* zero_ctr,
+                             int nzero, uint32_t* zero_ctr2, int nzero2, const int* n_dev);
 
 hipError_t launch_fill_u8(hipStream_t st, uint8_t* p, size_t n, uint8_t v);
 hipError_t launch_zero_bytes(hipStream_t st, void* p, size_t n);
 
 // Also: gram->valid = 1 (every active row's matrix now exists),
-// sctl->started counted.
+// sctl->started counted, gpre = the prefix sums of the Gram row sub-lists.
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
                                const uint8_t* active, Counters* cnt, SweepRecord* rec,
-                               SweepCtl* sctl, GramCtl* gctl);
+                               SweepCtl* sctl, GramCtl* gctl, const uint32_t* gcount,
+                               int32_t* gpre, int G);
 
 hipError_t launch_validate(hipStream_t st, int rows, int cols, int g, int bits,
                            const uint8_t* codes, const int32_t* zeros, Flags* flags);

@@ -30,14 +30,14 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
                                   uint8_t* __restrict__ active, int32_t* __restrict__ stopat,
                                   int sweep, float tau,
                                   const int32_t* __restrict__ rowmap,
-                                  uint32_t* __restrict__ zero_words, int nzero,
-                                  uint32_t* __restrict__ zero_words2, int nzero2,
+                                  uint32_t* __restrict__ zero_ctr, int nzero,
+                                  uint32_t* __restrict__ zero_ctr2, int nzero2,
                                   const int* __restrict__ n_dev) {
   // counters the code update appends to start it at zero (its per-panel and
   // per-group row lists)
   if (blockIdx.x == 0) {
-    if ((int)threadIdx.x < nzero) zero_words[threadIdx.x] = 0u;
-    for (int t = threadIdx.x; t < nzero2; t += blockDim.x) zero_words2[t] = 0u;
+    for (int t = threadIdx.x; t < nzero; t += blockDim.x) zero_ctr[(size_t)t * kCtrStride] = 0u;
+    for (int t = threadIdx.x; t < nzero2; t += blockDim.x) zero_ctr2[(size_t)t * kCtrStride] = 0u;
   }
   if (n_dev != nullptr) n = *n_dev;
   const int pos = blockIdx.x * blockDim.x + threadIdx.x;
@@ -61,12 +61,12 @@ __global__ void stop_check_kernel(int n, int nt, const double* __restrict__ part
 
 hipError_t launch_stop_check(hipStream_t st, int n, int nt, const double* objpart,
                              double* lcur, double* lprev, uint8_t* active, int32_t* stopat,
-                             int sweep, float tau, const int32_t* rowmap, uint32_t* zero_words,
-                             int nzero, uint32_t* zero_words2, int nzero2, const int* n_dev) {
-  if (n <= 0 || nzero < 0 || nzero > 256 || nzero2 < 0) return hipErrorInvalidValue;
+                             int sweep, float tau, const int32_t* rowmap, uint32_t* zero_ctr,
+                             int nzero, uint32_t* zero_ctr2, int nzero2, const int* n_dev) {
+  if (n <= 0 || nzero < 0 || nzero2 < 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stop_check_kernel, dim3((n + 255) / 256), dim3(256), 0, st, n, nt,
-                     objpart, lcur, lprev, active, stopat, sweep, tau, rowmap, zero_words, nzero,
-                     zero_words2, nzero2, n_dev);
+                     objpart, lcur, lprev, active, stopat, sweep, tau, rowmap, zero_ctr, nzero,
+                     zero_ctr2, nzero2, n_dev);
   return hipGetLastError();
 }
 
@@ -129,7 +129,17 @@ constexpr int kRecordThreads = 1024;
 __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     int rows, const double* __restrict__ lcur, const uint8_t* __restrict__ active,
     Counters* __restrict__ cnt, SweepRecord* __restrict__ rec, SweepCtl* __restrict__ sctl,
-    GramCtl* __restrict__ gctl) {
+    GramCtl* __restrict__ gctl, const uint32_t* __restrict__ gcount, int32_t* __restrict__ gpre,
+    int G) {
+  // prefix sums of the Gram row sub-lists, one group per thread
+  for (int x = threadIdx.x; x < G; x += kRecordThreads) {
+    int acc = 0;
+    for (int s = 0; s < kSubLists; ++s) {
+      gpre[x * (kSubLists + 1) + s] = acc;
+      acc += (int)gcount[((size_t)x * kSubLists + s) * kCtrStride];
+    }
+    gpre[x * (kSubLists + 1) + kSubLists] = acc;
+  }
   __shared__ double red[kRecordThreads];
   __shared__ unsigned int act[kRecordThreads];
   double s = 0.0;
@@ -160,13 +170,22 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     __syncthreads();
   }
   if (threadIdx.x == 0) {
+    Counters sum{};
+    for (int c = 0; c < kSubLists; ++c) {
+      sum.accepted += cnt[c].accepted;
+      sum.changed += cnt[c].changed;
+      sum.skipped += cnt[c].skipped;
+      sum.corr_blocks += cnt[c].corr_blocks;
+      sum.ridge_rows += cnt[c].ridge_rows;
+      sum.solve_failed += cnt[c].solve_failed;
+    }
     rec->objective_after_scales = red[0];
-    rec->accepted = cnt->accepted;
-    rec->changed = cnt->changed;
-    rec->skipped = cnt->skipped;
-    rec->corr_blocks = cnt->corr_blocks;
-    rec->ridge_rows = cnt->ridge_rows;
-    rec->solve_failed = cnt->solve_failed;
+    rec->accepted = sum.accepted;
+    rec->changed = sum.changed;
+    rec->skipped = sum.skipped;
+    rec->corr_blocks = sum.corr_blocks;
+    rec->ridge_rows = sum.ridge_rows;
+    rec->solve_failed = sum.solve_failed;
     rec->active_rows = act[0];
     const int started = sctl->n;
     rec->started_rows = (unsigned int)started;
@@ -175,21 +194,24 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
       sctl->started += 1;
       gctl->valid = 1;  // every row that took part has its matrix built
     }
-    cnt->accepted = 0;
-    cnt->changed = 0;
-    cnt->skipped = 0;
-    cnt->corr_blocks = 0;
-    cnt->ridge_rows = 0;
-    cnt->solve_failed = 0;
-    cnt->active_rows = 0;
+    for (int c = 0; c < kSubLists; ++c) {
+      cnt[c].accepted = 0;
+      cnt[c].changed = 0;
+      cnt[c].skipped = 0;
+      cnt[c].corr_blocks = 0;
+      cnt[c].ridge_rows = 0;
+      cnt[c].solve_failed = 0;
+      cnt[c].active_rows = 0;
+    }
   }
 }
 
 hipError_t launch_record_sweep(hipStream_t st, int rows, const double* lcur,
                                const uint8_t* active, Counters* cnt, SweepRecord* rec,
-                               SweepCtl* sctl, GramCtl* gctl) {
+                               SweepCtl* sctl, GramCtl* gctl, const uint32_t* gcount,
+                               int32_t* gpre, int G) {
   hipLaunchKernelGGL(record_sweep_kernel, dim3(1), dim3(kRecordThreads), 0, st, rows, lcur, active,
-                     cnt, rec, sctl, gctl);
+                     cnt, rec, sctl, gctl, gcount, gpre, G);
   return hipGetLastError();
 }
 

@@ -77,7 +77,7 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
     int rows, int cols, int g, int c0, int c1, const _Float16* __restrict__ dq,
     const _Float16* __restrict__ Mh, const _Float16* __restrict__ Ml,
     const float* __restrict__ bcol_inv, const float* __restrict__ scales,
-    const int32_t* __restrict__ plist, const uint32_t* __restrict__ pcount,
+    const int32_t* __restrict__ plist, const uint32_t* __restrict__ pcount, int list_cap,
     float* __restrict__ P, const int32_t* __restrict__ rowmap) {
   // Three stages in three distinct arrays: the loads of steps k + 1 and k + 2
   // fly while step k computes.
@@ -97,16 +97,28 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   const int ng = (c1 - c0) / g;
 
   // Only rows that accepted a change in the panel need an update: the code
-  // update listed them (plist, pcount entries); this work-group takes list
-  // positions m0 .. m0 + BM - 1, and work-groups past the end have nothing to do.
-  const int total = (int)*pcount;
+  // update listed them in kSubLists sub-lists (plist, pcount); this
+  // work-group takes positions m0 .. m0 + BM - 1 of their concatenation, and
+  // work-groups past the end have nothing to do.
+  int pre[kSubLists + 1];  // exclusive prefix sums of the sub-list lengths (uniform)
+  pre[0] = 0;
+#pragma unroll
+  for (int s = 0; s < kSubLists; ++s) pre[s + 1] = pre[s] + (int)pcount[s * kCtrStride];
+  const int total = pre[kSubLists];
   if (m0 >= total) return;  // uniform across the work-group
   const int nvalid = min(BM, total - m0);
   // The list lives in the third stage, which is first loaded after every
   // use of it (set-up, behind the loop's first barrier); a separate array
   // would push the work-group past half of the LDS (one per CU).
   int* rl_s = (int*)buf2;
-  if (tid < BM) rl_s[tid] = plist[m0 + (tid < nvalid ? tid : 0)];
+  if (tid < BM) {
+    // position m lies in the last sub-list that starts at or before it
+    const int m = m0 + (tid < nvalid ? tid : 0);
+    int s = 0;
+#pragma unroll
+    for (int q = 1; q < kSubLists; ++q) s = pre[q] <= m ? q : s;
+    rl_s[tid] = plist[(size_t)s * list_cap + (m - pre[s])];
+  }
   __syncthreads();
   // Tile row t is row rl_s[t] for t < nvalid; later tile rows repeat a valid row
   // and are never stored.
@@ -279,7 +291,9 @@ hipError_t launch_panel_update(hipStream_t st, int rows, int cols, int g, int c0
                      (const _Float16*)(ws + lay.dq), (const _Float16*)(ws + lay.mhi),
                      (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow), scales,
                      (const int32_t*)(ws + lay.plist),
-                     (const uint32_t*)(ws + lay.pcount) + c0 / (g * panel_groups_of(g)), P, rowmap);
+                     (const uint32_t*)(ws + lay.pcount) +
+                         (size_t)(c0 / (g * panel_groups_of(g))) * kSubLists * kCtrStride,
+                     sublist_cap(rows), P, rowmap);
   return hipGetLastError();
 }
 

@@ -19,9 +19,10 @@ of the same K sweeps from the host state with events around every stage.
 
 The roofline fraction counts the method's own work: 2 rows d^2 FLOP per
 residual product, against the dense fp16 matrix-core peak (the product runs
-on fp16 matrix cores, each fp32 operand held as two fp16 terms; the three
-fp16 products that this split executes are reported separately as the
-executed rate).
+on fp16 matrix cores as W M^T - What M^T: the layer's W M^T is formed once,
+and each sweep multiplies the exact codes minus zero points by M held as two
+fp16 terms, with the scales applied to each group's partial sum; the two fp16
+products executed per sweep are reported separately as the executed rate).
 
 After the sweeps, a set-up leg (not part of a sweep; --no-setup skips it)
 times the per-layer set-up on the GPU: the Hessian from the layer's 262,144
@@ -68,16 +69,16 @@ def log(msg):
 
 
 def stage_work(cfg, rows, corr_blocks):
-    """Algorithmic FLOP of each stage for one sweep (per row: residual product 2 d^2 as three
-    fp16 products, Gram (d^2 + d g)/2 MACs on two planes, Babai core 2 d g plus corrections)."""
+    """Executed FLOP of each stage for one sweep (per row: residual product 2 d^2 as two fp16
+    products, Gram (d^2 + d g)/2 MACs on two planes, objective two products over the
+    triangle of each group, Babai core 2 d g plus corrections)."""
     d, g = cfg.cols, cfg.group_size
     G = d // g
     return {
         "gram": 2.0 * 2.0 * rows * (d * d + d * g) / 2.0,   # two fp16 planes x (d^2+dg)/2 MACs
         "solve": rows * (G ** 3 / 3.0 + 4 * G * G + 2 * d),
-        "esplit": 0.0,
-        "residual": 3 * 2.0 * rows * d * d,                 # three fp16 products of U = E M^T
-        "objective": 2.0 * rows * d * g / 2.0,              # (R_i e_i) per group, triangular
+        "residual": 2 * 2.0 * rows * d * d,                 # two fp16 products of What M^T
+        "objective": 2 * 2.0 * rows * d * g / 2.0,          # cz R_i^T per group, triangular
         "babai": 2.0 * rows * d * g + 2.0 * 16 * g * g * 2 * corr_blocks,
         "panel": 0.0,                                       # in proportion to the rows that changed
     }
@@ -465,18 +466,18 @@ def main():
     blocks = float(np.mean(st["correction_blocks"][:n]))
     work = stage_work(cfg, rows, blocks)
 
-    # Roofline of the residual product kernel (split3_kernel, one launch per
+    # Roofline of the residual product kernel (resid_kernel, one launch per
     # sweep, timed alone by the library's events inside the timed calls): the
     # single kernel with the largest time per sweep.  achieved = the method's
     # own work, 2 rows d^2 FLOP per launch, over the average launch time,
     # against the dense fp16 matrix-core peak (the dtype the contraction runs
-    # in).  The three fp16 products the two-term split executes are reported
-    # as the executed rate and fraction.
+    # in).  The two fp16 products it executes are reported as the executed
+    # rate and fraction.
     t_res = res_ms * 1e-3
     algorithmic = 2.0 * rows * cols * cols
     achieved = algorithmic / t_res / 1e12
     executed = work["residual"] / t_res / 1e12
-    roofline = {"bound": "mfma", "kernel": "split3_kernel", "achieved": achieved,
+    roofline = {"bound": "mfma", "kernel": "resid_kernel", "achieved": achieved,
                 "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / PEAK_FP16_MFMA_TFLOPS, "traffic": traffic_from_profile(),
                 "launch_ms": res_ms, "algorithmic_flop_per_launch": algorithmic,
@@ -494,7 +495,7 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16x2-split/f32acc",
+        "dtype": "f16-codes x f16x2-split/f32acc",
         "data": "synthetic",
         "config": {"workload": workload_text(cfg, rows, cols, args.steps),
                    "rows": rows, "cols": cols, "group_size": g, "bits": bits,
@@ -504,8 +505,10 @@ def main():
         "ms_per_sweep_runs": per_sweep.tolist(),
         "ms_per_sweep_iqr": [q25, q75],
         "own_sweep_count": own_k,
-        "dtype_note": "contractions on fp16 matrix cores with fp32 operands split into two fp16 "
-                      "terms (22-bit products) and fp32 accumulation; scale solves in fp64",
+        "dtype_note": "contractions on fp16 matrix cores: exact codes minus zero points (fp16) "
+                      "times fp32 operands split into two fp16 terms (22-bit products), fp32 "
+                      "accumulation, group scales applied to each group's partial sum; the "
+                      "layer's W M^T formed once with three such products; scale solves in fp64",
         "prep_ms": prep_ms,
         "stage_ms": stage_ms,
         "stage_ms_note": "separate untimed run of the same sweeps with HIP events around every stage",

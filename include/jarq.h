@@ -50,14 +50,14 @@
 extern "C" {
 #endif
 
-#define JARQ_ABI_VERSION 8
+#define JARQ_ABI_VERSION 9
 /* Timed stages of a sweep (jarq_stats.stage_ms columns): 0 Gram matrices,
- * 1 scale solve, 2 residual split of E = W - What into fp16 planes,
- * 3 residual product U = E M^T, 4 row objectives and stopping test,
- * 5 code update: the Babai kernels (one per panel of groups), 6 code update:
- * the panel updates between them.  Stages 5 and 6 interleave; each of their
- * launches is timed on its own. */
-#define JARQ_NUM_STAGES 7
+ * 1 scale solve, 2 residual product U = E M^T (formed as W M^T - What M^T
+ * from the codes), 3 row objectives and stopping test, 4 code update: the
+ * Babai kernels (one per panel of groups), 5 code update: the panel updates
+ * between them.  Stages 4 and 5 interleave; each of their launches is timed
+ * on its own. */
+#define JARQ_NUM_STAGES 6
 #define JARQ_MAX_RECORDED_SWEEPS 64
 
 typedef enum jarq_status {
@@ -190,7 +190,7 @@ jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H,
  * device memory (code under graph capture, tight serving loops, harnesses
  * that forbid allocation): the same kernels run on a workspace that the
  * library holds in a static device array of JARQ_STATIC_WORKSPACE_BYTES
- * (384 MiB; enough for a 4096 x 4096 layer at g = 128), created on each GPU
+ * (512 MiB; enough for a 4096 x 4096 layer at g = 128), created on each GPU
  * the library runs on and held until the process ends.  The call allocates
  * nothing: no hipMalloc, no hipFree, no HIP event.  Layers whose
  * jarq_workspace_bytes exceeds the limit are rejected with
@@ -202,7 +202,7 @@ jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H,
  * GPU, from any stream or thread, race and must be serialised by the caller.
  * Synchronises `stream`.
  */
-#define JARQ_STATIC_WORKSPACE_BYTES (384u << 20)
+#define JARQ_STATIC_WORKSPACE_BYTES (512u << 20)
 jarq_status jarq_refine_static(const jarq_params* p, const float* W, const float* H,
                                uint8_t* codes, float* scales, const int32_t* zeros, void* stream,
                                jarq_stats* stats);

@@ -16,12 +16,12 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libjarq.so")
 
 MAX_RECORDED_SWEEPS = 64
-NUM_STAGES = 7           # Gram, scale solve, E split, residual product, objective, Babai, panel update
-STAGE_NAMES = ("gram", "solve", "esplit", "residual", "objective", "babai", "panel")
-ABI_VERSION = 8
+NUM_STAGES = 6           # Gram, scale solve, residual product, objective, Babai, panel update
+STAGE_NAMES = ("gram", "solve", "residual", "objective", "babai", "panel")
+ABI_VERSION = 9
 (JARQ_OK, JARQ_EINVAL, JARQ_ENOT_SPD, JARQ_ESCALE_SOLVE, JARQ_EHIP, JARQ_EWORKSPACE,
  JARQ_ESTATIC_LIMIT) = range(7)
-STATIC_WORKSPACE_BYTES = 384 << 20
+STATIC_WORKSPACE_BYTES = 512 << 20
 DEC_REJECT, DEC_ACCEPT, DEC_SKIP, DEC_STOPPED = 0, 1, 2, 3
 
 

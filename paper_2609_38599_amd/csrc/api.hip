@@ -44,10 +44,11 @@ Layout make_layout(int rows, int cols, int g) {
   L.mlo = take(C * C * 2);
   L.mrow = take(C * sizeof(float));
   L.mmax = take(C * sizeof(float));
-  L.ehi = take(R * C * 2);
-  L.elo = take(R * C * 2);
-  L.erow = take(R * sizeof(float));
+  L.wrow = take(R * sizeof(float));
   L.wh = take(R * C * sizeof(float));
+  L.tm = take(R * C * sizeof(float));
+  L.rw = take(R * C * sizeof(float));
+  L.cz = take(R * C * 2);
   L.gram = take(R * G * G * sizeof(float));
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
@@ -209,6 +210,14 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   JQ_HIP(launch_split_h(c.st, c.cols, H, c.ws, c.lay));
   JQ_HIP(launch_gemm_ah(c.st, c.rows, c.cols, c.g, false, W, nullptr, nullptr, nullptr, H, c.wh(),
                         nullptr));
+  // T = W M^T and RW = W_i L_i, the constant parts of the residual product
+  // and of the objective; W's two fp16 planes borrow P's memory
+  _Float16* whi = (_Float16*)c.pbuf();
+  _Float16* wlo = whi + (size_t)c.rows * c.cols;
+  float* wrow = (float*)(c.ws + c.lay.wrow);
+  JQ_HIP(launch_split_w(c.st, c.rows, c.cols, W, whi, wlo, wrow));
+  JQ_HIP(launch_wm_product(c.st, c.rows, c.cols, c.ws, c.lay, whi, wlo, wrow));
+  JQ_HIP(launch_rw_product(c.st, c.rows, c.cols, c.g, c.ws, c.lay, whi, wlo, wrow));
   Flags f{};
   JQ_HIP(hipMemcpyAsync(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost, c.st));
   JQ_HIP(hipStreamSynchronize(c.st));
@@ -216,10 +225,11 @@ jarq_status prepare_impl(const jarq_params* p, const float* W, const float* H, v
   return JARQ_OK;
 }
 
-// Stage boundaries with a HIP event each (stages 0-4 are consecutive runs of
-// kernels), and the code update's launches with a pair each (stage 5: the
-// Babai kernels, stage 6: the panel updates, which alternate).
-constexpr int kBoundaries = 6;
+// Stage boundaries with a HIP event each (stages 0-3 are consecutive runs of
+// kernels), and the code update's launches with a pair each (stage 4: the
+// Babai kernels, stage 5: the panel updates, which alternate).
+constexpr int kBoundaries = 5;
+constexpr int kFirstLaunchStage = kBoundaries - 1;
 
 // time_stages = false: no HIP events are created and stage_ms stays 0.
 jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
@@ -235,6 +245,8 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   JQ_HIP(hipStreamSynchronize(c.st));
   if (f.bad_codes || f.bad_zeros) return JARQ_EINVAL;
 
+  // q - z as fp16, kept in step with the codes by the code update
+  JQ_HIP(launch_codes_cz(c.st, c.rows, c.cols, c.g, codes, zeros, (_Float16*)(c.ws + c.lay.cz)));
   JQ_HIP(launch_fill_u8(c.st, c.active(), (size_t)c.rows, 1));
   JQ_HIP(launch_zero_bytes(c.st, c.ws + c.lay.stopat, (size_t)c.rows * sizeof(int32_t)));
   JQ_HIP(launch_zero_bytes(c.st, c.cnt(), kSubLists * sizeof(Counters)));
@@ -266,7 +278,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   const uint32_t tmask = (stats == nullptr || !time_stages) ? 0u
                          : (stats->stage_mask & all_stages) ? (stats->stage_mask & all_stages)
                                                              : all_stages;
-  // Boundary j is used when stage j - 1 or stage j (j < 5) is timed.
+  // Boundary j is used when stage j - 1 or stage j (j < kBoundaries - 1) is timed.
   auto boundary_used = [&](int j) {
     return (j > 0 && ((tmask >> (j - 1)) & 1u)) || (j < kBoundaries - 1 && ((tmask >> j) & 1u));
   };
@@ -286,7 +298,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
   for (int k = 0; k < K; ++k) {
     // launches of the code update timed with a pair of events each
     auto hook = [&](int kind, int q, int phase) -> hipError_t {
-      if (k >= nrec || !((tmask >> (5 + kind)) & 1u)) return hipSuccess;
+      if (k >= nrec || !((tmask >> (kFirstLaunchStage + kind)) & 1u)) return hipSuccess;
       const size_t at = (size_t)k * per_sweep + kBoundaries + 2 * (kind * npan + q) + phase;
       return hipEventRecord(ev[at], c.st);
     };
@@ -301,19 +313,18 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
                        rmap, n_dev);
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
-      e = launch_split_e(c.st, n, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay, rmap, n_dev);
+      e = launch_resid(c.st, n, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), rmap, n_dev);
     if (e == hipSuccess) e = mark(k, 3);
-    if (e == hipSuccess) e = launch_split_gemm(c.st, n, c.cols, c.ws, c.lay, c.pbuf(), n_dev);
-    if (e == hipSuccess) e = mark(k, 4);
     if (e == hipSuccess)
-      e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, c.pbuf(), c.objpart(), n_dev);
+      e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), c.objpart(),
+                                 rmap, n_dev);
     if (e == hipSuccess)
       e = launch_stop_check(c.st, n, c.G, c.objpart(), (double*)(c.ws + c.lay.lcur),
                             (double*)(c.ws + c.lay.lprev), c.active(),
                             (int32_t*)(c.ws + c.lay.stopat), k + 1, p->tau, rmap,
                             (uint32_t*)(c.ws + c.lay.pcount), npan * kSubLists, c.gcount(),
                             c.G * kSubLists, n_dev);
-    if (e == hipSuccess) e = mark(k, 5);
+    if (e == hipSuccess) e = mark(k, 4);
     if (e == hipSuccess)
       e = enqueue_babai(c, n, rmap, n_dev, codes, scales, zeros, c.active(), nullptr, nullptr,
                         /*counts_zeroed=*/true, /*lists=*/true, hook);
@@ -377,7 +388,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
         }
         for (int kind = 0; kind < 2; ++kind) {
           float tot = 0.f;
-          if ((tmask >> (5 + kind)) & 1u) {
+          if ((tmask >> (kFirstLaunchStage + kind)) & 1u) {
             for (int q = 0; q < npan - kind; ++q) {
               float ms = 0.f;
               const size_t at = b + kBoundaries + 2 * (kind * npan + q);
@@ -385,7 +396,7 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
               tot += ms;
             }
           }
-          stats->stage_ms[k][5 + kind] = tot;
+          stats->stage_ms[k][kFirstLaunchStage + kind] = tot;
         }
       }
       if (run > 0) {
@@ -472,9 +483,11 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
   jarq_status s = check_ws(p, workspace, workspace_bytes);
   if (s != JARQ_OK) return s;
   Ctx c = make_ctx(p, workspace, stream);
-  if (launch_split_e(c.st, c.rows, c.cols, c.g, W, codes, scales, zeros, c.ws, c.lay, nullptr,
-                     nullptr) != hipSuccess ||
-      launch_split_gemm(c.st, c.rows, c.cols, c.ws, c.lay, c.pbuf(), nullptr) != hipSuccess)
+  (void)W;
+  if (launch_codes_cz(c.st, c.rows, c.cols, c.g, codes, zeros, (_Float16*)(c.ws + c.lay.cz)) !=
+          hipSuccess ||
+      launch_resid(c.st, c.rows, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), nullptr, nullptr) !=
+          hipSuccess)
     return JARQ_EHIP;
   if (enqueue_babai(c, c.rows, nullptr, nullptr, codes, scales, zeros, nullptr, cand, decision) !=
       hipSuccess)

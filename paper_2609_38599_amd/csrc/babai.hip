@@ -179,7 +179,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     uint8_t* __restrict__ cand_out,
     uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt,
     const int32_t* __restrict__ rowmap, const int* __restrict__ n_dev,
-    int32_t* __restrict__ glist, uint32_t* __restrict__ gcount, int list_cap) {
+    int32_t* __restrict__ glist, uint32_t* __restrict__ gcount, int list_cap,
+    _Float16* __restrict__ cz) {
   if (n_dev != nullptr) rows = *n_dev;
   if ((int)blockIdx.x * 16 >= rows) return;  // the whole work-group: no row here
   constexpr int g = G_SIZE;
@@ -545,9 +546,10 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     }
   }
 
-  // ---- codes += accepted changes and dq = accepted changes, over the panel's
-  // columns: 16 columns per thread and step (16-byte code and 2 x 16-byte dq
-  // accesses).  dqp_s is complete since the last barrier.
+  // ---- codes += accepted changes, cz (q - z as fp16) likewise, and dq =
+  // accepted changes, over the panel's columns: 16 columns per thread and step
+  // (16-byte code, 2 x 16-byte cz and dq accesses).  dqp_s is complete since
+  // the last barrier.
   {
     const int per_row = (i1 - i0) * g / 16;
     for (int c = tid; c < RT * per_row; c += 512) {
@@ -555,11 +557,15 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       const int k = (c - r * per_row) * 16;
       if (r0 + r < rows) {
         const uint32_t o = (uint32_t)r * ucols + (uint32_t)(i0 * g + k);
-        uint8_t* codes_r = codes + (size_t)map_row(rowmap, r0 + r) * cols;
+        const size_t lrow_r = (size_t)map_row(rowmap, r0 + r);
+        uint8_t* codes_r = codes + lrow_r * cols;
+        _Float16* cz_r = cz + lrow_r * cols;
         const uint32_t oq = (uint32_t)(i0 * g + k);
         const f16x8 d0 = *(const f16x8*)(dqp_s + r * PW + k);
         const f16x8 d1 = *(const f16x8*)(dqp_s + r * PW + k + 8);
         const uint4 qw = ld_at((const uint4*)codes_r, oq);
+        const f16x8 c0 = ld_at((const f16x8*)cz_r, 2 * oq);
+        const f16x8 c1 = ld_at((const f16x8*)cz_r, 2 * oq + 16);
         uint32_t w[4] = {qw.x, qw.y, qw.z, qw.w};
         // Byte b of word b / 4 gains d_b; new codes stay in [0, 2^bits - 1],
         // so the word-wide add never carries into a neighbouring byte.
@@ -569,6 +575,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
           w[b >> 2] += (uint32_t)dv << (8 * (b & 3));
         }
         st_at((uint4*)codes_r, oq, make_uint4(w[0], w[1], w[2], w[3]));
+        st_at((f16x8*)cz_r, 2 * oq, c0 + d0);  // small integers: exact
+        st_at((f16x8*)cz_r, 2 * oq + 16, c1 + d1);
         st_at((f16x8*)dq_t, 2 * o, d0);
         st_at((f16x8*)dq_t, 2 * o + 16, d1);
       }
@@ -604,7 +612,8 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (const float*)(ws + lay.rdsq), codes, scales, active,
                      (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
                      (uint32_t*)(ws + lay.pcount) + (size_t)(i0 / PG) * kSubLists * kCtrStride,
-                     cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap);
+                     cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap,
+                     (_Float16*)(ws + lay.cz));
   return hipGetLastError();
 }
 

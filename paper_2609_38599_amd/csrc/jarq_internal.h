@@ -122,10 +122,12 @@ struct Layout {
   size_t mlo;       // [cols][cols] f16: low term
   size_t mrow;      // [cols] f32: 2^-t_n
   size_t mmax;      // [cols] f32: row maxima of M (prep scratch)
-  size_t ehi;       // [rows][cols] f16: E 2^t_row, high term
-  size_t elo;       // [rows][cols] f16: E 2^t_row, low term
-  size_t erow;      // [rows] f32: 2^-t_row
+  size_t wrow;      // [rows] f32: 2^-t_row of W's fp16 planes (prepare; the planes
+                    // themselves occupy p's memory until the first sweep)
   size_t wh;        // [rows][cols] f32: W H
+  size_t tm;        // [rows][cols] f32: T = W M^T (the residual product of W alone)
+  size_t rw;        // [rows][cols] f32: W_i L_i per group (the objective's part of W alone)
+  size_t cz;        // [rows][cols] f16: q - z, exact, by layer row (kept with the codes)
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
   size_t p;         // [rows][cols] f32: (W - What) H
   size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
@@ -170,18 +172,31 @@ hipError_t launch_split_h(hipStream_t st, int cols, const float* H, char* ws, co
 hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char* ws,
                           const Layout& lay);
 
-// `rows` positions of the sweep; position p holds layer row map_row(rowmap, p).
-hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
-                          const uint8_t* codes, const float* scales, const int32_t* zeros,
-                          char* ws, const Layout& lay, const int32_t* rowmap, const int* n_dev);
-
-// P = E H from the fp16 planes of E and H in the workspace (three products).
-hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
-                             const Layout& lay, float* C, const int* n_dev);
-// Per row and group, (R_i e_i) . U_i = e_i^T (H e)_i (fp64) into objpart[row][group].
+// The layer's constant parts of the per-sweep products (jarq_prepare), from
+// W as two fp16 planes (whi, wlo with row scales 2^-t in wrow, all rows):
+// T = W M^T into lay.tm (three products, sgemm.hip) and RW = W_i L_i per
+// group into lay.rw (objective.hip).
+hipError_t launch_split_w(hipStream_t st, int rows, int cols, const float* W, _Float16* whi,
+                          _Float16* wlo, float* wrow_inv);
+hipError_t launch_wm_product(hipStream_t st, int rows, int cols, const char* ws,
+                             const Layout& lay, const _Float16* whi, const _Float16* wlo,
+                             const float* wrow_inv);
+hipError_t launch_rw_product(hipStream_t st, int rows, int cols, int g, const char* ws,
+                             const Layout& lay, const _Float16* whi, const _Float16* wlo,
+                             const float* wrow_inv);
+// cz = q - z as fp16 for all rows (kept in step with the codes by the code update).
+hipError_t launch_codes_cz(hipStream_t st, int rows, int cols, int g, const uint8_t* codes,
+                           const int32_t* zeros, _Float16* cz);
+// U = T - What M^T from the exact codes (cz) and the scales, layer rows
+// through rowmap, U by position (sgemm.hip).
+hipError_t launch_resid(hipStream_t st, int rows, int cols, int g, const char* ws,
+                        const Layout& lay, const float* scales, float* U, const int32_t* rowmap,
+                        const int* n_dev);
+// Per position and group, (R_i e_i) . U_i = e_i^T (H e)_i (fp64) into
+// objpart[position][group], from RW, cz and the scales (layer rows via rowmap).
 hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, const char* ws,
-                                  const Layout& lay, const float* C, double* objpart,
-                                  const int* n_dev);
+                                  const Layout& lay, const float* scales, const float* U,
+                                  double* objpart, const int32_t* rowmap, const int* n_dev);
 
 // Row counts on the device: every per-row kernel of a sweep takes the number
 // of positions n as `rows` (the most it may be, which sizes the grid) and,

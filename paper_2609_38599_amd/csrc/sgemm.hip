@@ -278,17 +278,274 @@ static hipError_t launch_split3_t(hipStream_t st, int M, int N, int K, int lda, 
   return hipGetLastError();
 }
 
-hipError_t launch_split_gemm(hipStream_t st, int rows, int cols, const char* ws,
-                             const Layout& lay, float* C, const int* n_dev) {
+// T = W M^T for the layer, all rows (jarq_prepare): W's two fp16 planes
+// against M's, three products.
+hipError_t launch_wm_product(hipStream_t st, int rows, int cols, const char* ws,
+                             const Layout& lay, const _Float16* whi, const _Float16* wlo,
+                             const float* wrow_inv) {
   if (rows <= 0 || cols <= 0) return hipSuccess;
-  const _Float16* ah = (const _Float16*)(ws + lay.ehi);
-  const _Float16* al = (const _Float16*)(ws + lay.elo);
   const _Float16* bh = (const _Float16*)(ws + lay.mhi);
   const _Float16* bl = (const _Float16*)(ws + lay.mlo);
-  const float* ar = (const float*)(ws + lay.erow);
   const float* bc = (const float*)(ws + lay.mrow);
-  return launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, ah, al, ar, bh, bl, bc,
-                                 C, n_dev);
+  return launch_split3_t<256, 0>(st, rows, cols, cols, cols, cols, cols, whi, wlo, wrow_inv, bh,
+                                 bl, bc, (float*)(ws + lay.tm), nullptr);
+}
+
+// ---- residual product from the exact codes ----
+//
+// With E = W - What and What(j, k) = s(j, i) (q(j, k) - z(j, i)) for k in group
+// i (eq. (1)), U = E M^T = T - What M^T with T = W M^T fixed for the layer
+// (formed once by jarq_prepare with split3_kernel).  The codes minus
+// zero points are small integers, exact in fp16 (the cz plane), so
+//   (What M^T)(j, n) = 2^-t_n sum_i s(j, i) sum_{k in i} cz(j, k) (Mh + Ml)(n, k)
+// needs two products per k-slice instead of three; each group's partial sum
+// (seg, exact products accumulated in fp32 on the matrix cores) is scaled by
+// its row's s and added to the running sum in fp32 when the group ends.
+//
+// Tiling: 256 x 128 output tile per 512-thread work-group, 4 x 2 waves of
+// 64 x 64 (two 32 x 32 blocks each way: the accumulators and the group's
+// partial sums both fit next to the fragments at two waves per SIMD), K in
+// steps of 64 (32 when g = 32) straight from global memory into two LDS
+// stages by direct loads.  A stage row holds CPR 16-byte chunks; chunk c of
+// tile row r sits at position c ^ rswz(r), so the eight rows one read serves
+// per clock hit distinct banks.  Fragment reads run one k-slice ahead of the
+// products.  Rows of cz, the scales and T are the layer's rows (gathered
+// through the row map); U is stored by position.
+namespace {
+constexpr int RBM = 256, RBN = 128;
+template <int CPR>
+__device__ __forceinline__ int rswz(int r) {
+  if constexpr (CPR == 8) return r & 7;
+  return ((r >> 1) + (r >> 3)) & 3;
+}
+}  // namespace
+
+template <int G_SIZE>
+__global__ __launch_bounds__(512, 1) void resid_kernel(
+    int M, int N, int K, const _Float16* __restrict__ Cz, const float* __restrict__ scales,
+    const _Float16* __restrict__ Bh, const _Float16* __restrict__ Bl,
+    const float* __restrict__ bcol_inv, const float* __restrict__ T, float* __restrict__ U,
+    const int32_t* __restrict__ rowmap, const int* __restrict__ m_dev) {
+  if (m_dev != nullptr) M = *m_dev;
+  constexpr int g = G_SIZE;
+  constexpr int RBK = g >= 64 ? 64 : 32;                 // k per stage
+  constexpr int KQ = RBK / 16;                           // k-slices per stage
+  constexpr int CPR = RBK / 8;                           // 16-byte chunks per stage row
+  constexpr int RPP = 64 / CPR;                          // rows per 1 KB piece
+  constexpr int SPG = g / RBK;                           // stages per group
+  constexpr int A_PLANE = RBM * RBK, B_PLANE = RBN * RBK;  // halves
+  constexpr int APW = RBM / RPP / 8, BPW = RBN / RPP / 8;  // pieces per wave per plane
+  constexpr int STAGE = A_PLANE + 2 * B_PLANE;
+  __shared__ __attribute__((aligned(1024))) _Float16 buf0[STAGE];
+  __shared__ __attribute__((aligned(1024))) _Float16 buf1[STAGE];
+  __shared__ __attribute__((aligned(16))) float sc_s[2][RBM];  // s of the tile's rows, current / next group
+  __shared__ int lr_s[RBM];                                     // layer row of each tile row
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lm = lane & 31, kh = lane >> 5;
+  const int G = K / g;
+  const int nbm = (M + RBM - 1) / RBM, nbn = (N + RBN - 1) / RBN;
+  int tm, tn;
+  if (M <= 0 || !tile_of(blockIdx.x, nbm, nbn, tm, tn)) return;  // uniform across the work-group
+  const int m0 = tm * RBM, n0 = tn * RBN;
+  // Tile rows past the edge take the tile's first row: their products only
+  // reach outputs that are never stored.
+  if (tid < RBM) lr_s[tid] = map_row(rowmap, m0 + (m0 + tid < M ? tid : 0));
+  __syncthreads();
+
+  // Direct loads, 16 bytes per lane, one 1 KB piece (RPP rows) per
+  // instruction: wave w fills pieces w, w + 8, ... of each plane; lane L holds
+  // row RPP j + L / CPR at position L % CPR, i.e. chunk (L % CPR) ^ rswz(row).
+  unsigned aoff[APW], boff[BPW];
+#pragma unroll
+  for (int i = 0; i < APW; ++i) {
+    const int r = RPP * (wave + 8 * i) + lane / CPR;
+    aoff[i] = (unsigned)lr_s[r] * (unsigned)K + (unsigned)(((lane % CPR) ^ rswz<CPR>(r)) * 8);
+  }
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int r = RPP * (wave + 8 * i) + lane / CPR;
+    const int gn = n0 + r;
+    boff[i] = (unsigned)(gn < N ? gn : 0) * (unsigned)K + (unsigned)(((lane % CPR) ^ rswz<CPR>(r)) * 8);
+  }
+  // load j (0 .. NDMA - 1) of a stage's direct loads: the cz pieces first,
+  // then the M pieces, high and low plane in turn
+  constexpr int NDMA = APW + 2 * BPW;
+  auto issue_one = [&](int j, int k0, _Float16* stage) {
+    if (j < APW) {
+      dma16(Cz + k0 + aoff[j], stage + (wave + 8 * j) * 512);
+    } else {
+      const int i = (j - APW) >> 1;
+      if (((j - APW) & 1) == 0)
+        dma16(Bh + k0 + boff[i], stage + A_PLANE + (wave + 8 * i) * 512);
+      else
+        dma16(Bl + k0 + boff[i], stage + A_PLANE + B_PLANE + (wave + 8 * i) * 512);
+    }
+  };
+  auto issue = [&](int k0, _Float16* stage) {
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) issue_one(j, k0, stage);
+  };
+  // the tile's scales of group i into sc_s[i & 1] (threads 0..RBM-1)
+  auto stage_scales = [&](int i) {
+    if (tid < RBM) sc_s[i & 1][tid] = scales[(size_t)lr_s[tid] * G + i];
+  };
+
+  f32x16 acc[2][2], seg[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+
+  auto lds_rd = [&](const _Float16* plane, int r, int q) {
+    const int c = 2 * q + kh;  // k-slice q: chunks 2 q (lanes 0-31) and 2 q + 1
+    const uint32_t ad = (uint32_t)(size_t)(const __attribute__((address_space(3))) void*)(
+        plane + r * RBK + ((c ^ rswz<CPR>(r)) << 3));
+    f16x8 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(ad));
+    return v;
+  };
+  // One stage (KQ k-slices of 16) on `base`; `first`: the stage opens a group
+  // (its products start the partial sums from zero).  The six reads of slice
+  // q + 1 are issued before the wait for slice q (LDS returns in order), and
+  // the next stage's direct loads (into `stn` at k0n; none if k0n < 0) are
+  // spread over the slices.
+  auto compute = [&](const _Float16* base, bool first, int k0n, _Float16* stn) {
+    f16x8 af[2][2], bh[2][2], bl[2][2];  // [slot][block]
+    auto rd = [&](int q, int sl) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a) af[sl][a] = lds_rd(base, wm * 64 + a * 32 + lm, q);
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        bh[sl][b] = lds_rd(base + A_PLANE, wn * 64 + b * 32 + lm, q);
+        bl[sl][b] = lds_rd(base + A_PLANE + B_PLANE, wn * 64 + b * 32 + lm, q);
+      }
+    };
+    rd(0, 0);
+#pragma unroll
+    for (int q = 0; q < KQ; ++q) {
+      const int sl = q & 1;
+      if (k0n >= 0) {
+#pragma unroll
+        for (int j = q * NDMA / KQ; j < (q + 1) * NDMA / KQ; ++j) issue_one(j, k0n, stn);
+      }
+      if (q + 1 < KQ) {
+        rd(q + 1, sl ^ 1);
+        if (sl == 0)
+          asm volatile("s_waitcnt lgkmcnt(6)"
+                       : "+v"(af[0][0]), "+v"(af[0][1]), "+v"(bh[0][0]), "+v"(bh[0][1]),
+                         "+v"(bl[0][0]), "+v"(bl[0][1]));
+        else
+          asm volatile("s_waitcnt lgkmcnt(6)"
+                       : "+v"(af[1][0]), "+v"(af[1][1]), "+v"(bh[1][0]), "+v"(bh[1][1]),
+                         "+v"(bl[1][0]), "+v"(bl[1][1]));
+      } else {
+        if (sl == 0)
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(af[0][0]), "+v"(af[0][1]), "+v"(bh[0][0]), "+v"(bh[0][1]),
+                         "+v"(bl[0][0]), "+v"(bl[0][1]));
+        else
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(af[1][0]), "+v"(af[1][1]), "+v"(bh[1][0]), "+v"(bh[1][1]),
+                         "+v"(bl[1][0]), "+v"(bl[1][1]));
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const f32x16 c0 = (first && q == 0) ? f32x16{} : seg[a][b];
+          seg[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[sl][a], bh[sl][b], c0, 0, 0, 0);
+          seg[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[sl][a], bl[sl][b], seg[a][b], 0, 0, 0);
+        }
+    }
+  };
+  // acc += s (per row) * seg at the end of group i; element v of a block is
+  // row 8 (v / 4) + 4 (lane / 32) + v % 4
+  auto fold = [&](int i) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const f32x4 s4 = *(const f32x4*)&sc_s[i & 1][wm * 64 + a * 32 + 8 * v4 + 4 * kh];
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            acc[a][b][4 * v4 + u] = fmaf(seg[a][b][4 * v4 + u], s4[u], acc[a][b][4 * v4 + u]);
+      }
+    }
+  };
+
+  // Double buffering: the loads of stage k + 1 fly while stage k computes;
+  // the barrier at the end of a stage (which waits for this thread's
+  // outstanding loads) makes the next stage visible and frees the one just
+  // read.  The scales of group i + 1 are staged during group i (their buffer
+  // was last read by group i - 1's fold, before a barrier).
+  const int nk = K / RBK;
+  stage_scales(0);
+  issue(0, buf0);
+  __syncthreads();
+  for (int i = 0; i < G; ++i) {
+    if (i + 1 < G) stage_scales(i + 1);
+#pragma unroll
+    for (int ks = 0; ks < SPG; ++ks) {  // unrolled: whether a stage opens its group is known
+      const int kt = i * SPG + ks;
+      _Float16* cur = (kt & 1) ? buf1 : buf0;
+      _Float16* nxt = (kt & 1) ? buf0 : buf1;
+      compute(cur, ks == 0, kt + 1 < nk ? (kt + 1) * RBK : -1, nxt);
+      if (ks == SPG - 1) fold(i);
+      __syncthreads();
+    }
+  }
+
+  // Epilogue: U = T - acc 2^-t_n.  Accumulator element v of lane l in a
+  // 32 x 32 block: (row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32).
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int tb = wm * 64 + a * 32 + 4 * kh;  // tile row of element v: tb + 8 (v / 4) + v % 4
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int col = n0 + wn * 64 + b * 32 + lm;
+      const int colc = min(col, N - 1);
+      const float cs = bcol_inv[colc];
+      float tv[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        tv[v] = T[(size_t)lr_s[tb + 8 * (v / 4) + (v % 4)] * N + colc];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + tb + 8 * (v / 4) + (v % 4);
+        if (row < M && col < N) U[(size_t)row * N + col] = tv[v] - acc[a][b][v] * cs;
+      }
+    }
+  }
+}
+
+template <int G_SIZE>
+static hipError_t launch_resid_t(hipStream_t st, int rows, int cols, const char* ws,
+                                 const Layout& lay, const float* scales, float* U,
+                                 const int32_t* rowmap, const int* n_dev) {
+  const int tiles = ((rows + RBM - 1) / RBM) * ((cols + RBN - 1) / RBN);
+  hipLaunchKernelGGL((resid_kernel<G_SIZE>), dim3(tiles), dim3(512), 0, st, rows, cols, cols,
+                     (const _Float16*)(ws + lay.cz), scales, (const _Float16*)(ws + lay.mhi),
+                     (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow),
+                     (const float*)(ws + lay.tm), U, rowmap, n_dev);
+  return hipGetLastError();
+}
+
+hipError_t launch_resid(hipStream_t st, int rows, int cols, int g, const char* ws,
+                        const Layout& lay, const float* scales, float* U, const int32_t* rowmap,
+                        const int* n_dev) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (cols % BK != 0) return hipErrorInvalidValue;
+  switch (g) {
+    case 32: return launch_resid_t<32>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev);
+    case 64: return launch_resid_t<64>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev);
+    case 128: return launch_resid_t<128>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace jarq

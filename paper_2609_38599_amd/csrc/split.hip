@@ -13,6 +13,8 @@
 
 namespace jarq {
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
 __device__ __forceinline__ void atomic_max_abs(float* dst, float v) {
   // |v| >= 0: IEEE ordering of non-negative floats equals their bit ordering.
   atomicMax((unsigned int*)dst, __float_as_uint(fabsf(v)));
@@ -141,54 +143,28 @@ hipError_t launch_split_m(hipStream_t st, int cols, int g, const float* H, char*
   }
 }
 
-// One work-group per row: E = W - s (q - z) in fp32 (as in eq. (1)), its
-// row maximum, then the two fp16 planes and the row's inverse scale 2^-t.
-// Each thread keeps its NCH chunks of four weights and codes in registers
-// between the two passes (rows of at most 1024 NCH columns), so W and the
-// codes are read from memory once.
+// W as two fp16 planes for the layer's constant products (T = W M^T and
+// RW = W_i L_i, formed once by jarq_prepare): one work-group per row, the
+// row maximum, then the planes and the row's inverse scale 2^-t.  Each thread
+// keeps its NCH chunks of four weights in registers between the two passes
+// (rows of at most 1024 NCH columns), so W is read once.
 template <int NCH>
-__global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
-                                                      const float* __restrict__ W,
-                                                      const uint8_t* __restrict__ codes,
-                                                      const float* __restrict__ scales,
-                                                      const int32_t* __restrict__ zeros,
-                                                      _Float16* __restrict__ ehi,
-                                                      _Float16* __restrict__ elo,
-                                                      float* __restrict__ erow_inv,
-                                                      const int32_t* __restrict__ rowmap,
-                                                      const int* __restrict__ n_dev) {
-  // position pos of the sweep (E and its scale) holds layer row `row`
-  const int pos = blockIdx.x;
-  if (pos >= (n_dev != nullptr ? *n_dev : rows)) return;
-  const int row = map_row(rowmap, pos);
-  const int G = cols / g;
+__global__ __launch_bounds__(256) void split_w_kernel(int cols, const float* __restrict__ W,
+                                                      _Float16* __restrict__ whi,
+                                                      _Float16* __restrict__ wlo,
+                                                      float* __restrict__ wrow_inv) {
+  const int row = blockIdx.x;
   __shared__ float red[4];
   const float* wr = W + (size_t)row * cols;
-  const uint8_t* qr = codes + (size_t)row * cols;
-  const float* sr = scales + (size_t)row * G;
-  const int32_t* zr = zeros + (size_t)row * G;
-  auto err = [&](const f32x4& w, uint32_t q4, float s, int z, int i) {
-    return w[i] - s * (float)((int)((q4 >> (8 * i)) & 0xffu) - z);
-  };
   f32x4 wv[NCH];
-  uint32_t qv[NCH];
   float m = 0.f;
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     const int c = (threadIdx.x + 256 * k) * 4;
     if (c < cols) {
       wv[k] = *(const f32x4*)(wr + c);
-      qv[k] = *(const uint32_t*)(qr + c);
-    }
-  }
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) {
-    const int c = (threadIdx.x + 256 * k) * 4;
-    if (c < cols) {
-      const float s = sr[c / g];
-      const int z = zr[c / g];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(err(wv[k], qv[k], s, z, i)));
+      for (int i = 0; i < 4; ++i) m = fmaxf(m, fabsf(wv[k][i]));
     }
   }
 #pragma unroll
@@ -197,54 +173,72 @@ __global__ __launch_bounds__(256) void split_e_kernel(int rows, int cols, int g,
   __syncthreads();
   m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const int t = pow2_exponent(m);
-  if (threadIdx.x == 0) erow_inv[pos] = ldexpf(1.f, -t);
-  _Float16* hr = ehi + (size_t)pos * cols;
-  _Float16* lr = elo + (size_t)pos * cols;
+  if (threadIdx.x == 0) wrow_inv[row] = ldexpf(1.f, -t);
+  _Float16* hr = whi + (size_t)row * cols;
+  _Float16* lr = wlo + (size_t)row * cols;
   typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-  auto emit = [&](int c, const f32x4& w, uint32_t q4) {
-    const float s = sr[c / g];
-    const int z = zr[c / g];
-    h4 hv, lv;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float e = ldexpf(err(w, q4, s, z, i), t);
-      const _Float16 h = (_Float16)e;
-      hv[i] = h;
-      lv[i] = (_Float16)(e - (float)h);
-    }
-    *(h4*)(hr + c) = hv;
-    *(h4*)(lr + c) = lv;
-  };
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     const int c = (threadIdx.x + 256 * k) * 4;
-    if (c < cols) emit(c, wv[k], qv[k]);
+    if (c < cols) {
+      h4 hv, lv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = ldexpf(wv[k][i], t);
+        const _Float16 h = (_Float16)e;
+        hv[i] = h;
+        lv[i] = (_Float16)(e - (float)h);
+      }
+      *(h4*)(hr + c) = hv;
+      *(h4*)(lr + c) = lv;
+    }
   }
 }
 
-template <int NCH>
-static hipError_t launch_split_e_t(hipStream_t st, int rows, int cols, int g, const float* W,
-                                   const uint8_t* codes, const float* scales,
-                                   const int32_t* zeros, char* ws, const Layout& lay,
-                                   const int32_t* rowmap, const int* n_dev) {
-  hipLaunchKernelGGL(split_e_kernel<NCH>, dim3(rows), dim3(256), 0, st, rows, cols, g, W, codes,
-                     scales, zeros, (_Float16*)(ws + lay.ehi), (_Float16*)(ws + lay.elo),
-                     (float*)(ws + lay.erow), rowmap, n_dev);
+hipError_t launch_split_w(hipStream_t st, int rows, int cols, const float* W, _Float16* whi,
+                          _Float16* wlo, float* wrow_inv) {
+  if (rows <= 0) return hipSuccess;
+  if (cols <= 4096)
+    hipLaunchKernelGGL(split_w_kernel<4>, dim3(rows), dim3(256), 0, st, cols, W, whi, wlo, wrow_inv);
+  else if (cols <= 12288)
+    hipLaunchKernelGGL(split_w_kernel<12>, dim3(rows), dim3(256), 0, st, cols, W, whi, wlo, wrow_inv);
+  else if (cols <= 16384)   // the most a layer can have: 128 groups of at most 128
+    hipLaunchKernelGGL(split_w_kernel<16>, dim3(rows), dim3(256), 0, st, cols, W, whi, wlo, wrow_inv);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_split_e(hipStream_t st, int rows, int cols, int g, const float* W,
-                          const uint8_t* codes, const float* scales, const int32_t* zeros,
-                          char* ws, const Layout& lay, const int32_t* rowmap,
-                          const int* n_dev) {
-  if (rows <= 0) return hipSuccess;
-  if (cols <= 4096)
-    return launch_split_e_t<4>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap, n_dev);
-  if (cols <= 12288)
-    return launch_split_e_t<12>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap, n_dev);
-  if (cols <= 16384)   // the most a layer can have: 128 groups of at most 128
-    return launch_split_e_t<16>(st, rows, cols, g, W, codes, scales, zeros, ws, lay, rowmap, n_dev);
-  return hipErrorInvalidValue;
+// cz = q - z as fp16 (exact: codes and zero points are small integers), by
+// layer row; 16 codes per thread and step.
+__global__ void codes_cz_kernel(int rows, int cols, int g, const uint8_t* __restrict__ codes,
+                                const int32_t* __restrict__ zeros, _Float16* __restrict__ cz) {
+  const int G = cols / g;
+  const size_t chunks = (size_t)rows * cols / 16;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < chunks;
+       e += (size_t)gridDim.x * blockDim.x) {
+    const size_t off = e * 16;
+    const int r = (int)(off / cols), c = (int)(off % cols);
+    const uint4 q = *(const uint4*)(codes + off);
+    const float z = (float)zeros[(size_t)r * G + c / g];
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    f16x8 h0, h1;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      h0[b] = (_Float16)((float)((w[b >> 2] >> (8 * (b & 3))) & 0xffu) - z);
+      h1[b] = (_Float16)((float)((w[2 + (b >> 2)] >> (8 * (b & 3))) & 0xffu) - z);
+    }
+    *(f16x8*)(cz + off) = h0;
+    *(f16x8*)(cz + off + 8) = h1;
+  }
+}
+
+hipError_t launch_codes_cz(hipStream_t st, int rows, int cols, int g, const uint8_t* codes,
+                           const int32_t* zeros, _Float16* cz) {
+  if (rows <= 0 || cols % 16 != 0) return rows <= 0 ? hipSuccess : hipErrorInvalidValue;
+  hipLaunchKernelGGL(codes_cz_kernel, dim3(2048), dim3(256), 0, st, rows, cols, g, codes, zeros,
+                     cz);
+  return hipGetLastError();
 }
 
 }  // namespace jarq

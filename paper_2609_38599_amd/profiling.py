@@ -5,7 +5,7 @@
 
     python3 -m paper_2609_38599_amd.profiling traffic --fetch F.csv --write W.csv \
         --copy-fetch CF.csv --copy-write CW.csv --copy-bytes N \
-        --kernel split3_kernel --source paper_2609_38599_amd/csrc/sgemm.hip
+        --kernel resid_kernel --source paper_2609_38599_amd/csrc/sgemm.hip
         HBM bytes per dispatch from the FETCH_SIZE / WRITE_SIZE counters (KiB per
         dispatch), each scaled by the factor that makes the same counter read N
         bytes for a plain device copy of N bytes; prints key = value lines for

@@ -36,7 +36,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert binding.abi_version() == binding.ABI_VERSION == 8
+    assert binding.abi_version() == binding.ABI_VERSION == 9
     for s in range(7):
         assert binding.status_string(s)
     assert binding.status_string(99) == "unknown status"
@@ -45,8 +45,9 @@ def test_abi_version_and_status_strings(lib):
 def test_workspace_bytes_valid_and_invalid():
     p = binding.make_params(4096, 4096, 128, 3, 10)
     n = binding.workspace_bytes(p)
-    # W H, P, the accepted changes and the fp16 planes of H and E dominate
-    assert 3 * 64 * 2**20 < n < 400 * 2**20
+    # W H, W M^T, P, the accepted changes, q - z and the fp16 planes of H, M
+    # and E dominate
+    assert 5 * 64 * 2**20 < n < 512 * 2**20
     for bad in [dict(rows=0), dict(cols=100), dict(group_size=48), dict(bits=0), dict(bits=9),
                 dict(sweeps=-1), dict(cols=128 * 129), dict(ridge_lambda=-1.0)]:
         kw = dict(rows=64, cols=256, group_size=64, bits=3, sweeps=5)

@@ -131,14 +131,39 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     Counters* __restrict__ cnt, SweepRecord* __restrict__ rec, SweepCtl* __restrict__ sctl,
     GramCtl* __restrict__ gctl, const uint32_t* __restrict__ gcount, int32_t* __restrict__ gpre,
     int G) {
-  // prefix sums of the Gram row sub-lists, one group per thread
+  // prefix sums of the Gram row sub-lists, one group per thread (all loads
+  // first)
   for (int x = threadIdx.x; x < G; x += kRecordThreads) {
+    int c[kSubLists];
+#pragma unroll
+    for (int s = 0; s < kSubLists; ++s) c[s] = (int)gcount[((size_t)x * kSubLists + s) * kCtrStride];
     int acc = 0;
+#pragma unroll
     for (int s = 0; s < kSubLists; ++s) {
       gpre[x * (kSubLists + 1) + s] = acc;
-      acc += (int)gcount[((size_t)x * kSubLists + s) * kCtrStride];
+      acc += c[s];
     }
     gpre[x * (kSubLists + 1) + kSubLists] = acc;
+  }
+  // the counter copies: thread t < kSubLists reads copy t (then resets it)
+  __shared__ Counters csum_s[kSubLists];
+  if (threadIdx.x < kSubLists) {
+    Counters* ct = cnt + threadIdx.x;
+    Counters v{};
+    v.accepted = ct->accepted;
+    v.changed = ct->changed;
+    v.skipped = ct->skipped;
+    v.corr_blocks = ct->corr_blocks;
+    v.ridge_rows = ct->ridge_rows;
+    v.solve_failed = ct->solve_failed;
+    csum_s[threadIdx.x] = v;
+    ct->accepted = 0;
+    ct->changed = 0;
+    ct->skipped = 0;
+    ct->corr_blocks = 0;
+    ct->ridge_rows = 0;
+    ct->solve_failed = 0;
+    ct->active_rows = 0;
   }
   __shared__ double red[kRecordThreads];
   __shared__ unsigned int act[kRecordThreads];
@@ -171,13 +196,13 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
   }
   if (threadIdx.x == 0) {
     Counters sum{};
-    for (int c = 0; c < kSubLists; ++c) {
-      sum.accepted += cnt[c].accepted;
-      sum.changed += cnt[c].changed;
-      sum.skipped += cnt[c].skipped;
-      sum.corr_blocks += cnt[c].corr_blocks;
-      sum.ridge_rows += cnt[c].ridge_rows;
-      sum.solve_failed += cnt[c].solve_failed;
+    for (int c = 0; c < kSubLists; ++c) {  // LDS, written before the tree's barriers
+      sum.accepted += csum_s[c].accepted;
+      sum.changed += csum_s[c].changed;
+      sum.skipped += csum_s[c].skipped;
+      sum.corr_blocks += csum_s[c].corr_blocks;
+      sum.ridge_rows += csum_s[c].ridge_rows;
+      sum.solve_failed += csum_s[c].solve_failed;
     }
     rec->objective_after_scales = red[0];
     rec->accepted = sum.accepted;
@@ -193,15 +218,6 @@ __global__ __launch_bounds__(kRecordThreads) void record_sweep_kernel(
     if (started > 0) {
       sctl->started += 1;
       gctl->valid = 1;  // every row that took part has its matrix built
-    }
-    for (int c = 0; c < kSubLists; ++c) {
-      cnt[c].accepted = 0;
-      cnt[c].changed = 0;
-      cnt[c].skipped = 0;
-      cnt[c].corr_blocks = 0;
-      cnt[c].ridge_rows = 0;
-      cnt[c].solve_failed = 0;
-      cnt[c].active_rows = 0;
     }
   }
 }

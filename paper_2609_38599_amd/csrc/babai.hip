@@ -29,11 +29,14 @@
 //     itself waits for its decision, the others are applied meanwhile.
 //   R~ = R_{i+1} with unit diagonal, staged into LDS by direct loads.
 // Back substitution: 16 lanes per row, lane j owns positions j + 16 t and keeps
-// y_l = u_l / R(l,l) - sum of R~(l, m) d_m over the positions m decided so far;
+// y_l = u_l / R(l,l) - sum of R~(l, m) d_m over the positions m > l decided so
+// far (R~ = R with rows scaled by 1/R(m,m), staged without its unit diagonal);
 // at step l the owner's change d_l = clip(rint(y_l)) is broadcast within the
-// row (DPP row broadcast) and every lane subtracts R~(m, l) d_l from its y_m.
-// After the last step u_l / R(l,l) - y_l = a_l above.  No branches and no LDS
-// round trip on the dependency chain.  The accept test then reduces over the
+// row (DPP row broadcast) and every lane subtracts R~(m, l) d_l from its y_m,
+// m < l.  A position's y is final once it is decided, so d_l is taken again
+// from the final y after the last step (nothing is recorded per step), and
+// u_l / R(l,l) - y_l + d_l = a_l above.  No branches and no LDS round trip on
+// the dependency chain.  The accept test then reduces over the
 // row's lanes with DPP.  Decisions stay in LDS: codes and dq of the panel are
 // written once, with 16-byte stores, after its last group.
 #include "jarq_internal.h"
@@ -62,13 +65,11 @@ __device__ __forceinline__ void dma16(const float* src, float* lds) {
 }
 
 // Per lane and position l = j + 16 t of the row: y = u~_l - sum_m R~(l, m) d_m
-// over the positions m already decided (R~ = R_i with unit diagonal, so the
-// position's own change is in the sum once it is decided), the code change d
-// taken at l, and the bounds -q_l, 2^b - 1 - q_l of that change.
+// over the positions m > l already decided, and the bounds -q_l, 2^b - 1 - q_l
+// of the code change taken at l.
 template <int NT>
 struct ChainState {
   float y[NT];
-  float d[NT];
   float lo[NT];
   float hi[NT];
 };
@@ -150,7 +151,6 @@ struct ChainStep {
     constexpr int JL = L & 15;
     const RCol<NT> c4 = load_rcol<L - 4, NT>(rc, cj);
     const float dv = __builtin_amdgcn_fmed3f(rintf(s.y[TL]), s.lo[TL], s.hi[TL]);
-    s.d[TL] = cj == JL ? dv : s.d[TL];
     const float db = row_bcast<JL>(dv);
 #pragma unroll
     for (int t = 0; t <= TL; ++t) s.y[t] = fmaf(-c0.v[t], db, s.y[t]);
@@ -379,7 +379,6 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         const float q = row_in ? (float)nq[t] : 0.f;
         qold[t] = q;
         cs.y[t] = ut[t];
-        cs.d[t] = 0.f;
         cs.lo[t] = -q;
         cs.hi[t] = qmax - q;
       }
@@ -387,15 +386,18 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
       ChainStep<g - 1, NT>::run(cs, rc_i, cj, load_rcol<g - 1, NT>(rc_i, cj),
                                 load_rcol<g - 2, NT>(rc_i, cj), load_rcol<g - 3, NT>(rc_i, cj),
                                 load_rcol<g - 4, NT>(rc_i, cj));
-      // a_l = sum_{m >= l} R~(l, m) d_m = u~_l - y_l; the change of F divided
-      // by s_i^2 is sum_l R(l, l)^2 a_l (a_l - 2 u~_l).
+      // d_l again from the final y_l (unchanged since its step), a_l =
+      // sum_{m >= l} R~(l, m) d_m = u~_l - y_l + d_l (unit diagonal of R~);
+      // the change of F divided by s_i^2 is sum_l R(l, l)^2 a_l (a_l - 2 u~_l).
       float dF = 0.f;
       int changed = 0;
+      float dd[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const float a = ut[t] - cs.y[t];
+        dd[t] = __builtin_amdgcn_fmed3f(rintf(cs.y[t]), cs.lo[t], cs.hi[t]);
+        const float a = (ut[t] - cs.y[t]) + dd[t];
         dF = fmaf(rdsq_i[t] * a, a - 2.f * ut[t], dF);
-        changed += cs.d[t] != 0.f;
+        changed += dd[t] != 0.f;
       }
       dF = row_sum(dF);
       changed = row_sum(changed);
@@ -405,14 +407,14 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         const int l = cj + 16 * t;
-        dqp_s[crow * PW + (i - i0) * g + l] = accept ? (_Float16)cs.d[t] : (_Float16)0.f;
+        dqp_s[crow * PW + (i - i0) * g + l] = accept ? (_Float16)dd[t] : (_Float16)0.f;
       }
       if (cand_out != nullptr && row_in) {
         const size_t cbase = (size_t)crid * cols + (size_t)i * g;
 #pragma unroll
         for (int t = 0; t < NT; ++t)
           cand_out[cbase + cj + 16 * t] =
-              (uint8_t)(do_row ? fminf(fmaxf(qold[t] + cs.d[t], 0.f), qmax) : qold[t]);
+              (uint8_t)(do_row ? fminf(fmaxf(qold[t] + dd[t], 0.f), qmax) : qold[t]);
       }
       acc_bits |= accept ? 1 << (i - i0) : 0;
       if (row_in && cj == 0) {

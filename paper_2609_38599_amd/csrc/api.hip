@@ -50,6 +50,7 @@ Layout make_layout(int rows, int cols, int g) {
   L.rw = take(R * C * sizeof(float));
   L.cz = take(R * C * 2);
   L.gram = take(R * G * G * sizeof(float));
+  L.rhs = take(R * G * sizeof(double));
   L.p = take(R * C * sizeof(float));
   L.dq = take(R * C * 2);
   const size_t cap = (size_t)sublist_cap(rows);
@@ -149,8 +150,9 @@ hipError_t enqueue_scale_step(const Ctx& c, const float* H, const uint8_t* codes
   hipError_t e = launch_gram(c.st, c.rows, c.cols, c.g, c.ws, c.lay, codes, zeros, c.gram(),
                              nullptr, nullptr, /*incremental=*/false);
   if (e != hipSuccess) return e;
-  return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, active,
-                      c.cnt(), c.flags(), lam, rcond, accept, nullptr, nullptr);
+  return launch_solve(c.st, c.rows, c.cols, c.g, c.gram(), c.wh(), codes, zeros,
+                      (double*)(c.ws + c.lay.rhs), nullptr, scales, active, c.cnt(), c.flags(),
+                      lam, rcond, accept, nullptr, nullptr);
 }
 
 struct NoHook {
@@ -308,9 +310,9 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
                       /*incremental=*/true);
     if (e == hipSuccess) e = mark(k, 1);
     if (e == hipSuccess)
-      e = launch_solve(c.st, n, c.cols, c.g, c.gram(), c.wh(), codes, zeros, scales, c.active(),
-                       c.cnt(), c.flags(), p->ridge_lambda, p->ridge_rcond, p->ridge_accept,
-                       rmap, n_dev);
+      e = launch_solve(c.st, n, c.cols, c.g, c.gram(), c.wh(), codes, zeros,
+                       (double*)(c.ws + c.lay.rhs), c.gctl(), scales, c.active(), c.cnt(),
+                       c.flags(), p->ridge_lambda, p->ridge_rcond, p->ridge_accept, rmap, n_dev);
     if (e == hipSuccess) e = mark(k, 2);
     if (e == hipSuccess)
       e = launch_resid(c.st, n, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), rmap, n_dev);

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     uint8_t* __restrict__ dec_out, Counters* __restrict__ cnt,
     const int32_t* __restrict__ rowmap, const int* __restrict__ n_dev,
     int32_t* __restrict__ glist, uint32_t* __restrict__ gcount, int list_cap,
-    _Float16* __restrict__ cz) {
+    _Float16* __restrict__ cz, const float* __restrict__ wh, double* __restrict__ rhs) {
   if (n_dev != nullptr) rows = *n_dev;
   if ((int)blockIdx.x * 16 >= rows) return;  // the whole work-group: no row here
   constexpr int g = G_SIZE;
@@ -550,7 +550,9 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 
   // ---- codes += accepted changes, cz (q - z as fp16) likewise, and dq =
   // accepted changes, over the panel's columns: 16 columns per thread and step
-  // (16-byte code, 2 x 16-byte cz and dq accesses).  dqp_s is complete since
+  // (16-byte code, 2 x 16-byte cz and dq accesses).  The scale systems'
+  // right-hand sides follow the codes: r_i += d_i^T (W H)_i, summed in fp64
+  // over the g / 16 consecutive threads of a group.  dqp_s is complete since
   // the last barrier.
   {
     const int per_row = (i1 - i0) * g / 16;
@@ -565,9 +567,18 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         const uint32_t oq = (uint32_t)(i0 * g + k);
         const f16x8 d0 = *(const f16x8*)(dqp_s + r * PW + k);
         const f16x8 d1 = *(const f16x8*)(dqp_s + r * PW + k + 8);
+        bool any = false;
+#pragma unroll
+        for (int b = 0; b < 8; ++b) any |= (d0[b] != (_Float16)0.f) | (d1[b] != (_Float16)0.f);
         const uint4 qw = ld_at((const uint4*)codes_r, oq);
         const f16x8 c0 = ld_at((const f16x8*)cz_r, 2 * oq);
         const f16x8 c1 = ld_at((const f16x8*)cz_r, 2 * oq + 16);
+        f32x4 w4[4];  // (W H) of the 16 columns, only where a code changes
+        if (any) {
+          const float* whp = wh + lrow_r * cols + oq;
+#pragma unroll
+          for (int b4 = 0; b4 < 4; ++b4) w4[b4] = *(const f32x4*)(whp + 4 * b4);
+        }
         uint32_t w[4] = {qw.x, qw.y, qw.z, qw.w};
         // Byte b of word b / 4 gains d_b; new codes stay in [0, 2^bits - 1],
         // so the word-wide add never carries into a neighbouring byte.
@@ -581,6 +592,21 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         st_at((f16x8*)cz_r, 2 * oq + 16, c1 + d1);
         st_at((f16x8*)dq_t, 2 * o, d0);
         st_at((f16x8*)dq_t, 2 * o + 16, d1);
+        double part = 0.0;
+        if (any) {
+#pragma unroll
+          for (int b4 = 0; b4 < 4; ++b4)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int b = 4 * b4 + e;
+              part = fma((double)(b < 8 ? d0[b] : d1[b - 8]), (double)w4[b4][e], part);
+            }
+        }
+        if (__ballot(any) != 0) {  // waves without a change skip the reduction
+#pragma unroll
+          for (int off = 1; off < g / 16; off <<= 1) part += __shfl_xor(part, off);
+          if (k % g == 0 && part != 0.0) rhs[lrow_r * G + (size_t)(i0 + k / g)] += part;
+        }
       }
     }
   }
@@ -615,7 +641,7 @@ static hipError_t launch_babai_t(hipStream_t st, int rows, int cols, int bits, i
                      (_Float16*)(ws + lay.dq), (int32_t*)(ws + lay.plist),
                      (uint32_t*)(ws + lay.pcount) + (size_t)(i0 / PG) * kSubLists * kCtrStride,
                      cand, decision, cnt, rowmap, n_dev, glist, gcount, list_cap,
-                     (_Float16*)(ws + lay.cz));
+                     (_Float16*)(ws + lay.cz), (const float*)(ws + lay.wh), (double*)(ws + lay.rhs));
   return hipGetLastError();
 }
 

@@ -129,6 +129,7 @@ struct Layout {
   size_t rw;        // [rows][cols] f32: W_i L_i per group (the objective's part of W alone)
   size_t cz;        // [rows][cols] f16: q - z, exact, by layer row (kept with the codes)
   size_t gram;      // [rows][G][G] f32: upper triangle of B^T B
+  size_t rhs;       // [rows][G] f64: the scale systems' right-hand sides c_i^T (W H)_i
   size_t p;         // [rows][cols] f32: (W - What) H
   size_t dq;        // [rows][cols] f16: q_new - q_old of accepted groups, 0 elsewhere
   size_t plist;     // [kSubLists][cap] i32: rows that accepted a change in the last panel (any order)
@@ -212,8 +213,12 @@ hipError_t launch_gram(hipStream_t st, int rows, int cols, int g, const char* ws
                        const Layout& lay, const uint8_t* codes, const int32_t* zeros,
                        float* gram, const int32_t* rowmap, const int* n_dev, bool incremental);
 
+// The scale solves.  Right-hand sides come from rhs_cache ([layer rows][G]
+// fp64) when rctl says the matrices and right-hand sides of the last sweep
+// are complete (rctl->valid), else from W H and the codes (then stored there).
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
+                        double* rhs_cache, const GramCtl* rctl,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
                         float lam, float rcond, int accept, const int32_t* rowmap,
                         const int* n_dev);

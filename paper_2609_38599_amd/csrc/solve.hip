@@ -23,6 +23,59 @@
 
 namespace jarq {
 
+// Right-hand sides of the scale systems, r_i = c_i^T (W H)_i for group i of a
+// row (eq. (6)), in fp64.  They depend on the row's codes of group i only, so
+// the sweep keeps them in `cache` ([layer rows][G]): the first scale solve of
+// a run (ctl->valid == 0, or no ctl) forms them from W H and the codes and
+// stores them; later ones read them, the code update having added
+// d^T (W H)_i for every change d it made since.
+struct RhsSrc {
+  const float* wh;
+  const uint8_t* codes;
+  const int32_t* zeros;
+  double* cache;
+  const GramCtl* ctl;
+};
+
+template <int g>
+__device__ __forceinline__ double rhs_entry(const RhsSrc& rs, int grow, int i, int cols, int G) {
+  const float* whp = rs.wh + (size_t)grow * cols + (size_t)i * g;
+  const uint8_t* qp = rs.codes + (size_t)grow * cols + (size_t)i * g;
+  const double z = (double)rs.zeros[(size_t)grow * G + i];
+  double r = 0.0;
+  constexpr int CH = g < 32 ? g : 32;  // columns per batch of loads
+#pragma unroll
+  for (int c0 = 0; c0 < g; c0 += CH) {
+    uint4 qv[CH / 16];
+    f32x4 wv[CH / 4];
+#pragma unroll
+    for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
+#pragma unroll
+    for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
+#pragma unroll
+    for (int u = 0; u < CH / 4; ++u) {
+      const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
+                           : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        r = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], r);
+    }
+  }
+  return r;
+}
+
+// r_i of layer row grow; `store`: this lane owns the entry (stores it when it
+// forms it).
+template <int g>
+__device__ __forceinline__ double rhs_of(const RhsSrc& rs, int grow, int i, int cols, int G,
+                                         bool store) {
+  const bool cached = rs.ctl != nullptr && rs.ctl->valid != 0;
+  if (cached) return rs.cache[(size_t)grow * G + i];
+  const double r = rhs_entry<g>(rs, grow, i, cols, G);
+  if (store) rs.cache[(size_t)grow * G + i] = r;
+  return r;
+}
+
 // 1 / sqrt(x) in fp64: the hardware estimate (about 23 bits) and two Newton
 // steps y <- y (3/2 - x y^2 / 2), each of which doubles the correct bits.
 __device__ __forceinline__ double rsqrt_f64(double x) {
@@ -36,9 +89,7 @@ __device__ __forceinline__ double rsqrt_f64(double x) {
 template <int GM, int GS>
 __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
                                                        const float* __restrict__ gram,
-                                                       const float* __restrict__ wh,
-                                                       const uint8_t* __restrict__ codes,
-                                                       const int32_t* __restrict__ zeros,
+                                                       const RhsSrc rs,
                                                        float* __restrict__ scales,
                                                        const uint8_t* __restrict__ active,
                                                        Counters* __restrict__ cnt,
@@ -69,31 +120,8 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   __shared__ double lt[RPW][GM][GM + 1];
 
   // ---- right-hand side r_i = sum over group i of (q - z) (W H) ----
-  double r0 = 0.0;
-  {
-    const float* whp = wh + (size_t)grow * cols + (size_t)ic * g;
-    const uint8_t* qp = codes + (size_t)grow * cols + (size_t)ic * g;
-    const double z = (double)zeros[(size_t)grow * G + ic];
-    constexpr int CH = g < 32 ? g : 32;  // columns per batch of loads
-#pragma unroll
-    for (int c0 = 0; c0 < g; c0 += CH) {
-      uint4 qv[CH / 16];
-      f32x4 wv[CH / 4];
-#pragma unroll
-      for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
-#pragma unroll
-      for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
-#pragma unroll
-      for (int u = 0; u < CH / 4; ++u) {
-        const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
-                             : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          r0 = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], r0);
-      }
-    }
-    if (!live) r0 = 0.0;
-  }
+  double r0 = rhs_of<g>(rs, grow, ic, cols, G, live && row_ok);
+  if (!live) r0 = 0.0;
 
   // ---- row i of the Gram matrix (entry (i, j) stored at (min, max)) ----
   double A[GM];
@@ -233,9 +261,7 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
 template <int GS>
 __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
                                                         const float* __restrict__ gram,
-                                                        const float* __restrict__ wh,
-                                                        const uint8_t* __restrict__ codes,
-                                                        const int32_t* __restrict__ zeros,
+                                                        const RhsSrc rs,
                                                         float* __restrict__ scales,
                                                         const uint8_t* __restrict__ active,
                                                         Counters* __restrict__ cnt,
@@ -262,30 +288,7 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
   double* red = rk_s + G;       // two wavefronts' partial max / flags
 
   // right-hand side r_i = sum over group i of (q - z) (W H)
-  double r0 = 0.0;
-  {
-    const float* whp = wh + (size_t)grow * cols + (size_t)ic * g;
-    const uint8_t* qp = codes + (size_t)grow * cols + (size_t)ic * g;
-    const double z = (double)zeros[(size_t)grow * G + ic];
-    constexpr int CH = g < 32 ? g : 32;
-#pragma unroll
-    for (int c0 = 0; c0 < g; c0 += CH) {
-      uint4 qv[CH / 16];
-      f32x4 wv[CH / 4];
-#pragma unroll
-      for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
-#pragma unroll
-      for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
-#pragma unroll
-      for (int u = 0; u < CH / 4; ++u) {
-        const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
-                             : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          r0 = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], r0);
-      }
-    }
-  }
+  const double r0 = rhs_of<g>(rs, grow, ic, cols, G, live);
 
   const float* gr = gram + (size_t)grow * G * G;  // stored by layer row
   double diag = 0.0;
@@ -476,9 +479,7 @@ __device__ __forceinline__ void Unroll4(F&& f) {
 template <int TPL, int GS>
 __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
                                                         const float* __restrict__ gram,
-                                                        const float* __restrict__ wh,
-                                                        const uint8_t* __restrict__ codes,
-                                                        const int32_t* __restrict__ zeros,
+                                                        const RhsSrc rs,
                                                         float* __restrict__ scales,
                                                         const uint8_t* __restrict__ active,
                                                         Counters* __restrict__ cnt,
@@ -509,30 +510,8 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
   for (int sl = 0; sl < 2; ++sl) {
     const int i = lane + 64 * sl;
     if (i < G) {
-      const float* whp = wh + (size_t)grow * cols + (size_t)i * g;
-      const uint8_t* qp = codes + (size_t)grow * cols + (size_t)i * g;
-      const double z = (double)zeros[(size_t)grow * G + i];
-      double acc = 0.0;
-      constexpr int CH = g < 32 ? g : 32;
-#pragma unroll
-      for (int c0 = 0; c0 < g; c0 += CH) {
-        uint4 qv[CH / 16];
-        f32x4 wv[CH / 4];
-#pragma unroll
-        for (int u = 0; u < CH / 16; ++u) qv[u] = *(const uint4*)(qp + c0 + 16 * u);
-#pragma unroll
-        for (int u = 0; u < CH / 4; ++u) wv[u] = *(const f32x4*)(whp + c0 + 4 * u);
-#pragma unroll
-        for (int u = 0; u < CH / 4; ++u) {
-          const uint32_t w32 = (u & 3) == 0 ? qv[u / 4].x : (u & 3) == 1 ? qv[u / 4].y
-                               : (u & 3) == 2 ? qv[u / 4].z : qv[u / 4].w;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc = fma((double)((w32 >> (8 * e)) & 0xffu) - z, (double)wv[u][e], acc);
-        }
-      }
-      r0[sl] = acc;
-      finite &= isfinite(acc);
+      r0[sl] = rhs_of<g>(rs, grow, i, cols, G, true);
+      finite &= isfinite(r0[sl]);
     }
   }
 
@@ -742,7 +721,7 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
 
 template <int TPL, int GS>
 static hipError_t launch_solve_tile(hipStream_t st, int rows, int cols, const float* gram,
-                                    const float* wh, const uint8_t* codes, const int32_t* zeros,
+                                    const RhsSrc& rs,
                                     float* scales, const uint8_t* active, Counters* cnt,
                                     Flags* flags, float lam, float rcond, int accept,
                                     const int32_t* rowmap, const int* n_dev) {
@@ -756,14 +735,14 @@ static hipError_t launch_solve_tile(hipStream_t st, int rows, int cols, const fl
                                    lds_set);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_tile_kernel<TPL, GS>), dim3(rows), dim3(64), lds, st, rows, cols,
-                     gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept,
+                     gram, rs, scales, active, cnt, flags, lam, rcond, accept,
                      rowmap, n_dev);
   return hipGetLastError();
 }
 
 template <int GS>
 static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const float* gram,
-                                   const float* wh, const uint8_t* codes, const int32_t* zeros,
+                                   const RhsSrc& rs,
                                    float* scales, const uint8_t* active, Counters* cnt,
                                    Flags* flags, float lam, float rcond, int accept,
                                    const int32_t* rowmap, const int* n_dev) {
@@ -776,51 +755,53 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
                                    ((size_t)128 * 129 + 2 * 128 + 2) * sizeof(double), lds_set);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
-                     cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
+                     cols, gram, rs, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
   return hipGetLastError();
 }
 
 template <int GM, int GS>
 static hipError_t launch_solve_reg(hipStream_t st, int rows, int cols, const float* gram,
-                                   const float* wh, const uint8_t* codes, const int32_t* zeros,
+                                   const RhsSrc& rs,
                                    float* scales, const uint8_t* active, Counters* cnt,
                                    Flags* flags, float lam, float rcond, int accept,
                                    const int32_t* rowmap, const int* n_dev) {
   constexpr int RPW = 64 / GM;
   hipLaunchKernelGGL((solve_reg_kernel<GM, GS>), dim3((rows + RPW - 1) / RPW), dim3(64), 0, st,
-                     rows, cols, gram, wh, codes, zeros, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
+                     rows, cols, gram, rs, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* gram,
                         const float* wh, const uint8_t* codes, const int32_t* zeros,
+                        double* rhs_cache, const GramCtl* rctl,
                         float* scales, const uint8_t* active, Counters* cnt, Flags* flags,
                         float lam, float rcond, int accept, const int32_t* rowmap,
                         const int* n_dev) {
   const int G = cols / g;
   const int T = (G + 3) / 4, NT = T * (T + 1) / 2;  // 4 x 4 tiles of the lower triangle
+  const RhsSrc rs{wh, codes, zeros, rhs_cache, rctl};
 #define JARQ_SOLVE_TILE(TPL)                                                                     \
   switch (g) {                                                                                   \
-    case 32: return launch_solve_tile<TPL, 32>(st, rows, cols, gram, wh, codes, zeros, scales,   \
+    case 32: return launch_solve_tile<TPL, 32>(st, rows, cols, gram, rs, scales,   \
                                                active, cnt, flags, lam, rcond, accept, rowmap,   \
                                                n_dev);                                           \
-    case 64: return launch_solve_tile<TPL, 64>(st, rows, cols, gram, wh, codes, zeros, scales,   \
+    case 64: return launch_solve_tile<TPL, 64>(st, rows, cols, gram, rs, scales,   \
                                                active, cnt, flags, lam, rcond, accept, rowmap,   \
                                                n_dev);                                           \
-    case 128: return launch_solve_tile<TPL, 128>(st, rows, cols, gram, wh, codes, zeros, scales, \
+    case 128: return launch_solve_tile<TPL, 128>(st, rows, cols, gram, rs, scales, \
                                                  active, cnt, flags, lam, rcond, accept, rowmap, \
                                                  n_dev);                                         \
     default: return hipErrorInvalidValue;                                                        \
   }
   if (G <= 32) {  // two systems per wavefront, a row of the system per lane
     switch (g) {
-      case 32: return launch_solve_reg<32, 32>(st, rows, cols, gram, wh, codes, zeros, scales,
+      case 32: return launch_solve_reg<32, 32>(st, rows, cols, gram, rs, scales,
                                                active, cnt, flags, lam, rcond, accept, rowmap,
                                                n_dev);
-      case 64: return launch_solve_reg<32, 64>(st, rows, cols, gram, wh, codes, zeros, scales,
+      case 64: return launch_solve_reg<32, 64>(st, rows, cols, gram, rs, scales,
                                                active, cnt, flags, lam, rcond, accept, rowmap,
                                                n_dev);
-      case 128: return launch_solve_reg<32, 128>(st, rows, cols, gram, wh, codes, zeros, scales,
+      case 128: return launch_solve_reg<32, 128>(st, rows, cols, gram, rs, scales,
                                                  active, cnt, flags, lam, rcond, accept, rowmap,
                                                  n_dev);
       default: return hipErrorInvalidValue;
@@ -833,11 +814,11 @@ hipError_t launch_solve(hipStream_t st, int rows, int cols, int g, const float* 
 #undef JARQ_SOLVE_TILE
   if (G <= 128) {  // the widest layers: the system in LDS, one work-group per row
     switch (g) {
-      case 32: return launch_solve_col<32>(st, rows, cols, gram, wh, codes, zeros, scales, active,
+      case 32: return launch_solve_col<32>(st, rows, cols, gram, rs, scales, active,
                                            cnt, flags, lam, rcond, accept, rowmap, n_dev);
-      case 64: return launch_solve_col<64>(st, rows, cols, gram, wh, codes, zeros, scales, active,
+      case 64: return launch_solve_col<64>(st, rows, cols, gram, rs, scales, active,
                                            cnt, flags, lam, rcond, accept, rowmap, n_dev);
-      case 128: return launch_solve_col<128>(st, rows, cols, gram, wh, codes, zeros, scales,
+      case 128: return launch_solve_col<128>(st, rows, cols, gram, rs, scales,
                                              active, cnt, flags, lam, rcond, accept, rowmap, n_dev);
       default: break;
     }

@@ -20,7 +20,7 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // kDotRowBlocks rows x one group; each wave takes kDotRowBlocks blocks of 16
 // consecutive rows.  Rows of cz, RW, W and the scales are layer rows
 // (through the row map), U and the partials are by position.
-constexpr int kDotRowBlocks = 2;   // 16-row blocks per wave
+constexpr int kDotRowBlocks = 4;   // 16-row blocks per wave
 
 template <int G_SIZE, int kMode>
 __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
@@ -56,14 +56,28 @@ __global__ __launch_bounds__(256) void group_dot_kernel(int rows, int cols,
   const int wave = threadIdx.x >> 6;
   const int mr = lane & 15, kq = lane >> 4;
   {
+    // all of this thread's pieces are requested before any is stored
     const _Float16* Rh = rph + (size_t)i * g * g;
     const _Float16* Rl = rpl + (size_t)i * g * g;
-    for (int e = threadIdx.x; e < g * g / 8; e += 256) {
+    constexpr int NE = (g * g / 8 + 255) / 256;
+    f16x8 th[NE], tl[NE];
+#pragma unroll
+    for (int u = 0; u < NE; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int c = e / (g / 8), k0 = 8 * (e % (g / 8));
+      if (e < g * g / 8 && k0 >= 32 * (c >> 5)) {
+        th[u] = *(const f16x8*)(Rh + (size_t)c * g + k0);
+        tl[u] = *(const f16x8*)(Rl + (size_t)c * g + k0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NE; ++u) {
+      const int e = threadIdx.x + 256 * u;
       const int c = e / (g / 8), k0 = 8 * (e % (g / 8));
       const int kb = 32 * (c >> 5);
-      if (k0 >= kb) {
-        *(f16x8*)(rs_h + roff(c) + k0 - kb) = *(const f16x8*)(Rh + (size_t)c * g + k0);
-        *(f16x8*)(rs_l + roff(c) + k0 - kb) = *(const f16x8*)(Rl + (size_t)c * g + k0);
+      if (e < g * g / 8 && k0 >= kb) {
+        *(f16x8*)(rs_h + roff(c) + k0 - kb) = th[u];
+        *(f16x8*)(rs_l + roff(c) + k0 - kb) = tl[u];
       }
     }
   }

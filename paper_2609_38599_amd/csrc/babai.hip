@@ -459,16 +459,19 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         if (i + 2 < i1) u_from_p(i + 2, un);
         // block h = i0 + k sits in fa for even k, fb for odd k; the next
         // block loads while the current one is applied, and the last one,
-        // M(i + 1, i), stays in flight across the barrier
-        load_t(i + 1, i0, fa);
+        // M(i + 1, i), stays in flight across the barrier.  A block of an
+        // earlier group that no row of the tile accepted (decided before this
+        // position) is neither loaded nor applied.
+        auto wanted = [&](int k) { return k == p || tacc_s[k] != 0; };
+        if (wanted(0)) load_t(i + 1, i0, fa);
         Unroll<0, p>::run([&](auto kc) {
           constexpr int k = decltype(kc)::value;
           if constexpr (k % 2 == 0) {
-            load_t(i + 1, i0 + k + 1, fb);
-            apply_t(i0 + k, fa, false, uc);
+            if (wanted(k + 1)) load_t(i + 1, i0 + k + 1, fb);
+            apply_t(i0 + k, fa, true, uc);
           } else {
-            load_t(i + 1, i0 + k + 1, fa);
-            apply_t(i0 + k, fb, false, uc);
+            if (wanted(k + 1)) load_t(i + 1, i0 + k + 1, fa);
+            apply_t(i0 + k, fb, true, uc);
           }
         });
       }

@@ -78,8 +78,9 @@ def per_kernel_mean(path: str, counter: str = None) -> dict:
 
 
 def _find(means: dict, name: str):
-    """The kernel whose name contains `name` (the first by sorted name)."""
-    keys = sorted(k for k in means if name in k)
+    """The kernel whose name, or short name (template arguments demangled),
+    contains `name` (the first by sorted name)."""
+    keys = sorted(k for k in means if name in k or name in short_name(k))
     return keys[0] if keys else None
 
 

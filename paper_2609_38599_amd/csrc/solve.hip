@@ -13,11 +13,22 @@
 //     row per work-group of 128 lanes.
 // The stabilised branch of
 // App. E.2 (add lambda I and factor again) is taken when an entry is not
-// finite, a pivot is not positive, or the smallest pivot is at most
-// r_cond * max(largest diagonal, 2^-23).  Every Cholesky pivot is a Schur
+// finite, a pivot is not positive, the smallest pivot is at most
+// r_cond * max(largest diagonal, 2^-23), or the smallest eigenvalue is at
+// most t = r_cond * max(||A||_F, 2^-23).  Every Cholesky pivot is a Schur
 // complement and bounded below by the smallest eigenvalue, and the largest
-// diagonal bounds the largest eigenvalue from below, so this test only fires
-// where the paper's eigenvalue test fires.  A second failure leaves the row's
+// diagonal bounds the largest eigenvalue from below, so the pivot test only
+// fires where the paper's eigenvalue test fires; it can miss a nearly
+// singular matrix whose pivots all stay large, which the last test catches.
+// ||A||_F bounds the largest eigenvalue from above, so the last test fires
+// wherever the paper's does, and beyond it only where the smallest
+// eigenvalue lies in (r_cond lambda_max, t].  It is settled cheaply where it
+// clearly does not fire: with L's comparison matrix C (|diagonal|, minus
+// |off-diagonal|), C^{-1} >= |L^{-1}| entrywise, so x = C^{-1} 1 (solved
+// beside the forward substitution) gives ||L^{-1}||_inf <= max x and
+// lambda_min = 1 / ||L^{-1}||_2^2 >= 1 / (G (max x)^2).  Only where that
+// bound is not above t is A - t I factored: it is positive definite exactly
+// when lambda_min > t.  A second failure after lambda I leaves the row's
 // scales unchanged and is counted.
 #include "jarq_internal.h"
 
@@ -87,7 +98,7 @@ __device__ __forceinline__ double rsqrt_f64(double x) {
 }
 
 template <int GM, int GS>
-__global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
+__global__ __launch_bounds__(64, 2) void solve_reg_kernel(int rows, int cols,
                                                        const float* __restrict__ gram,
                                                        const RhsSrc rs,
                                                        float* __restrict__ scales,
@@ -116,7 +127,9 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   const int ic = live ? i : G - 1;
 
   // column exchange of the factorisation steps and the transposed factor
+  // (col_rt: r and the comparison system's x side by side, one access each)
   __shared__ double col_a[RPW][GM], col_r[RPW][GM];
+  __shared__ double2 col_rt[RPW][GM];
   __shared__ double lt[RPW][GM][GM + 1];
 
   // ---- right-hand side r_i = sum over group i of (q - z) (W H) ----
@@ -125,10 +138,11 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
 
   // ---- row i of the Gram matrix (entry (i, j) stored at (min, max)) ----
   double A[GM];
-  double diag = 0.0;
+  double diag = 0.0, sq = 0.0;  // A_ii; sum of squares of row i
   bool finite = isfinite(r0);
   const float* gr = gram + (size_t)grow * G * G;  // stored by layer row
   auto load_rows = [&](double shift) __attribute__((always_inline)) {
+    sq = 0.0;
 #pragma unroll
     for (int j = 0; j < GM; ++j) {
       const bool in = live && j < G;
@@ -136,6 +150,7 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
       const float v = gr[idx];
       if (in) finite &= isfinite(v);
       if (j == i) diag = in ? (double)v : 1.0;
+      if (in) sq = fma((double)v, (double)v, sq);
       A[j] = in ? (double)v + (j == i ? shift : 0.0) : (j == i ? 1.0 : 0.0);
     }
   };
@@ -146,20 +161,24 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
   // (one wavefront: its LDS accesses complete in order, so no barrier); the
   // trailing update A_ij -= A_ik A_jk / A_kk and r_i -= A_ik r_k / A_kk run in
   // every lane (entries above the diagonal are never read).  Afterwards lane
-  // i holds L(i, 0..i), y_i and 1 / L(i, i).
-  double r, dinv = 0.0, minpiv;
+  // i holds L(i, 0..i), y_i and 1 / L(i, i).  The comparison system C x = 1
+  // runs along the same way (|l_ik| x_k added where l_ik y_k is subtracted);
+  // lane i ends with x_i.
+  double r, dinv = 0.0, minpiv, xc;
   bool pivots_ok;
   auto factor = [&]() __attribute__((always_inline)) {
     r = r0;
+    xc = 1.0;
     minpiv = INFINITY;
     pivots_ok = true;
 #pragma unroll
     for (int k = 0; k < GM; ++k) {
       if (k < G) {
         col_a[slot][i] = A[k];
-        col_r[slot][i] = r;
+        col_rt[slot][i] = double2{r, xc};
         const double piv = col_a[slot][k];
-        const double rk = col_r[slot][k];
+        const double2 rt = col_rt[slot][k];
+        const double rk = rt.x, tk = rt.y;
         pivots_ok &= piv > 0.0 && isfinite(piv);
         minpiv = fmin(minpiv, piv);
         const double rs = rsqrt_f64(piv);
@@ -167,43 +186,41 @@ __global__ __launch_bounds__(64) void solve_reg_kernel(int rows, int cols,
 #pragma unroll
         for (int j = k + 1; j < GM; ++j) A[j] = fma(-li, col_a[slot][j], A[j]);
         r = i > k ? fma(-li, rk, r) : (i == k ? rk * rs : r);
+        xc = i > k ? fma(fabs(li), tk, xc) : (i == k ? tk * rs : xc);
         A[k] *= rs;
         if (i == k) dinv = rs;
       }
     }
   };
   factor();
-  double dmax = live ? diag : 0.0;
+  double dmax = live ? diag : 0.0, fro = live ? sq : 0.0;
+  double xm = live ? (xc == xc ? xc : INFINITY) : 0.0;  // a NaN bound clears nothing
 #pragma unroll
-  for (int off = GM / 2; off >= 1; off >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, off));
+  for (int off = GM / 2; off >= 1; off >>= 1) {
+    dmax = fmax(dmax, __shfl_xor(dmax, off));
+    fro += __shfl_xor(fro, off);
+    xm = fmax(xm, __shfl_xor(xm, off));
+  }
+  const double tshift = (double)rcond * fmax(sqrt(fro), (double)kFp32Eps);
   const unsigned long long bad = __ballot(!finite);
   const unsigned long long slot_mask = GM == 64 ? ~0ull : (((1ull << GM) - 1) << (slot * GM));
   const bool all_finite = (bad & slot_mask) == 0;
-  const bool ridge = !all_finite || !pivots_ok ||
-                     !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  bool ridge = !all_finite || !pivots_ok ||
+               !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  // lambda_min >= 1 / (G (max x)^2); where that does not clear t, factor A - t I
+  const bool unsure = !ridge && !((double)G * xm * xm * tshift < 1.0);
+  if (__any(unsure)) {
+    load_rows(unsure ? -tshift : 0.0);
+    factor();
+    ridge = ridge || (unsure && !(pivots_ok && minpiv > 0.0));
+  }
+  // A + lam I for the rows that need it; the other rows of the wavefront
+  // factor A again (the same arithmetic, so the same factor)
   bool failed = false;
-  if (__any(ridge)) {
-    // A + lam I from the stored matrix, for the rows that need it (a row that
-    // shares the wavefront and does not keeps its first factorisation)
-    if constexpr (RPW == 1) {
-      load_rows((double)lam);
-      factor();
-      failed = !(pivots_ok && minpiv > 0.0);
-    } else {
-      double keepA[GM];
-      const double keep_r = r, keep_dinv = dinv;
-#pragma unroll
-      for (int j = 0; j < GM; ++j) keepA[j] = A[j];
-      load_rows((double)lam);
-      factor();
-      failed = ridge && !(pivots_ok && minpiv > 0.0);
-      if (!ridge) {
-#pragma unroll
-        for (int j = 0; j < GM; ++j) A[j] = keepA[j];
-        r = keep_r;
-        dinv = keep_dinv;
-      }
-    }
+  if (__any(ridge || unsure)) {
+    load_rows(ridge ? (double)lam : 0.0);
+    factor();
+    failed = ridge && !(pivots_ok && minpiv > 0.0);
   }
 
   // ---- backward substitution L^T s = y: L transposed through LDS ----
@@ -286,17 +303,19 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
   double* r_s = A + (size_t)G * LD;  // broadcast slot of r / s
   double* rk_s = r_s + G;       // 1 / sqrt(pivot k)
   double* red = rk_s + G;       // two wavefronts' partial max / flags
+  double* x_s = red + 2;        // broadcast slot of the comparison system
 
   // right-hand side r_i = sum over group i of (q - z) (W H)
   const double r0 = rhs_of<g>(rs, grow, ic, cols, G, live);
 
   const float* gr = gram + (size_t)grow * G * G;  // stored by layer row
-  double diag = 0.0;
+  double diag = 0.0, sq = 0.0;  // A_ii; sum of squares of row i
   bool finite = !live || isfinite(r0);
   // column-major copy of the system (+ shift on the diagonal); entry (i, j)
   // of the Gram matrix is stored at (min, max)
   // (batches of 8: loads first, from clamped indices, then the LDS stores)
   auto load = [&](double shift) __attribute__((always_inline)) {
+    sq = 0.0;
     if (live) {
       for (int j0 = 0; j0 < G; j0 += 8) {
         float v[8];
@@ -311,6 +330,7 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
           if (j < G) {
             finite &= isfinite(v[u]);
             if (j == i) diag = (double)v[u];
+            sq = fma((double)v[u], (double)v[u], sq);
             A[(size_t)j * LD + i] = (double)v[u] + (j == i ? shift : 0.0);
           }
         }
@@ -318,18 +338,24 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
     }
   };
   // Right-looking factorisation with the forward substitution; returns in r
-  // this lane's y_i.  Pivot k is read by every lane from LDS.
-  double r = 0.0, minpiv = INFINITY;
+  // this lane's y_i, and in xc its x_i of the comparison system C x = 1.
+  // Pivot k is read by every lane from LDS.
+  double r = 0.0, xc = 1.0, minpiv = INFINITY;
   bool pivots_ok = true;
   auto factor = [&]() __attribute__((always_inline)) {
     r = r0;
+    xc = 1.0;
     minpiv = INFINITY;
     pivots_ok = true;
-    if (live) r_s[i] = r;
+    if (live) {
+      r_s[i] = r;
+      x_s[i] = xc;
+    }
     __syncthreads();
     for (int k = 0; k < G; ++k) {
       const double piv = A[(size_t)k * LD + k];
       const double rk = r_s[k];
+      const double xk = x_s[k];
       pivots_ok &= piv > 0.0 && isfinite(piv);
       minpiv = fmin(minpiv, piv);
       const double rs = rsqrt_f64(piv);
@@ -351,9 +377,12 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
         }
         r = fma(-li, rk, r);
         r_s[i] = r;
+        xc = fma(fabs(li), xk, xc);
+        x_s[i] = xc;
       }
       if (i == k) {
         r = rk * rs;
+        xc = xk * rs;
         rk_s[k] = rs;
       }
       __syncthreads();
@@ -378,12 +407,38 @@ __global__ __launch_bounds__(128) void solve_col_kernel(int rows, int cols,
     return res;
   };
 
+  auto slot_sum = [&](double v) {  // over the work-group's lanes
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    if ((i & 63) == 0) red[i >> 6] = v;
+    __syncthreads();
+    v = red[0];
+    if (nthr > 64) v += red[1];
+    __syncthreads();
+    return v;
+  };
+
   load(0.0);
   const double dmax = slot_max(live ? diag : 0.0);
+  const double tshift = (double)rcond * fmax(sqrt(slot_sum(live ? sq : 0.0)), (double)kFp32Eps);
   const bool all_finite = all_true(finite);
   factor();
-  const bool ridge = !all_finite || !pivots_ok ||
-                     !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  bool ridge = !all_finite || !pivots_ok ||
+               !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  // lambda_min >= 1 / (G (max x)^2); where that does not clear t, factor
+  // A - t I and then A again (a NaN bound clears nothing)
+  const double xm = slot_max(live ? (xc == xc ? xc : INFINITY) : 0.0);
+  if (!ridge && !((double)G * xm * xm * tshift < 1.0)) {  // uniform
+    __syncthreads();
+    load(-tshift);
+    factor();
+    ridge = !(pivots_ok && minpiv > 0.0);
+    if (!ridge) {
+      __syncthreads();
+      load(0.0);
+      factor();
+    }
+  }
   bool failed = false;
   if (ridge) {  // uniform: every lane saw the same pivots
     __syncthreads();
@@ -540,8 +595,9 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
     kend[m] = e;
   }
   const float* gr = gram + (size_t)grow * G * G;  // upper triangle, stored by layer row
-  double diag = 0.0;
+  double diag = 0.0, sq = 0.0;  // largest diagonal; sum of squares (both triangles)
   auto load = [&](double shift) __attribute__((always_inline)) {
+    sq = 0.0;
 #pragma unroll
     for (int m = 0; m < TPL; ++m) {
 #pragma unroll
@@ -553,6 +609,7 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
           const float v = in ? gr[(size_t)c * G + r] : 0.f;
           if (in) finite &= isfinite(v);
           if (in && r == c) diag = fmax(diag, (double)v);
+          sq = fma((r == c ? 1.0 : 2.0) * (double)v, (double)v, sq);
           ta[m][a][b] = (double)v + (in && r == c ? shift : 0.0);
         }
       }
@@ -563,11 +620,14 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
 
   // The column published at step k is the Schur complement's column k
   // (unscaled); every lane forms 1/sqrt(pivot) from it, and reads scale by it.
-  double rr[2], rs_own[2] = {0.0, 0.0}, minpiv = INFINITY;
+  // The comparison system C x = 1 runs beside the forward substitution (xx).
+  double rr[2], xx[2], rs_own[2] = {0.0, 0.0}, minpiv = INFINITY;
   bool pivots_ok = true;
   auto factor = [&]() __attribute__((always_inline)) {
     rr[0] = r0[0];
     rr[1] = r0[1];
+    xx[0] = 1.0;
+    xx[1] = 1.0;
     minpiv = INFINITY;
     pivots_ok = true;
     for (int kc = 0; kc < T; ++kc) {
@@ -597,12 +657,18 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
         const double rs2 = rs * rs;
         // forward substitution: y_k = r_k / l_kk, r_i -= l_ik y_k for i > k
         const double yk = __shfl(k >> 6 ? rr[1] : rr[0], k & 63) * rs;
+        const double xk = __shfl(k >> 6 ? xx[1] : xx[0], k & 63) * rs;
 #pragma unroll
         for (int sl = 0; sl < 2; ++sl) {
           const int i = lane + 64 * sl;
-          if (i > k && i < G) rr[sl] = fma(-(colk[i] * rs), yk, rr[sl]);
+          if (i > k && i < G) {
+            const double lik = colk[i] * rs;
+            rr[sl] = fma(-lik, yk, rr[sl]);
+            xx[sl] = fma(fabs(lik), xk, xx[sl]);
+          }
           if (i == k) {
             rr[sl] = yk;
+            xx[sl] = xk;
             rs_own[sl] = rs;
           }
         }
@@ -635,13 +701,36 @@ __global__ __launch_bounds__(64) void solve_tile_kernel(int rows, int cols,
   };
 
   load(0.0);
-  double dmax = diag;
+  double dmax = diag, fro = sq;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, off));
+  for (int off = 32; off >= 1; off >>= 1) {
+    dmax = fmax(dmax, __shfl_xor(dmax, off));
+    fro += __shfl_xor(fro, off);
+  }
+  const double tshift = (double)rcond * fmax(sqrt(fro), (double)kFp32Eps);
   const bool all_finite = __all(finite);
   factor();
-  const bool ridge = !all_finite || !pivots_ok ||
-                     !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  bool ridge = !all_finite || !pivots_ok ||
+               !(minpiv > (double)rcond * fmax(dmax, (double)kFp32Eps));
+  // lambda_min >= 1 / (G (max x)^2); where that does not clear t, factor
+  // A - t I and then A again (a NaN bound clears nothing)
+  double xm = 0.0;
+#pragma unroll
+  for (int sl = 0; sl < 2; ++sl)
+    if (lane + 64 * sl < G) xm = fmax(xm, xx[sl] == xx[sl] ? xx[sl] : INFINITY);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) xm = fmax(xm, __shfl_xor(xm, off));
+  if (!ridge && !((double)G * xm * xm * tshift < 1.0)) {  // uniform
+    __syncthreads();  // the last step's reads are done before the columns are rewritten
+    load(-tshift);
+    factor();
+    ridge = !(pivots_ok && minpiv > 0.0);
+    if (!ridge) {
+      __syncthreads();
+      load(0.0);
+      factor();
+    }
+  }
   bool failed = false;
   if (ridge) {  // uniform: every lane saw the same pivots
     __syncthreads();  // the last step's reads are done before the columns are rewritten
@@ -748,11 +837,11 @@ static hipError_t launch_solve_col(hipStream_t st, int rows, int cols, const flo
                                    const int32_t* rowmap, const int* n_dev) {
   const int G = cols / GS;
   const int LD = G | 1;
-  const size_t lds = ((size_t)G * LD + 2 * (size_t)G + 2) * sizeof(double);
+  const size_t lds = ((size_t)G * LD + 3 * (size_t)G + 2) * sizeof(double);
   static std::atomic<unsigned long long> lds_set{0};
   // the widest layer: G = 128 (odd stride 129)
   hipError_t e = allow_dynamic_lds((const void*)solve_col_kernel<GS>,
-                                   ((size_t)128 * 129 + 2 * 128 + 2) * sizeof(double), lds_set);
+                                   ((size_t)128 * 129 + 3 * 128 + 2) * sizeof(double), lds_set);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((solve_col_kernel<GS>), dim3(rows), dim3(G <= 64 ? 64 : 128), lds, st, rows,
                      cols, gram, rs, scales, active, cnt, flags, lam, rcond, accept, rowmap, n_dev);

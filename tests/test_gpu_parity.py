@@ -306,6 +306,53 @@ def test_ridge_branch_matches_oracle():
     assert st["ridge_rows"][0] == 2
 
 
+def _near_singular_layer(rows, cols, g, kahan_rows, seed):
+    """Rows in kahan_rows get a nearly singular Gram matrix whose Cholesky pivots are all 1.
+
+    H = E K E^T + D: K = R^T R (R unit upper triangular, -1 above the
+    diagonal: every pivot 1, smallest eigenvalue below 1e-10 of the largest
+    from G = 16 on) on the first weight of every group, D = 1 on every other
+    weight.  A row whose codes minus zero points are 1 on each group's first
+    weight and 0 elsewhere has Gram matrix K exactly (eq. (5)); the other rows
+    have random codes and well-conditioned Gram matrices.  The first weights
+    of W are multiples of 1/8, so W H and every right-hand side are exact."""
+    rng = np.random.default_rng(seed)
+    G = cols // g
+    R = np.eye(G) + np.triu(-np.ones((G, G)), 1)
+    first = np.arange(G) * g
+    H = np.eye(cols)
+    H[first, first] = 0.0
+    H[np.ix_(first, first)] = R.T @ R
+    W = 0.02 * rng.standard_normal((rows, cols))
+    W[:, first] = rng.integers(-8, 9, size=(rows, G)) / 8.0
+    W = W.astype(np.float32)
+    q, s, z = rtn_quantize(W, g, 3)
+    q, z = q.copy(), z.copy()
+    for j in kahan_rows:
+        z[j] = 3
+        q[j] = 3
+        q[j, first] = 4
+    return W, np.ascontiguousarray(H.astype(np.float32)), q, s, z
+
+
+@pytest.mark.parametrize("cols,g", [(512, 32), (1024, 32), (4608, 64), (3200, 32), (3840, 32)])
+def test_ridge_trigger_on_large_pivots_matches_oracle(cols, g):
+    # G = 16 and 32 (register solve, two rows per wavefront: rows 1 and 6
+    # share theirs with a well-conditioned row), 72 and 100 (tile solve), 120
+    # (LDS solve).  The pivot test alone would miss rows 1 and 6; the
+    # eigenvalue bound and the factorisation of A - t I must catch them.
+    W, H, q, s, z = _near_singular_layer(8, cols, g, (1, 6), seed=cols)
+    gl = GpuLayer(W, H, q, s, z, g, 3)
+    gl.scale_step()
+    _, s_gpu = gl.state()
+    s_ref, ridge = jarq.scale_step(W, H, q, z, g)
+    assert list(np.nonzero(ridge)[0]) == [1, 6]
+    check_scales(s_gpu, s_ref, f" near-singular G {cols // g}")
+    g2 = GpuLayer(W, H, q, s, z, g, 3, sweeps=1)
+    st = jq.sweeps(g2.p, g2.W, g2.H, g2.codes, g2.scales, g2.zeros, g2.ws)
+    assert st["ridge_rows"][0] == 2
+
+
 @pytest.mark.parametrize("cols,g", [(256, 64), (4608, 64)])
 def test_ridge_acceptance_matches_oracle(cols, g):
     # Rows 3 and 17 have a group at its zero point (rank-deficient B_j).  With H

@@ -37,6 +37,7 @@ def _battery():
         ("lstsq", lambda: pins.test_scale_step_matches_lstsq(tl)),
         ("independent", lambda: pins.test_block_diagonal_hessian_gives_independent_fits()),
         ("ridge", lambda: pins.test_ridge_branch_on_singular_gram()),
+        ("ridge_large_pivots", pins.test_ridge_trigger_is_the_spectrum_not_the_pivots),
         ("qr_form", lambda: pins.test_qr_form_equals_hessian_form(tl)),
         ("monotone", lambda: pins.test_monotone_descent_and_host_bound(tl)),
         ("babai_bound", lambda: pins.test_unclipped_babai_residual_bound(tl)),
@@ -143,6 +144,17 @@ def _solve_factory(always_ridge=False, never_ridge=False):
     return solve_scales
 
 
+def _needs_ridge_from_pivots(Gs, rcond):
+    """The trigger taken from the Cholesky pivots instead of the spectrum."""
+    if not np.all(np.isfinite(Gs)):
+        return True
+    try:
+        L = np.linalg.cholesky(Gs)
+    except np.linalg.LinAlgError:
+        return True
+    return np.min(np.diag(L)) ** 2 <= rcond * max(np.max(np.diag(Gs)), jarq.FP32_EPS)
+
+
 def _factors_lower(H, g):
     return np.transpose(_ORIG["group_factors"](H, g), (0, 2, 1))
 
@@ -225,6 +237,7 @@ MUTATIONS = {
     "rhs_sign_flipped": ("gram_system", _gram_factory(rhs_sign=-1.0)),
     "ridge_always": ("solve_scales", _solve_factory(always_ridge=True)),
     "ridge_never": ("solve_scales", _solve_factory(never_ridge=True)),
+    "ridge_from_pivots": ("_needs_ridge", _needs_ridge_from_pivots),
     "factor_lower_not_upper": ("group_factors", _factors_lower),
     "objective_without_hessian": ("objective_rows", _objective_without_h),
     "dequantize_drops_zero_point": ("dequantize", _dequantize_no_zero),

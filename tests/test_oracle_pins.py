@@ -327,6 +327,35 @@ def test_ridge_branch_on_singular_gram():
     assert np.allclose(s[0], expect, rtol=1e-10)
 
 
+def kahan_gram(G):
+    """R^T R with R unit upper triangular, -1 above the diagonal.
+
+    Its Cholesky factor is R^T itself, so every pivot is exactly 1, while
+    sigma_min(R) falls like 2^-G: from G = 16 on its smallest eigenvalue is
+    below 1e-10 of its largest.  A trigger that looked only at the pivots
+    would never fire on it."""
+    R = np.eye(G) + np.triu(-np.ones((G, G)), 1)
+    return R.T @ R
+
+
+def test_ridge_trigger_is_the_spectrum_not_the_pivots():
+    """App. E.2 tests the smallest eigenvalue, not the factorisation's pivots."""
+    G = 20
+    Gt = kahan_gram(G)
+    assert np.array_equal(np.diag(np.linalg.cholesky(Gt)), np.ones(G))   # every pivot is 1
+    ev = np.linalg.eigvalsh(Gt)
+    assert ev[0] <= jarq.RIDGE_RCOND * ev[-1]
+    rhs = np.arange(1.0, G + 1.0)
+    s, ridge = jarq.solve_scales(Gt[None], rhs[None])
+    assert ridge[0]
+    expect = np.linalg.solve(Gt + jarq.RIDGE_LAMBDA * np.eye(G), rhs)
+    assert np.allclose(s[0], expect, rtol=1e-8)
+    # a well-conditioned neighbour is solved exactly
+    s2, ridge2 = jarq.solve_scales((Gt + np.eye(G))[None], rhs[None])
+    assert not ridge2[0]
+    assert np.allclose(s2[0], np.linalg.solve(Gt + np.eye(G), rhs), rtol=1e-10)
+
+
 def _ridge_worse_layer(h_scale=1e-8, seed=23):
     """A layer whose row 0 takes the ridge branch (one group at its zero point,
     so B_0 is rank deficient).  With H scaled by 1e-8, lambda = 1e-4 dominates

@@ -286,11 +286,14 @@ __global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
 
 // ---- incremental build: persistent work-groups over (x, tile, chunk) ----
 // Item (x, c, t): tile t (128 rows) of the list of group x, blocks b in chunk
-// c (kChunk consecutive blocks); block b forms entry (b, x) for b < x and
+// c (`chunk` consecutive blocks); block b forms entry (b, x) for b < x and
 // (x, b) for b >= x.  The codes of x stay staged while the chunk runs.  Items
 // are numbered with the tile fastest, and each round of the grid deals a
 // contiguous range of items to each XCD (work-groups go to the 8 XCDs in
-// turn), so the tiles that read the same H blocks share that XCD's L2.
+// turn), so the tiles that read the same H blocks share that XCD's L2.  The
+// chunk is 4 blocks, or 2 or 1 when the lists are so short that 4 would
+// leave work-groups idle: a work-group's blocks run one after another, each
+// behind its own H loads, so fewer per item shortens the launch.
 constexpr int kChunk = 4;
 
 template <int G_SIZE>
@@ -304,19 +307,19 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
   const int G = cols / S::g;
   const int n = n_dev != nullptr ? *n_dev : rows;
   if (!gram_use_lists(ctl, gpre, G, n)) return;  // uniform
-  const int nch = (G + kChunk - 1) / kChunk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
   const float hinv = *h_inv;
   extern __shared__ _Float16 sm[];
   _Float16* cx_s = sm;                        // RT x LDC: c of group x
   _Float16* cb_s = cx_s + RT * S::LDC;        // RT x LDC: c of block b
   double* red = (double*)(cb_s + RT * S::LDC);  // NAB x RT
-  // first_s[x]: first item of group x's list (exclusive scan of the item
-  // counts over the groups, Hillis-Steele over 128 + 1 entries)
+  // first_s[x]: first item of group x's list (an exclusive scan of the tile
+  // counts over the groups, Hillis-Steele over 128 + 1 entries, times the
+  // chunks per tile)
   __shared__ int first_s[kMaxGramGroups + 1];
   __shared__ int scan_s[kMaxGramGroups];
   if (tid < kMaxGramGroups)
-    scan_s[tid] = tid < G ? ((list_length(gpre, tid) + RT - 1) / RT) * nch : 0;
+    scan_s[tid] = tid < G ? (list_length(gpre, tid) + RT - 1) / RT : 0;
   __syncthreads();
   for (int w = 1; w < kMaxGramGroups; w <<= 1) {
     const int v = (tid < kMaxGramGroups && tid >= w) ? scan_s[tid - w] : 0;
@@ -324,7 +327,13 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
     if (tid < kMaxGramGroups) scan_s[tid] += v;
     __syncthreads();
   }
-  if (tid <= kMaxGramGroups) first_s[tid] = tid == 0 ? 0 : scan_s[tid - 1];
+  const int tiles_all = scan_s[kMaxGramGroups - 1];  // same in every work-group
+  const int grid = (int)gridDim.x;
+  const int chunk = tiles_all * ((G + kChunk - 1) / kChunk) >= grid ? kChunk
+                    : tiles_all * ((G + 1) / 2) >= grid          ? 2
+                                                                  : 1;
+  const int nch = (G + chunk - 1) / chunk;
+  if (tid <= kMaxGramGroups) first_s[tid] = tid == 0 ? 0 : scan_s[tid - 1] * nch;
   __syncthreads();
   const int items = first_s[G];
   const int trow = tid / S::TPR, tpart = tid % S::TPR;
@@ -364,8 +373,8 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
     it.lrow = list_row(x, it.r0 + (it.r0 + trow < len ? trow : 0));
     // the output row of thread tid < RT
     it.orow = list_row(x, it.r0 + (tid < RT && it.r0 + tid < len ? tid : 0));
-    it.b0 = c * kChunk;
-    it.b1 = min(it.b0 + kChunk, G);
+    it.b0 = c * chunk;
+    it.b1 = min(it.b0 + chunk, G);
     return it;
   };
   // position of this work-group in its round: XCD-major

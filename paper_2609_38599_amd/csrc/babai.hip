@@ -192,6 +192,10 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   constexpr int LDH = g + 4;
   constexpr int PG = panel_groups_of(g);
   constexpr int PW = PG * g;             // panel width
+  // dqp_s row stride: 16 bytes past the panel width, so that the 16 rows a
+  // fragment read serves start in 16 distinct 16-byte bank groups (a stride
+  // of PW halves would put all 16 in one)
+  constexpr int PWS = PW + 8;
   constexpr int RC_PER_THREAD = g * g / (256 * 4);  // f32x4 copies per prep thread to stage R~
   const int G = cols / g;
   const float qmax = (float)((1 << bits) - 1);
@@ -201,7 +205,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   __shared__ __attribute__((aligned(1024))) float rc0_s[g * g];
   __shared__ __attribute__((aligned(1024))) float rc1_s[g * g];
   __shared__ float u_s[RT * LDH];                    // u s of the current group
-  __shared__ __attribute__((aligned(16))) _Float16 dqp_s[RT * PW];  // accepted changes in the panel
+  __shared__ __attribute__((aligned(16))) _Float16 dqp_s[RT * PWS];  // accepted changes in the panel
   __shared__ int tacc_s[PG];                         // any row of the tile accepted group
   __shared__ int cnt_s[4];                           // accepted, changed, skipped, blocks
   __shared__ int racc_s[RT];                         // bit i - i0: the row accepted group i
@@ -310,7 +314,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     f16x8 a[KS];
 #pragma unroll
     for (int kc = 0; kc < KS; ++kc)
-      a[kc] = *(const f16x8*)(dqp_s + mr * PW + (h - i0) * g + kc * 32 + 8 * kq);
+      a[kc] = *(const f16x8*)(dqp_s + mr * PWS + (h - i0) * g + kc * 32 + 8 * kq);
 #pragma unroll
     for (int b = 0; b < BPW; ++b) {
       f32x4 seg = {0.f, 0.f, 0.f, 0.f};
@@ -407,7 +411,7 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         const int l = cj + 16 * t;
-        dqp_s[crow * PW + (i - i0) * g + l] = accept ? (_Float16)dd[t] : (_Float16)0.f;
+        dqp_s[crow * PWS + (i - i0) * g + l] = accept ? (_Float16)dd[t] : (_Float16)0.f;
       }
       if (cand_out != nullptr && row_in) {
         const size_t cbase = (size_t)crid * cols + (size_t)i * g;
@@ -568,8 +572,8 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
         uint8_t* codes_r = codes + lrow_r * cols;
         _Float16* cz_r = cz + lrow_r * cols;
         const uint32_t oq = (uint32_t)(i0 * g + k);
-        const f16x8 d0 = *(const f16x8*)(dqp_s + r * PW + k);
-        const f16x8 d1 = *(const f16x8*)(dqp_s + r * PW + k + 8);
+        const f16x8 d0 = *(const f16x8*)(dqp_s + r * PWS + k);
+        const f16x8 d1 = *(const f16x8*)(dqp_s + r * PWS + k + 8);
         bool any = false;
 #pragma unroll
         for (int b = 0; b < 8; ++b) any |= (d0[b] != (_Float16)0.f) | (d1[b] != (_Float16)0.f);

@@ -307,15 +307,19 @@ hipError_t launch_wm_product(hipStream_t st, int rows, int cols, const char* ws,
 // partial sums both fit next to the fragments at two waves per SIMD), K in
 // steps of 64 (32 when g = 32) straight from global memory into two LDS
 // stages by direct loads.  A stage row holds CPR 16-byte chunks; chunk c of
-// tile row r sits at position c ^ rswz(r), so the eight rows one read serves
-// per clock hit distinct banks.  Fragment reads run one k-slice ahead of the
-// products.  Rows of cz, the scales and T are the layer's rows (gathered
+// tile row r sits at position c ^ rswz(r).  A 16-byte read serves 16 lanes
+// (256 bytes, all 64 banks) per clock, and the lanes of a fragment read are
+// 16 consecutive rows at one chunk: with 128-byte rows, two rows share each
+// 256-byte bank line, so row r's position must differ from every other row
+// of the 16 with the same parity (rswz = (r / 2) mod 8); with 64-byte rows,
+// four rows share a line and ((r / 2) + (r / 8)) mod 4 separates the rows of
+// each residue mod 4.  Fragment reads run one k-slice ahead of the products.  Rows of cz, the scales and T are the layer's rows (gathered
 // through the row map); U is stored by position.
 namespace {
 constexpr int RBM = 256, RBN = 128;
 template <int CPR>
 __device__ __forceinline__ int rswz(int r) {
-  if constexpr (CPR == 8) return r & 7;
+  if constexpr (CPR == 8) return (r >> 1) & 7;
   return ((r >> 1) + (r >> 3)) & 3;
 }
 }  // namespace

@@ -28,9 +28,13 @@ constexpr int A_TILE = BM * BK, B_TILE = BN * BK;  // halves
 constexpr int STAGE = A_TILE + 2 * B_TILE;
 constexpr int DMA_PER_WAVE = STAGE / 512 / 4;     // 1 KB pieces per wave per stage
 
-// Chunk c (16 bytes) of row r of a staged tile sits at position c ^ swz(r):
-// fragment reads then touch distinct banks (see sgemm.hip).
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) + (r >> 3)) & 3; }
+// Chunk c (16 bytes) of row r of a staged tile sits at position c ^ swz(r).
+// A fragment read serves 16 consecutive rows at one chunk per clock, and the
+// 64-byte rows share 256-byte bank lines four at a time: rows r, r + 4,
+// r + 8, r + 12 need distinct positions.  (r >> 2) & 3 gives them (no
+// conflict cycles in the counters; ((r >> 1) + (r >> 3)) & 3 left every
+// fragment read 2-way conflicted.)
+__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
 __device__ __forceinline__ void dma16(const _Float16* src, _Float16* lds) {
   __builtin_amdgcn_global_load_lds((const void*)src,

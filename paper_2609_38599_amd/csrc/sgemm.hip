@@ -52,10 +52,11 @@ __device__ __forceinline__ bool tile_of(int wid, int nbm, int nbn, int& tm, int&
 }
 
 // LDS holds each plane tile as rows of 32 halves (four 16-byte chunks); chunk
-// c of row r sits at position c ^ swz(r).  Fragment reads (lane = row, two
-// chunks across the wave halves) then touch distinct banks within every group
-// of 8 or 16 consecutive lanes.
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) + (r >> 3)) & 3; }
+// c of row r sits at position c ^ swz(r).  A fragment read (lane = row, two
+// chunks across the wave halves) serves 16 consecutive rows per clock, and
+// the 64-byte rows share 256-byte bank lines four at a time: rows r, r + 4,
+// r + 8 and r + 12 take distinct positions.
+__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
 // One 16-byte direct global -> LDS load per lane (lane L writes lds + 16 L bytes).
 // A plain device function: the builtin and the LDS address space exist on the
@@ -312,15 +313,16 @@ hipError_t launch_wm_product(hipStream_t st, int rows, int cols, const char* ws,
 // 16 consecutive rows at one chunk: with 128-byte rows, two rows share each
 // 256-byte bank line, so row r's position must differ from every other row
 // of the 16 with the same parity (rswz = (r / 2) mod 8); with 64-byte rows,
-// four rows share a line and ((r / 2) + (r / 8)) mod 4 separates the rows of
-// each residue mod 4.  Fragment reads run one k-slice ahead of the products.  Rows of cz, the scales and T are the layer's rows (gathered
-// through the row map); U is stored by position.
+// four rows share a line and (r / 4) mod 4 separates the rows of each
+// residue mod 4.  Fragment reads run one k-slice ahead of the products.  Rows
+// of cz, the scales and T are the layer's rows (gathered through the row
+// map); U is stored by position.
 namespace {
 constexpr int RBM = 256, RBN = 128;
 template <int CPR>
 __device__ __forceinline__ int rswz(int r) {
   if constexpr (CPR == 8) return (r >> 1) & 7;
-  return ((r >> 1) + (r >> 3)) & 3;
+  return (r >> 2) & 3;
 }
 }  // namespace
 

@@ -1,5 +1,7 @@
-// Residual product of the sweep: C = A H on fp32 matrix cores (paper Sec. 3.3.2,
-// the conditional residual of eq. (7) needs H (w - what) for every row).
+// C = A H on fp32 matrix cores, for the per-layer W H of the scale
+// right-hand sides (prepare) and for the stand-alone objective (jarq_objective,
+// from H (w - what) of every row; paper Sec. 3.3.2 and eq. (7)); the sweep's
+// own residual product runs on fp16 matrix cores (sgemm.hip).
 //
 // A = W (per-layer WH for the scale right-hand sides) or A = E = W - What with
 // What = s_i (q - z_i) formed on the fly from the codes, scales and zero points

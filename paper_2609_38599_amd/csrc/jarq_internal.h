@@ -249,9 +249,10 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // Early stopping shrinks the set of rows a sweep works on.  Per-sweep
-// intermediates (Gram matrices, E planes, U, objective partials, dq, the
-// panel row lists) are indexed by position p < n in the sweep's row list; the
-// layer's state (W, codes, scales, zeros, W H, stopping state) by row.  The
+// intermediates (U, objective partials, dq, the panel row lists) are indexed
+// by position p < n in the sweep's row list; the layer's state (W, codes,
+// q - z, scales, zeros, W H, the cached scale right-hand sides, the Gram
+// matrices, which persist across sweeps, and the stopping state) by row.  The
 // list is null while every row takes part (position = row).
 __device__ __forceinline__ int map_row(const int32_t* rowmap, int p) {
   return rowmap != nullptr ? rowmap[p] : p;

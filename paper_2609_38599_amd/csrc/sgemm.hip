@@ -1,15 +1,18 @@
-// Split-precision products on fp16 matrix cores: the residual product of the
-// sweep (paper Sec. 3.3.2: the conditional residual of eq. (7) needs (H e)_i
-// for every row and group, used in the coordinates of eq. (10)).
+// Split-precision products on fp16 matrix cores for the residual product of
+// the sweep (paper Sec. 3.3.2: the conditional residual of eq. (7) needs
+// (H e)_i for every row and group, used in the coordinates of eq. (10)).
+// split3_kernel (three products of two-term planes of both operands) forms
+// the layer's fixed T = W M^T once per layer; resid_kernel (further below)
+// forms every sweep's U = T - What M^T with the exact q - z as one operand.
 //
 // Operands arrive as two-term fp16 planes with power-of-two scales (split.hip):
 // A = (Ah + Al) ra_m per row m, B(k, n) = Bt(n, k) with Bt = (Bh + Bl) rb_n per
 // row n.  The product keeps the three terms above 2^-22 relative,
 // A B = (Ah Bh + Ah Bl + Al Bh) ra_m rb_n, accumulated in fp32 by
 // v_mfma_f32_32x32x16_f16 — fp32-class accuracy at 3/16 of the fp32 matrix
-// work.  For the sweep Bt = M = blockdiag(L_i^{-1}) H, so the product is
-// U = E M^T: group i's columns of row j hold L_i^{-1} (H e_j)_i, the u of
-// eq. (10) before division by the scale.
+// work.  With Bt = M = blockdiag(L_i^{-1}) H the product E M^T has in group
+// i's columns of row j L_i^{-1} (H e_j)_i, the u of eq. (10) before division
+// by the scale.
 //
 // Epilogues: store C = A B, or subtract, C -= A B.  The objective that
 // follows the residual product is in objective.hip.

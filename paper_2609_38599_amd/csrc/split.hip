@@ -7,7 +7,7 @@
 //   H:  one scale for the whole matrix, chosen so max |H| 2^t lies in [2^13, 2^14).
 //   M = blockdiag(L_i^{-1}) H (the code update's coordinates, eq. (10)): one
 //       scale per row of M, same rule.
-//   E = W - What (eq. (1)), per sweep: one scale per row, same rule.
+//   W: one scale per row, same rule (for the layer's fixed W M^T and W_i L_i).
 // Small-integer operands (codes minus zero points, code changes) are exact in fp16.
 #include "jarq_internal.h"
 

@@ -255,32 +255,41 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
 
   // Accumulator element v of lane l in a 32x32 block:
   // (row 8 * (v / 4) + 4 * (l / 32) + v % 4, column l % 32).
-  // All loads of P are issued before any store (the compiler cannot prove the
-  // addresses distinct and would otherwise serialise the round trips), and
-  // they are unconditional, from a clamped address (a load under a branch is
-  // waited for inside the branch).
-  float pold[2][2][16];
+  // Per 32-row block a: all loads of P (unconditional, from a clamped
+  // address) are issued first and every loaded value is taken into its
+  // register (the empty asm statements) before the first store.  With loads
+  // still in flight at a store under a branch, the compiler waited for every
+  // outstanding memory operation, the stores before it included, at each
+  // store (one write round trip after another); holding all 64 values at
+  // once spills registers.
+  float csv[2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int b = 0; b < 2; ++b) csv[b] = bcol_inv[min(n0 + wn * 64 + b * 32 + lm, cols - 1)];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    float pold[2][16];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int col = min(n0 + wn * 64 + b * 32 + lm, cols - 1);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) pold[a][b][v] = P[(size_t)erow[a][v] * cols + col];
+      for (int v = 0; v < 16; ++v) pold[b][v] = P[(size_t)erow[a][v] * cols + col];
     }
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) asm volatile("" : "+v"(pold[b][v]));
+    if (a == 0) asm volatile("" : "+v"(csv[0]), "+v"(csv[1]));
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int col = n0 + wn * 64 + b * 32 + lm;
-      const float cs = bcol_inv[min(col, cols - 1)];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int t = wm * 64 + a * 32 + 8 * (v / 4) + 4 * kh + (v % 4);
         if (t < nvalid && col < cols)
-          P[(size_t)erow[a][v] * cols + col] = pold[a][b][v] - acc[a][b][v] * cs;
+          P[(size_t)erow[a][v] * cols + col] = pold[b][v] - acc[a][b][v] * csv[b];
       }
     }
+  }
 }
 
 int panel_groups(int g) { return panel_groups_of(g); }

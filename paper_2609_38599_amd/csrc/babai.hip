@@ -44,6 +44,7 @@
 namespace jarq {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Load / store at base + byte offset.  With a wave-uniform base and a 32-bit
 // offset the access takes the scalar-base form (SGPR pair + one offset VGPR):
@@ -356,14 +357,53 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     }
     ns = scales_c[i];
   };
+  // ---- epilogue items: 16 columns of one row of the panel, item c = row
+  // c / per_row, columns 16 (c % per_row) onwards.  The preparation threads
+  // take them all (items ptid and ptid + 256; a panel is at most 512 columns
+  // wide) and load the old codes, cz and scale-system right-hand sides during
+  // the panel's last back substitution, which they do not take part in.
+  const int per_row = (i1 - i0) * g / 16;
+  const int n_items = RT * per_row;
+  static_assert(RT * (PG * g / 16) <= 512, "two epilogue items per preparation thread");
+  u32x4 e_qw[2];
+  f16x8 e_c0[2], e_c1[2];
+  double e_rhs[2];
+  int e_lrow[2];  // layer rows of the two items (both row-map loads go out first)
+  auto epi_load = [&]() {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int r = (ptid + 256 * u) / per_row;
+      e_lrow[u] = map_row(rowmap, r0 + r < rows ? r0 + r : r0);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = ptid + 256 * u;
+      const int r = c / per_row;
+      const int k = (c - r * per_row) * 16;
+      if (c < n_items && r0 + r < rows) {
+        const size_t lrow_r = (size_t)e_lrow[u];
+        const uint32_t oq = (uint32_t)(i0 * g + k);
+        e_qw[u] = ld_at((const u32x4*)(codes + lrow_r * cols), oq);
+        e_c0[u] = ld_at((const f16x8*)(cz + lrow_r * cols), 2 * oq);
+        e_c1[u] = ld_at((const f16x8*)(cz + lrow_r * cols), 2 * oq + 16);
+        if (k % g == 0) e_rhs[u] = rhs[lrow_r * G + (size_t)(i0 + k / g)];
+      }
+    }
+  };
+
   // The two roles run separate loops with the same barriers (two per group),
   // so neither role's loop-carried registers are live in the other's code.
   // Barriers inside the loops are on LDS only: global loads stay in flight
   // across them.
   if (chain_wave) {
     chain_prefetch(i0);
+    // The loads of group i0's codes, scale and diagonal factors go out before
+    // the barrier and stay in flight behind the preparation role's staging
+    // (the pointers handed to the empty statement keep the compiler from
+    // sinking them below it).
+    asm volatile("" ::"v"(codes_c), "v"(scales_c), "s"(rdinv), "s"(rdsq) : "memory");
     int acc_bits = 0;  // bit i - i0: this row accepted group i
-    __syncthreads();       // u and R~ of group i0 staged
+    lds_barrier();  // u and R~ of group i0 staged
     for (int i = i0; i < i1; ++i) {
       // ---- back substitution of group i, 16 lanes per row ----
       const bool has_next = i + 1 < i1;
@@ -448,9 +488,13 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     if (prep_live) {
       u_from_p(i0, ua1);
       write_u(ua1);
-      if (i0 + 1 < i1) u_from_p(i0 + 1, ua0);
     }
-    __syncthreads();  // u and R~ of group i0 staged
+    // R~ of group i0 (direct loads) has landed once this wave's vector memory
+    // counter is zero; u of group i0 + 1 then stays in flight across the
+    // barrier.
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
+    if (prep_live && i0 + 1 < i1) u_from_p(i0 + 1, ua0);
+    lds_barrier();  // u and R~ of group i0 staged
     auto prep_at = [&](auto pc) {
       constexpr int p = decltype(pc)::value;
       const int i = i0 + p;
@@ -503,7 +547,14 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
     Unroll<0, PG - 1>::run([&](auto pc) {
       if (i0 + decltype(pc)::value + 1 < i1) prep_at(pc);
     });
-    // last group of the panel: nothing to prepare
+    // last group of the panel: nothing to prepare; the epilogue's loads go out
+    epi_load();
+    // Taken into registers here, where these waves only wait for the back
+    // substitution (the compiler would otherwise wait for them in the
+    // epilogue, behind its stores).
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      asm volatile("" : "+v"(e_qw[u]), "+v"(e_c0[u]), "+v"(e_c1[u]), "+v"(e_rhs[u]), "+v"(e_lrow[u]));
     if (i1 > i0) {
       lds_barrier();
       lds_barrier();
@@ -556,64 +607,83 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   }
 
   // ---- codes += accepted changes, cz (q - z as fp16) likewise, and dq =
-  // accepted changes, over the panel's columns: 16 columns per thread and step
-  // (16-byte code, 2 x 16-byte cz and dq accesses).  The scale systems'
-  // right-hand sides follow the codes: r_i += d_i^T (W H)_i, summed in fp64
-  // over the g / 16 consecutive threads of a group.  dqp_s is complete since
-  // the last barrier.
-  {
-    const int per_row = (i1 - i0) * g / 16;
-    for (int c = tid; c < RT * per_row; c += 512) {
+  // accepted changes, over the panel's columns: 16 columns per item (16-byte
+  // code, 2 x 16-byte cz and dq accesses), by the preparation threads.  The
+  // scale systems' right-hand sides follow the codes: r_i += d_i^T (W H)_i,
+  // summed in fp64 over the g / 16 consecutive threads of a group.  dqp_s is
+  // complete since the last barrier.
+  if (!chain_wave) {
+    // the changes of both items and, where a code changes, their (W H) first:
+    // no load waits behind a store
+    f16x8 d0[2], d1[2];
+    bool any[2];
+    f32x4 w4[2][4];  // (W H) of the 16 columns, only where a code changes
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = ptid + 256 * u;
       const int r = c / per_row;
       const int k = (c - r * per_row) * 16;
-      if (r0 + r < rows) {
+      const bool live = c < n_items && r0 + r < rows;
+      const int rr = live ? r : 0;
+      const int kk = live ? k : 0;
+      d0[u] = *(const f16x8*)(dqp_s + rr * PWS + kk);
+      d1[u] = *(const f16x8*)(dqp_s + rr * PWS + kk + 8);
+      any[u] = false;
+#pragma unroll
+      for (int b = 0; b < 8; ++b)
+        any[u] |= (d0[u][b] != (_Float16)0.f) | (d1[u][b] != (_Float16)0.f);
+      any[u] = any[u] && live;
+      if (any[u]) {
+        const float* whp = wh + (size_t)e_lrow[u] * cols + (uint32_t)(i0 * g + k);
+#pragma unroll
+        for (int b4 = 0; b4 < 4; ++b4) w4[u][b4] = *(const f32x4*)(whp + 4 * b4);
+      }
+    }
+    // then the right-hand side increments d^T (W H) (summed over the g / 16
+    // threads of a group), then every store
+    double part[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      part[u] = 0.0;
+      if (any[u]) {
+#pragma unroll
+        for (int b4 = 0; b4 < 4; ++b4)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int b = 4 * b4 + e;
+            part[u] = fma((double)(b < 8 ? d0[u][b] : d1[u][b - 8]), (double)w4[u][b4][e], part[u]);
+          }
+      }
+      if (__ballot(any[u]) != 0) {  // waves without a change skip the reduction
+#pragma unroll
+        for (int off = 1; off < g / 16; off <<= 1) part[u] += __shfl_xor(part[u], off);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = ptid + 256 * u;
+      const int r = c / per_row;
+      const int k = (c - r * per_row) * 16;
+      if (c < n_items && r0 + r < rows) {
         const uint32_t o = (uint32_t)r * ucols + (uint32_t)(i0 * g + k);
-        const size_t lrow_r = (size_t)map_row(rowmap, r0 + r);
+        const size_t lrow_r = (size_t)e_lrow[u];
         uint8_t* codes_r = codes + lrow_r * cols;
         _Float16* cz_r = cz + lrow_r * cols;
         const uint32_t oq = (uint32_t)(i0 * g + k);
-        const f16x8 d0 = *(const f16x8*)(dqp_s + r * PWS + k);
-        const f16x8 d1 = *(const f16x8*)(dqp_s + r * PWS + k + 8);
-        bool any = false;
-#pragma unroll
-        for (int b = 0; b < 8; ++b) any |= (d0[b] != (_Float16)0.f) | (d1[b] != (_Float16)0.f);
-        const uint4 qw = ld_at((const uint4*)codes_r, oq);
-        const f16x8 c0 = ld_at((const f16x8*)cz_r, 2 * oq);
-        const f16x8 c1 = ld_at((const f16x8*)cz_r, 2 * oq + 16);
-        f32x4 w4[4];  // (W H) of the 16 columns, only where a code changes
-        if (any) {
-          const float* whp = wh + lrow_r * cols + oq;
-#pragma unroll
-          for (int b4 = 0; b4 < 4; ++b4) w4[b4] = *(const f32x4*)(whp + 4 * b4);
-        }
-        uint32_t w[4] = {qw.x, qw.y, qw.z, qw.w};
+        uint32_t w[4] = {e_qw[u][0], e_qw[u][1], e_qw[u][2], e_qw[u][3]};
         // Byte b of word b / 4 gains d_b; new codes stay in [0, 2^bits - 1],
         // so the word-wide add never carries into a neighbouring byte.
 #pragma unroll
         for (int b = 0; b < 16; ++b) {
-          const int dv = (int)(b < 8 ? d0[b] : d1[b - 8]);
+          const int dv = (int)(b < 8 ? d0[u][b] : d1[u][b - 8]);
           w[b >> 2] += (uint32_t)dv << (8 * (b & 3));
         }
         st_at((uint4*)codes_r, oq, make_uint4(w[0], w[1], w[2], w[3]));
-        st_at((f16x8*)cz_r, 2 * oq, c0 + d0);  // small integers: exact
-        st_at((f16x8*)cz_r, 2 * oq + 16, c1 + d1);
-        st_at((f16x8*)dq_t, 2 * o, d0);
-        st_at((f16x8*)dq_t, 2 * o + 16, d1);
-        double part = 0.0;
-        if (any) {
-#pragma unroll
-          for (int b4 = 0; b4 < 4; ++b4)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int b = 4 * b4 + e;
-              part = fma((double)(b < 8 ? d0[b] : d1[b - 8]), (double)w4[b4][e], part);
-            }
-        }
-        if (__ballot(any) != 0) {  // waves without a change skip the reduction
-#pragma unroll
-          for (int off = 1; off < g / 16; off <<= 1) part += __shfl_xor(part, off);
-          if (k % g == 0 && part != 0.0) rhs[lrow_r * G + (size_t)(i0 + k / g)] += part;
-        }
+        st_at((f16x8*)cz_r, 2 * oq, e_c0[u] + d0[u]);  // small integers: exact
+        st_at((f16x8*)cz_r, 2 * oq + 16, e_c1[u] + d1[u]);
+        st_at((f16x8*)dq_t, 2 * o, d0[u]);
+        st_at((f16x8*)dq_t, 2 * o + 16, d1[u]);
+        if (k % g == 0 && part[u] != 0.0) rhs[lrow_r * G + (size_t)(i0 + k / g)] = e_rhs[u] + part[u];
       }
     }
   }

@@ -159,8 +159,10 @@ jarq_status jarq_code_step(const jarq_params* p, const float* W, const float* H,
  * groups whose codes the previous sweep changed when that is cheaper (entry
  * (a, h) depends on the codes of groups a and h alone, eq. (5)); the entries
  * are bit-identical to a full build.  With early stopping the set of active
- * rows stays on the device; the host looks at it every fourth sweep and stops
- * launching once no row is left.
+ * rows stays on the device; every fourth sweep its size is copied behind that
+ * sweep into pinned host memory (allocated and freed by the call), and the
+ * host stops launching once a copy that has landed shows no row left (the
+ * stream is never drained for it).
  */
 jarq_status jarq_sweeps(const jarq_params* p, const float* W, const float* H,
                         uint8_t* codes, float* scales, const int32_t* zeros,
@@ -192,7 +194,9 @@ jarq_status jarq_refine(const jarq_params* p, const float* W, const float* H,
  * library holds in a static device array of JARQ_STATIC_WORKSPACE_BYTES
  * (512 MiB; enough for a 4096 x 4096 layer at g = 128), created on each GPU
  * the library runs on and held until the process ends.  The call allocates
- * nothing: no hipMalloc, no hipFree, no HIP event.  Layers whose
+ * nothing: no hipMalloc, no hipFree, no HIP event, no pinned host memory (with
+ * early stopping its fourth-sweep look at the active count is a blocking
+ * copy instead).  Layers whose
  * jarq_workspace_bytes exceeds the limit are rejected with
  * JARQ_ESTATIC_LIMIT before anything is enqueued.  Results are those of
  * jarq_refine on the same inputs; stats (nullable) is filled the same way

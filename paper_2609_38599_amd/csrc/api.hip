@@ -234,9 +234,11 @@ constexpr int kBoundaries = 5;
 constexpr int kFirstLaunchStage = kBoundaries - 1;
 
 // time_stages = false: no HIP events are created and stage_ms stays 0.
+// host_alloc = false: nothing is allocated (the early-stopping check then
+// reads the active count with a blocking copy).
 jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, uint8_t* codes,
                         float* scales, const int32_t* zeros, void* ws, void* stream,
-                        jarq_stats* stats, bool time_stages = true) {
+                        jarq_stats* stats, bool time_stages = true, bool host_alloc = true) {
   (void)H;
   Ctx c = make_ctx(p, ws, stream);
   // Device-side input checks (codes in range, |zero point| <= 1024).
@@ -296,6 +298,22 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
     if (tmask == 0u || k >= nrec || !boundary_used(j)) return hipSuccess;
     return hipEventRecord(ev[(size_t)k * per_sweep + j], c.st);
   };
+  // Early stopping: every fourth sweep the active count is copied behind that
+  // sweep into pinned host memory; the host looks at it once the copy has
+  // landed (an event query, no wait) and ends the run when no row is left.
+  // The stream never drains for it; without pinned memory the copy blocks.
+  SweepCtl* host_sc = nullptr;
+  hipEvent_t sc_ev = nullptr;
+  bool sc_pending = false;
+  if (stopping && host_alloc) {
+    if (hipHostMalloc((void**)&host_sc, sizeof(SweepCtl), hipHostMallocDefault) != hipSuccess)
+      host_sc = nullptr;
+    else if (hipEventCreateWithFlags(&sc_ev, hipEventDisableTiming) != hipSuccess) {
+      (void)hipHostFree(host_sc);
+      host_sc = nullptr;
+      sc_ev = nullptr;
+    }
+  }
   jarq_status status = JARQ_OK;
   for (int k = 0; k < K; ++k) {
     // launches of the code update timed with a pair of events each
@@ -345,19 +363,42 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
       break;
     }
     if (stopping && (k + 1) % 4 == 0 && k + 1 < K) {
-      // Every fourth sweep the host looks whether any row is left (the
-      // sweeps in between run without waiting; one with no row left costs
-      // its launches only).
-      SweepCtl sc{};
-      if (hipMemcpyAsync(&sc, c.sctl(), sizeof(sc), hipMemcpyDeviceToHost, c.st) != hipSuccess ||
-          hipStreamSynchronize(c.st) != hipSuccess) {
-        status = JARQ_EHIP;
-        break;
+      // Every fourth sweep the host looks whether any row is left (a sweep
+      // with no row left costs its launches only).
+      if (host_sc != nullptr) {
+        if (sc_pending) {
+          const hipError_t q = hipEventQuery(sc_ev);
+          if (q == hipSuccess) {
+            sc_pending = false;
+            if (host_sc->n == 0) break;
+          } else if (q != hipErrorNotReady) {
+            status = JARQ_EHIP;
+            break;
+          }
+        }
+        if (!sc_pending) {
+          if (hipMemcpyAsync(host_sc, c.sctl(), sizeof(SweepCtl), hipMemcpyDeviceToHost, c.st) !=
+                  hipSuccess ||
+              hipEventRecord(sc_ev, c.st) != hipSuccess) {
+            status = JARQ_EHIP;
+            break;
+          }
+          sc_pending = true;
+        }
+      } else {
+        SweepCtl sc{};
+        if (hipMemcpyAsync(&sc, c.sctl(), sizeof(sc), hipMemcpyDeviceToHost, c.st) != hipSuccess ||
+            hipStreamSynchronize(c.st) != hipSuccess) {
+          status = JARQ_EHIP;
+          break;
+        }
+        if (sc.n == 0) break;
       }
-      if (sc.n == 0) break;
     }
   }
   if (hipStreamSynchronize(c.st) != hipSuccess) status = JARQ_EHIP;
+  if (sc_ev != nullptr) (void)hipEventDestroy(sc_ev);
+  if (host_sc != nullptr) (void)hipHostFree(host_sc);
   SweepCtl sc{};
   if (status == JARQ_OK) {
     if (hipMemcpy(&f, c.flags(), sizeof(Flags), hipMemcpyDeviceToHost) != hipSuccess ||
@@ -561,7 +602,8 @@ jarq_status jarq_refine_static(const jarq_params* p, const float* W, const float
   if (s != JARQ_OK) return s;
   s = prepare_impl(p, W, H, ws, stream);
   if (s != JARQ_OK) return s;
-  return sweeps_impl(p, W, H, codes, scales, zeros, ws, stream, stats, /*time_stages=*/false);
+  return sweeps_impl(p, W, H, codes, scales, zeros, ws, stream, stats, /*time_stages=*/false,
+                     /*host_alloc=*/false);
 }
 
 jarq_status jarq_objective(const jarq_params* p, const float* W, const float* H,

@@ -290,10 +290,12 @@ __global__ __launch_bounds__(256, 2) void gram_kernel(int rows, int cols,
 // (x, b) for b >= x.  The codes of x stay staged while the chunk runs.  Items
 // are numbered with the tile fastest, and each round of the grid deals a
 // contiguous range of items to each XCD (work-groups go to the 8 XCDs in
-// turn), so the tiles that read the same H blocks share that XCD's L2.  The
-// chunk is 4 blocks, or 2 or 1 when the lists are so short that 4 would
-// leave work-groups idle: a work-group's blocks run one after another, each
-// behind its own H loads, so fewer per item shortens the launch.
+// turn), so the tiles that read the same H blocks share that XCD's L2.  A
+// work-group's blocks run one after another, each behind its own H loads, so
+// the launch lasts as long as the busiest work-group's blocks: the chunk (4,
+// 2 or 1 blocks) is the one that gives the fewest blocks to the busiest
+// work-group, rounds x chunk with rounds = ceil(items / grid), the larger
+// chunk on a tie (fewer stagings of the codes of x).
 constexpr int kChunk = 4;
 
 template <int G_SIZE>
@@ -329,9 +331,17 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
   }
   const int tiles_all = scan_s[kMaxGramGroups - 1];  // same in every work-group
   const int grid = (int)gridDim.x;
-  const int chunk = tiles_all * ((G + kChunk - 1) / kChunk) >= grid ? kChunk
-                    : tiles_all * ((G + 1) / 2) >= grid          ? 2
-                                                                  : 1;
+  int chunk = kChunk;
+  {
+    int best = ((tiles_all * ((G + kChunk - 1) / kChunk) + grid - 1) / grid) * kChunk;
+    for (int c = kChunk / 2; c >= 1; c /= 2) {
+      const int busiest = ((tiles_all * ((G + c - 1) / c) + grid - 1) / grid) * c;
+      if (busiest < best) {
+        best = busiest;
+        chunk = c;
+      }
+    }
+  }
   const int nch = (G + chunk - 1) / chunk;
   if (tid <= kMaxGramGroups) first_s[tid] = tid == 0 ? 0 : scan_s[tid - 1] * nch;
   __syncthreads();
@@ -377,9 +387,21 @@ __global__ __launch_bounds__(256, 2) void gram_listed_kernel(
     it.b1 = min(it.b0 + chunk, G);
     return it;
   };
-  // position of this work-group in its round: XCD-major
+  // Position of this work-group in its round.  Work-groups go to the 8 XCDs
+  // in turn, two per CU: the first half of the positions takes the first
+  // per_xcd / 2 work-groups of every XCD (one per CU), XCD-major, the second
+  // half the others, so a short last round spreads over every XCD, one
+  // work-group per CU, while runs of consecutive items (tiles that read the
+  // same H blocks) still share an XCD's L2.
   const int per_xcd = gridDim.x / 8;
-  const int slot = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+  const int wg = (int)blockIdx.x, local = wg / 8;
+  int slot;
+  if (per_xcd % 2 == 0) {
+    const int half = per_xcd / 2;
+    slot = (local / half) * (int)(gridDim.x / 2) + (wg % 8) * half + local % half;
+  } else {
+    slot = (wg % 8) * per_xcd + local;
+  }
   int item = slot;
   if (item >= items) return;  // uniform
   Item it = locate(item);

@@ -132,9 +132,9 @@ __device__ __forceinline__ RCol<NT> load_rcol(const float* __restrict__ rc, int 
   constexpr int W = RCol<NT>::W;
   RCol<NT> r;
   if constexpr (L >= 0) {
+    constexpr int base = RcolLayout<16 * NT>::offset(L);
 #pragma unroll
-    for (int t = 0; t <= (L >> 4); ++t)
-      r.v[t] = rc[((L * (NT / W) + t / W) * 16 + cj) * W + t % W];
+    for (int t = 0; t <= (L >> 4); ++t) r.v[t] = rc[base + ((t / W) * 16 + cj) * W + t % W];
   }
   return r;
 }
@@ -197,14 +197,16 @@ __global__ __launch_bounds__(512, 1) void babai_kernel(
   // fragment read serves start in 16 distinct 16-byte bank groups (a stride
   // of PW halves would put all 16 in one)
   constexpr int PWS = PW + 8;
-  constexpr int RC_PER_THREAD = g * g / (256 * 4);  // f32x4 copies per prep thread to stage R~
+  constexpr int RC_FLOATS = RcolLayout<g>::total;  // the staged part of a group's R~
+  static_assert(RC_FLOATS % 1024 == 0, "R~ staged in 1 KB pieces, four per preparation lane set");
+  constexpr int RC_PER_THREAD = RC_FLOATS / (256 * 4);  // f32x4 copies per prep thread to stage R~
   const int G = cols / g;
   const float qmax = (float)((1 << bits) - 1);
 
   // R~ columns [l][j][t] of two groups in two distinct arrays (written by
   // direct global -> LDS loads while the other one is read).
-  __shared__ __attribute__((aligned(1024))) float rc0_s[g * g];
-  __shared__ __attribute__((aligned(1024))) float rc1_s[g * g];
+  __shared__ __attribute__((aligned(1024))) float rc0_s[RC_FLOATS];
+  __shared__ __attribute__((aligned(1024))) float rc1_s[RC_FLOATS];
   __shared__ float u_s[RT * LDH];                    // u s of the current group
   __shared__ __attribute__((aligned(16))) _Float16 dqp_s[RT * PWS];  // accepted changes in the panel
   __shared__ int tacc_s[PG];                         // any row of the tile accepted group

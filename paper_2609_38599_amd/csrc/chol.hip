@@ -8,12 +8,13 @@
 // column by column, and writes the fp32 forms the sweep kernels read (and
 // keeps L_i^{-1} in fp64 in place of L_i):
 //   rinv  row n = row n of L_i^{-1}       (u = R_i^{-T} he = L_i^{-1} he)
-//   rcol  [l][c][j][w] = R_i(m, l) / R_i(m, m) for m < l, 0 for m >= l, with
-//         m = j + 16 (W c + w), W = min(4, g / 16) (column l of R_i above
-//         the diagonal with each row scaled by its inverse diagonal, cut into
-//         chunks of W positions per lane and laid out lane-contiguous, as the
-//         16 lanes of a row own positions j + 16 t and read one chunk each
-//         with one W-float access)
+//   rcol  column l, chunk c, lane j, w: R_i(m, l) / R_i(m, m) for m < l, 0
+//         for m >= l, with m = j + 16 (W c + w), W = min(4, g / 16) (column l
+//         of R_i above the diagonal with each row scaled by its inverse
+//         diagonal, cut into chunks of W positions per lane and laid out
+//         lane-contiguous, as the 16 lanes of a row own positions j + 16 t
+//         and read one chunk each with one W-float access); only the chunks
+//         a back-substitution step reads are kept (RcolLayout)
 //   rdinv 1 / R_i(l, l),  rdsq R_i(l, l)^2,  rmat R_i (row-major).
 #include "jarq_internal.h"
 
@@ -89,15 +90,20 @@ __global__ __launch_bounds__(256) void chol_groups_kernel(const float* __restric
   for (int e = tid; e < g * g; e += blockDim.x) {
     const int r = e / g, c = e % g;
     rinv_b[e] = (float)A[r * LD + c];
-    // rcol[l][c][j][w], e = ((l NC + c) 16 + j) W + w: R(m, l) / R(m, m),
-    // m = j + 16 (W c + w), R = L^T
-    constexpr int W = NT < 4 ? NT : 4;
+    // column l, chunk c, lane j, w for e = ((l NC + c) 16 + j) W + w:
+    // R(m, l) / R(m, m), m = j + 16 (W c + w), R = L^T; kept where the back
+    // substitution reads it (c < RcolLayout<g>::chunks(l))
+    using RL = RcolLayout<g>;
+    constexpr int W = RL::W;
     const int l = e / (16 * NT);
     const int rem = e % (16 * NT);
     const int j = (rem / W) % 16;
-    const int t = (rem / (16 * W)) * W + rem % W;
+    const int cc = rem / (16 * W);
+    const int t = cc * W + rem % W;
     const int m = j + 16 * t;
-    rcol_b[e] = (float)(m < l ? Lb[l * g + m] / Lb[m * g + m] : 0.0);
+    if (cc < RL::chunks(l))
+      rcol_b[RL::offset(l) + (cc * 16 + j) * W + rem % W] =
+          (float)(m < l ? Lb[l * g + m] / Lb[m * g + m] : 0.0);
   }
   // R_i = L_i^T in fp32, row m: rmat[m][n] = L_i(n, m) (zero below the diagonal).
   float* rmat_b = rmat + (size_t)blk * g * g;

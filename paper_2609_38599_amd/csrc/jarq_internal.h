@@ -264,6 +264,26 @@ hipError_t launch_compact_rows(hipStream_t st, int rows, const uint8_t* active, 
                                SweepCtl* sctl);
 
 // Groups per panel of the code update (512 columns, at most 16 groups).
+// R~ columns of a group for the back substitution (written by chol.hip, read
+// by babai.hip).  The 16 lanes of a row own positions j + 16 t, t < NT = g /
+// 16, and read a column in chunks of W = min(4, NT) positions per lane, one
+// W-float access each (chunk c: t = W c .. W c + W - 1, lane-contiguous, 16 W
+// floats).  Step l reads only t <= l / 16, so column l keeps its first
+// (l / 16) / W + 1 chunks; columns follow one another.  With B = 16 W, column
+// l in band b = l / B has b + 1 chunks and starts at
+// 16 W (B b (b - 1) / 2 + b (l - B b) + l) floats.
+template <int g>
+struct RcolLayout {
+  static constexpr int NT = g / 16;
+  static constexpr int W = NT < 4 ? NT : 4;
+  static constexpr int B = 16 * W;
+  __host__ __device__ static constexpr int chunks(int l) { return l / B + 1; }
+  __host__ __device__ static constexpr int offset(int l) {
+    return 16 * W * (B * (l / B) * (l / B - 1) / 2 + (l / B) * (l - B * (l / B)) + l);
+  }
+  static constexpr int total = 16 * W * (B * (g / B) * (g / B - 1) / 2 + g);
+};
+
 constexpr int kMaxPanelGroups = 16;
 constexpr int panel_groups_of(int g) { return 512 / g < kMaxPanelGroups ? 512 / g : kMaxPanelGroups; }
 int panel_groups(int g);

@@ -128,10 +128,6 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   // and are never stored.
   auto row_of = [&](int t) { return rl_s[t < nvalid ? t : 0]; };
 
-  for (int e = tid; e < BM * ng; e += 256) {
-    const int r = e / ng, h = e % ng;
-    sc_s[h][r] = scales[(size_t)map_row(rowmap, row_of(r)) * G + h0 + h];  // list holds positions
-  }
   // Rows of this lane's accumulator elements (element v of a 32x32 block is
   // row 8 (v / 4) + 4 (lane / 32) + v % 4), kept for the epilogue.
   int erow[2][16];
@@ -236,9 +232,42 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   // then all waves meet, which also frees the stage read at step k - 1 for the
   // loads of step k + 2.
   const int nk = (c1 - c0) / BK;  // >= 1
-  issue(c0, buf0);
-  if (nk > 1) issue(c0 + BK, buf1);
-  __syncthreads();  // sc_s
+  // The tile rows' scales of the panel's groups into sc_s (the list holds
+  // positions; scales are by layer row).  The row-map loads go out before the
+  // first two stages' direct loads and the scale loads right after them, so
+  // waiting for a scale never waits for a stage that was issued later, and the
+  // stages land while the scales are fetched.  Thread e of the BM x ng
+  // entries takes e, e + 256, ... (past the end: the last entry again, loaded
+  // and not stored).
+  constexpr int SCV = kMaxPanelGroups * BM / 256;
+  // one straight-line copy per form of the row map, so that the compiler's
+  // waits count exactly the loads each copy issues
+  auto stage_first = [&](auto&& layer_row) __attribute__((always_inline)) {
+    int lrow[SCV];
+    float scv[SCV];
+#pragma unroll
+    for (int u = 0; u < SCV; ++u) {
+      const int e = min(tid + 256 * u, BM * ng - 1);
+      lrow[u] = layer_row(row_of(e / ng));
+    }
+    issue(c0, buf0);
+    if (nk > 1) issue(c0 + BK, buf1);
+#pragma unroll
+    for (int u = 0; u < SCV; ++u) {
+      const int e = min(tid + 256 * u, BM * ng - 1);
+      scv[u] = scales[(size_t)lrow[u] * G + h0 + e % ng];
+    }
+#pragma unroll
+    for (int u = 0; u < SCV; ++u) {
+      const int e = tid + 256 * u;
+      if (e < BM * ng) sc_s[e % ng][e / ng] = scv[u];
+    }
+  };
+  if (rowmap != nullptr)
+    stage_first([&](int p) { return (int)rowmap[p]; });
+  else
+    stage_first([](int p) { return p; });
+  lds_barrier();  // sc_s; the stages' direct loads are waited for in the loop
   for (int kt = 0; kt < nk; kt += 3) {
     if (kt + 1 < nk) wait_vm_and_barrier<DMA_PER_WAVE>(); else wait_vm_and_barrier<0>();
     if (kt + 2 < nk) issue(c0 + (kt + 2) * BK, buf2);

@@ -233,12 +233,12 @@ __global__ __launch_bounds__(256, 2) void panel_update_kernel(
   // loads of step k + 2.
   const int nk = (c1 - c0) / BK;  // >= 1
   // The tile rows' scales of the panel's groups into sc_s (the list holds
-  // positions; scales are by layer row).  The row-map loads go out before the
-  // first two stages' direct loads and the scale loads right after them, so
-  // waiting for a scale never waits for a stage that was issued later, and the
-  // stages land while the scales are fetched.  Thread e of the BM x ng
-  // entries takes e, e + 256, ... (past the end: the last entry again, loaded
-  // and not stored).
+  // positions; scales are by layer row).  The first two stages' direct loads
+  // go out first and every scale load right behind them, so both are in
+  // flight together (one round trip where the scales used to be waited for
+  // before the stages were issued); the row-map loads, where rows are
+  // compacted, precede the stages.  Thread e of the BM x ng entries takes e,
+  // e + 256, ... (past the end: the last entry again, loaded and not stored).
   constexpr int SCV = kMaxPanelGroups * BM / 256;
   // one straight-line copy per form of the row map, so that the compiler's
   // waits count exactly the loads each copy issues

@@ -36,7 +36,11 @@ def _static(W, H, q, s, z, g, bits, K, tau):
 @pytest.mark.parametrize("order", ["large_then_small"])
 def test_static_refine_matches_refine_on_two_calls(order):
     cases = [(300, 1024, 128, 3, 4, -1.0, 11),     # larger layer, every row active
-             (37, 256, 64, 4, 6, 1e-5, 12)]        # smaller layer, early stopping on
+             (37, 256, 64, 4, 6, 1e-5, 12),        # smaller layer, early stopping on
+             # every row stops by sweep 6 of 40: jarq_refine ends the run when
+             # its look at the active count (pinned memory, no wait) has landed,
+             # jarq_refine_static with its blocking read; same results
+             (48, 384, 128, 3, 40, 2e-4, 14)]
     for rows, cols, g, bits, K, tau, seed in cases:
         W, H, q, s, z = random_layer(rows, cols, g, bits, seed=seed)
         say(f"[no-alloc] rows {rows} cols {cols} g {g} bits {bits} K {K} tau {tau}")
@@ -49,6 +53,8 @@ def test_static_refine_matches_refine_on_two_calls(order):
         assert st["objective_after_scales"] == st_ref["objective_after_scales"]
         assert all(ms == 0.0 for row in st["stage_ms"] for ms in row)
         assert not np.array_equal(q_st, q)          # the call did refine the layer
+        if K == 40:
+            assert st["sweeps_run"] < K
 
 
 def test_static_refine_rejects_a_layer_beyond_the_limit():

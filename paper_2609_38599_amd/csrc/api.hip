@@ -298,6 +298,11 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
     if (tmask == 0u || k >= nrec || !boundary_used(j)) return hipSuccess;
     return hipEventRecord(ev[(size_t)k * per_sweep + j], c.st);
   };
+  // boundary j's event, or null when it is not used
+  auto boundary_event = [&](int k, int j) -> hipEvent_t {
+    if (tmask == 0u || k >= nrec || !boundary_used(j)) return nullptr;
+    return ev[(size_t)k * per_sweep + j];
+  };
   // Early stopping: every fourth sweep the active count is copied behind that
   // sweep into pinned host memory; the host looks at it once the copy has
   // landed (an event query, no wait) and ends the run when no row is left.
@@ -331,10 +336,11 @@ jarq_status sweeps_impl(const jarq_params* p, const float* W, const float* H, ui
       e = launch_solve(c.st, n, c.cols, c.g, c.gram(), c.wh(), codes, zeros,
                        (double*)(c.ws + c.lay.rhs), c.gctl(), scales, c.active(), c.cnt(),
                        c.flags(), p->ridge_lambda, p->ridge_rcond, p->ridge_accept, rmap, n_dev);
-    if (e == hipSuccess) e = mark(k, 2);
+    // boundaries 2 and 3 are the residual product's own start and end times
+    // (events attached to its dispatch: no marker in the stream around it)
     if (e == hipSuccess)
-      e = launch_resid(c.st, n, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), rmap, n_dev);
-    if (e == hipSuccess) e = mark(k, 3);
+      e = launch_resid(c.st, n, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), rmap, n_dev,
+                       boundary_event(k, 2), boundary_event(k, 3));
     if (e == hipSuccess)
       e = launch_group_objective(c.st, n, c.cols, c.g, c.ws, c.lay, scales, c.pbuf(), c.objpart(),
                                  rmap, n_dev);

@@ -189,10 +189,13 @@ hipError_t launch_rw_product(hipStream_t st, int rows, int cols, int g, const ch
 hipError_t launch_codes_cz(hipStream_t st, int rows, int cols, int g, const uint8_t* codes,
                            const int32_t* zeros, _Float16* cz);
 // U = T - What M^T from the exact codes (cz) and the scales, layer rows
-// through rowmap, U by position (sgemm.hip).
+// through rowmap, U by position (sgemm.hip).  ev_start / ev_stop (nullable):
+// events that take the kernel's own start and end times (no marker of their
+// own in the stream).
 hipError_t launch_resid(hipStream_t st, int rows, int cols, int g, const char* ws,
                         const Layout& lay, const float* scales, float* U, const int32_t* rowmap,
-                        const int* n_dev);
+                        const int* n_dev, hipEvent_t ev_start = nullptr,
+                        hipEvent_t ev_stop = nullptr);
 // Per position and group, (R_i e_i) . U_i = e_i^T (H e)_i (fp64) into
 // objpart[position][group], from RW, cz and the scales (layer rows via rowmap).
 hipError_t launch_group_objective(hipStream_t st, int rows, int cols, int g, const char* ws,

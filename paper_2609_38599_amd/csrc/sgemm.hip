@@ -27,6 +27,8 @@
 // compute).  One work-group per CU.  Tiles are ordered so that
 // each XCD (work-groups are dealt to the 8 XCDs round-robin) works on a
 // compact block of tiles that share A row-tiles and B column-tiles in its L2.
+#include <hip/hip_ext.h>
+
 #include "jarq_internal.h"
 
 namespace jarq {
@@ -535,24 +537,43 @@ __global__ __launch_bounds__(512, 1) void resid_kernel(
 template <int G_SIZE>
 static hipError_t launch_resid_t(hipStream_t st, int rows, int cols, const char* ws,
                                  const Layout& lay, const float* scales, float* U,
-                                 const int32_t* rowmap, const int* n_dev) {
+                                 const int32_t* rowmap, const int* n_dev, hipEvent_t ev_start,
+                                 hipEvent_t ev_stop) {
   const int tiles = ((rows + RBM - 1) / RBM) * ((cols + RBN - 1) / RBN);
-  hipLaunchKernelGGL((resid_kernel<G_SIZE>), dim3(tiles), dim3(512), 0, st, rows, cols, cols,
-                     (const _Float16*)(ws + lay.cz), scales, (const _Float16*)(ws + lay.mhi),
-                     (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow),
-                     (const float*)(ws + lay.tm), U, rowmap, n_dev);
+  if (ev_start != nullptr || ev_stop != nullptr) {
+    // timed: the events take the dispatch's own timestamps
+    hipExtLaunchKernelGGL((resid_kernel<G_SIZE>), dim3(tiles), dim3(512), 0, st, ev_start,
+                          ev_stop, 0u, rows, cols, cols, (const _Float16*)(ws + lay.cz), scales,
+                          (const _Float16*)(ws + lay.mhi), (const _Float16*)(ws + lay.mlo),
+                          (const float*)(ws + lay.mrow), (const float*)(ws + lay.tm), U, rowmap,
+                          n_dev);
+  } else {
+    hipLaunchKernelGGL((resid_kernel<G_SIZE>), dim3(tiles), dim3(512), 0, st, rows, cols, cols,
+                       (const _Float16*)(ws + lay.cz), scales, (const _Float16*)(ws + lay.mhi),
+                       (const _Float16*)(ws + lay.mlo), (const float*)(ws + lay.mrow),
+                       (const float*)(ws + lay.tm), U, rowmap, n_dev);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_resid(hipStream_t st, int rows, int cols, int g, const char* ws,
                         const Layout& lay, const float* scales, float* U, const int32_t* rowmap,
-                        const int* n_dev) {
-  if (rows <= 0 || cols <= 0) return hipSuccess;
+                        const int* n_dev, hipEvent_t ev_start, hipEvent_t ev_stop) {
+  if (rows <= 0 || cols <= 0) {  // nothing to launch: the events still mark the spot
+    hipError_t e = hipSuccess;
+    if (ev_start != nullptr) e = hipEventRecord(ev_start, st);
+    if (e == hipSuccess && ev_stop != nullptr) e = hipEventRecord(ev_stop, st);
+    return e;
+  }
   if (cols % BK != 0) return hipErrorInvalidValue;
   switch (g) {
-    case 32: return launch_resid_t<32>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev);
-    case 64: return launch_resid_t<64>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev);
-    case 128: return launch_resid_t<128>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev);
+    case 32:
+      return launch_resid_t<32>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev, ev_start, ev_stop);
+    case 64:
+      return launch_resid_t<64>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev, ev_start, ev_stop);
+    case 128:
+      return launch_resid_t<128>(st, rows, cols, ws, lay, scales, U, rowmap, n_dev, ev_start,
+                                 ev_stop);
     default: return hipErrorInvalidValue;
   }
 }

@@ -12,10 +12,11 @@ reported value is the median over the repetitions of the time per sweep (the
 interquartile range beside it).  K defaults to the layer's own sweep count
 (10 for the headline layer); when another K is asked for, the layer's own K is
 timed the same way and reported beside it.  Inside the timed calls the library
-records HIP events on its stream around the residual product only (the
-roofline kernel): every event leaves the GPU idle for a few microseconds
-between kernels.  The per-stage breakdown comes from a separate, untimed call
-of the same K sweeps from the host state with events around every stage.
+times the residual product only (the roofline kernel), with HIP events
+attached to its dispatch (they take the kernel's own start and end times; no
+marker is added to the stream).  The per-stage breakdown comes from a
+separate, untimed call of the same K sweeps from the host state with events
+around every stage.
 
 The roofline fraction counts the method's own work: 2 rows d^2 FLOP per
 residual product, against the dense fp16 matrix-core peak (the product runs
@@ -467,7 +468,7 @@ def main():
     work = stage_work(cfg, rows, blocks)
 
     # Roofline of the residual product kernel (resid_kernel, one launch per
-    # sweep, timed alone by the library's events inside the timed calls): the
+    # sweep, timed by events attached to its dispatch inside the timed calls): the
     # single kernel with the largest time per sweep.  achieved = the method's
     # own work, 2 rows d^2 FLOP per launch, over the average launch time,
     # against the dense fp16 matrix-core peak (the dtype the contraction runs
